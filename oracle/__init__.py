@@ -1,0 +1,145 @@
+"""CPU oracle for DReSD's dense retrieval step -- test infrastructure only.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library never calls it and
+shares no code with it; the product path fails loudly when its HIP extension
+is missing instead of falling back here.
+
+The arithmetic lives in ``dresd_oracle.c`` (plain C, fp64 accumulation,
+rounded once to fp32; ranking by score descending then lowest row index).
+It follows DReSD Section 3.5, Eq. 3 (cosine similarity argmax over a
+key -> next-tokens store) with unit-norm keys and queries (Section 3.4,
+Eq. 2), generalised to the k best keys that batch verification consumes
+(Section 3.6).  This module only marshals numpy arrays into that library and
+builds it with gcc when it is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dresd_oracle.c")
+_LIB = os.path.join(_HERE, "libdresd_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+DTYPE_CODES = {"f32": 0, "f16": 1, "bf16": 2}
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O3", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+               "-fPIC", "-shared", "-Wall", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            build()
+            lib = ctypes.CDLL(_LIB)
+            P = ctypes.c_void_p
+            lib.oracle_topk.argtypes = [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
+                                        P, ctypes.c_int32, ctypes.c_int32, P, ctypes.c_int32,
+                                        P, P, P, P, ctypes.c_int32]
+            lib.oracle_topk.restype = ctypes.c_int
+            lib.oracle_score_rows.argtypes = [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
+                                              P, P, ctypes.c_int64, P]
+            lib.oracle_score_rows.restype = ctypes.c_int
+            lib.oracle_set_mutation.argtypes = [ctypes.c_int]
+            lib.oracle_set_mutation.restype = None
+            _lib = lib
+    return _lib
+
+
+def _emb_bits(emb: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        if emb.dtype != np.float32:
+            raise TypeError("f32 keys must be a float32 array")
+    elif dtype == "f16":
+        if emb.dtype not in (np.float16, np.uint16):
+            raise TypeError("f16 keys must be float16 (or their uint16 bits)")
+    elif dtype == "bf16":
+        if emb.dtype != np.uint16:
+            raise TypeError("bf16 keys must be passed as their uint16 bits")
+    else:
+        raise ValueError("unknown key dtype %r" % dtype)
+    if emb.ndim != 2:
+        raise ValueError("keys must be [N, d]")
+    return np.ascontiguousarray(emb)
+
+
+def topk(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
+         cont: np.ndarray | None = None, threads: int = 0):
+    """Exact top-k by inner product.
+
+    Returns ``(idx[B,k] int64, score[B,k] f32, tokens[B,k,L] int32 or None,
+    next_score[B] f32)`` where ``next_score`` is the (k+1)-th best score
+    (NaN when k == N).
+    """
+    e = _emb_bits(emb, dtype)
+    q = np.ascontiguousarray(queries, dtype=np.float32)
+    if q.ndim != 2 or q.shape[1] != e.shape[1]:
+        raise ValueError("queries must be [B, d]")
+    N, d = e.shape
+    B = q.shape[0]
+    if not (1 <= k <= N):
+        raise ValueError("need 1 <= k <= N")
+    idx = np.empty((B, k), np.int64)
+    score = np.empty((B, k), np.float32)
+    nxt = np.empty((B,), np.float32)
+    tok = None
+    L = 0
+    cptr = None
+    if cont is not None:
+        c = np.ascontiguousarray(cont, dtype=np.int32)
+        if c.ndim != 2 or c.shape[0] != N:
+            raise ValueError("continuations must be [N, L]")
+        L = c.shape[1]
+        tok = np.empty((B, k, L), np.int32)
+        cptr = c.ctypes.data
+    rc = _load().oracle_topk(e.ctypes.data, DTYPE_CODES[dtype], N, d, q.ctypes.data, B, k,
+                             cptr, L, idx.ctypes.data, score.ctypes.data,
+                             tok.ctypes.data if tok is not None else None,
+                             nxt.ctypes.data, int(threads))
+    if rc != 0:
+        raise RuntimeError("oracle_topk failed")
+    return idx, score, tok, nxt
+
+
+def score_rows(emb: np.ndarray, dtype: str, query: np.ndarray, rows) -> np.ndarray:
+    """Oracle scores of the given rows for one query (fp32)."""
+    e = _emb_bits(emb, dtype)
+    q = np.ascontiguousarray(query, dtype=np.float32).reshape(-1)
+    r = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1)
+    out = np.empty(r.shape, np.float32)
+    rc = _load().oracle_score_rows(e.ctypes.data, DTYPE_CODES[dtype], e.shape[0], e.shape[1],
+                                   q.ctypes.data, r.ctypes.data, r.size, out.ctypes.data)
+    if rc != 0:
+        raise RuntimeError("oracle_score_rows failed (row out of range?)")
+    return out
+
+
+class mutation:
+    """Context manager that plants a numbered mistake in the oracle (CPU tests only)."""
+
+    def __init__(self, m: int):
+        self.m = m
+
+    def __enter__(self):
+        _load().oracle_set_mutation(self.m)
+        return self
+
+    def __exit__(self, *exc):
+        _load().oracle_set_mutation(0)
+        return False

@@ -1,0 +1,229 @@
+/*
+ * CPU oracle for DReSD's dense retrieval step -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Only the test suite, the smoke check and the benchmark's CPU-baseline leg
+ * may load this library.  The product path (the HIP library) never calls it,
+ * shares no code, header, table or helper with it, and must fail loudly when
+ * its own extension is missing instead of falling back to this file.
+ *
+ * What it computes (DReSD, Section 3.5, Eq. 3, read with Section 3.4, Eq. 2):
+ * the datastore is a key -> value map whose keys are L2-normalised token
+ * embeddings and whose values are the next L tokens.  Retrieval returns the
+ * value of the key with the highest cosine similarity to the (L2-normalised)
+ * query.  For unit-norm keys and queries the cosine is the plain inner
+ * product, so the denominator max(|a||b|, eps) of Eq. 3 is 1 and is not
+ * applied.  Batch verification (Section 3.6) consumes several drafts, so the
+ * argmax of Eq. 3 is taken as the k best keys.
+ *
+ * Precision: the paper fixes none.  Each score is the exact inner product,
+ * accumulated in fp64 in dimension order (every product of an fp32 query
+ * element and an fp32/f16/bf16 key element is exact in fp64), then rounded
+ * once to fp32.  Ranking is decided on that fp32 value, which is the
+ * precision the device path decides in: score descending, equal scores by
+ * lowest row index.  No blocking, fusion or reordering of the arithmetic
+ * beyond that definition; queries are looped inside rows only so that the
+ * datastore is read once per batch, which does not change any value.
+ *
+ * Parity pins live in the CPU tests (closed forms, exact brute force,
+ * invariants, duplicates, self-retrieval MRR of Eq. 4, planted mutations).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { ORACLE_F32 = 0, ORACLE_F16 = 1, ORACLE_BF16 = 2 };
+
+/* Planted-mistake hooks: a non-zero value makes the oracle wrong on purpose
+ * so that the CPU tests can show each pin catches that class of mistake.
+ * Zero (the default) is the oracle as specified. */
+static int g_mutation = 0;
+void oracle_set_mutation(int m) { g_mutation = m; }
+
+/* IEEE binary16 bits -> value, from the format's definition:
+ * sign, 5-bit biased exponent (bias 15), 10-bit fraction, subnormals at
+ * exponent 0 scaled by 2^-24. */
+static double f16_bits_value(uint16_t h) {
+  int sign = h >> 15;
+  int ex = (h >> 10) & 0x1f;
+  int fr = h & 0x3ff;
+  double v;
+  if (ex == 0)
+    v = ldexp((double)fr, -24);
+  else if (ex == 31)
+    v = fr ? NAN : INFINITY;
+  else
+    v = ldexp((double)(fr | 0x400), ex - 25);
+  return sign ? -v : v;
+}
+
+/* bfloat16 bits are the upper half of an IEEE binary32. */
+static double bf16_bits_value(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+double oracle_decode(const void *emb, int dtype, int64_t off) {
+  switch (dtype) {
+  case ORACLE_F32:
+    return (double)((const float *)emb)[off];
+  case ORACLE_F16:
+    return f16_bits_value(((const uint16_t *)emb)[off]);
+  default:
+    return bf16_bits_value(((const uint16_t *)emb)[off]);
+  }
+}
+
+/* Eq. 3 with unit norms: the exact inner product of query q and key row i,
+ * summed in dimension order in fp64, rounded once to fp32. */
+static float score_row(const void *emb, int dtype, int32_t d, int64_t i,
+                       const float *q) {
+  double s = 0.0;
+  int32_t jn = (g_mutation == 1) ? d - 1 : d; /* mutation 1: drop a term */
+  for (int32_t j = 0; j < jn; ++j) {
+    /* mutation 3: key element taken at the mirrored dimension */
+    int32_t je = (g_mutation == 3) ? d - 1 - j : j;
+    double p = (double)q[j] * oracle_decode(emb, dtype, i * (int64_t)d + je);
+    s = (g_mutation == 2 && j == 0) ? s - p : s + p; /* mutation 2: sign */
+  }
+  float f = (float)s;
+  if (g_mutation == 6) { /* mutation 6: score truncated to 16 bits */
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    u &= 0xffff0000u;
+    memcpy(&f, &u, sizeof f);
+  }
+  return f;
+}
+
+typedef struct {
+  float s;
+  int64_t i;
+} item;
+
+/* Ranking order: higher score first; equal scores by lower row index. */
+static int better(item a, item b) {
+  if (g_mutation == 4) /* mutation 4: ties broken by highest index */
+    return a.s > b.s || (a.s == b.s && a.i > b.i);
+  if (g_mutation == 5) /* mutation 5: ascending scores */
+    return a.s < b.s || (a.s == b.s && a.i < b.i);
+  return a.s > b.s || (a.s == b.s && a.i < b.i);
+}
+
+static int cmp_items(const void *pa, const void *pb) {
+  item a = *(const item *)pa, b = *(const item *)pb;
+  if (better(a, b)) return -1;
+  if (better(b, a)) return 1;
+  return 0;
+}
+
+/* Keep the m best items seen so far in 'best' (sorted, best first). */
+static void offer(item *best, int64_t *count, int64_t m, item x) {
+  int64_t c = *count;
+  if (c == m && !better(x, best[m - 1])) return;
+  int64_t pos = (c < m) ? c : m - 1;
+  while (pos > 0 && better(x, best[pos - 1])) {
+    best[pos] = best[pos - 1];
+    --pos;
+  }
+  best[pos] = x;
+  if (c < m) *count = c + 1;
+}
+
+/*
+ * Exact top-k for B queries over N keys.
+ *   emb   [N, d] row-major, dtype ORACLE_F32 / ORACLE_F16 / ORACLE_BF16
+ *   Q     [B, d] fp32 row-major
+ *   cont  [N, L] int32 (may be NULL when L == 0)
+ * Outputs (caller-owned):
+ *   idx [B, k] int64, score [B, k] fp32, tokens [B, k, L] int32 (NULL ok),
+ *   next_score [B] fp32: the (k+1)-th best score, NaN when k == N (NULL ok).
+ * Returns 0, or -1 on invalid arguments / allocation failure.
+ */
+int oracle_topk(const void *emb, int dtype, int64_t N, int32_t d,
+                const float *Q, int32_t B, int32_t k, const int32_t *cont,
+                int32_t L, int64_t *idx, float *score, int32_t *tokens,
+                float *next_score, int32_t nthreads) {
+  if (!emb || !Q || !idx || !score || N < 1 || d < 1 || B < 0 || k < 1 ||
+      k > N || dtype < 0 || dtype > 2)
+    return -1;
+  if (B == 0) return 0;
+  int64_t m = (k < N) ? (int64_t)k + 1 : (int64_t)k;
+  int nt = 1;
+#ifdef _OPENMP
+  nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#endif
+  item *all = (item *)malloc(sizeof(item) * (size_t)nt * (size_t)B * (size_t)m);
+  int64_t *cnt = (int64_t *)calloc((size_t)nt * (size_t)B, sizeof(int64_t));
+  if (!all || !cnt) {
+    free(all);
+    free(cnt);
+    return -1;
+  }
+#ifdef _OPENMP
+#pragma omp parallel num_threads(nt)
+#endif
+  {
+    int t = 0, T = 1;
+#ifdef _OPENMP
+    t = omp_get_thread_num();
+    T = omp_get_num_threads();
+#endif
+    int64_t lo = N * t / T, hi = N * (t + 1) / T;
+    for (int64_t i = lo; i < hi; ++i)
+      for (int32_t b = 0; b < B; ++b) {
+        item x;
+        x.s = score_row(emb, dtype, d, i, Q + (int64_t)b * d);
+        x.i = i;
+        offer(all + ((size_t)t * B + b) * m, cnt + (size_t)t * B + b, m, x);
+      }
+  }
+  item *merged = (item *)malloc(sizeof(item) * (size_t)nt * (size_t)m);
+  if (!merged) {
+    free(all);
+    free(cnt);
+    return -1;
+  }
+  for (int32_t b = 0; b < B; ++b) {
+    int64_t tot = 0;
+    for (int t = 0; t < nt; ++t) {
+      int64_t c = cnt[(size_t)t * B + b];
+      memcpy(merged + tot, all + ((size_t)t * B + b) * m, sizeof(item) * (size_t)c);
+      tot += c;
+    }
+    qsort(merged, (size_t)tot, sizeof(item), cmp_items);
+    for (int32_t r = 0; r < k; ++r) {
+      idx[(int64_t)b * k + r] = merged[r].i;
+      score[(int64_t)b * k + r] = merged[r].s;
+      if (tokens && cont && L > 0) {
+        int64_t src = merged[r].i;
+        if (g_mutation == 7 && src + 1 < N) ++src; /* mutation 7: off-by-one */
+        memcpy(tokens + ((int64_t)b * k + r) * L, cont + src * L,
+               sizeof(int32_t) * (size_t)L);
+      }
+    }
+    if (next_score) next_score[b] = (k < N) ? merged[k].s : NAN;
+  }
+  free(merged);
+  free(all);
+  free(cnt);
+  return 0;
+}
+
+/* Scores of the given rows for one query (the same arithmetic as above);
+ * used to re-score whatever indices the device path returns. */
+int oracle_score_rows(const void *emb, int dtype, int64_t N, int32_t d,
+                      const float *q, const int64_t *rows, int64_t nrows,
+                      float *out) {
+  if (!emb || !q || !rows || !out || d < 1) return -1;
+  for (int64_t r = 0; r < nrows; ++r) {
+    if (rows[r] < 0 || rows[r] >= N) return -1;
+    out[r] = score_row(emb, dtype, d, rows[r], q);
+  }
+  return 0;
+}

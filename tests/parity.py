@@ -1,0 +1,103 @@
+"""Parity rules between the device path and the oracle (per query).
+
+The rules follow the acceptance statement for exact top-k retrieval:
+scores agree within ``tol`` (1e-5 for fp32 keys, 2e-3 for 16-bit keys);
+index sets are identical except at ranks where the oracle's rank-k and
+rank-(k+1) scores differ by less than ``tol``; gathered continuation tokens
+are bit-exact for the returned indices.
+
+  R1  |g_score[r] - o_score[r]| <= tol for every rank r
+  R2  |g_score[r] - exact(g_idx[r])| <= tol (exact = oracle re-score of that row)
+  R3  g_score non-increasing; equal g_score values have ascending g_idx
+  R4  g_idx distinct and inside [0, N)
+  R5  must-include M = {o_idx[r] : o_score[r] - o_next >= tol} is contained in
+      set(g_idx), which is contained in A = {i : exact(i) > o_score[k-1] - tol}
+      (identical sets whenever the rank-k / rank-(k+1) gap is >= tol)
+  R7  tokens[r, :] == cont[g_idx[r], :] bit for bit
+Also reported (not gating): exact-order agreement and max |g - exact|.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+TOL = {"f32": 1e-5, "f16": 2e-3, "bf16": 2e-3}
+
+
+class ParityError(AssertionError):
+    pass
+
+
+def check_query(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont=None,
+                tol=1e-5):
+    """Check one query.  ``exact_of(rows) -> fp32 scores`` re-scores rows with
+    the oracle.  Returns a small report dict; raises ParityError on failure."""
+    g_idx = np.asarray(g_idx, np.int64)
+    g_score = np.asarray(g_score, np.float32)
+    o_idx = np.asarray(o_idx, np.int64)
+    o_score = np.asarray(o_score, np.float32)
+    k = o_idx.size
+    if g_idx.shape != (k,) or g_score.shape != (k,):
+        raise ParityError("shape mismatch")
+    # R4
+    if g_idx.min() < 0 or g_idx.max() >= N:
+        raise ParityError("R4: index out of range")
+    if np.unique(g_idx).size != k:
+        raise ParityError("R4: duplicate indices")
+    # R3
+    ds = np.diff(g_score.astype(np.float64))
+    if np.any(ds > 0):
+        raise ParityError("R3: scores increase at rank %d" % int(np.argmax(ds > 0)))
+    eq = ds == 0
+    if np.any(eq & (np.diff(g_idx) < 0)):
+        raise ParityError("R3: equal scores not in ascending index order")
+    # R1
+    d1 = np.abs(g_score.astype(np.float64) - o_score.astype(np.float64))
+    if np.any(d1 > tol):
+        r = int(np.argmax(d1))
+        raise ParityError("R1: rank %d score %r vs oracle %r" % (r, g_score[r], o_score[r]))
+    # R2
+    ex = np.asarray(exact_of(g_idx), np.float32)
+    d2 = np.abs(g_score.astype(np.float64) - ex.astype(np.float64))
+    if np.any(d2 > tol):
+        r = int(np.argmax(d2))
+        raise ParityError("R2: rank %d row %d score %r vs exact %r" % (r, g_idx[r], g_score[r],
+                                                                        ex[r]))
+    # R5
+    if o_next is None or np.isnan(o_next):
+        must = set(o_idx.tolist())
+    else:
+        must = {int(i) for i, s in zip(o_idx, o_score) if float(s) - float(o_next) >= tol}
+    gset = set(g_idx.tolist())
+    if not must <= gset:
+        raise ParityError("R5: missing must-include rows %s" % sorted(must - gset)[:8])
+    floor = float(o_score[-1]) - tol
+    if np.any(ex.astype(np.float64) <= floor):
+        raise ParityError("R5: returned a row scoring <= rank-k score - tol")
+    # R7
+    if g_tok is not None and cont is not None:
+        want = np.asarray(cont)[g_idx]
+        if not np.array_equal(np.asarray(g_tok), want):
+            raise ParityError("R7: gathered tokens differ")
+    return {
+        "exact_order": bool(np.array_equal(g_idx, o_idx)),
+        "max_abs_vs_exact": float(d2.max()) if d2.size else 0.0,
+        "max_abs_vs_oracle": float(d1.max()) if d1.size else 0.0,
+    }
+
+
+def check_batch(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of_b, N, cont=None,
+                tol=1e-5):
+    """``exact_of_b(b, rows)`` re-scores rows for query b."""
+    reps = []
+    for b in range(o_idx.shape[0]):
+        try:
+            reps.append(check_query(g_idx[b], g_score[b], None if g_tok is None else g_tok[b],
+                                    o_idx[b], o_score[b], None if o_next is None else o_next[b],
+                                    lambda rows, b=b: exact_of_b(b, rows), N, cont, tol))
+        except ParityError as e:
+            raise ParityError("query %d: %s" % (b, e)) from None
+    return {
+        "exact_order_rate": float(np.mean([r["exact_order"] for r in reps])) if reps else 1.0,
+        "max_abs_vs_exact": max([r["max_abs_vs_exact"] for r in reps], default=0.0),
+        "max_abs_vs_oracle": max([r["max_abs_vs_oracle"] for r in reps], default=0.0),
+    }
