@@ -1,0 +1,152 @@
+/*
+ * dresd.h -- C ABI of the MI355X (gfx950) dense-retrieval library.
+ *
+ * The library implements the drafting step of DReSD (Dense Retrieval for
+ * Speculative Decoding): the datastore is a key -> value map whose keys are
+ * L2-normalised token embeddings and whose values are the next L tokens that
+ * followed each key (Section 3.5).  A query embedding, itself L2-normalised
+ * (Section 3.4, Eq. 2), retrieves the value of the most similar key under
+ * cosine similarity (Section 3.5, Eq. 3).  Keys and queries have unit norm, so
+ * the cosine is the inner product and the library computes the raw inner
+ * product without dividing by the norms.  Batch verification consumes several
+ * drafts per decode step (Section 3.6), so the argmax of Eq. 3 is returned as
+ * the k best keys.  The search is exact (every key is scored), not the
+ * approximate search the paper used.
+ *
+ * Conventions shared by every call:
+ *  - Pointers marked "device" are HIP device pointers on the current device.
+ *    Pointers marked "host" are ordinary host memory.
+ *  - dresd_stream is a hipStream_t (NULL = the null stream).  Work is enqueued
+ *    on it and the call returns; results are valid once the stream has
+ *    completed, except where a call says it synchronises.
+ *  - Every argument is validated before any work is enqueued: on an error
+ *    return nothing has been written to any output.
+ *  - No C++ exception crosses this interface.  A failing call returns a status
+ *    code and sets a thread-local message readable with dresd_last_error().
+ *  - Inputs must be finite.  Keys and queries are expected to be
+ *    L2-normalised; the library does not renormalise.
+ */
+#ifndef DRESD_H
+#define DRESD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct dresd_index dresd_index; /* opaque, library-owned */
+typedef void *dresd_stream;             /* a hipStream_t */
+
+/* Storage type of the keys.  Queries are always fp32; scores are fp32. */
+typedef enum { DRESD_F32 = 0, DRESD_F16 = 1, DRESD_BF16 = 2 } dresd_dtype;
+
+typedef enum {
+  DRESD_OK = 0,
+  DRESD_EINVAL = 1,      /* an argument is out of its documented range     */
+  DRESD_ENOMEM = 2,      /* a device allocation failed (nothing leaked)    */
+  DRESD_EDEVICE = 3,     /* a HIP call failed; message in dresd_last_error */
+  DRESD_EUNSUPPORTED = 4 /* valid request this build cannot serve          */
+} dresd_status;
+
+/* Largest k a search may ask for. */
+#define DRESD_K_MAX 1024
+/* Largest datastore: row indices are carried in 32 bits inside the kernels. */
+#define DRESD_N_MAX 4294967040LL
+
+/*
+ * Build an index over N keys (Section 3.5: keys are token embeddings, values
+ * the next L tokens; building the datastore is a one-time cost, Section 5.6).
+ *
+ *   embeddings    device, [N, d] row-major, element type `dtype`
+ *                 (f32, IEEE binary16, or bfloat16), each row L2-normalised.
+ *   continuations device, [N, L] row-major int32 token ids (opaque; copied
+ *                 bit for bit, including any padding id).
+ *   N, d, L       1 <= N <= DRESD_N_MAX, 1 <= d <= 16384, 1 <= L <= 4096.
+ *   dtype         a dresd_dtype value.
+ *   stream        stream used for the copies.
+ *   out           host; receives the new index.
+ *
+ * Ownership: both arrays are copied into library-owned device memory (keys
+ * re-laid out for the scan).  The call synchronises `stream` before it
+ * returns, so the caller may free or reuse its arrays immediately.  The index
+ * lives on the device that was current during this call.
+ * Errors: EINVAL (null pointer, size out of range, unknown dtype), ENOMEM,
+ * EDEVICE.  On error *out is left unchanged and nothing is allocated.
+ */
+dresd_status dresd_index_create(const void *embeddings,
+                                const int32_t *continuations, int64_t N,
+                                int32_t d, int32_t L, int32_t dtype,
+                                dresd_stream stream, dresd_index **out);
+
+/*
+ * Exact top-k retrieval for a batch of B queries (Eq. 3 taken as the k best
+ * keys; the drafts of Section 3.6 are their continuations).
+ *
+ *   ix        index from dresd_index_create.
+ *   queries   device, [B, d] fp32 row-major, each row L2-normalised.
+ *   B         B >= 0; B == 0 is a no-op returning DRESD_OK.
+ *   k         1 <= k <= min(N, DRESD_K_MAX).
+ *   idx       device, [B, k] int64: row indices of the k best keys.
+ *   score     device, [B, k] fp32: their inner products with the query.
+ *   tokens    device, [B, k, L] int32: continuations of those rows, gathered
+ *             bit for bit; may be NULL to skip the gather.
+ *   stream    stream the search runs on.
+ *
+ * Order: rank r holds the r-th largest score; equal scores are ordered by
+ * ascending row index.  Scores are accumulated in fp32.  Keys stored as f16
+ * or bf16 are multiplied by the query split into a high and a low 16-bit part
+ * when the batch is small (and always for bf16), so scores stay within about
+ * 1e-5 of the exact inner product; large f16 batches round the query to f16
+ * once (score error below 5e-4).
+ * Determinism: identical inputs give bitwise identical outputs.
+ * Ownership: outputs are caller-owned and must stay alive until `stream`
+ * completes.  The index owns a workspace that grows on first use with a new
+ * batch shape (that growth allocates and synchronises); concurrent searches
+ * on one index are not supported.
+ * Errors: EINVAL (null index/queries/idx/score, k out of range, B < 0),
+ * ENOMEM (workspace growth failed), EDEVICE.
+ */
+dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B,
+                          int32_t k, int64_t *idx, float *score,
+                          int32_t *tokens, dresd_stream stream);
+
+/* Describe an index.  Any output pointer (host) may be NULL.
+ * Errors: EINVAL when ix is NULL. */
+dresd_status dresd_index_info(const dresd_index *ix, int64_t *N, int32_t *d,
+                              int32_t *L, int32_t *dtype);
+
+/* Free an index and its workspace (synchronises its device).  NULL is
+ * ignored. */
+void dresd_index_destroy(dresd_index *ix);
+
+/* Message for the last failing call on this thread ("" if none).  The
+ * pointer stays valid until the next call on this thread. */
+const char *dresd_last_error(void);
+
+/*
+ * Measurement support.  When enabled, every search records HIP events on its
+ * stream around the main scan kernel (the full pass over the keys) and around
+ * the whole search.  dresd_profile_read synchronises those events and
+ * returns the summed device milliseconds and the number of searches since
+ * the last read, then clears them.  Outputs are host pointers (NULL allowed).
+ * Errors: EINVAL when ix is NULL; EDEVICE.
+ */
+dresd_status dresd_profile_enable(dresd_index *ix, int32_t on);
+dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms,
+                                double *search_ms, int64_t *searches);
+
+/*
+ * Describe how the next search of this shape would run (host outputs, NULL
+ * allowed): the number of passes over sampled keys before the main pass, the
+ * number of waves of the main scan, and the bytes of workspace it needs.
+ * Errors: EINVAL for the same argument errors as dresd_search.
+ */
+dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,
+                               int32_t *sample_passes, int32_t *scan_waves,
+                               int64_t *workspace_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DRESD_H */

@@ -79,16 +79,20 @@ double oracle_decode(const void *emb, int dtype, int64_t off) {
   }
 }
 
-/* Eq. 3 with unit norms: the exact inner product of query q and key row i,
- * summed in dimension order in fp64, rounded once to fp32. */
-static float score_row(const void *emb, int dtype, int32_t d, int64_t i,
-                       const float *q) {
+/* Key row i decoded to fp64 (exact for every storage type). */
+static void decode_row(const void *emb, int dtype, int32_t d, int64_t i, double *e) {
+  for (int32_t j = 0; j < d; ++j) e[j] = oracle_decode(emb, dtype, i * (int64_t)d + j);
+}
+
+/* Eq. 3 with unit norms: the exact inner product of query q and a decoded
+ * key row e, summed in dimension order in fp64, rounded once to fp32. */
+static float score_row(const double *e, int32_t d, const float *q) {
   double s = 0.0;
   int32_t jn = (g_mutation == 1) ? d - 1 : d; /* mutation 1: drop a term */
   for (int32_t j = 0; j < jn; ++j) {
     /* mutation 3: key element taken at the mirrored dimension */
     int32_t je = (g_mutation == 3) ? d - 1 - j : j;
-    double p = (double)q[j] * oracle_decode(emb, dtype, i * (int64_t)d + je);
+    double p = (double)q[j] * e[je];
     s = (g_mutation == 2 && j == 0) ? s - p : s + p; /* mutation 2: sign */
   }
   float f = (float)s;
@@ -158,6 +162,7 @@ int oracle_topk(const void *emb, int dtype, int64_t N, int32_t d,
 #ifdef _OPENMP
   nt = nthreads > 0 ? nthreads : omp_get_max_threads();
 #endif
+  int fail = 0;
   item *all = (item *)malloc(sizeof(item) * (size_t)nt * (size_t)B * (size_t)m);
   int64_t *cnt = (int64_t *)calloc((size_t)nt * (size_t)B, sizeof(int64_t));
   if (!all || !cnt) {
@@ -175,13 +180,23 @@ int oracle_topk(const void *emb, int dtype, int64_t N, int32_t d,
     T = omp_get_num_threads();
 #endif
     int64_t lo = N * t / T, hi = N * (t + 1) / T;
-    for (int64_t i = lo; i < hi; ++i)
+    double *e = (double *)malloc(sizeof(double) * (size_t)d);
+    if (!e) fail = 1;
+    for (int64_t i = lo; e && i < hi; ++i) {
+      decode_row(emb, dtype, d, i, e);
       for (int32_t b = 0; b < B; ++b) {
         item x;
-        x.s = score_row(emb, dtype, d, i, Q + (int64_t)b * d);
+        x.s = score_row(e, d, Q + (int64_t)b * d);
         x.i = i;
         offer(all + ((size_t)t * B + b) * m, cnt + (size_t)t * B + b, m, x);
       }
+    }
+    free(e);
+  }
+  if (fail) {
+    free(all);
+    free(cnt);
+    return -1;
   }
   item *merged = (item *)malloc(sizeof(item) * (size_t)nt * (size_t)m);
   if (!merged) {
@@ -221,9 +236,16 @@ int oracle_score_rows(const void *emb, int dtype, int64_t N, int32_t d,
                       const float *q, const int64_t *rows, int64_t nrows,
                       float *out) {
   if (!emb || !q || !rows || !out || d < 1) return -1;
+  double *e = (double *)malloc(sizeof(double) * (size_t)d);
+  if (!e) return -1;
   for (int64_t r = 0; r < nrows; ++r) {
-    if (rows[r] < 0 || rows[r] >= N) return -1;
-    out[r] = score_row(emb, dtype, d, rows[r], q);
+    if (rows[r] < 0 || rows[r] >= N) {
+      free(e);
+      return -1;
+    }
+    decode_row(emb, dtype, d, rows[r], e);
+    out[r] = score_row(e, d, q);
   }
+  free(e);
   return 0;
 }

@@ -1,0 +1,110 @@
+"""MI355X-native exact dense retrieval for DReSD (Dense Retrieval for
+Speculative Decoding): a datastore of L2-normalised token embeddings mapped to
+their next tokens (Section 3.5), searched by inner product (Eq. 3 with unit
+norms) for the k best keys whose continuations become drafts (Section 3.6).
+
+The search runs in hand-written gfx950 HIP kernels behind the C ABI of
+``include/dresd.h``; this module only passes torch device pointers and the
+current stream to it.
+"""
+from __future__ import annotations
+
+import ctypes
+
+from . import _lib
+from ._lib import DresdError, K_MAX  # noqa: F401
+
+__all__ = ["Index", "DresdError", "K_MAX"]
+
+_DTYPES = None
+
+
+def _dtype_code(t):
+    import torch
+    global _DTYPES
+    if _DTYPES is None:
+        _DTYPES = {torch.float32: _lib.F32, torch.float16: _lib.F16, torch.bfloat16: _lib.BF16}
+    if t.dtype not in _DTYPES:
+        raise TypeError("keys must be float32, float16 or bfloat16, not %s" % t.dtype)
+    return _DTYPES[t.dtype]
+
+
+def _stream_handle(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Index:
+    """An exact inner-product index over ``keys[N, d]`` with values ``cont[N, L]``.
+
+    Both tensors must be contiguous and on the current GPU; they are copied
+    into library-owned memory, so they may be freed after construction.
+    """
+
+    def __init__(self, keys, cont, stream=None):
+        import torch
+        if not (keys.is_cuda and cont.is_cuda):
+            raise ValueError("keys and continuations must be GPU tensors")
+        if keys.dim() != 2 or cont.dim() != 2 or cont.shape[0] != keys.shape[0]:
+            raise ValueError("keys must be [N, d] and continuations [N, L]")
+        if cont.dtype != torch.int32:
+            raise TypeError("continuations must be int32")
+        keys = keys.contiguous()
+        cont = cont.contiguous()
+        self._lib = _lib.load()
+        self._h = ctypes.c_void_p()
+        self.N, self.d = int(keys.shape[0]), int(keys.shape[1])
+        self.L = int(cont.shape[1])
+        self.device = keys.device
+        _lib.check(self._lib.dresd_index_create(
+            ctypes.c_void_p(keys.data_ptr()), ctypes.c_void_p(cont.data_ptr()), self.N, self.d,
+            self.L, _dtype_code(keys), _stream_handle(stream), ctypes.byref(self._h)))
+
+    def search(self, queries, k: int, tokens: bool = True, out=None, stream=None):
+        """Top-k by inner product.  Returns ``(idx int64[B,k], score f32[B,k],
+        tokens int32[B,k,L] or None)``."""
+        import torch
+        if not queries.is_cuda or queries.dtype != torch.float32:
+            raise TypeError("queries must be a float32 GPU tensor")
+        if queries.dim() != 2 or queries.shape[1] != self.d:
+            raise ValueError("queries must be [B, %d]" % self.d)
+        q = queries.contiguous()
+        B = int(q.shape[0])
+        if out is None:
+            idx = torch.empty((B, k), dtype=torch.int64, device=q.device)
+            score = torch.empty((B, k), dtype=torch.float32, device=q.device)
+            tok = torch.empty((B, k, self.L), dtype=torch.int32, device=q.device) if tokens else None
+        else:
+            idx, score, tok = out
+        _lib.check(self._lib.dresd_search(
+            self._h, ctypes.c_void_p(q.data_ptr()), B, int(k), ctypes.c_void_p(idx.data_ptr()),
+            ctypes.c_void_p(score.data_ptr()),
+            ctypes.c_void_p(tok.data_ptr()) if tok is not None else None, _stream_handle(stream)))
+        return idx, score, tok
+
+    def plan(self, B: int, k: int):
+        sp, w, ws = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+        _lib.check(self._lib.dresd_search_plan(self._h, int(B), int(k), ctypes.byref(sp),
+                                               ctypes.byref(w), ctypes.byref(ws)))
+        return {"sample_passes": sp.value, "scan_waves": w.value, "workspace_bytes": ws.value}
+
+    def profile(self, on: bool = True):
+        _lib.check(self._lib.dresd_profile_enable(self._h, 1 if on else 0))
+
+    def profile_read(self):
+        a, b, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+        _lib.check(self._lib.dresd_profile_read(self._h, ctypes.byref(a), ctypes.byref(b),
+                                                ctypes.byref(n)))
+        return {"scan_ms": a.value, "search_ms": b.value, "searches": n.value}
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            self._lib.dresd_index_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

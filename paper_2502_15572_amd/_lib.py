@@ -1,0 +1,73 @@
+"""ctypes binding of libdresd.so (the C ABI declared in include/dresd.h).
+
+Argument marshalling only: every step of the search runs in the library's
+HIP kernels.  There is no fallback: if the library cannot be loaded, loading
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdresd.so")
+
+OK, EINVAL, ENOMEM, EDEVICE, EUNSUPPORTED = 0, 1, 2, 3, 4
+K_MAX = 1024
+F32, F16, BF16 = 0, 1, 2
+
+EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_index_destroy",
+           "dresd_last_error", "dresd_profile_enable", "dresd_profile_read",
+           "dresd_search_plan"]
+
+_lock = threading.Lock()
+_lib = None
+
+
+class DresdError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("dresd status %d: %s" % (status, msg))
+        self.status = status
+
+
+def _declare(lib):
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.dresd_index_create.argtypes = [P, P, I64, I32, I32, I32, P, ctypes.POINTER(P)]
+    lib.dresd_index_create.restype = ctypes.c_int
+    lib.dresd_search.argtypes = [P, P, I32, I32, P, P, P, P]
+    lib.dresd_search.restype = ctypes.c_int
+    lib.dresd_index_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I32),
+                                     ctypes.POINTER(I32), ctypes.POINTER(I32)]
+    lib.dresd_index_info.restype = ctypes.c_int
+    lib.dresd_index_destroy.argtypes = [P]
+    lib.dresd_index_destroy.restype = None
+    lib.dresd_last_error.argtypes = []
+    lib.dresd_last_error.restype = ctypes.c_char_p
+    lib.dresd_profile_enable.argtypes = [P, I32]
+    lib.dresd_profile_enable.restype = ctypes.c_int
+    lib.dresd_profile_read.argtypes = [P, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]
+    lib.dresd_profile_read.restype = ctypes.c_int
+    lib.dresd_search_plan.argtypes = [P, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(I32),
+                                      ctypes.POINTER(I64)]
+    lib.dresd_search_plan.restype = ctypes.c_int
+    return lib
+
+
+def load(path: str | None = None):
+    """Load the library (building it first only if no build exists)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            p = path or LIB_PATH
+            if not os.path.exists(p):
+                from . import build as _build
+                _build.build()
+            _lib = _declare(ctypes.CDLL(p))
+    return _lib
+
+
+def check(status: int):
+    if status != OK:
+        raise DresdError(status, load().dresd_last_error().decode())

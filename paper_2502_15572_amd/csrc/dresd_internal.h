@@ -1,0 +1,67 @@
+// Internal declarations shared by the host runtime and the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dresd {
+
+// Keys are stored in tiles of 16 rows.  A tile is a run of 1 KiB blocks, one
+// per group of dimensions (32 dims for 16-bit keys, 16 dims for fp32 keys).
+// Inside a block, 16-byte chunk c (c = 0..63) holds row (c % 16) of the tile
+// and dims [w*(c/16), w*(c/16) + w) of the block, w = 8 (16-bit) or 4 (fp32):
+// exactly the per-lane operand of one 16x16 MFMA, so wave lane c loads chunk c
+// and every wave load is one contiguous 1 KiB.
+constexpr int kTileRows = 16;
+constexpr int kBlockBytes = 1024;
+constexpr int kWaveSize = 64;
+constexpr int kScanThreads = 256;   // 4 waves per workgroup
+constexpr int kMergeThreads = 256;
+constexpr int kMergeCap = 4096;     // candidates a merge keeps in LDS
+#define DRESD_K_MAX_INTERNAL 1024   // equals DRESD_K_MAX of the public header
+
+enum DType { kF32 = 0, kF16 = 1, kBF16 = 2 };
+
+struct ScanParams {
+  const void *data;          // tiled keys
+  const float *queries;      // [B, d] fp32
+  int64_t N;                 // rows
+  int64_t nvisit;            // tiles this pass visits: tile = j * stride
+  int64_t stride;            // tile stride of the pass (1 = every tile)
+  const uint64_t *tau;       // [B] keys below tau are pruned (0 = none); may be null
+  uint64_t *lists;           // [B][G][C] per-wave candidate lists
+  uint64_t *pool;            // [B][pool_cap] per-query candidate pools
+  uint32_t *pool_cnt;        // [B]
+  int64_t pool_cap;
+  int B, d, KB, k, C, G;     // batch, dims, blocks per tile, k, list capacity, waves
+};
+
+struct MergeParams {
+  const uint64_t *pool;      // [B][pool_cap]
+  uint32_t *pool_cnt;        // [B]; reset to 0 by the merge
+  int64_t pool_cap;
+  int B, k;
+  uint64_t *tau_out;         // sample mode: k-th best key per query (0 if < k)
+  int64_t *idx;              // final mode outputs
+  float *score;
+  int32_t *tokens;           // may be null
+  const int32_t *cont;       // [N, L]
+  int L;
+  int final_mode;
+};
+
+struct LayoutParams {
+  const void *src;           // [N, d] row-major
+  void *dst;                 // tiles
+  int64_t N;
+  int64_t chunks;            // total 16-byte chunks of the tiled layout
+  int d, KB;
+};
+
+// Kernel launch entry points (defined in dresd_kernels.hip).
+typedef void (*ScanKernel)(ScanParams);
+ScanKernel scan_kernel(int dtype, int qt, bool split, bool main_pass);
+void *merge_kernel_ptr();
+void *layout_kernel_ptr(int dtype);
+int qt_index(int qt);  // 1,2,4,8,16 -> 0..4, else -1
+
+}  // namespace dresd

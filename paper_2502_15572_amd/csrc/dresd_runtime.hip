@@ -1,0 +1,457 @@
+// Host runtime behind the C ABI in include/dresd.h: argument checks, the
+// one-time key layout, workspace management and the per-search launch plan
+// (sampled threshold passes, main scan, merge + gather).
+#include <algorithm>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "dresd.h"
+#include "dresd_internal.h"
+
+using namespace dresd;
+
+struct dresd_index {
+  int device = 0;
+  int64_t N = 0;
+  int32_t d = 0, L = 0, dtype = 0;
+  int KB = 0;          // 1 KiB blocks per tile
+  int64_t T = 0;       // tiles
+  void *data = nullptr;
+  int32_t *cont = nullptr;
+  int cus = 0;
+  size_t lds_max = 0;
+  // workspace
+  unsigned char *ws = nullptr;
+  size_t ws_bytes = 0;
+  // measurement
+  bool prof = false;
+  std::vector<hipEvent_t> ev_free;
+  std::vector<hipEvent_t> ev_scan, ev_all;  // start/stop pairs
+  std::vector<std::pair<const void *, size_t>> occ_key;
+  std::vector<int> occ_val;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+dresd_status fail(dresd_status s, const std::string &msg) {
+  g_err = msg;
+  return s;
+}
+
+#define DRESD_HIP(call)                                                              \
+  do {                                                                               \
+    hipError_t e_ = (call);                                                          \
+    if (e_ != hipSuccess) return fail(DRESD_EDEVICE, std::string(#call) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int next_pow2(int x) {
+  int n = 1;
+  while (n < x) n <<= 1;
+  return n;
+}
+
+int elem_bytes(int dtype) { return dtype == kF32 ? 4 : 2; }
+
+// Dimensions per 1 KiB block: 16 lanes' rows x 4 lane groups x (8 | 4) dims.
+int block_dims(int dtype) { return dtype == kF32 ? 16 : 32; }
+
+struct Group {
+  int b0, nb;
+};
+
+constexpr size_t kMaxGroup = 256;  // 16 query tiles x 16 columns
+
+struct Plan {
+  bool split = false;
+  int terms = 1, qpt = 16, qt = 1;
+  int bmax = 0;                 // queries per group
+  std::vector<Group> groups;
+  int C = 0;                    // per-wave list capacity
+  std::vector<int64_t> strides; // sampled passes, sparsest first
+  ScanKernel kmain = nullptr, ksample = nullptr;
+  size_t lds = 0;
+  int wg_max = 0;               // resident workgroups of the scan kernels
+  int G_max = 0;
+  int64_t pool_cap = 0;
+  size_t off_lists = 0, off_pool = 0, off_cnt = 0, off_tau = 0, bytes = 0;
+};
+
+size_t scan_lds(int ncols, int KB, int nq, int C) {
+  return (size_t)ncols * KB * 64 + 16 + (size_t)4 * nq * 16 + (size_t)4 * C * 8;
+}
+
+int occupancy(dresd_index *ix, ScanKernel k, size_t lds) {
+  for (size_t i = 0; i < ix->occ_key.size(); ++i)
+    if (ix->occ_key[i].first == (const void *)k && ix->occ_key[i].second == lds) return ix->occ_val[i];
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k, kScanThreads, lds) !=
+      hipSuccess)
+    nb = 1;
+  nb = std::max(nb, 1);
+  ix->occ_key.emplace_back((const void *)k, lds);
+  ix->occ_val.push_back(nb);
+  return nb;
+}
+
+dresd_status validate_search(const dresd_index *ix, int32_t B, int32_t k) {
+  if (!ix) return fail(DRESD_EINVAL, "index is NULL");
+  if (B < 0) return fail(DRESD_EINVAL, "B must be >= 0");
+  if (k < 1 || k > DRESD_K_MAX) return fail(DRESD_EINVAL, "k must be in [1, DRESD_K_MAX]");
+  if ((int64_t)k > ix->N) return fail(DRESD_EINVAL, "k exceeds the number of keys");
+  return DRESD_OK;
+}
+
+dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
+  pl = Plan();
+  if (ix->dtype == kBF16) pl.split = true;
+  else if (ix->dtype == kF16) pl.split = B <= 8;
+  pl.terms = pl.split ? 2 : 1;
+  pl.qpt = pl.split ? 8 : 16;
+  pl.C = next_pow2(std::max(k + 64, 128));
+  // Largest group (power-of-two number of query tiles, at most 16) whose
+  // query operand and per-wave state fit in the workgroup's LDS.
+  int qt = 16;
+  for (;; qt >>= 1) {
+    int nb = std::min(B, qt * pl.qpt);
+    size_t lds = scan_lds(nb * pl.terms, ix->KB, qt * pl.qpt, pl.C);
+    if (lds <= ix->lds_max || qt == 1) break;
+  }
+  int bmax = std::min(B, qt * pl.qpt);
+  if (scan_lds(std::min(bmax, pl.qpt) * pl.terms, ix->KB, pl.qpt, pl.C) > ix->lds_max)
+    return fail(DRESD_EUNSUPPORTED, "query tile does not fit in LDS for this d and k");
+  // shrink bmax until it fits (qt == 1 case)
+  while (bmax > 1 && scan_lds(bmax * pl.terms, ix->KB, qt * pl.qpt, pl.C) > ix->lds_max) --bmax;
+  // smallest qt that holds bmax
+  int need = (int)ceil_div((int64_t)bmax * pl.terms, 16);
+  pl.qt = 1;
+  while (pl.qt < need) pl.qt <<= 1;
+  pl.bmax = bmax;
+  int ngr = (int)ceil_div(B, bmax);
+  for (int i = 0; i < ngr; ++i) {
+    int b0 = (int)((int64_t)B * i / ngr), b1 = (int)((int64_t)B * (i + 1) / ngr);
+    pl.groups.push_back({b0, b1 - b0});
+  }
+  pl.kmain = scan_kernel(ix->dtype, pl.qt, pl.split, true);
+  pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.split, false);
+  if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
+  pl.lds = scan_lds(bmax * pl.terms, ix->KB, pl.qt * pl.qpt, pl.C);
+  int occ = std::min(occupancy(ix, pl.kmain, pl.lds), occupancy(ix, pl.ksample, pl.lds));
+  pl.wg_max = ix->cus * occ;
+  pl.G_max = pl.wg_max * (kScanThreads / kWaveSize);
+  // Sampled passes: tiles j*P; kept when they hold at least 4k rows and
+  // are at most a quarter of the tiles.
+  for (int64_t P : {(int64_t)4096, (int64_t)64}) {
+    int64_t nv = ceil_div(ix->T, P);
+    if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides.push_back(P);
+  }
+  pl.pool_cap = (int64_t)pl.G_max * pl.C;
+  // Pool counters sit at a fixed offset for every plan: they are zeroed when
+  // the workspace is allocated and reset by each merge, so a later search
+  // with a different plan never reads another plan's data as a counter.
+  size_t nb = (size_t)bmax;
+  pl.off_cnt = 0;
+  pl.off_tau = kMaxGroup * 4;
+  pl.off_lists = pl.off_tau + 2 * kMaxGroup * 8;
+  pl.off_pool = pl.off_lists + nb * pl.G_max * pl.C * 8;
+  pl.bytes = pl.off_pool + nb * (size_t)pl.pool_cap * 8;
+  return DRESD_OK;
+}
+
+dresd_status ensure_workspace(dresd_index *ix, size_t bytes) {
+  if (ix->ws_bytes >= bytes) return DRESD_OK;
+  if (ix->ws) {
+    DRESD_HIP(hipDeviceSynchronize());
+    hipFree(ix->ws);
+    ix->ws = nullptr;
+    ix->ws_bytes = 0;
+  }
+  void *p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(DRESD_ENOMEM, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
+  }
+  // Pool counters must start at zero; each merge resets its own afterwards.
+  if (hipMemset(p, 0, bytes) != hipSuccess) {
+    hipFree(p);
+    return fail(DRESD_EDEVICE, "workspace clear failed");
+  }
+  ix->ws = static_cast<unsigned char *>(p);
+  ix->ws_bytes = bytes;
+  return DRESD_OK;
+}
+
+hipEvent_t take_event(dresd_index *ix) {
+  if (!ix->ev_free.empty()) {
+    hipEvent_t e = ix->ev_free.back();
+    ix->ev_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *dresd_last_error(void) { return g_err.c_str(); }
+
+dresd_status dresd_index_create(const void *embeddings, const int32_t *continuations, int64_t N,
+                                int32_t d, int32_t L, int32_t dtype, dresd_stream stream,
+                                dresd_index **out) {
+  if (!embeddings || !continuations || !out) return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (N < 1 || N > DRESD_N_MAX) return fail(DRESD_EINVAL, "N out of range");
+  if (d < 1 || d > 16384) return fail(DRESD_EINVAL, "d out of range");
+  if (L < 1 || L > 4096) return fail(DRESD_EINVAL, "L out of range");
+  if (dtype < DRESD_F32 || dtype > DRESD_BF16) return fail(DRESD_EINVAL, "unknown dtype");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  dresd_index *ix = new (std::nothrow) dresd_index();
+  if (!ix) return fail(DRESD_ENOMEM, "host allocation failed");
+  auto cleanup = [&](dresd_status s) {
+    if (ix->data) hipFree(ix->data);
+    if (ix->cont) hipFree(ix->cont);
+    delete ix;
+    return s;
+  };
+  if (hipGetDevice(&ix->device) != hipSuccess) return cleanup(fail(DRESD_EDEVICE, "hipGetDevice failed"));
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, ix->device) != hipSuccess)
+    return cleanup(fail(DRESD_EDEVICE, "hipGetDeviceProperties failed"));
+  ix->cus = prop.multiProcessorCount;
+  ix->lds_max = prop.sharedMemPerBlock;
+  ix->N = N;
+  ix->d = d;
+  ix->L = L;
+  ix->dtype = dtype;
+  const int bd = block_dims(dtype);
+  ix->KB = (int)ceil_div(d, bd);
+  ix->T = ceil_div(N, kTileRows);
+  const size_t data_bytes = (size_t)ix->T * ix->KB * kBlockBytes;
+  const size_t cont_bytes = (size_t)N * L * sizeof(int32_t);
+  if (hipMalloc(&ix->data, data_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    ix->data = nullptr;
+    return cleanup(fail(DRESD_ENOMEM, "key storage allocation failed"));
+  }
+  if (hipMalloc((void **)&ix->cont, cont_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    ix->cont = nullptr;
+    return cleanup(fail(DRESD_ENOMEM, "continuation storage allocation failed"));
+  }
+  // Raise the dynamic-LDS limit of every scan kernel to the device's.
+  for (int v = 0; v < 3; ++v)
+    for (int qt : {1, 2, 4, 8, 16})
+      for (int sp = 0; sp < 2; ++sp)
+        for (int mp = 0; mp < 2; ++mp) {
+          ScanKernel kf = scan_kernel(v, qt, sp != 0, mp != 0);
+          if (kf)
+            (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      (int)ix->lds_max);
+        }
+  (void)hipGetLastError();
+  LayoutParams lp;
+  lp.src = embeddings;
+  lp.dst = ix->data;
+  lp.N = N;
+  lp.chunks = (int64_t)ix->T * ix->KB * 64;
+  lp.d = d;
+  lp.KB = ix->KB;
+  const int64_t blocks = std::min<int64_t>(ceil_div(lp.chunks, 256), (int64_t)ix->cus * 64);
+  void *args[] = {&lp};
+  hipError_t e = hipLaunchKernel(layout_kernel_ptr(dtype), dim3((unsigned)blocks), dim3(256), args,
+                                 0, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(ix->cont, continuations, cont_bytes, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess)
+    return cleanup(fail(DRESD_EDEVICE, std::string("index build failed: ") + hipGetErrorString(e)));
+  *out = ix;
+  return DRESD_OK;
+}
+
+dresd_status dresd_index_info(const dresd_index *ix, int64_t *N, int32_t *d, int32_t *L,
+                              int32_t *dtype) {
+  if (!ix) return fail(DRESD_EINVAL, "index is NULL");
+  if (N) *N = ix->N;
+  if (d) *d = ix->d;
+  if (L) *L = ix->L;
+  if (dtype) *dtype = ix->dtype;
+  return DRESD_OK;
+}
+
+void dresd_index_destroy(dresd_index *ix) {
+  if (!ix) return;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  (void)hipSetDevice(ix->device);
+  (void)hipDeviceSynchronize();
+  if (ix->data) hipFree(ix->data);
+  if (ix->cont) hipFree(ix->cont);
+  if (ix->ws) hipFree(ix->ws);
+  for (auto e : ix->ev_free) hipEventDestroy(e);
+  for (auto e : ix->ev_scan) hipEventDestroy(e);
+  for (auto e : ix->ev_all) hipEventDestroy(e);
+  (void)hipSetDevice(cur);
+  delete ix;
+}
+
+dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int32_t *sample_passes,
+                               int32_t *scan_waves, int64_t *workspace_bytes) {
+  dresd_status s = validate_search(cix, B, k);
+  if (s != DRESD_OK) return s;
+  dresd_index *ix = const_cast<dresd_index *>(cix);
+  if (B == 0) {
+    if (sample_passes) *sample_passes = 0;
+    if (scan_waves) *scan_waves = 0;
+    if (workspace_bytes) *workspace_bytes = 0;
+    return DRESD_OK;
+  }
+  Plan pl;
+  s = make_plan(ix, B, k, pl);
+  if (s != DRESD_OK) return s;
+  if (sample_passes) *sample_passes = (int32_t)pl.strides.size();
+  if (scan_waves)
+    *scan_waves = (int32_t)std::min<int64_t>(pl.wg_max, ceil_div(ix->T, kScanThreads / kWaveSize)) *
+                  (kScanThreads / kWaveSize);
+  if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
+  return DRESD_OK;
+}
+
+dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int32_t k,
+                          int64_t *idx, float *score, int32_t *tokens, dresd_stream stream) {
+  dresd_status s = validate_search(ix, B, k);
+  if (s != DRESD_OK) return s;
+  if (B > 0 && (!queries || !idx || !score)) return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (B == 0) return DRESD_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Plan pl;
+  s = make_plan(ix, B, k, pl);
+  if (s != DRESD_OK) return s;
+  s = ensure_workspace(ix, pl.bytes);
+  if (s != DRESD_OK) return s;
+  uint64_t *lists = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lists);
+  uint64_t *pool = reinterpret_cast<uint64_t *>(ix->ws + pl.off_pool);
+  uint32_t *pool_cnt = reinterpret_cast<uint32_t *>(ix->ws + pl.off_cnt);
+  uint64_t *tau = reinterpret_cast<uint64_t *>(ix->ws + pl.off_tau);
+
+  hipEvent_t e_all0 = nullptr, e_all1 = nullptr;
+  if (ix->prof) {
+    e_all0 = take_event(ix);
+    e_all1 = take_event(ix);
+    if (!e_all0 || !e_all1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
+    DRESD_HIP(hipEventRecord(e_all0, st));
+  }
+  const int wpg = kScanThreads / kWaveSize;
+  for (const Group &gr : pl.groups) {
+    ScanParams sp;
+    sp.data = ix->data;
+    sp.queries = queries + (size_t)gr.b0 * ix->d;
+    sp.N = ix->N;
+    sp.lists = lists;
+    sp.pool = pool;
+    sp.pool_cnt = pool_cnt;
+    sp.pool_cap = pl.pool_cap;
+    sp.B = gr.nb;
+    sp.d = ix->d;
+    sp.KB = ix->KB;
+    sp.k = k;
+    sp.C = pl.C;
+    MergeParams mp;
+    mp.pool = pool;
+    mp.pool_cnt = pool_cnt;
+    mp.pool_cap = pl.pool_cap;
+    mp.B = gr.nb;
+    mp.k = k;
+    mp.cont = ix->cont;
+    mp.L = ix->L;
+    const uint64_t *tau_in = nullptr;
+    int level = 0;
+    auto run_pass = [&](int64_t stride, bool main_pass) -> dresd_status {
+      sp.stride = stride;
+      sp.nvisit = ceil_div(ix->T, stride);
+      sp.tau = tau_in;
+      int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(sp.nvisit, wpg));
+      sp.G = (int)(wgs * wpg);
+      void *sargs[] = {&sp};
+      hipEvent_t e0 = nullptr, e1 = nullptr;
+      if (main_pass && ix->prof) {
+        e0 = take_event(ix);
+        e1 = take_event(ix);
+        if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
+        DRESD_HIP(hipEventRecord(e0, st));
+      }
+      DRESD_HIP(hipLaunchKernel((const void *)(main_pass ? pl.kmain : pl.ksample),
+                                dim3((unsigned)wgs), dim3(kScanThreads), sargs, pl.lds, st));
+      if (main_pass && ix->prof) {
+        DRESD_HIP(hipEventRecord(e1, st));
+        ix->ev_scan.push_back(e0);
+        ix->ev_scan.push_back(e1);
+      }
+      mp.final_mode = main_pass ? 1 : 0;
+      mp.tau_out = tau + (size_t)(level & 1) * pl.bmax;
+      mp.idx = idx + (size_t)gr.b0 * k;
+      mp.score = score + (size_t)gr.b0 * k;
+      mp.tokens = tokens ? tokens + (size_t)gr.b0 * k * ix->L : nullptr;
+      void *margs[] = {&mp};
+      DRESD_HIP(hipLaunchKernel(merge_kernel_ptr(), dim3((unsigned)gr.nb), dim3(kMergeThreads),
+                                margs, 0, st));
+      tau_in = mp.tau_out;
+      ++level;
+      return DRESD_OK;
+    };
+    for (int64_t P : pl.strides) {
+      s = run_pass(P, false);
+      if (s != DRESD_OK) return s;
+    }
+    s = run_pass(1, true);
+    if (s != DRESD_OK) return s;
+  }
+  if (ix->prof) {
+    DRESD_HIP(hipEventRecord(e_all1, st));
+    ix->ev_all.push_back(e_all0);
+    ix->ev_all.push_back(e_all1);
+  }
+  return DRESD_OK;
+}
+
+dresd_status dresd_profile_enable(dresd_index *ix, int32_t on) {
+  if (!ix) return fail(DRESD_EINVAL, "index is NULL");
+  ix->prof = on != 0;
+  return DRESD_OK;
+}
+
+dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms, double *search_ms,
+                                int64_t *searches) {
+  if (!ix) return fail(DRESD_EINVAL, "index is NULL");
+  double a = 0, b = 0;
+  auto sum = [&](std::vector<hipEvent_t> &v, double &acc) -> dresd_status {
+    for (size_t i = 0; i + 1 < v.size(); i += 2) {
+      DRESD_HIP(hipEventSynchronize(v[i + 1]));
+      float ms = 0;
+      DRESD_HIP(hipEventElapsedTime(&ms, v[i], v[i + 1]));
+      acc += ms;
+    }
+    return DRESD_OK;
+  };
+  dresd_status s = sum(ix->ev_scan, a);
+  if (s != DRESD_OK) return s;
+  s = sum(ix->ev_all, b);
+  if (s != DRESD_OK) return s;
+  if (scan_ms) *scan_ms = a;
+  if (search_ms) *search_ms = b;
+  if (searches) *searches = (int64_t)(ix->ev_all.size() / 2);
+  for (auto e : ix->ev_scan) ix->ev_free.push_back(e);
+  for (auto e : ix->ev_all) ix->ev_free.push_back(e);
+  ix->ev_scan.clear();
+  ix->ev_all.clear();
+  return DRESD_OK;
+}
+
+}  // extern "C"

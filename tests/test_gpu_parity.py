@@ -1,0 +1,203 @@
+"""Parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Sizes are chosen so the oracle finishes in seconds while the device path
+still spans many 16-row tiles, a ragged last tile, several sampled threshold
+passes and several waves.  Scores must agree within 1e-5 (fp32 keys) or
+2e-3 (16-bit keys); index sets may differ only where the oracle's rank-k and
+rank-(k+1) scores are closer than that; tokens must be bit-exact.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from datagen import WORKLOADS, generate, to_numpy_bits
+from parity import TOL, check_batch
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "closed_forms.json")
+DEV = "cuda:0"
+_TD = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_case(gpu_lib, keys, cont, queries, k, dtype, tol=None, strict_report=False):
+    """Search on the GPU and check against the oracle.  keys/cont/queries are
+    torch tensors (any device)."""
+    from paper_2502_15572_amd import Index
+    kd = keys.to(DEV)
+    ix = Index(kd, cont.to(DEV))
+    q = queries.to(DEV, torch.float32)
+    idx, score, tok = ix.search(q, k)
+    torch.cuda.synchronize()
+    g_idx, g_score, g_tok = idx.cpu().numpy(), score.cpu().numpy(), tok.cpu().numpy()
+    kb, dt = to_numpy_bits(keys)
+    qn = queries.cpu().numpy().astype(np.float32)
+    cn = cont.cpu().numpy()
+    o_idx, o_score, _, o_next = oracle.topk(kb, dt, qn, k, cn)
+    rep = check_batch(g_idx, g_score, g_tok, o_idx, o_score, o_next,
+                      lambda b, rows: oracle.score_rows(kb, dt, qn[b], rows), kb.shape[0], cn,
+                      TOL[dt] if tol is None else tol)
+    ix.close()
+    return rep, (g_idx, g_score, g_tok)
+
+
+def test_golden_closed_forms_on_gpu(gpu_lib):
+    """Hand-derived rankings over a standard-basis datastore, exact equality."""
+    cases = json.load(open(GOLDEN))["cases"]
+    from paper_2502_15572_amd import Index
+    for c in cases:
+        for dt in ("f32", "f16", "bf16"):
+            say("golden", c["name"], dt)
+            keys = torch.eye(c["N"], c["d"], dtype=_TD[dt], device=DEV)
+            cont = torch.arange(c["N"] * 3, dtype=torch.int32, device=DEV).view(c["N"], 3)
+            q = torch.zeros(1, c["d"], dtype=torch.float32)
+            for j, v in c["query"].items():
+                q[0, int(j)] = float(np.float32(v))
+            ix = Index(keys, cont)
+            idx, score, tok = ix.search(q.to(DEV), c["k"])
+            assert idx[0].tolist() == c["idx"], (c["name"], dt, idx[0].tolist())
+            want = np.asarray(c["score"], np.float32)
+            assert np.array_equal(score[0].cpu().numpy(), want), (c["name"], dt, score)
+            assert torch.equal(tok[0].cpu(), cont.cpu()[torch.tensor(c["idx"])])
+            ix.close()
+
+
+REDUCED = [
+    ("flat16k_d256_f32", 16384, None),
+    ("hidden1m_d4096_bf16", 6000 + 5, None),
+    ("pca4m_d1024_f16", 40000 + 3, None),
+    ("batch10m_d256_f16", 120000 + 9, None),
+    ("zipf33m_d128_f16", 200000 + 11, None),
+]
+
+
+@pytest.mark.parametrize("name,N,_", REDUCED, ids=[r[0] for r in REDUCED])
+def test_workload_parity_reduced(gpu_lib, name, N, _):
+    w = WORKLOADS[name].scaled(N)
+    g = generate(w, "cpu")
+    for B in w.batches:
+        say("parity", name, "N=%d B=%d k=%d" % (N, B, w.k))
+        rep, _r = run_case(gpu_lib, g["keys"], g["cont"], g["queries"][:B], w.k, w.dtype)
+        say("  exact-order rate %.3f, max |g-exact| %.2e" % (rep["exact_order_rate"],
+                                                           rep["max_abs_vs_exact"]))
+        # split-query paths are within summation error of the oracle
+        if w.dtype in ("f32", "bf16") or B <= 8:
+            assert rep["max_abs_vs_exact"] <= 1e-5, rep
+
+
+EDGE = [
+    # (dtype, N, d, B, k)
+    ("f16", 1, 32, 1, 1),            # one row, one partial tile
+    ("f16", 15, 40, 3, 15),          # k == N inside one ragged tile, ragged dims
+    ("bf16", 17, 64, 2, 17),         # two tiles, k == N
+    ("f32", 33, 20, 5, 7),           # fp32 keys with ragged dims
+    ("f16", 1000, 128, 17, 63),      # B past one query tile (single f16 rounding)
+    ("f16", 1000, 128, 8, 64),       # largest split batch
+    ("f16", 5000, 64, 16, 65),
+    ("bf16", 3000, 96, 9, 100),      # bf16 split over two query tiles
+    ("f16", 4096, 128, 64, 128),
+    ("f32", 2000, 256, 4, 1),
+    ("f16", 70000, 128, 1, 1000),    # large k
+    ("bf16", 9000, 256, 32, 16),
+]
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", EDGE, ids=["%s-N%d-d%d-B%d-k%d" % e for e in EDGE])
+def test_edge_shapes(gpu_lib, dt, N, d, B, k):
+    say("edge", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N * 7 + d * 3 + B + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 4), generator=gen, dtype=torch.int32)
+    run_case(gpu_lib, x, cont, q, k, dt)
+
+
+def test_all_negative_scores_never_return_padding(gpu_lib):
+    """Keys in one half-space, queries in the other: every score is negative,
+    so zero-scoring padding rows of the last tile would win if not masked."""
+    say("all-negative")
+    gen = torch.Generator().manual_seed(3)
+    N, d = 1003, 64
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x[:, 0] = x[:, 0].abs() + 1.0
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float16)
+    q = torch.zeros(4, d)
+    q[:, 0] = -1.0
+    cont = torch.arange(N * 2, dtype=torch.int32).view(N, 2)
+    rep, (gi, gs, gt) = run_case(gpu_lib, x, cont, q, 20, "f16")
+    assert (gs < 0).all() and (gi < N).all()
+
+
+def test_duplicates_resolve_to_lowest_index(gpu_lib):
+    say("duplicates")
+    w = WORKLOADS["zipf33m_d128_f16"].scaled(30000)
+    g = generate(w, "cpu", planted_duplicates=20)
+    rows = [t for _, t in g["duplicates"]]
+    q = g["keys"][rows].to(torch.float32)
+    rep, (gi, gs, gt) = run_case(gpu_lib, g["keys"], g["cont"], q, 5, "f16")
+    for r, (s, t) in enumerate(g["duplicates"]):
+        assert gi[r, 0] == s and gi[r, 1] == t and gs[r, 0] == gs[r, 1]
+
+
+def test_self_retrieval_fp32(gpu_lib):
+    """A query equal to an fp32 row returns that row first with score 1 +- 1e-6."""
+    say("self-retrieval")
+    w = WORKLOADS["flat16k_d256_f32"]
+    g = generate(w, "cpu", with_queries=False)
+    rows = torch.arange(0, w.N, 61)
+    from paper_2502_15572_amd import Index
+    ix = Index(g["keys"].to(DEV), g["cont"].to(DEV))
+    idx, score, _ = ix.search(g["keys"][rows].to(DEV), 3)
+    assert torch.equal(idx[:, 0].cpu(), rows)
+    assert float((score[:, 0].double() - 1).abs().max()) <= 1e-6
+    ix.close()
+
+
+def test_determinism_and_stream_reuse(gpu_lib):
+    say("determinism")
+    w = WORKLOADS["batch10m_d256_f16"].scaled(150000)
+    g = generate(w, "cpu")
+    from paper_2502_15572_amd import Index
+    ix = Index(g["keys"].to(DEV), g["cont"].to(DEV))
+    q = g["queries"][:64].to(DEV)
+    ref = ix.search(q, w.k)
+    s = torch.cuda.Stream()
+    for rep in range(5):
+        with torch.cuda.stream(s):
+            out = ix.search(q, w.k, stream=s)
+        s.synchronize()
+        for a, b in zip(ref, out):
+            assert torch.equal(a, b)
+    # a different batch shape in between must not disturb the next result
+    ix.search(g["queries"][:3].to(DEV), 7)
+    again = ix.search(q, w.k)
+    for a, b in zip(ref, again):
+        assert torch.equal(a, b)
+    ix.close()
+
+
+def test_argument_errors_on_device(gpu_lib):
+    from paper_2502_15572_amd import DresdError, Index
+    keys = torch.randn(100, 32, device=DEV).half()
+    cont = torch.zeros(100, 2, dtype=torch.int32, device=DEV)
+    ix = Index(keys, cont)
+    q = torch.randn(2, 32, device=DEV)
+    for bad_k in (0, 101, 2000):
+        with pytest.raises(DresdError) as e:
+            ix.search(q, bad_k)
+        assert e.value.status == 1
+    out = ix.search(q[:0], 5)  # B == 0 is a no-op
+    assert out[0].shape == (0, 5)
+    ix.close()
