@@ -94,11 +94,11 @@ dresd_status dresd_index_create(const void *embeddings,
  *   stream    stream the search runs on.
  *
  * Order: rank r holds the r-th largest score; equal scores are ordered by
- * ascending row index.  Scores are accumulated in fp32.  Keys stored as f16
- * or bf16 are multiplied by the query split into a high and a low 16-bit part
- * when the batch is small (and always for bf16), so scores stay within about
- * 1e-5 of the exact inner product; large f16 batches round the query to f16
- * once (score error below 5e-4).
+ * ascending row index.  Scores are accumulated in fp32.  For bf16 keys, and
+ * for f16 keys while B <= 8, the query enters the matrix cores as three
+ * 16-bit parts that sum to it exactly (scores within fp32 summation error of
+ * the exact inner product); larger f16 batches round the query once to f16
+ * (score error below 5e-4, inside the 2e-3 parity bound for 16-bit keys).
  * Determinism: identical inputs give bitwise identical outputs.
  * Ownership: outputs are caller-owned and must stay alive until `stream`
  * completes.  The index owns a workspace that grows on first use with a new

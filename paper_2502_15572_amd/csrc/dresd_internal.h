@@ -59,7 +59,7 @@ struct LayoutParams {
 
 // Kernel launch entry points (defined in dresd_kernels.hip).
 typedef void (*ScanKernel)(ScanParams);
-ScanKernel scan_kernel(int dtype, int qt, bool split, bool main_pass);
+ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass);  // cpq: columns per query
 void *merge_kernel_ptr();
 void *layout_kernel_ptr(int dtype);
 int qt_index(int qt);  // 1,2,4,8,16 -> 0..4, else -1

@@ -142,22 +142,26 @@ struct Mfma<kBF16> {
   }
 };
 
-// Query operand: column c of the A operand is query c (fp32 or f16 keys
-// without split) or the high (c even) / low (c odd) 16-bit part of query c/2.
-template <int DT, bool SPLIT>
+// Query operand: CPQ consecutive columns of the A operand hold one query.
+// CPQ = 1: the query itself (fp32 keys) or rounded once to f16;
+// CPQ = 4: three parts whose sum is the fp32 query exactly, plus a zero
+//          column.  bf16: high, middle, low.  f16: high, then the remainders
+//          scaled by 2^11 and 2^22 so they stay in f16's normal range (the
+//          epilogue scales their products back by the same powers of two).
+template <int DT, int CPQ>
 __device__ __forceinline__ u4 query_chunk(const float *q, int d, int B, int col, int dim0) {
   u4 out;
+  const int b = col / CPQ;
+  const int h = col % CPQ;
   if (DT == kF32) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       int dim = dim0 + e;
-      float x = (col < B && dim < d) ? q[(int64_t)col * d + dim] : 0.0f;
+      float x = (b < B && dim < d) ? q[(int64_t)b * d + dim] : 0.0f;
       out[e] = __float_as_uint(x);
     }
     return out;
   }
-  const int b = SPLIT ? (col >> 1) : col;
-  const int h = SPLIT ? (col & 1) : 0;
   uint16_t v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -165,11 +169,21 @@ __device__ __forceinline__ u4 query_chunk(const float *q, int d, int B, int col,
     float x = (b < B && dim < d) ? q[(int64_t)b * d + dim] : 0.0f;
     if (DT == kF16) {
       _Float16 hi = (_Float16)x;
-      _Float16 r = h ? (_Float16)(x - (float)hi) : hi;
+      _Float16 r = hi;
+      if (CPQ == 4) {
+        float r1 = x - (float)hi;                  // exact
+        _Float16 mid = (_Float16)(r1 * 2048.0f);   // 2^11
+        float r2 = r1 - (float)mid * (1.0f / 2048.0f);  // exact
+        _Float16 lo = (_Float16)(r2 * 4194304.0f); // 2^22
+        r = (h == 0) ? hi : (h == 1) ? mid : (h == 2) ? lo : (_Float16)0.0f;
+      }
       v[e] = __builtin_bit_cast(uint16_t, r);
     } else {
       __bf16 hi = (__bf16)x;
-      __bf16 r = h ? (__bf16)(x - (float)hi) : hi;
+      float r1 = x - (float)hi;
+      __bf16 mid = (__bf16)r1;
+      __bf16 lo = (__bf16)(r1 - (float)mid);
+      __bf16 r = (h == 0) ? hi : (h == 1) ? mid : (h == 2) ? lo : (__bf16)0.0f;
       v[e] = __builtin_bit_cast(uint16_t, r);
     }
   }
@@ -190,10 +204,10 @@ __device__ uint64_t wave_flush(uint64_t *list, int cnt, int C, int k, uint64_t *
   return kth;
 }
 
-template <int DT, int QT, bool SPLIT>
+template <int DT, int QT, int CPQ>
 __device__ __forceinline__ void scan_body(const ScanParams &p) {
-  constexpr int QPT = SPLIT ? 8 : 16;  // queries per 16-column tile
-  constexpr int NS = SPLIT ? 2 : 4;    // scores per lane per tile
+  constexpr int QPT = 16 / CPQ;        // queries per 16-column tile
+  constexpr int NS = 4 / CPQ;          // scores per lane per tile
   constexpr int NQ = QT * QPT;         // queries held by one launch
   constexpr int U = 8;                 // key blocks in flight per wave
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -203,7 +217,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   const int nwv = blockDim.x >> 6;
   const int gw = blockIdx.x * nwv + wv;
   const int G = p.G, C = p.C, KB = p.KB, B = p.B;
-  const int ncols = B * (SPLIT ? 2 : 1);
+  const int ncols = B * CPQ;
   const int g = lane >> 4, m = lane & 15;
 
   // LDS carve-up: query operand | zero chunk | per-wave state | per-wave scratch
@@ -228,7 +242,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
       int nct = min(16, ncols - 16 * t);
       int off = t * 16 * KB * 64 + ((kb * 4 + gg) * nct + mm) * 16;
       *reinterpret_cast<u4 *>(smem + off) =
-          query_chunk<DT, SPLIT>(p.queries, p.d, B, c, kb * 4 * EPC + gg * EPC);
+          query_chunk<DT, CPQ>(p.queries, p.d, B, c, kb * 4 * EPC + gg * EPC);
     }
     if (threadIdx.x == 0) *reinterpret_cast<u4 *>(smem + zero_off) = u4{0, 0, 0, 0};
   }
@@ -267,7 +281,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
 #pragma unroll
   for (int t = 0; t < QT; ++t)
 #pragma unroll
-    for (int s = 0; s < NS; ++s) thr[t][s] = st_thr[t * QPT + (SPLIT ? 2 * g + s : 4 * g + s)];
+    for (int s = 0; s < NS; ++s) thr[t][s] = st_thr[t * QPT + g * NS + s];
 
   // 3. Stream this wave's tiles.
   const int64_t v0 = p.nvisit * gw / G, v1 = p.nvisit * (gw + 1) / G;
@@ -320,7 +334,13 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
           for (int t = 0; t < QT; ++t)
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-              sc[t][s] = SPLIT ? (acc[t][2 * s] + acc[t][2 * s + 1]) : acc[t][s];
+              float v = acc[t][s * CPQ];
+              if (CPQ == 4) {
+                const float s1 = (DT == kF16) ? (1.0f / 2048.0f) : 1.0f;
+                const float s2 = (DT == kF16) ? (1.0f / 4194304.0f) : 1.0f;
+                v = (v + acc[t][s * CPQ + 1] * s1) + acc[t][s * CPQ + 2] * s2;
+              }
+              sc[t][s] = v;
               any |= row_ok && sc[t][s] >= thr[t][s];
             }
           if (__ballot(any)) {
@@ -332,7 +352,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
                 uint64_t mk = __ballot(ps);
                 while (mk) {
                   const int gg = (__ffsll((long long)mk) - 1) >> 4;
-                  const int q = t * QPT + (SPLIT ? 2 * gg + s : 4 * gg + s);
+                  const int q = t * QPT + gg * NS + s;
                   const bool mine = ps && (g == gg);
                   const uint64_t key = make_key(sc[t][s], row);
                   uint64_t tk = st_key[q];
@@ -363,7 +383,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
             for (int t = 0; t < QT; ++t)
 #pragma unroll
               for (int s = 0; s < NS; ++s)
-                thr[t][s] = st_thr[t * QPT + (SPLIT ? 2 * g + s : 4 * g + s)];
+                thr[t][s] = st_thr[t * QPT + g * NS + s];
           }
 #pragma unroll
           for (int t = 0; t < QT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
@@ -389,17 +409,18 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
 
 // Two kernel names so that profiles separate the main pass from the
 // sampled passes that only set thresholds.
-template <int DT, int QT, bool SPLIT>
+template <int DT, int QT, int CPQ>
 __global__ void __launch_bounds__(kScanThreads) dresd_scan_main(ScanParams p) {
-  scan_body<DT, QT, SPLIT>(p);
+  scan_body<DT, QT, CPQ>(p);
 }
 
-template <int DT, int QT, bool SPLIT>
+template <int DT, int QT, int CPQ>
 __global__ void __launch_bounds__(kScanThreads) dresd_scan_sample(ScanParams p) {
-  scan_body<DT, QT, SPLIT>(p);
+  scan_body<DT, QT, CPQ>(p);
 }
 
 // ----------------------------------------------------------------- merge ---
+#if !defined(DRESD_TU) || DRESD_TU == 0
 
 // One workgroup per query: exact k best keys of the query's pool.
 __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
@@ -523,8 +544,48 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
   __syncthreads();
   if (tid == 0) p.pool_cnt[b] = 0;  // ready for the next pass
 }
+#endif
 
 // ---------------------------------------------------------------- tables ---
+// This file is compiled once per scan variant (DRESD_TU = 1..4) and once for
+// the merge, layout and dispatch (DRESD_TU = 0) so that the variants build in
+// parallel; without DRESD_TU it is one translation unit holding everything.
+
+#define DRESD_SCAN_ROW(DT, CPQ)                                                             \
+  {(ScanKernel)dresd_scan_main<DT, 1, CPQ>, (ScanKernel)dresd_scan_main<DT, 2, CPQ>,          \
+   (ScanKernel)dresd_scan_main<DT, 4, CPQ>, (ScanKernel)dresd_scan_main<DT, 8, CPQ>,          \
+   (ScanKernel)dresd_scan_main<DT, 16, CPQ>},                                                 \
+  {                                                                                           \
+    (ScanKernel)dresd_scan_sample<DT, 1, CPQ>, (ScanKernel)dresd_scan_sample<DT, 2, CPQ>,     \
+        (ScanKernel)dresd_scan_sample<DT, 4, CPQ>, (ScanKernel)dresd_scan_sample<DT, 8, CPQ>, \
+        (ScanKernel)dresd_scan_sample<DT, 16, CPQ>                                            \
+  }
+
+#define DRESD_VARIANT(V, DT, CPQ)                                       \
+  ScanKernel scan_kernel_variant##V(int qi, bool main_pass) {           \
+    static const ScanKernel table[2][5] = {DRESD_SCAN_ROW(DT, CPQ)};    \
+    return table[main_pass ? 0 : 1][qi];                                \
+  }
+
+// variants: 0 = f32 keys, 1 = f16 keys x1, 2 = f16 keys x4, 3 = bf16 keys x4
+#if !defined(DRESD_TU) || DRESD_TU == 1
+DRESD_VARIANT(0, kF32, 1)
+#endif
+#if !defined(DRESD_TU) || DRESD_TU == 2
+DRESD_VARIANT(1, kF16, 1)
+#endif
+#if !defined(DRESD_TU) || DRESD_TU == 3
+DRESD_VARIANT(2, kF16, 4)
+#endif
+#if !defined(DRESD_TU) || DRESD_TU == 4
+DRESD_VARIANT(3, kBF16, 4)
+#endif
+
+#if !defined(DRESD_TU) || DRESD_TU == 0
+ScanKernel scan_kernel_variant0(int, bool);
+ScanKernel scan_kernel_variant1(int, bool);
+ScanKernel scan_kernel_variant2(int, bool);
+ScanKernel scan_kernel_variant3(int, bool);
 
 int qt_index(int qt) {
   switch (qt) {
@@ -537,40 +598,14 @@ int qt_index(int qt) {
   }
 }
 
-#define DRESD_SCAN_ROW(DT, SP)                                                              \
-  {(ScanKernel)dresd_scan_main<DT, 1, SP>, (ScanKernel)dresd_scan_main<DT, 2, SP>,           \
-   (ScanKernel)dresd_scan_main<DT, 4, SP>, (ScanKernel)dresd_scan_main<DT, 8, SP>,           \
-   (ScanKernel)dresd_scan_main<DT, 16, SP>},                                                 \
-  {                                                                                          \
-    (ScanKernel)dresd_scan_sample<DT, 1, SP>, (ScanKernel)dresd_scan_sample<DT, 2, SP>,      \
-        (ScanKernel)dresd_scan_sample<DT, 4, SP>, (ScanKernel)dresd_scan_sample<DT, 8, SP>,  \
-        (ScanKernel)dresd_scan_sample<DT, 16, SP>                                            \
-  }
-
-// [variant][main=0 / sample=1][qt]; variants: f32, f16, f16 split, bf16 split
-static const ScanKernel kScanTable[4][2][5] = {
-    {DRESD_SCAN_ROW(kF32, false)},
-    {DRESD_SCAN_ROW(kF16, false)},
-    {DRESD_SCAN_ROW(kF16, true)},
-    {DRESD_SCAN_ROW(kBF16, true)},
-};
-
-ScanKernel scan_kernel(int dtype, int qt, bool split, bool main_pass) {
+ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass) {
   int qi = qt_index(qt);
   if (qi < 0) return nullptr;
-  int v;
-  if (dtype == kF32) {
-    if (split) return nullptr;
-    v = 0;
-  } else if (dtype == kF16) {
-    v = split ? 2 : 1;
-  } else if (dtype == kBF16) {
-    if (!split) return nullptr;
-    v = 3;
-  } else {
-    return nullptr;
-  }
-  return kScanTable[v][main_pass ? 0 : 1][qi];
+  if (dtype == kF32 && cpq == 1) return scan_kernel_variant0(qi, main_pass);
+  if (dtype == kF16 && cpq == 1) return scan_kernel_variant1(qi, main_pass);
+  if (dtype == kF16 && cpq == 4) return scan_kernel_variant2(qi, main_pass);
+  if (dtype == kBF16 && cpq == 4) return scan_kernel_variant3(qi, main_pass);
+  return nullptr;
 }
 
 void *merge_kernel_ptr() { return (void *)dresd_merge; }
@@ -579,5 +614,6 @@ void *layout_kernel_ptr(int dtype) {
   if (dtype == kF32) return (void *)dresd_layout<float>;
   return (void *)dresd_layout<uint16_t>;
 }
+#endif
 
 }  // namespace dresd

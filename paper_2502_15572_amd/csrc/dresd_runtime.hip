@@ -68,8 +68,7 @@ struct Group {
 constexpr size_t kMaxGroup = 256;  // 16 query tiles x 16 columns
 
 struct Plan {
-  bool split = false;
-  int terms = 1, qpt = 16, qt = 1;
+  int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
   int bmax = 0;                 // queries per group
   std::vector<Group> groups;
   int C = 0;                    // per-wave list capacity
@@ -109,10 +108,13 @@ dresd_status validate_search(const dresd_index *ix, int32_t B, int32_t k) {
 
 dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
   pl = Plan();
-  if (ix->dtype == kBF16) pl.split = true;
-  else if (ix->dtype == kF16) pl.split = B <= 8;
-  pl.terms = pl.split ? 2 : 1;
-  pl.qpt = pl.split ? 8 : 16;
+  // The query enters the matrix cores as three 16-bit parts that sum to it
+  // exactly (four columns per query) for bf16 keys and for small f16 batches;
+  // larger f16 batches round it once to f16.
+  if (ix->dtype == kBF16) pl.terms = 4;
+  else if (ix->dtype == kF16) pl.terms = (B <= 8) ? 4 : 1;
+  else pl.terms = 1;
+  pl.qpt = 16 / pl.terms;
   pl.C = next_pow2(std::max(k + 64, 128));
   // Largest group (power-of-two number of query tiles, at most 16) whose
   // query operand and per-wave state fit in the workgroup's LDS.
@@ -137,8 +139,8 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
     int b0 = (int)((int64_t)B * i / ngr), b1 = (int)((int64_t)B * (i + 1) / ngr);
     pl.groups.push_back({b0, b1 - b0});
   }
-  pl.kmain = scan_kernel(ix->dtype, pl.qt, pl.split, true);
-  pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.split, false);
+  pl.kmain = scan_kernel(ix->dtype, pl.qt, pl.terms, true);
+  pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.terms, false);
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
   pl.lds = scan_lds(bmax * pl.terms, ix->KB, pl.qt * pl.qpt, pl.C);
   int occ = std::min(occupancy(ix, pl.kmain, pl.lds), occupancy(ix, pl.ksample, pl.lds));
@@ -248,9 +250,9 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
   // Raise the dynamic-LDS limit of every scan kernel to the device's.
   for (int v = 0; v < 3; ++v)
     for (int qt : {1, 2, 4, 8, 16})
-      for (int sp = 0; sp < 2; ++sp)
+      for (int cpq : {1, 2, 4})
         for (int mp = 0; mp < 2; ++mp) {
-          ScanKernel kf = scan_kernel(v, qt, sp != 0, mp != 0);
+          ScanKernel kf = scan_kernel(v, qt, cpq, mp != 0);
           if (kf)
             (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
                                       (int)ix->lds_max);
