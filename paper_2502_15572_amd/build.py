@@ -1,7 +1,7 @@
 """Build the HIP retrieval library (gfx950) in-tree: libdresd.so.
 
-The kernel file is compiled as five translation units in parallel (one per
-scan variant, one for merge/layout/dispatch), then linked with the runtime.
+The scan file is compiled as five translation units in parallel (one per
+scan variant, one for layout/dispatch), beside the merge and the runtime.
 Usage: python -m paper_2502_15572_amd.build [-v]
 """
 from __future__ import annotations
@@ -29,7 +29,7 @@ HIPCC_FLAGS = [
 
 # (source, extra defines, object name)
 UNITS = [("dresd_kernels.hip", ["-DDRESD_TU=%d" % t], "kernels%d" % t) for t in range(5)] + [
-    ("dresd_runtime.hip", [], "runtime")]
+    ("dresd_merge.hip", [], "merge"), ("dresd_runtime.hip", [], "runtime")]
 
 
 def _compile(hipcc, src, defs, obj, verbose):

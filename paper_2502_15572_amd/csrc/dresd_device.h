@@ -1,0 +1,82 @@
+// Device helpers shared by the gfx950 scan and merge kernels.
+//
+// Ranking keys are 64-bit: high half = order-preserving bits of the fp32
+// score, low half = ~row.  Larger key = better; equal scores rank the lower
+// row first.  Keys are unique, so every selection over them is deterministic.
+#pragma once
+#include "dresd_internal.h"
+
+namespace dresd {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef __bf16 b8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t order_bits(float f) {
+  uint32_t u = (f == 0.0f) ? 0u : __float_as_uint(f);  // -0 ranks as +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float order_value(uint32_t h) {
+  uint32_t u = (h & 0x80000000u) ? (h & 0x7fffffffu) : ~h;
+  return __uint_as_float(u);
+}
+
+__device__ __forceinline__ uint64_t make_key(float s, uint32_t row) {
+  return ((uint64_t)order_bits(s) << 32) | (uint64_t)(uint32_t)(~row);
+}
+
+// The value of lane 0, so the compiler keeps it in scalar registers.
+__device__ __forceinline__ int64_t wave_uniform(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ void wave_sync_lds() {
+  // Orders this wave's LDS accesses across lanes (DS ops of one wave run in
+  // order; this keeps the compiler from moving them across the point).
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Sort n (power of two, >= 2) keys in LDS, descending, by one wave.
+__device__ inline void wave_bitonic_desc(uint64_t *s, int n, int lane) {
+  for (int size = 2; size <= n; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int p = lane; p < (n >> 1); p += kWaveSize) {
+        int lo = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
+        int hi = lo + stride;
+        uint64_t a = s[lo], b = s[hi];
+        bool desc = (lo & size) == 0;
+        if ((a < b) == desc) {
+          s[lo] = b;
+          s[hi] = a;
+        }
+      }
+      wave_sync_lds();
+    }
+  }
+}
+
+// Same, by a whole workgroup.
+__device__ inline void block_bitonic_desc(uint64_t *s, int n) {
+  for (int size = 2; size <= n; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int p = threadIdx.x; p < (n >> 1); p += blockDim.x) {
+        int lo = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
+        int hi = lo + stride;
+        uint64_t a = s[lo], b = s[hi];
+        bool desc = (lo & size) == 0;
+        if ((a < b) == desc) {
+          s[lo] = b;
+          s[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+}  // namespace dresd

@@ -15,7 +15,7 @@ constexpr int kTileRows = 16;
 constexpr int kBlockBytes = 1024;
 constexpr int kWaveSize = 64;
 constexpr int kScanThreads = 256;   // 4 waves per workgroup
-constexpr int kMergeThreads = 256;
+constexpr int kMergeThreads = 1024;
 constexpr int kMergeCap = 4096;     // candidates a merge keeps in LDS
 #define DRESD_K_MAX_INTERNAL 1024   // equals DRESD_K_MAX of the public header
 
@@ -29,17 +29,24 @@ struct ScanParams {
   int64_t stride;            // tile stride of the pass (1 = every tile)
   const uint64_t *tau;       // [B] keys below tau are pruned (0 = none); may be null
   uint64_t *lists;           // [B][G][C] per-wave candidate lists
-  uint64_t *pool;            // [B][pool_cap] per-query candidate pools
-  uint32_t *pool_cnt;        // [B]
-  int64_t pool_cap;
+  uint32_t *lcnt;            // [B][G] list lengths; bit 31 set = sorted descending
+  uint64_t *lkth;            // [B][G] k-th best key of a sorted list of k keys, else 0
+  uint64_t *lfirst;          // [B][G] best key of a sorted list; ~0 unknown; 0 empty
   int B, d, KB, k, C, G;     // batch, dims, blocks per tile, k, list capacity, waves
+  int sort_lists;            // sort every list at the end (small batches)
 };
 
+// A list summary flag: the list is sorted, best key first.
+constexpr uint32_t kSortedFlag = 0x80000000u;
+
 struct MergeParams {
-  const uint64_t *pool;      // [B][pool_cap]
-  uint32_t *pool_cnt;        // [B]; reset to 0 by the merge
-  int64_t pool_cap;
-  int B, k;
+  const uint64_t *lists;     // [B][G][C] from the scan
+  const uint32_t *lcnt;      // [B][G]
+  const uint64_t *lkth;      // [B][G]
+  const uint64_t *lfirst;    // [B][G]
+  uint64_t *spill;           // [B][spill_cap] candidates past the LDS cache
+  int64_t spill_cap;
+  int B, k, C, G;
   uint64_t *tau_out;         // sample mode: k-th best key per query (0 if < k)
   int64_t *idx;              // final mode outputs
   float *score;

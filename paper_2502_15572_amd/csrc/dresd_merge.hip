@@ -1,0 +1,229 @@
+// gfx950 merge + gather kernel: one workgroup per query turns the scan's
+// per-wave candidate lists into the exact k best keys of that query
+// (DReSD Section 3.5, Eq. 3 taken as top-k for batch verification,
+// Section 3.6), then gathers the winners' continuations -- the value map of
+// the key -> next-tokens datastore.  For a sampled pass it instead emits the
+// k-th best key, a lower bound that prunes the next pass.
+#include "dresd_device.h"
+
+namespace dresd {
+
+// Candidate counts up to this are sorted whole by one wave.
+constexpr int kSmallMerge = 256;
+
+struct MergeShared {
+  uint32_t hist[4096];
+  uint32_t part[kMergeThreads / kWaveSize];
+  uint64_t cache[kMergeCap];
+  uint64_t win[DRESD_K_MAX_INTERNAL];
+  uint64_t sel_prefix, sel_mask, bound;
+  uint32_t sel_krem, sel_done, win_cnt, ncand;
+};
+
+// Largest value v such that at least kk of the M values src(i) are >= v
+// (the kk-th largest value; 1 <= kk <= M), by radix selection 12 bits at a
+// time from the top.  Called by the whole workgroup.
+template <class Src>
+__device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk) {
+  constexpr int BPT = 4096 / kMergeThreads;  // histogram bins per thread
+  const int tid = threadIdx.x, nth = blockDim.x;
+  const int lane = tid & (kWaveSize - 1), wid = tid / kWaveSize;
+  if (tid == 0) {
+    sh.sel_prefix = 0;
+    sh.sel_mask = 0;
+    sh.sel_krem = kk;
+    sh.sel_done = 0;
+  }
+  __syncthreads();
+  const int shifts[6] = {52, 40, 28, 16, 4, 0};
+  for (int di = 0; di < 6 && !sh.sel_done; ++di) {
+    const int s = shifts[di];
+    const uint32_t wmask = (di == 5) ? 0xFu : 0xFFFu;
+    for (int i = tid; i < 4096; i += nth) sh.hist[i] = 0;
+    __syncthreads();
+    const uint64_t pre = sh.sel_prefix, pm = sh.sel_mask;
+    for (uint32_t i = tid; i < M; i += nth) {
+      const uint64_t key = src(i);
+      if ((key & pm) == pre) atomicAdd(&sh.hist[(uint32_t)(key >> s) & wmask], 1u);
+    }
+    __syncthreads();
+    // Suffix sums: thread t owns bins [BPT t, BPT t + BPT); `above` = count in
+    // the bins of all higher threads (lanes scan within the wave, then the
+    // waves' totals are summed from LDS).
+    uint32_t mine = 0;
+    for (int jb = 0; jb < BPT; ++jb) mine += sh.hist[tid * BPT + jb];
+    uint32_t incl = mine;
+    for (int off = 1; off < kWaveSize; off <<= 1) {
+      const uint32_t v = __shfl_down(incl, off, kWaveSize);
+      if (lane + off < kWaveSize) incl += v;
+    }
+    if (lane == 0) sh.part[wid] = incl;
+    __syncthreads();
+    uint32_t later = 0;
+    for (int w = wid + 1; w < nth / kWaveSize; ++w) later += sh.part[w];
+    const uint32_t krem = sh.sel_krem;
+    const uint32_t above = later + incl - mine;
+    __syncthreads();
+    if (above < krem && krem <= above + mine) {
+      uint32_t cum = above;
+      for (int jb = BPT - 1; jb >= 0; --jb) {
+        const uint32_t h = sh.hist[tid * BPT + jb];
+        if (cum + h >= krem) {
+          const uint32_t dg = (uint32_t)(tid * BPT + jb);
+          sh.sel_prefix = pre | ((uint64_t)dg << s);
+          sh.sel_mask = pm | ((uint64_t)wmask << s);
+          sh.sel_krem = krem - cum;
+          if (h == krem - cum) sh.sel_done = 1u;  // the whole bin is in
+          break;
+        }
+        cum += h;
+      }
+    }
+    __syncthreads();
+  }
+  return sh.sel_prefix;
+}
+
+// Output of one query from its sorted winners win[0..kk): the k-th best key
+// (sampled pass) or indices, scores and gathered continuations (final pass).
+__device__ inline void write_result(const MergeParams &p, int b, const uint64_t *win,
+                                    uint32_t kk, int tid, int nth) {
+  if (!p.final_mode) {
+    if (tid == 0) p.tau_out[b] = (kk >= (uint32_t)p.k) ? win[p.k - 1] : 0ull;
+    return;
+  }
+  for (int r = tid; r < p.k; r += nth) {
+    const size_t o = (size_t)b * p.k + r;
+    if (r < (int)kk) {
+      const uint64_t key = win[r];
+      p.idx[o] = (int64_t)(uint32_t)(~(uint32_t)key);
+      p.score[o] = order_value((uint32_t)(key >> 32));
+    } else {  // cannot happen when N >= k; filled defensively
+      p.idx[o] = -1;
+      p.score[o] = -__builtin_inff();
+    }
+  }
+  if (p.tokens) {
+    const int L = p.L;
+    for (int i = tid; i < p.k * L; i += nth) {
+      const int r = i / L, l = i - r * L;
+      int32_t v = 0;
+      if (r < (int)kk) {
+        const uint32_t row = ~(uint32_t)win[r];
+        v = p.cont[(size_t)row * L + l];
+      }
+      p.tokens[((size_t)b * p.k + r) * L + l] = v;
+    }
+  }
+}
+
+// 1. A lower bound on the query's k-th best key: the larger of (a) the best
+//    k-th key published by any list holding k sorted keys and (b) the k-th
+//    largest of the lists' known best keys -- k distinct listed keys reach
+//    each, and the answer is among the listed keys.
+// 2. Candidates: listed keys at or above the bound; lists whose best key is
+//    below it are not opened, sorted lists stop at their first key under it.
+// 3. The k best candidates: one wave sorts them when few, else a radix
+//    select finds the k-th and the keys at or above it are sorted.
+__global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
+  __shared__ MergeShared sh;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int nth = blockDim.x;
+  const int G = p.G;
+  const uint32_t *lcnt = p.lcnt + (size_t)b * G;
+  const uint64_t *lkth = p.lkth + (size_t)b * G;
+  const uint64_t *lfirst = p.lfirst + (size_t)b * G;
+  const uint64_t *lists = p.lists + (size_t)b * G * p.C;
+  uint64_t *spill = p.spill + (size_t)b * p.spill_cap;
+  if (tid == 0) {
+    sh.bound = 0;
+    sh.ncand = 0;
+    sh.win_cnt = 0;
+  }
+  // (a) and the known best keys (0 for empty lists and unknown ones)
+  uint64_t mb = 0;
+  const bool first_in_lds = G <= kMergeCap;
+  for (int w = tid; w < G; w += nth) {
+    const uint64_t v = lkth[w];
+    mb = v > mb ? v : mb;
+    if (first_in_lds) {
+      const uint64_t f = lfirst[w];
+      sh.cache[w] = (f == ~0ull) ? 0ull : f;
+    }
+  }
+  __syncthreads();
+  if (mb) atomicMax((unsigned long long *)&sh.bound, (unsigned long long)mb);
+  // (b)
+  if (G >= p.k) {
+    uint64_t t1;
+    if (first_in_lds) {
+      t1 = radix_kth(sh, [&](uint32_t i) { return sh.cache[i]; }, (uint32_t)G, (uint32_t)p.k);
+    } else {
+      t1 = radix_kth(
+          sh, [&](uint32_t i) { const uint64_t f = lfirst[i]; return f == ~0ull ? 0ull : f; },
+          (uint32_t)G, (uint32_t)p.k);
+    }
+    if (tid == 0 && t1 > sh.bound) sh.bound = t1;
+  }
+  __syncthreads();
+  const uint64_t bnd = sh.bound;
+
+  // 2. gather the candidates
+  for (int w = tid; w < G; w += nth) {
+    if (lfirst[w] < bnd) continue;
+    uint32_t c = lcnt[w];
+    const bool sorted = (c & kSortedFlag) != 0;
+    c &= ~kSortedFlag;
+    const uint64_t *l = lists + (size_t)w * p.C;
+    for (uint32_t e = 0; e < c; ++e) {
+      const uint64_t key = l[e];
+      if (key >= bnd) {
+        const uint32_t at = atomicAdd(&sh.ncand, 1u);
+        if (at < (uint32_t)kMergeCap) sh.cache[at] = key;
+        else if ((int64_t)(at - kMergeCap) < p.spill_cap) spill[at - kMergeCap] = key;
+      } else if (sorted) {
+        break;
+      }
+    }
+  }
+  __threadfence_block();
+  __syncthreads();
+  const uint32_t M = sh.ncand;
+  const uint32_t kk = M < (uint32_t)p.k ? M : (uint32_t)p.k;
+
+  // 3. the k best
+  if (M <= (uint32_t)kSmallMerge) {
+    if (tid < kWaveSize) {
+      int n = 2;
+      while (n < (int)M) n <<= 1;
+      for (int i = (int)M + tid; i < n; i += kWaveSize) sh.cache[i] = 0ull;
+      wave_sync_lds();
+      wave_bitonic_desc(sh.cache, n, tid);
+      write_result(p, b, sh.cache, kk, tid, kWaveSize);
+    }
+    return;
+  }
+  auto cand = [&](uint32_t i) {
+    return i < (uint32_t)kMergeCap ? sh.cache[i] : spill[i - kMergeCap];
+  };
+  const uint64_t cut = (kk == M) ? 0ull : radix_kth(sh, cand, M, kk);
+  for (uint32_t i = tid; i < M; i += nth) {
+    const uint64_t key = cand(i);
+    if (key >= cut) {
+      const uint32_t at = atomicAdd(&sh.win_cnt, 1u);
+      if (at < (uint32_t)DRESD_K_MAX_INTERNAL) sh.win[at] = key;
+    }
+  }
+  __syncthreads();
+  int n = 1;
+  while (n < (int)kk) n <<= 1;
+  for (int i = (int)kk + tid; i < n; i += nth) sh.win[i] = 0ull;
+  __syncthreads();
+  if (n >= 2) block_bitonic_desc(sh.win, n);
+  write_result(p, b, sh.win, kk, tid, nth);
+}
+
+void *merge_kernel_ptr() { return (void *)dresd_merge; }
+
+}  // namespace dresd

@@ -66,6 +66,7 @@ struct Group {
 };
 
 constexpr size_t kMaxGroup = 256;  // 16 query tiles x 16 columns
+constexpr int kMaxScanWgPerCu = 4;
 
 struct Plan {
   int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
@@ -77,8 +78,10 @@ struct Plan {
   size_t lds = 0;
   int wg_max = 0;               // resident workgroups of the scan kernels
   int G_max = 0;
-  int64_t pool_cap = 0;
-  size_t off_lists = 0, off_pool = 0, off_cnt = 0, off_tau = 0, bytes = 0;
+  int64_t spill_cap = 0;        // merge candidates per query beyond its LDS cache
+  bool sort_lists = false;
+  size_t off_tau = 0, off_lcnt = 0, off_lkth = 0, off_lfirst = 0, off_lists = 0, off_spill = 0;
+  size_t bytes = 0;
 };
 
 size_t scan_lds(int ncols, int KB, int nq, int C) {
@@ -144,24 +147,34 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
   pl.lds = scan_lds(bmax * pl.terms, ix->KB, pl.qt * pl.qpt, pl.C);
   int occ = std::min(occupancy(ix, pl.kmain, pl.lds), occupancy(ix, pl.ksample, pl.lds));
-  pl.wg_max = ix->cus * occ;
+  // At most 4 workgroups (16 waves) per CU: enough loads in flight to keep
+  // HBM busy, and few enough per-wave lists for the merge to keep their
+  // best keys in LDS.
+  pl.wg_max = ix->cus * std::min(occ, kMaxScanWgPerCu);
   pl.G_max = pl.wg_max * (kScanThreads / kWaveSize);
-  // Sampled passes: tiles j*P; kept when they hold at least 4k rows and
-  // are at most a quarter of the tiles.
-  for (int64_t P : {(int64_t)4096, (int64_t)64}) {
-    int64_t nv = ceil_div(ix->T, P);
-    if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides.push_back(P);
-  }
-  pl.pool_cap = (int64_t)pl.G_max * pl.C;
-  // Pool counters sit at a fixed offset for every plan: they are zeroed when
-  // the workspace is allocated and reset by each merge, so a later search
-  // with a different plan never reads another plan's data as a counter.
+  // Small batches: every wave keeps its own running top-k and sorts it at
+  // the end; the merge then prunes with the best per-wave k-th key.  Larger
+  // batches first set per-query thresholds from sampled passes over tiles
+  // j*P (kept when they hold at least 4k rows and are at most a quarter of
+  // the tiles), so the main pass lists only a few candidates per wave.
+  pl.sort_lists = B <= 8;
+  if (!pl.sort_lists)
+    for (int64_t P : {(int64_t)4096, (int64_t)64}) {
+      int64_t nv = ceil_div(ix->T, P);
+      if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides.push_back(P);
+    }
+  // Lists end with at most k keys each, so a query never has more than
+  // G_max * k merge candidates.
+  pl.spill_cap = std::max<int64_t>(0, (int64_t)pl.G_max * k - kMergeCap);
   size_t nb = (size_t)bmax;
-  pl.off_cnt = 0;
-  pl.off_tau = kMaxGroup * 4;
-  pl.off_lists = pl.off_tau + 2 * kMaxGroup * 8;
-  pl.off_pool = pl.off_lists + nb * pl.G_max * pl.C * 8;
-  pl.bytes = pl.off_pool + nb * (size_t)pl.pool_cap * 8;
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  pl.off_tau = 0;
+  pl.off_lcnt = up(2 * kMaxGroup * 8);
+  pl.off_lkth = pl.off_lcnt + up(nb * pl.G_max * 4);
+  pl.off_lfirst = pl.off_lkth + up(nb * pl.G_max * 8);
+  pl.off_lists = pl.off_lfirst + up(nb * pl.G_max * 8);
+  pl.off_spill = pl.off_lists + up(nb * pl.G_max * pl.C * 8);
+  pl.bytes = pl.off_spill + up(nb * (size_t)std::max<int64_t>(1, pl.spill_cap) * 8);
   return DRESD_OK;
 }
 
@@ -178,7 +191,8 @@ dresd_status ensure_workspace(dresd_index *ix, size_t bytes) {
     (void)hipGetLastError();
     return fail(DRESD_ENOMEM, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
   }
-  // Pool counters must start at zero; each merge resets its own afterwards.
+  // Every region is written before it is read in each search; clearing it
+  // once keeps a fresh workspace deterministic to inspect.
   if (hipMemset(p, 0, bytes) != hipSuccess) {
     hipFree(p);
     return fail(DRESD_EDEVICE, "workspace clear failed");
@@ -338,10 +352,12 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
   if (s != DRESD_OK) return s;
   s = ensure_workspace(ix, pl.bytes);
   if (s != DRESD_OK) return s;
-  uint64_t *lists = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lists);
-  uint64_t *pool = reinterpret_cast<uint64_t *>(ix->ws + pl.off_pool);
-  uint32_t *pool_cnt = reinterpret_cast<uint32_t *>(ix->ws + pl.off_cnt);
   uint64_t *tau = reinterpret_cast<uint64_t *>(ix->ws + pl.off_tau);
+  uint32_t *lcnt = reinterpret_cast<uint32_t *>(ix->ws + pl.off_lcnt);
+  uint64_t *lkth = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lkth);
+  uint64_t *lfirst = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lfirst);
+  uint64_t *lists = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lists);
+  uint64_t *spill = reinterpret_cast<uint64_t *>(ix->ws + pl.off_spill);
 
   hipEvent_t e_all0 = nullptr, e_all1 = nullptr;
   if (ix->prof) {
@@ -357,18 +373,23 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
     sp.queries = queries + (size_t)gr.b0 * ix->d;
     sp.N = ix->N;
     sp.lists = lists;
-    sp.pool = pool;
-    sp.pool_cnt = pool_cnt;
-    sp.pool_cap = pl.pool_cap;
+    sp.lcnt = lcnt;
+    sp.lkth = lkth;
+    sp.lfirst = lfirst;
+    sp.sort_lists = pl.sort_lists ? 1 : 0;
     sp.B = gr.nb;
     sp.d = ix->d;
     sp.KB = ix->KB;
     sp.k = k;
     sp.C = pl.C;
     MergeParams mp;
-    mp.pool = pool;
-    mp.pool_cnt = pool_cnt;
-    mp.pool_cap = pl.pool_cap;
+    mp.lists = lists;
+    mp.lcnt = lcnt;
+    mp.lkth = lkth;
+    mp.lfirst = lfirst;
+    mp.spill = spill;
+    mp.spill_cap = pl.spill_cap;
+    mp.C = pl.C;
     mp.B = gr.nb;
     mp.k = k;
     mp.cont = ix->cont;
@@ -396,6 +417,7 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
         ix->ev_scan.push_back(e0);
         ix->ev_scan.push_back(e1);
       }
+      mp.G = sp.G;
       mp.final_mode = main_pass ? 1 : 0;
       mp.tau_out = tau + (size_t)(level & 1) * pl.bmax;
       mp.idx = idx + (size_t)gr.b0 * k;
