@@ -32,9 +32,21 @@ struct ScanParams {
   uint32_t *lcnt;            // [B][G] list lengths; bit 31 set = sorted descending
   uint64_t *lkth;            // [B][G] k-th best key of a sorted list of k keys, else 0
   uint64_t *lfirst;          // [B][G] best key of a sorted list; ~0 unknown; 0 empty
-  int B, d, KB, k, C, G;     // batch, dims, blocks per tile, k, list capacity, waves
+  int B, d, KB, k, C, G;     // batch, dims, blocks per tile, k, list capacity, lists
+  int CL;                    // per-query LDS stage in front of each HBM list
   int sort_lists;            // sort every list at the end (small batches)
 };
+
+// LDS bytes of one wave's candidate state: staged keys [nq][cl], sort
+// scratch [C], exact thresholds [nq], parked scores [nscore][64] and three
+// counters per query.
+__host__ __device__ inline size_t scan_wave_bytes(int nq, int nscore, int cl, int C) {
+  return (size_t)nq * cl * 8 + (size_t)C * 8 + (size_t)nq * 8 + (size_t)nscore * 64 * 4 +
+         (size_t)nq * 12;
+}
+__host__ __device__ inline size_t scan_mq_wave_bytes(int nq, int nscore, int cl, int C) {
+  return (scan_wave_bytes(nq, nscore, cl, C) + 15) / 16 * 16;
+}
 
 // A list summary flag: the list is sorted, best key first.
 constexpr uint32_t kSortedFlag = 0x80000000u;
@@ -67,6 +79,14 @@ struct LayoutParams {
 // Kernel launch entry points (defined in dresd_kernels.hip).
 typedef void (*ScanKernel)(ScanParams);
 ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass);  // cpq: columns per query
+// Shared-key scan (dresd_scan_mq.hip): qtw query tiles per wave, kbt blocks per key tile.
+ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass);
+ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass);
+inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass) {
+  if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass);
+  if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass);
+  return nullptr;
+}
 void *merge_kernel_ptr();
 void *layout_kernel_ptr(int dtype);
 int qt_index(int qt);  // 1,2,4,8,16 -> 0..4, else -1

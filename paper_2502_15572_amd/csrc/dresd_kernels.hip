@@ -9,7 +9,7 @@
 //            and cut to its k best at the end.
 // The merge that turns the per-wave lists into the answer is in
 // dresd_merge.hip.
-#include "dresd_device.h"
+#include "dresd_scan_common.h"
 
 namespace dresd {
 
@@ -123,19 +123,6 @@ __device__ __forceinline__ u4 query_chunk(const float *q, int d, int B, int col,
   return out;
 }
 
-// Re-select a wave's list: keep its k best keys (sorted) and return the k-th.
-__device__ inline uint64_t wave_flush(uint64_t *list, int cnt, int C, int k, uint64_t *scr,
-                                      int lane) {
-  __threadfence_block();  // this wave's list stores are visible to its loads
-  for (int e = lane; e < C; e += kWaveSize) scr[e] = (e < cnt) ? list[e] : 0ull;
-  wave_sync_lds();
-  wave_bitonic_desc(scr, C, lane);
-  for (int e = lane; e < k; e += kWaveSize) list[e] = scr[e];
-  uint64_t kth = scr[k - 1];
-  wave_sync_lds();
-  return kth;
-}
-
 template <int DT, int QT, int CPQ, bool MAIN>
 __device__ __forceinline__ void scan_body(const ScanParams &p) {
   constexpr int QPT = 16 / CPQ;  // queries per 16-column tile
@@ -152,14 +139,24 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   const int ncols = B * CPQ;
   const int g = lane >> 4, m = lane & 15;
 
-  // LDS carve-up: query operand | zero chunk | per-wave state | per-wave scratch
+  // LDS carve-up: query operand | zero chunk | one candidate region per wave
+  // (staged keys, sort scratch, thresholds, counters)
   const int qop_bytes = ncols * KB * 64;
   const int zero_off = qop_bytes;
-  unsigned char *st = smem + qop_bytes + 16;
-  uint64_t *st_key = reinterpret_cast<uint64_t *>(st) + wv * NQ;
-  uint32_t *st_cnt = reinterpret_cast<uint32_t *>(st + (size_t)nwv * NQ * 8) + wv * NQ;
-  float *st_thr = reinterpret_cast<float *>(st + (size_t)nwv * NQ * 12) + wv * NQ;
-  uint64_t *scr = reinterpret_cast<uint64_t *>(st + (size_t)nwv * NQ * 16) + (size_t)wv * C;
+  const int CL = p.CL;
+  CandSink sink;
+  sink.stg = reinterpret_cast<uint64_t *>(smem + qop_bytes + 16 +
+                                          (size_t)wv * scan_mq_wave_bytes(NQ, 0, CL, C));
+  sink.scr = sink.stg + (size_t)NQ * CL;
+  sink.st_key = sink.scr + C;
+  sink.st_cnt = reinterpret_cast<uint32_t *>(sink.st_key + NQ);
+  sink.st_thr = reinterpret_cast<float *>(sink.st_cnt + NQ);
+  sink.stg_cnt = reinterpret_cast<uint32_t *>(sink.st_thr + NQ);
+  sink.cl = CL;
+  sink.C = C;
+  sink.k = p.k;
+  sink.lane = lane;
+  auto list_of = [&](int q) { return p.lists + ((size_t)q * G + gw) * C; };
 
   // 1. Query operand, in the lane order of the A operand.
   {
@@ -178,20 +175,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
     if (threadIdx.x == 0) *reinterpret_cast<u4 *>(smem + zero_off) = u4{0, 0, 0, 0};
   }
   // 2. Per-wave state: thresholds start at the pass's tau (or none).
-  for (int q = lane; q < NQ; q += kWaveSize) {
-    uint64_t tk = 0;
-    float tf = -__builtin_inff();
-    if (q >= B) {
-      tk = ~0ull;
-      tf = __builtin_inff();
-    } else if (p.tau && p.tau[q] != 0) {
-      tk = p.tau[q] - 1;  // keep keys >= tau
-      tf = order_value((uint32_t)(tk >> 32));
-    }
-    st_key[q] = tk;
-    st_cnt[q] = 0;
-    st_thr[q] = tf;
-  }
+  sink_init(sink, NQ, B, p.tau);
   __syncthreads();
 
   // Per-lane A-operand addresses: column m of tile t, or the zero chunk.
@@ -212,7 +196,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
 #pragma unroll
   for (int t = 0; t < QT; ++t)
 #pragma unroll
-    for (int s = 0; s < NS; ++s) thr[t][s] = st_thr[t * QPT + g * NS + s];
+    for (int s = 0; s < NS; ++s) thr[t][s] = sink.st_thr[t * QPT + g * NS + s];
 
   // 3. Stream this wave's tiles.  Everything that steers the loop is
   // wave-uniform (scalar registers), so control flow never masks lanes.
@@ -271,6 +255,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
         any |= row_ok && sc[t][s] >= thr[t][s];
       }
     if (__ballot(any)) {
+      bool spilled = false;
 #pragma unroll
       for (int t = 0; t < QT; ++t)
 #pragma unroll
@@ -280,40 +265,17 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
           while (mk) {
             const int gg = (__ffsll((long long)mk) - 1) >> 4;
             const int q = t * QPT + gg * NS + s;
-            const bool mine = ps && (g == gg);
-            const uint64_t key = make_key(sc[t][s], row);
-            uint64_t tk = st_key[q];
-            bool take = mine && key > tk;
-            uint64_t tm = __ballot(take);
-            int n = __popcll(tm);
-            int cnt = (int)st_cnt[q];
-            uint64_t *list = p.lists + ((size_t)q * G + gw) * C;
-            if (cnt + n > C) {
-              tk = wave_flush(list, cnt, C, p.k, scr, lane);
-              cnt = p.k;
-              st_key[q] = tk;
-              st_thr[q] = order_value((uint32_t)(tk >> 32));
-              take = mine && key > tk;
-              tm = __ballot(take);
-              n = __popcll(tm);
-            }
-            if (take) {
-              int pos = cnt + __popcll(tm & ((1ull << lane) - 1ull));
-              list[pos] = key;
-            }
-            st_cnt[q] = (uint32_t)(cnt + n);
-            wave_sync_lds();
+            spilled |= sink_offer(sink, q, ps && (g == gg), make_key(sc[t][s], row), list_of(q));
             mk &= ~(0xFFFFull << (16 * gg));
           }
         }
 #pragma unroll
       for (int t = 0; t < QT; ++t)
 #pragma unroll
-        for (int s = 0; s < NS; ++s) thr[t][s] = st_thr[t * QPT + g * NS + s];
-      // Drain this rare path's memory operations here, so that after it the
-      // only loads in flight are the ring's and the fast path keeps its exact
-      // wait counts.
-      __threadfence_block();
+        for (int s = 0; s < NS; ++s) thr[t][s] = sink.st_thr[t * QPT + g * NS + s];
+      // A spill used vector memory: drain it here, so that afterwards the only
+      // loads in flight are the ring's and the fast path keeps exact waits.
+      if (spilled) __threadfence_block();
     }
 #pragma unroll
     for (int t = 0; t < QT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
@@ -341,37 +303,12 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
     }
   }
 
-  // 4. Publish the lists.  A list holding more than k keys is cut to its k
-  // best; with sort_lists every list is sorted.  A sorted list publishes its
-  // best key, and its k-th key when it holds k keys: the best k-th key of any
-  // list bounds the query's answer from below, and the merge skips every
-  // list whose best key is under that bound.
-  __threadfence_block();
+  // 4. Publish the lists: lists holding more than k keys are cut to their k
+  // best (every list is sorted with sort_lists); each publishes its length,
+  // best key and k-th key, with which the merge bounds the answer.
   for (int q = 0; q < B; ++q) {
-    const int cnt = (int)st_cnt[q];
-    uint64_t first = (cnt == 0) ? 0ull : ~0ull;  // ~0: unknown, always visited
-    if (cnt > p.k || (p.sort_lists && cnt > 0)) {
-      uint64_t *list = p.lists + ((size_t)q * G + gw) * C;
-      int n = 2;
-      while (n < cnt) n <<= 1;
-      for (int e = lane; e < n; e += kWaveSize) scr[e] = (e < cnt) ? list[e] : 0ull;
-      wave_sync_lds();
-      wave_bitonic_desc(scr, n, lane);
-      const int keep = cnt < p.k ? cnt : p.k;
-      for (int e = lane; e < keep; e += kWaveSize) list[e] = scr[e];
-      first = scr[0];
-      st_key[q] = (keep == p.k) ? scr[p.k - 1] : 0ull;
-      st_cnt[q] = (uint32_t)keep | kSortedFlag;
-    } else {
-      st_key[q] = 0ull;
-      if (cnt == 1) st_cnt[q] = 1u | kSortedFlag;
-    }
-    if (lane == 0) p.lfirst[(size_t)q * G + gw] = first;
-    wave_sync_lds();
-  }
-  for (int q = lane; q < B; q += kWaveSize) {
-    p.lcnt[(size_t)q * G + gw] = st_cnt[q];
-    p.lkth[(size_t)q * G + gw] = st_key[q];
+    const size_t o = (size_t)q * G + gw;
+    sink_publish(sink, q, list_of(q), p.sort_lists != 0, p.lcnt + o, p.lfirst + o, p.lkth + o);
   }
 }
 

@@ -70,9 +70,11 @@ constexpr int kMaxScanWgPerCu = 4;
 
 struct Plan {
   int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
+  bool mq = false;                  // shared-key scan (queries in registers)
   int bmax = 0;                 // queries per group
   std::vector<Group> groups;
   int C = 0;                    // per-wave list capacity
+  int CL = 0;                   // per-query LDS stage
   std::vector<int64_t> strides; // sampled passes, sparsest first
   ScanKernel kmain = nullptr, ksample = nullptr;
   size_t lds = 0;
@@ -84,9 +86,19 @@ struct Plan {
   size_t bytes = 0;
 };
 
-size_t scan_lds(int ncols, int KB, int nq, int C) {
-  return (size_t)ncols * KB * 64 + 16 + (size_t)4 * nq * 16 + (size_t)4 * C * 8;
+// Single-tile scan: query operand | zero chunk | candidate region per wave.
+size_t scan_lds(int ncols, int KB, int nq, int cl, int C) {
+  return (size_t)ncols * KB * 64 + 16 + (size_t)4 * scan_mq_wave_bytes(nq, 0, cl, C);
 }
+
+// Shared-key scan: two 8-block stages of keys | candidate region per wave
+// (with room to park one tile's scores: nscore x 64 lanes).
+size_t scan_mq_lds(int nqw, int nscore, int cl, int C) {
+  return (size_t)2 * 8 * kBlockBytes + (size_t)4 * scan_mq_wave_bytes(nqw, nscore, cl, C);
+}
+
+// Per-query LDS stage in front of each HBM list: larger when few queries share the wave.
+int stage_cap(int nq) { return nq >= 64 ? 8 : nq >= 16 ? 16 : 32; }
 
 int occupancy(dresd_index *ix, ScanKernel k, size_t lds) {
   for (size_t i = 0; i < ix->occ_key.size(); ++i)
@@ -119,39 +131,64 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
   else pl.terms = 1;
   pl.qpt = 16 / pl.terms;
   pl.C = next_pow2(std::max(k + 64, 128));
-  // Largest group (power-of-two number of query tiles, at most 16) whose
-  // query operand and per-wave state fit in the workgroup's LDS.
-  int qt = 16;
-  for (;; qt >>= 1) {
-    int nb = std::min(B, qt * pl.qpt);
-    size_t lds = scan_lds(nb * pl.terms, ix->KB, qt * pl.qpt, pl.C);
-    if (lds <= ix->lds_max || qt == 1) break;
+  const int qt_all = (int)ceil_div((int64_t)B * pl.terms, 16);  // query tiles of the batch
+  const bool mq_type = (ix->dtype == kF16 && pl.terms == 1) || ix->dtype == kBF16;
+  const bool mq_kb = ix->KB == 4 || ix->KB == 8 || ix->KB == 16 || ix->KB == 32;
+  if (mq_type && mq_kb && qt_all >= 4) {
+    // Several query tiles: queries stationary in registers, keys shared
+    // through LDS.  Each of the 4 waves holds qtw tiles (operands for all
+    // KB blocks: qtw * KB <= 32 chunks of 16 bytes).
+    pl.mq = true;
+    int qtw = 1;
+    while (qtw < 4 && 4 * qtw < qt_all && 2 * qtw * ix->KB <= 32) qtw <<= 1;
+    pl.qt = 4 * qtw;
+    pl.bmax = std::min(B, pl.qt * pl.qpt);
+    pl.kmain = scan_mq_kernel(ix->dtype, qtw, ix->KB, true);
+    pl.ksample = scan_mq_kernel(ix->dtype, qtw, ix->KB, false);
+    pl.CL = stage_cap(qtw * pl.qpt);
+    pl.lds = scan_mq_lds(qtw * pl.qpt, qtw * (4 / pl.terms), pl.CL, pl.C);
+  } else {
+    // Largest group (power-of-two number of query tiles, at most 16) whose
+    // query operand and per-wave state fit in the workgroup's LDS.
+    int qt = 16;
+    for (;; qt >>= 1) {
+      int nb = std::min(B, qt * pl.qpt);
+      size_t lds = scan_lds(nb * pl.terms, ix->KB, qt * pl.qpt, stage_cap(qt * pl.qpt), pl.C);
+      if (lds <= ix->lds_max || qt == 1) break;
+    }
+    int bmax = std::min(B, qt * pl.qpt);
+    pl.CL = stage_cap(qt * pl.qpt);
+    if (scan_lds(std::min(bmax, pl.qpt) * pl.terms, ix->KB, pl.qpt, pl.CL, pl.C) > ix->lds_max)
+      return fail(DRESD_EUNSUPPORTED, "query tile does not fit in LDS for this d and k");
+    // shrink bmax until it fits (qt == 1 case)
+    while (bmax > 1 &&
+           scan_lds(bmax * pl.terms, ix->KB, qt * pl.qpt, pl.CL, pl.C) > ix->lds_max)
+      --bmax;
+    // smallest qt that holds bmax
+    int need = (int)ceil_div((int64_t)bmax * pl.terms, 16);
+    pl.qt = 1;
+    while (pl.qt < need) pl.qt <<= 1;
+    pl.bmax = bmax;
+    pl.kmain = scan_kernel(ix->dtype, pl.qt, pl.terms, true);
+    pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.terms, false);
+    pl.CL = stage_cap(pl.qt * pl.qpt);
+    pl.lds = scan_lds(bmax * pl.terms, ix->KB, pl.qt * pl.qpt, pl.CL, pl.C);
   }
-  int bmax = std::min(B, qt * pl.qpt);
-  if (scan_lds(std::min(bmax, pl.qpt) * pl.terms, ix->KB, pl.qpt, pl.C) > ix->lds_max)
-    return fail(DRESD_EUNSUPPORTED, "query tile does not fit in LDS for this d and k");
-  // shrink bmax until it fits (qt == 1 case)
-  while (bmax > 1 && scan_lds(bmax * pl.terms, ix->KB, qt * pl.qpt, pl.C) > ix->lds_max) --bmax;
-  // smallest qt that holds bmax
-  int need = (int)ceil_div((int64_t)bmax * pl.terms, 16);
-  pl.qt = 1;
-  while (pl.qt < need) pl.qt <<= 1;
-  pl.bmax = bmax;
+  const int bmax = pl.bmax;
   int ngr = (int)ceil_div(B, bmax);
   for (int i = 0; i < ngr; ++i) {
     int b0 = (int)((int64_t)B * i / ngr), b1 = (int)((int64_t)B * (i + 1) / ngr);
     pl.groups.push_back({b0, b1 - b0});
   }
-  pl.kmain = scan_kernel(ix->dtype, pl.qt, pl.terms, true);
-  pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.terms, false);
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
-  pl.lds = scan_lds(bmax * pl.terms, ix->KB, pl.qt * pl.qpt, pl.C);
+  if (pl.lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS");
   int occ = std::min(occupancy(ix, pl.kmain, pl.lds), occupancy(ix, pl.ksample, pl.lds));
   // At most 4 workgroups (16 waves) per CU: enough loads in flight to keep
   // HBM busy, and few enough per-wave lists for the merge to keep their
   // best keys in LDS.
   pl.wg_max = ix->cus * std::min(occ, kMaxScanWgPerCu);
-  pl.G_max = pl.wg_max * (kScanThreads / kWaveSize);
+  // lists per query: one per wave, or one per workgroup for the shared-key scan
+  pl.G_max = pl.mq ? pl.wg_max : pl.wg_max * (kScanThreads / kWaveSize);
   // Small batches: every wave keeps its own running top-k and sorts it at
   // the end; the merge then prunes with the best per-wave k-th key.  Larger
   // batches first set per-query thresholds from sampled passes over tiles
@@ -262,6 +299,15 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
     return cleanup(fail(DRESD_ENOMEM, "continuation storage allocation failed"));
   }
   // Raise the dynamic-LDS limit of every scan kernel to the device's.
+  for (int v = 0; v < 3; ++v)
+    for (int qtw : {1, 2, 4})
+      for (int kbt : {4, 8, 16, 32})
+        for (int mp = 0; mp < 2; ++mp) {
+          ScanKernel kf = scan_mq_kernel(v, qtw, kbt, mp != 0);
+          if (kf)
+            (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      (int)ix->lds_max);
+        }
   for (int v = 0; v < 3; ++v)
     for (int qt : {1, 2, 4, 8, 16})
       for (int cpq : {1, 2, 4})
@@ -382,6 +428,7 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
     sp.KB = ix->KB;
     sp.k = k;
     sp.C = pl.C;
+    sp.CL = pl.CL;
     MergeParams mp;
     mp.lists = lists;
     mp.lcnt = lcnt;
@@ -400,8 +447,8 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
       sp.stride = stride;
       sp.nvisit = ceil_div(ix->T, stride);
       sp.tau = tau_in;
-      int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(sp.nvisit, wpg));
-      sp.G = (int)(wgs * wpg);
+      int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(sp.nvisit, pl.mq ? 1 : wpg));
+      sp.G = (int)(pl.mq ? wgs : wgs * wpg);
       void *sargs[] = {&sp};
       hipEvent_t e0 = nullptr, e1 = nullptr;
       if (main_pass && ix->prof) {
