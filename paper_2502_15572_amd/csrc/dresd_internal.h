@@ -37,15 +37,25 @@ struct ScanParams {
   int sort_lists;            // sort every list at the end (small batches)
 };
 
-// LDS bytes of one wave's candidate state: staged keys [nq][cl], sort
-// scratch [C], exact thresholds [nq], parked scores [nscore][64] and three
-// counters per query.
-__host__ __device__ inline size_t scan_wave_bytes(int nq, int nscore, int cl, int C) {
-  return (size_t)nq * cl * 8 + (size_t)C * 8 + (size_t)nq * 8 + (size_t)nscore * 64 * 4 +
-         (size_t)nq * 12;
+// LDS bytes of one wave's candidate state in the single-tile scan: staged
+// keys [nq][cl], sort scratch [C], exact thresholds [nq] and three counters
+// per query, rounded up to 16 bytes.
+__host__ __device__ inline size_t scan_wave_bytes(int nq, int cl, int C) {
+  return ((size_t)nq * cl * 8 + (size_t)C * 8 + (size_t)nq * 8 + (size_t)nq * 12 + 15) / 16 * 16;
 }
-__host__ __device__ inline size_t scan_mq_wave_bytes(int nq, int nscore, int cl, int C) {
-  return (scan_wave_bytes(nq, nscore, cl, C) + 15) / 16 * 16;
+
+// Shared-key scan: a wave's candidate buffer holds kMqCandBuf (key, query)
+// entries; its LDS region is key buffer [kMqCandBuf] u64 | sort scratch [C]
+// u64 | exact thresholds [nqw] u64 | query of each buffered key [kMqCandBuf]
+// u16 | list lengths [nqw] u32 | float thresholds [nqw] f32.
+constexpr int kMqCandBuf = 256;
+constexpr int kMqStageBlocks = 8;  // 1 KiB key blocks per LDS stage
+__host__ __device__ inline size_t scan_mq_wave_bytes(int nqw, int C) {
+  return ((size_t)kMqCandBuf * 10 + (size_t)C * 8 + (size_t)nqw * 16 + 15) / 16 * 16;
+}
+__host__ __device__ inline size_t scan_mq_lds_bytes(int stages, int nqw, int C) {
+  return (size_t)stages * kMqStageBlocks * kBlockBytes +
+         (size_t)(kScanThreads / kWaveSize) * scan_mq_wave_bytes(nqw, C);
 }
 
 // A list summary flag: the list is sorted, best key first.
@@ -79,12 +89,13 @@ struct LayoutParams {
 // Kernel launch entry points (defined in dresd_kernels.hip).
 typedef void (*ScanKernel)(ScanParams);
 ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass);  // cpq: columns per query
-// Shared-key scan (dresd_scan_mq.hip): qtw query tiles per wave, kbt blocks per key tile.
-ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass);
-ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass);
-inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass) {
-  if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass);
-  if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass);
+// Shared-key scan (dresd_scan_mq.hip): qtw query tiles per wave, kbt blocks
+// per key tile; *stages receives the depth of its LDS ring of key stages.
+ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, int *stages);
+ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, int *stages);
+inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, int *stages) {
+  if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass, stages);
+  if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass, stages);
   return nullptr;
 }
 void *merge_kernel_ptr();

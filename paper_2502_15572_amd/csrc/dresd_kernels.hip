@@ -146,7 +146,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   const int CL = p.CL;
   CandSink sink;
   sink.stg = reinterpret_cast<uint64_t *>(smem + qop_bytes + 16 +
-                                          (size_t)wv * scan_mq_wave_bytes(NQ, 0, CL, C));
+                                          (size_t)wv * scan_wave_bytes(NQ, CL, C));
   sink.scr = sink.stg + (size_t)NQ * CL;
   sink.st_key = sink.scr + C;
   sink.st_cnt = reinterpret_cast<uint32_t *>(sink.st_key + NQ);

@@ -88,13 +88,7 @@ struct Plan {
 
 // Single-tile scan: query operand | zero chunk | candidate region per wave.
 size_t scan_lds(int ncols, int KB, int nq, int cl, int C) {
-  return (size_t)ncols * KB * 64 + 16 + (size_t)4 * scan_mq_wave_bytes(nq, 0, cl, C);
-}
-
-// Shared-key scan: two 8-block stages of keys | candidate region per wave
-// (with room to park one tile's scores: nscore x 64 lanes).
-size_t scan_mq_lds(int nqw, int nscore, int cl, int C) {
-  return (size_t)2 * 8 * kBlockBytes + (size_t)4 * scan_mq_wave_bytes(nqw, nscore, cl, C);
+  return (size_t)ncols * KB * 64 + 16 + (size_t)4 * scan_wave_bytes(nq, cl, C);
 }
 
 // Per-query LDS stage in front of each HBM list: larger when few queries share the wave.
@@ -143,10 +137,11 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
     while (qtw < 4 && 4 * qtw < qt_all && 2 * qtw * ix->KB <= 32) qtw <<= 1;
     pl.qt = 4 * qtw;
     pl.bmax = std::min(B, pl.qt * pl.qpt);
-    pl.kmain = scan_mq_kernel(ix->dtype, qtw, ix->KB, true);
-    pl.ksample = scan_mq_kernel(ix->dtype, qtw, ix->KB, false);
-    pl.CL = stage_cap(qtw * pl.qpt);
-    pl.lds = scan_mq_lds(qtw * pl.qpt, qtw * (4 / pl.terms), pl.CL, pl.C);
+    int stages = 0;
+    pl.kmain = scan_mq_kernel(ix->dtype, qtw, ix->KB, true, &stages);
+    pl.ksample = scan_mq_kernel(ix->dtype, qtw, ix->KB, false, &stages);
+    pl.CL = 0;
+    pl.lds = scan_mq_lds_bytes(stages, qtw * pl.qpt, pl.C);
   } else {
     // Largest group (power-of-two number of query tiles, at most 16) whose
     // query operand and per-wave state fit in the workgroup's LDS.
@@ -303,7 +298,8 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
     for (int qtw : {1, 2, 4})
       for (int kbt : {4, 8, 16, 32})
         for (int mp = 0; mp < 2; ++mp) {
-          ScanKernel kf = scan_mq_kernel(v, qtw, kbt, mp != 0);
+          int stages = 0;
+          ScanKernel kf = scan_mq_kernel(v, qtw, kbt, mp != 0, &stages);
           if (kf)
             (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
                                       (int)ix->lds_max);

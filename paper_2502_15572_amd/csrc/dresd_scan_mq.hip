@@ -5,16 +5,18 @@
 // The queries stay in registers and the keys are shared through LDS:
 //   * the workgroup's 4 waves split the query tiles; each wave holds its
 //     tiles' A operands for every 32-dim block of the keys in VGPRs;
-//   * the workgroup streams its key tiles in stages of SB 1 KiB blocks; each
-//     wave loads LPS blocks of a stage into registers D stages ahead, writes
-//     them to a double-buffered LDS stage, and after one barrier every wave
-//     reads every block of the stage once (4 KiB of LDS reads per KiB of HBM,
-//     independent of the batch);
-//   * every stage issues exactly LPS loads per wave (loads past the end
-//     re-read the last block), so the wait before each stage is a constant.
-// Candidates are filtered and listed exactly as in the single-tile scan,
-// with one list per (query, workgroup).
-#include "dresd_scan_common.h"
+//   * the workgroup streams its key tiles through a ring of S LDS stages of
+//     8 blocks (8 KiB).  Each wave copies 2 blocks of every stage straight
+//     from HBM into LDS (global_load_lds_dwordx4, no VGPR round trip), S - 1
+//     stages ahead; one barrier per stage publishes a stage to all waves,
+//     which each read every block once (4 KiB of LDS reads per KiB of HBM);
+//   * every stage issues exactly 2 copies per wave (copies past the end
+//     re-read the last blocks), so the wait before each stage is a constant.
+// The per-tile test against the per-query thresholds is a few VALU
+// instructions; tiles with candidates append (key, query) pairs to a small
+// per-wave LDS buffer, which is moved into per-(query, workgroup) lists in
+// HBM only when it fills up.
+#include "dresd_device.h"
 
 namespace dresd {
 
@@ -75,49 +77,65 @@ __device__ __forceinline__ u4 query_chunk_mq(const float *q, int d, int B, int c
   return out;
 }
 
+// Copy two consecutive 1 KiB blocks at `src` into LDS at `lds` and lds + 1 KiB:
+// lane l's 16 bytes go to lds + 16 l (the LDS address comes from M0 and the
+// lane index, not from the global address).  Written as inline assembly so
+// that the compiler's wait-count model, which does not know which LDS bytes
+// an LDS-DMA copy writes, adds no waits for these copies before unrelated LDS
+// reads; the caller waits with wait_vmcnt and a barrier before reading them.
+__device__ __forceinline__ void copy2_to_lds(const void *src, uint32_t voff0, uint32_t voff1,
+                                             uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %3\n\t"
+      "global_load_lds_dwordx4 %0, %2 nt\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %1, %2 nt"
+      :
+      : "v"(voff0), "v"(voff1), "s"(src), "s"(lds)
+      : "memory");
+}
+
+// Wait until at most N of this wave's vector memory operations are pending
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
 }  // namespace
 
 // QTW query tiles per wave, KBT 32-dim blocks per key tile (must equal the
-// index's blocks per tile), CPQ operand columns per query.
-template <int DT, int QTW, int KBT, int CPQ, bool MAIN>
+// index's blocks per tile), CPQ operand columns per query, S LDS stages.
+template <int DT, int QTW, int KBT, int CPQ, int S>
 __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
-  constexpr int NW = kScanThreads / kWaveSize;  // waves per workgroup
-  constexpr int QPT = 16 / CPQ;
-  constexpr int NS = 4 / CPQ;
+  constexpr int QPT = 16 / CPQ;   // queries per tile
+  constexpr int NS = 4 / CPQ;     // scores per lane per query tile
   constexpr int NQW = QTW * QPT;  // queries per wave
-  constexpr int SB = 8;           // blocks per stage
-  constexpr int LPS = SB / NW;    // loads per wave per stage
-  constexpr int D = 4;            // stages loaded ahead (= stages per group)
-  constexpr int GB = SB * D;      // blocks per group; a whole number of tiles
-  static_assert(GB % KBT == 0, "a group must hold whole key tiles");
+  constexpr int NP = QTW * NS;    // scores per lane per key tile
+  constexpr int SB = kMqStageBlocks;
+  constexpr int TPS = KBT >= SB ? 1 : SB / KBT;  // key tiles per stage
+  constexpr int SPT = KBT >= SB ? KBT / SB : 1;  // stages per key tile
+  constexpr int BPT = KBT >= SB ? SB : KBT;      // blocks of a tile per stage
+  constexpr int CB = kMqCandBuf;
+  constexpr int WAIT = 2 * (S - 2);  // copies of later stages still in flight
+  static_assert(KBT >= 4 && S >= 3 && NP <= 32, "shape");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, m = lane & 15;
-  const int B = p.B, C = p.C;
-  const int G = p.G;  // lists per query = workgroups
+  const int B = p.B, C = p.C, k = p.k, G = p.G;
   const int wg = blockIdx.x;
 
-  // LDS: two stages of keys, then one region per wave:
-  //   staged keys [NQW][CL] | sort scratch [C] | thresholds [NQW] |
-  //   scores of a tile with candidates [QTW*NS][64] | counts [NQW] x 3
-  u4 *stage_buf = reinterpret_cast<u4 *>(smem);
-  const int CL = p.CL;
-  const size_t wreg = scan_mq_wave_bytes(NQW, QTW * NS, CL, C);
-  unsigned char *w0 = smem + 2 * SB * kBlockBytes + (size_t)wv * wreg;
-  CandSink sink;
-  sink.stg = reinterpret_cast<uint64_t *>(w0);
-  sink.scr = sink.stg + (size_t)NQW * CL;
-  sink.st_key = sink.scr + C;
-  float *scs = reinterpret_cast<float *>(sink.st_key + NQW);
-  sink.st_cnt = reinterpret_cast<uint32_t *>(scs + (size_t)QTW * NS * kWaveSize);
-  sink.st_thr = reinterpret_cast<float *>(sink.st_cnt + NQW);
-  sink.stg_cnt = reinterpret_cast<uint32_t *>(sink.st_thr + NQW);
-  sink.cl = CL;
-  sink.C = C;
-  sink.k = p.k;
-  sink.lane = lane;
+  // LDS: ring of S stages, then one candidate region per wave.
+  const size_t wreg = scan_mq_wave_bytes(NQW, C);
+  unsigned char *w0 = smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg;
+  uint64_t *ck = reinterpret_cast<uint64_t *>(w0);  // buffered keys [CB]
+  uint64_t *scr = ck + CB;                          // sort scratch [C]
+  uint64_t *st_key = scr + C;                       // keep keys > st_key [NQW]
+  uint16_t *cq = reinterpret_cast<uint16_t *>(st_key + NQW);  // query of ck[e] [CB]
+  uint32_t *st_cnt = reinterpret_cast<uint32_t *>(cq + CB);   // HBM list length [NQW]
+  float *st_thr = reinterpret_cast<float *>(st_cnt + NQW);    // float threshold [NQW]
 
   // Queries of this wave: tiles [wv*QTW, wv*QTW + QTW) of the batch.
   const int q0 = wv * NQW;
@@ -128,36 +146,123 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     for (int kb = 0; kb < KBT; ++kb)
       qreg[t][kb] = query_chunk_mq<DT, CPQ>(p.queries, p.d, B, (wv * QTW + t) * 16 + m,
                                             kb * 32 + g * 8);
-  sink_init(sink, NQW, B - q0, p.tau ? p.tau + q0 : nullptr);
+  for (int i = lane; i < NQW; i += kWaveSize) {
+    uint64_t tk = 0;
+    float tf = -__builtin_inff();
+    if (q0 + i >= B) {
+      tk = ~0ull;
+      tf = __builtin_inff();
+    } else if (p.tau && p.tau[q0 + i] != 0) {
+      tk = p.tau[q0 + i] - 1;  // keep keys >= tau
+      tf = order_value((uint32_t)(tk >> 32));
+    }
+    st_key[i] = tk;
+    st_cnt[i] = 0;
+    st_thr[i] = tf;
+  }
+  wave_sync_lds();
+  // Score slot j = t * NS + s of a lane belongs to query t * QPT + g * NS + s.
+  float thr[NP];
+  auto load_thr = [&]() {
+#pragma unroll
+    for (int j = 0; j < NP; ++j) thr[j] = st_thr[(j / NS) * QPT + g * NS + (j % NS)];
+  };
+  load_thr();
   auto list_of = [&](int i) { return p.lists + ((size_t)(q0 + i) * G + wg) * C; };
 
-  // This workgroup's key blocks: tiles [v0, v1), KBT blocks each.
-  const int64_t v0 = wave_uniform(p.nvisit * wg / G);
-  const int64_t v1 = wave_uniform(p.nvisit * (wg + 1) / G);
-  const int64_t NB = (v1 - v0) * KBT;
-  const u4 *base = static_cast<const u4 *>(p.data) + lane;
-  // Address of the workgroup's block j, clamped to its last block.
-  auto block = [&](int64_t j) -> const u4 * {
-    j = j < NB ? j : NB - 1;
-    const int64_t vt = j / KBT;
-    return base + ((v0 + vt) * p.stride * KBT + (j - vt * KBT)) * 64;
+  // Cut query i's full HBM list to its k best keys and raise its threshold.
+  auto cut = [&](int i) {
+    uint64_t *list = list_of(i);
+    __threadfence_block();  // this wave's list stores are visible to its loads
+    for (int e = lane; e < C; e += kWaveSize) scr[e] = list[e];
+    wave_sync_lds();
+    wave_bitonic_desc(scr, C, lane);
+    for (int e = lane; e < k; e += kWaveSize) list[e] = scr[e];
+    const uint64_t kth = scr[k - 1];
+    wave_sync_lds();
+    if (lane == 0) {
+      st_cnt[i] = (uint32_t)k;
+      if (kth > st_key[i]) {
+        st_key[i] = kth;
+        st_thr[i] = order_value((uint32_t)(kth >> 32));
+      }
+    }
+    wave_sync_lds();
   };
 
-  u4 ring[D][LPS];
-  if (NB > 0) {
-#pragma unroll
-    for (int r = 0; r < D; ++r)
-#pragma unroll
-      for (int i = 0; i < LPS; ++i) ring[r][i] = __builtin_nontemporal_load(block(r * SB + wv * LPS + i));
-  }
+  // Move the buffered candidates into the HBM lists (keys that still beat
+  // their query's exact threshold), cutting lists that fill up.
+  int cnt = 0;  // buffered candidates (wave-uniform)
+  auto flush = [&]() {
+    wave_sync_lds();
+    for (int e0 = 0; e0 < cnt; e0 += kWaveSize) {
+      const int e = e0 + lane;
+      const bool valid = e < cnt;
+      const int q = valid ? (int)cq[e] : 0;
+      const uint64_t key = valid ? ck[e] : 0ull;
+      bool has = valid && key > st_key[q];
+      while (__ballot(has)) {
+        const uint32_t pos = has ? atomicAdd(&st_cnt[q], 1u) : 0u;
+        const bool over = has && pos >= (uint32_t)C;
+        if (has && !over) list_of(q)[pos] = key;
+        uint64_t om = __ballot(over);
+        if (om == 0) break;
+        if (over) st_cnt[q] = (uint32_t)C;
+        wave_sync_lds();
+        while (om) {
+          const int qq = __builtin_amdgcn_readlane(q, __ffsll((long long)om) - 1);
+          cut(qq);
+          om &= ~__ballot(over && q == qq);
+        }
+        has = over && key > st_key[q];
+      }
+    }
+    cnt = 0;
+    wave_sync_lds();
+    load_thr();
+  };
 
+  // This workgroup's key tiles: visited tiles [v0, v1), KBT blocks each.
+  const int64_t v0 = wave_uniform(p.nvisit * wg / G);
+  const int64_t v1 = wave_uniform(p.nvisit * (wg + 1) / G);
+  const int64_t ntile = v1 - v0;
   f4 acc[QTW];
-  auto tile_end = [&](int64_t tile) {
+
+  // Buffer the candidates of key tile `tile` (rows tile*16 .. +15); rare.
+  auto candidates = [&](int64_t tile, const float (&sc)[NP]) {
     const int64_t row64 = tile * kTileRows + m;
     const bool row_ok = row64 < p.N;
     const uint32_t row = (uint32_t)row64;
-    float sc[QTW][NS];
-    bool any = false;
+    const uint64_t below = (1ull << lane) - 1ull;
+    uint32_t done = 0;  // slots already buffered
+    for (;;) {
+      bool stalled = false;
+#pragma unroll
+      for (int j = 0; j < NP; ++j) {
+        if (!(done & (1u << j))) {
+          const bool h = row_ok && sc[j] >= thr[j];
+          const uint64_t mk = __ballot(h);
+          const int n = __popcll(mk);
+          if (cnt + n <= CB) {
+            if (h) {
+              const int at = cnt + __popcll(mk & below);
+              ck[at] = make_key(sc[j], row);
+              cq[at] = (uint16_t)((j / NS) * QPT + g * NS + (j % NS));
+            }
+            cnt += n;
+            done |= 1u << j;
+          } else {
+            stalled = true;
+          }
+        }
+      }
+      if (!stalled) break;
+      flush();  // at least one more slot fits afterwards
+    }
+  };
+
+  auto tile_end = [&](int64_t vt) {
+    float sc[NP];
 #pragma unroll
     for (int t = 0; t < QTW; ++t)
 #pragma unroll
@@ -168,106 +273,142 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
           const float s2 = (DT == kF16) ? (1.0f / 4194304.0f) : 1.0f;
           v = (v + acc[t][s * CPQ + 1] * s1) + acc[t][s * CPQ + 2] * s2;
         }
-        sc[t][s] = v;
-        any |= row_ok && v >= sink.st_thr[t * QPT + g * NS + s];
+        sc[t * NS + s] = v;
       }
-    if (__ballot(any)) {
-      // Rare: park the scores in LDS and walk them in a rolled loop (keeps
-      // the unrolled stream loop small).
-      bool spilled = false;
+    // v >= thr exactly when v - thr >= 0 (round-to-nearest keeps the sign).
+    float mx = sc[0] - thr[0];
 #pragma unroll
-      for (int t = 0; t < QTW; ++t)
-#pragma unroll
-        for (int s = 0; s < NS; ++s) scs[(t * NS + s) * kWaveSize + lane] = sc[t][s];
-      wave_sync_lds();
-#pragma unroll 1
-      for (int ts = 0; ts < QTW * NS; ++ts) {
-        const int t = ts / NS, s = ts - t * NS;
-        const float v = scs[ts * kWaveSize + lane];
-        const bool ps = row_ok && v >= sink.st_thr[t * QPT + g * NS + s];
-        uint64_t mk = __ballot(ps);
-        while (mk) {
-          const int gg = (__ffsll((long long)mk) - 1) >> 4;
-          const int i = t * QPT + gg * NS + s;  // query q0 + i
-          spilled |= sink_offer(sink, i, ps && (g == gg), make_key(v, row), list_of(i));
-          mk &= ~(0xFFFFull << (16 * gg));
-        }
-      }
-      // A spill used vector memory: drain it here so that afterwards only the
-      // ring's loads are in flight and the stream keeps exact wait counts.
-      if (spilled) __threadfence_block();
-    }
+    for (int j = 1; j < NP; ++j) mx = fmaxf(mx, sc[j] - thr[j]);
+    if (__ballot(mx >= 0.0f)) candidates((v0 + vt) * p.stride, sc);
   };
 
-  // Groups of D stages, so that ring slots and the block -> (tile, block of
-  // tile) map are static.  Every stage: stage data to LDS, reload its ring
-  // slot D stages ahead, one barrier, then all waves consume the stage.
-  for (int64_t j0 = 0; j0 < NB; j0 += GB) {
-    const int64_t jb = wave_uniform(j0);
+  if (ntile > 0) {
+    const int64_t NB = ntile * KBT;
+    const int64_t tstep = p.stride * KBT * kBlockBytes;  // bytes between visited tiles
+    const unsigned char *dbase = static_cast<const unsigned char *>(p.data) + v0 * tstep;
+    const uint32_t voff0 = (uint32_t)lane * 16u, voff1 = voff0 + kBlockBytes;
+    // LDS offset of the ring: the low half of a generic LDS address.
+    const uint32_t ring = (uint32_t)(uintptr_t)smem;
+    // Copy this wave's 2 blocks of stage `st` into ring slot `slot`.
+    auto issue = [&](int64_t st, int slot) {
+      int64_t j = st * SB + wv * 2;
+      j = j < NB - 2 ? j : NB - 2;  // past the end: the last two blocks again
+      const int64_t vt = j / KBT;
+      const unsigned char *src = dbase + vt * tstep + (j - vt * KBT) * kBlockBytes;
+      copy2_to_lds(src, voff0, voff1,
+                   ring + (uint32_t)(slot * SB + wv * 2) * (uint32_t)kBlockBytes);
+    };
 #pragma unroll
-    for (int r = 0; r < D; ++r) {
-      u4 *buf = stage_buf + (size_t)(r & 1) * SB * 64;
+    for (int st = 0; st < S - 1; ++st) issue(st, st);
+    int64_t next_st = S - 1;  // next stage to copy
+    int next_slot = S - 1;    // its ring slot
+    int cur_slot = 0;         // ring slot of the stage being consumed
+    const int64_t ntile_pad = (ntile + TPS - 1) / TPS * TPS;
+    for (int64_t vt = 0; vt < ntile_pad; ++vt) {
 #pragma unroll
-      for (int i = 0; i < LPS; ++i) buf[(wv * LPS + i) * 64 + lane] = ring[r][i];
-#pragma unroll
-      for (int i = 0; i < LPS; ++i)
-        ring[r][i] = __builtin_nontemporal_load(block(jb + GB + r * SB + wv * LPS + i));
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < SB; ++i) {
-        const int j = r * SB + i;  // block of the group (static)
-        const int kb = j % KBT;
-        if (jb + j < NB) {
-          if (kb == 0) {
-#pragma unroll
-            for (int t = 0; t < QTW; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-          }
-          const u4 blk = buf[i * 64 + lane];
-#pragma unroll
-          for (int t = 0; t < QTW; ++t) acc[t] = MfmaMQ<DT>::run(qreg[t][kb], blk, acc[t]);
-          if (kb == KBT - 1) tile_end((v0 + (jb + j) / KBT) * p.stride);
+      for (int c = 0; c < SPT; ++c) {
+        if (TPS == 1 || (vt & (TPS - 1)) == 0) {
+          // Stage start: this wave's copies of it have landed; after the
+          // barrier so have every wave's, and the slot consumed last is free
+          // for the copy S - 1 stages ahead.
+          wait_vmcnt<WAIT>();
+          __syncthreads();
+          issue(next_st, next_slot);
+          ++next_st;
+          next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
         }
+        const u4 *blk =
+            reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes +
+                                         (size_t)((TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * KBT) *
+                                             kBlockBytes) +
+            lane;
+        u4 kv[BPT];
+#pragma unroll
+        for (int i = 0; i < BPT; ++i) kv[i] = blk[i * 64];
+#pragma unroll
+        for (int i = 0; i < BPT; ++i) {
+          const int kb = c * SB + i;
+#pragma unroll
+          for (int t = 0; t < QTW; ++t)
+            acc[t] = MfmaMQ<DT>::run(qreg[t][kb], kv[i],
+                                     kb == 0 ? f4{0.f, 0.f, 0.f, 0.f} : acc[t]);
+        }
+        if (TPS == 1 || (vt & (TPS - 1)) == TPS - 1)  // stage end
+          cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
       }
+      if (vt < ntile) tile_end(vt);
+    }
+    wait_vmcnt<0>();  // no LDS copy may land after the workgroup ends
+  }
+
+  // Publish this wave's lists (one per query per workgroup): cut lists
+  // longer than k to their k best (sorting every list when sort_lists), and
+  // record per list its length (kSortedFlag when sorted), best key (~0 when
+  // unknown, 0 when empty) and k-th key (0 unless it holds k sorted keys).
+  if (cnt > 0) flush();
+  for (int i = 0; i < NQW && q0 + i < B; ++i) {
+    uint64_t *list = list_of(i);
+    const int n = (int)st_cnt[i];
+    uint64_t first = (n == 0) ? 0ull : ~0ull;
+    uint64_t kth = 0ull;
+    uint32_t flag = (n == 1) ? kSortedFlag : 0u;
+    int keep = n;
+    if (n > k || (p.sort_lists && n > 0)) {
+      __threadfence_block();
+      int np2 = 2;
+      while (np2 < n) np2 <<= 1;
+      for (int e = lane; e < np2; e += kWaveSize) scr[e] = (e < n) ? list[e] : 0ull;
+      wave_sync_lds();
+      wave_bitonic_desc(scr, np2, lane);
+      keep = n < k ? n : k;
+      for (int e = lane; e < keep; e += kWaveSize) list[e] = scr[e];
+      first = scr[0];
+      kth = (keep == k) ? scr[k - 1] : 0ull;
+      flag = kSortedFlag;
+      wave_sync_lds();
+    }
+    if (lane == 0) {
+      const size_t o = (size_t)(q0 + i) * G + wg;
+      p.lcnt[o] = (uint32_t)keep | flag;
+      p.lfirst[o] = first;
+      p.lkth[o] = kth;
     }
   }
-
-  // Publish this wave's lists (one per query per workgroup).
-  for (int i = 0; i < NQW && q0 + i < B; ++i) {
-    const size_t o = (size_t)(q0 + i) * G + wg;
-    sink_publish(sink, i, list_of(i), p.sort_lists != 0, p.lcnt + o, p.lfirst + o, p.lkth + o);
-  }
 }
 
-template <int DT, int QTW, int KBT, int CPQ>
+template <int DT, int QTW, int KBT, int CPQ, int S>
 __global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_main(ScanParams p) {
-  scan_mq_body<DT, QTW, KBT, CPQ, true>(p);
+  scan_mq_body<DT, QTW, KBT, CPQ, S>(p);
 }
 
-template <int DT, int QTW, int KBT, int CPQ>
+template <int DT, int QTW, int KBT, int CPQ, int S>
 __global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_sample(ScanParams p) {
-  scan_mq_body<DT, QTW, KBT, CPQ, false>(p);
+  scan_mq_body<DT, QTW, KBT, CPQ, S>(p);
 }
 
-// (QTW, KBT) pairs with QTW * KBT <= 32 (query operands <= 128 VGPRs).
-#define DRESD_MQ_CASE(DT, CPQ, QTW, KBT)                                          \
-  if (qtw == QTW && kbt == KBT)                                                   \
-    return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ>           \
-                     : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ>;
+// (QTW, KBT) pairs with QTW * KBT <= 32 (query operands <= 128 VGPRs), each
+// with its ring depth S.
+#define DRESD_MQ_CASE(DT, CPQ, QTW, KBT, S)                                      \
+  if (qtw == QTW && kbt == KBT) {                                                \
+    *stages = S;                                                                 \
+    return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S>       \
+                     : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S>;    \
+  }
 #define DRESD_MQ_ALL(DT, CPQ)                                                     \
-  DRESD_MQ_CASE(DT, CPQ, 1, 4) DRESD_MQ_CASE(DT, CPQ, 1, 8)                       \
-  DRESD_MQ_CASE(DT, CPQ, 1, 16) DRESD_MQ_CASE(DT, CPQ, 1, 32)                     \
-  DRESD_MQ_CASE(DT, CPQ, 2, 4) DRESD_MQ_CASE(DT, CPQ, 2, 8)                       \
-  DRESD_MQ_CASE(DT, CPQ, 2, 16) DRESD_MQ_CASE(DT, CPQ, 4, 4)                      \
-  DRESD_MQ_CASE(DT, CPQ, 4, 8)
+  DRESD_MQ_CASE(DT, CPQ, 1, 4, 4) DRESD_MQ_CASE(DT, CPQ, 1, 8, 4)                 \
+  DRESD_MQ_CASE(DT, CPQ, 1, 16, 4) DRESD_MQ_CASE(DT, CPQ, 1, 32, 6)               \
+  DRESD_MQ_CASE(DT, CPQ, 2, 4, 4) DRESD_MQ_CASE(DT, CPQ, 2, 8, 4)                 \
+  DRESD_MQ_CASE(DT, CPQ, 2, 16, 6) DRESD_MQ_CASE(DT, CPQ, 4, 4, 4)                \
+  DRESD_MQ_CASE(DT, CPQ, 4, 8, 6)
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
-ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass) {
+ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, int *stages) {
   DRESD_MQ_ALL(kF16, 1)
   return nullptr;
 }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
-ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass) {
+ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, int *stages) {
   DRESD_MQ_ALL(kBF16, 4)
   return nullptr;
 }

@@ -124,6 +124,51 @@ def test_edge_shapes(gpu_lib, dt, N, d, B, k):
     run_case(gpu_lib, x, cont, q, k, dt)
 
 
+# Batches of several 16-column query tiles take the shared-key scan (queries
+# in registers, keys staged through LDS): cover every (query tiles per wave,
+# blocks per key tile) class it has, ragged batches and dims, fewer key tiles
+# than workgroups, k = 1 and large k (list cuts), and both key types.
+MQ_EDGE = [
+    # (dtype, N, d, B, k)
+    ("f16", 777, 128, 50, 10),        # 49 tiles: fewer tiles than workgroups
+    ("f16", 9999, 128, 64, 1),        # k = 1
+    ("f16", 12345, 100, 256, 50),     # ragged dims, 4 tiles per wave, 4 blocks per tile
+    ("f16", 20011, 512, 100, 32),     # 16 blocks per tile
+    ("f16", 30001, 1024, 64, 16),     # 32 blocks per tile
+    ("bf16", 15013, 256, 64, 40),     # three-part bf16 queries, 4 tiles per wave
+    ("bf16", 7001, 128, 13, 9),       # smallest bf16 batch that fills 4 query tiles
+    ("f16", 40009, 256, 200, 1000),   # large k: lists cut to k many times
+]
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", MQ_EDGE, ids=["%s-N%d-d%d-B%d-k%d" % e for e in MQ_EDGE])
+def test_shared_key_scan_shapes(gpu_lib, dt, N, d, B, k):
+    say("shared-key", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N * 5 + d * 11 + B + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 3), generator=gen, dtype=torch.int32)
+    run_case(gpu_lib, x, cont, q, k, dt)
+
+
+def test_shared_key_scan_all_scores_equal(gpu_lib):
+    """Every key identical: every score passes every float threshold, so the
+    candidate buffers overflow on every tile; the result must still be the
+    k lowest rows."""
+    say("all-equal")
+    gen = torch.Generator().manual_seed(11)
+    N, d, B, k = 5003, 128, 64, 20
+    v = torch.randn(d, generator=gen, dtype=torch.float64)
+    x = (v / v.norm()).to(torch.float16).expand(N, d).contiguous()
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.arange(N * 2, dtype=torch.int32).view(N, 2)
+    rep, (gi, gs, gt) = run_case(gpu_lib, x, cont, q, k, "f16")
+    assert (gi == np.arange(k)[None, :]).all()
+
+
 def test_all_negative_scores_never_return_padding(gpu_lib):
     """Keys in one half-space, queries in the other: every score is negative,
     so zero-scoring padding rows of the last tile would win if not masked."""
