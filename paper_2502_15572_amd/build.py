@@ -7,7 +7,9 @@ Usage: python -m paper_2502_15572_amd.build [-v]
 from __future__ import annotations
 
 import concurrent.futures as cf
+import hashlib
 import os
+import shutil
 import subprocess
 import sys
 
@@ -48,17 +50,42 @@ def _compile(hipcc, src, defs, obj, verbose):
     return obj
 
 
-def build(verbose: bool = False, jobs: int | None = None) -> str:
+def _unit_key(src, defs):
+    """Hash of a unit's source, every header it may include, and its flags."""
+    h = hashlib.sha256()
+    h.update(" ".join(HIPCC_FLAGS + list(defs)).encode())
+    for d in (CSRC, os.path.join(ROOT, "include")):
+        for f in sorted(os.listdir(d)):
+            if f.endswith(".h"):
+                h.update(f.encode() + open(os.path.join(d, f), "rb").read())
+    h.update(open(os.path.join(CSRC, src), "rb").read())
+    return h.hexdigest()[:24]
+
+
+def build(verbose: bool = False, jobs: int | None = None, cache_dir: str | None = None) -> str:
+    """Compile every unit and link libdresd.so.  With cache_dir, objects of
+    units whose sources, headers and flags are unchanged are reused."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     tag = "%d" % os.getpid()
     objs = [os.path.join(CSRC, "_%s.%s.o" % (name, tag)) for _, _, name in UNITS]
     jobs = jobs or min(len(UNITS), max(1, (os.cpu_count() or 2)))
+    cached = [None] * len(UNITS)
+    if cache_dir:
+        os.makedirs(cache_dir, exist_ok=True)
+        for i, (src, defs, name) in enumerate(UNITS):
+            c = os.path.join(cache_dir, "%s.%s.o" % (name, _unit_key(src, defs)))
+            cached[i] = c
+            if os.path.exists(c):
+                objs[i] = c
     try:
         with cf.ThreadPoolExecutor(jobs) as ex:
             futs = [ex.submit(_compile, hipcc, src, defs, obj, verbose)
-                    for (src, defs, _), obj in zip(UNITS, objs)]
+                    for (src, defs, _), obj in zip(UNITS, objs) if not obj.startswith(cache_dir or "\0")]
             for f in futs:
                 f.result()
+        for i, c in enumerate(cached):
+            if c and objs[i] != c:
+                shutil.copyfile(objs[i], c)
         tmp = OUT + ".tmp" + tag
         cmd = [hipcc, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp]
         if verbose:
@@ -67,7 +94,7 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
         os.replace(tmp, OUT)
     finally:
         for o in objs:
-            if os.path.exists(o):
+            if os.path.exists(o) and not (cache_dir and o.startswith(cache_dir)):
                 os.remove(o)
     return OUT
 

@@ -17,6 +17,7 @@ constexpr int kWaveSize = 64;
 constexpr int kScanThreads = 256;   // 4 waves per workgroup
 constexpr int kMergeThreads = 1024;
 constexpr int kMergeCap = 4096;     // candidates a merge keeps in LDS
+constexpr int kMergeLists = 4096;   // most candidate lists per query a merge accepts
 #define DRESD_K_MAX_INTERNAL 1024   // equals DRESD_K_MAX of the public header
 
 enum DType { kF32 = 0, kF16 = 1, kBF16 = 2 };
@@ -47,11 +48,12 @@ __host__ __device__ inline size_t scan_wave_bytes(int nq, int cl, int C) {
 // Shared-key scan: a wave's candidate buffer holds kMqCandBuf (key, query)
 // entries; its LDS region is key buffer [kMqCandBuf] u64 | sort scratch [C]
 // u64 | exact thresholds [nqw] u64 | query of each buffered key [kMqCandBuf]
-// u16 | list lengths [nqw] u32 | float thresholds [nqw] f32.
+// u8 | list lengths [nqw] u32 | float thresholds [nqw] f32 | best listed
+// key [nqw] u64.
 constexpr int kMqCandBuf = 256;
 constexpr int kMqStageBlocks = 8;  // 1 KiB key blocks per LDS stage
 __host__ __device__ inline size_t scan_mq_wave_bytes(int nqw, int C) {
-  return ((size_t)kMqCandBuf * 10 + (size_t)C * 8 + (size_t)nqw * 16 + 15) / 16 * 16;
+  return ((size_t)kMqCandBuf * 9 + (size_t)C * 8 + (size_t)nqw * 24 + 15) / 16 * 16;
 }
 __host__ __device__ inline size_t scan_mq_lds_bytes(int stages, int nqw, int C) {
   return (size_t)stages * kMqStageBlocks * kBlockBytes +

@@ -4,41 +4,93 @@
 // Section 3.6), then gathers the winners' continuations -- the value map of
 // the key -> next-tokens datastore.  For a sampled pass it instead emits the
 // k-th best key, a lower bound that prunes the next pass.
+//
+// Latency matters more than throughput here (one short kernel per pass), so
+// every step is one round of independent loads followed by a few barriers:
+// list summaries, then all listed keys at once (flattened over lists), and
+// radix selections that start at the highest bit where the keys differ.
 #include "dresd_device.h"
 
 namespace dresd {
 
 // Candidate counts up to this are sorted whole by one wave.
 constexpr int kSmallMerge = 256;
+// Each thread owns this many lists (their offsets share the histogram).
+constexpr int kListsPerThread = kMergeLists / kMergeThreads;
 
 struct MergeShared {
-  uint32_t hist[4096];
+  uint32_t hist[4096];  // radix histogram; list offsets during the gather
   uint32_t part[kMergeThreads / kWaveSize];
   uint64_t cache[kMergeCap];
   uint64_t win[DRESD_K_MAX_INTERNAL];
-  uint64_t sel_prefix, sel_mask, bound;
-  uint32_t sel_krem, sel_done, win_cnt, ncand;
+  uint64_t sel_prefix, sel_mask, bound, v_and, v_or;
+  uint32_t sel_krem, sel_done, win_cnt, ncand, total, any_known;
+  int sel_top;
 };
 
+__device__ inline uint64_t wave_and(uint64_t v) {
+  for (int off = 32; off > 0; off >>= 1) v &= __shfl_xor(v, off, kWaveSize);
+  return v;
+}
+__device__ inline uint64_t wave_or(uint64_t v) {
+  for (int off = 32; off > 0; off >>= 1) v |= __shfl_xor(v, off, kWaveSize);
+  return v;
+}
+__device__ inline uint64_t wave_max(uint64_t v) {
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t o = __shfl_xor(v, off, kWaveSize);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
 // Largest value v such that at least kk of the M values src(i) are >= v
-// (the kk-th largest value; 1 <= kk <= M), by radix selection 12 bits at a
-// time from the top.  Called by the whole workgroup.
+// (1 <= kk <= M; the kk-th largest value, or a lower boundary of the digit
+// bin holding exactly the kk largest values).  Radix selection 12 bits at a
+// time from the highest bit in which the values differ.  Called by the whole
+// workgroup.
 template <class Src>
 __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk) {
   constexpr int BPT = 4096 / kMergeThreads;  // histogram bins per thread
   const int tid = threadIdx.x, nth = blockDim.x;
   const int lane = tid & (kWaveSize - 1), wid = tid / kWaveSize;
   if (tid == 0) {
-    sh.sel_prefix = 0;
-    sh.sel_mask = 0;
-    sh.sel_krem = kk;
-    sh.sel_done = 0;
+    sh.v_and = ~0ull;
+    sh.v_or = 0ull;
   }
   __syncthreads();
-  const int shifts[6] = {52, 40, 28, 16, 4, 0};
-  for (int di = 0; di < 6 && !sh.sel_done; ++di) {
-    const int s = shifts[di];
-    const uint32_t wmask = (di == 5) ? 0xFu : 0xFFFu;
+  uint64_t va = ~0ull, vo = 0ull;
+  for (uint32_t i = tid; i < M; i += nth) {
+    const uint64_t key = src(i);
+    va &= key;
+    vo |= key;
+  }
+  va = wave_and(va);
+  vo = wave_or(vo);
+  if (lane == 0) {
+    atomicAnd((unsigned long long *)&sh.v_and, (unsigned long long)va);
+    atomicOr((unsigned long long *)&sh.v_or, (unsigned long long)vo);
+  }
+  __syncthreads();
+  const uint64_t diff = sh.v_and ^ sh.v_or;
+  if (diff == 0) return sh.v_or;  // one distinct value
+  const int top0 = 63 - __clzll((long long)diff);
+  const uint64_t above = (top0 == 63) ? 0ull : ~((2ull << top0) - 1ull);
+  __syncthreads();
+  if (tid == 0) {
+    sh.sel_prefix = sh.v_and & above;
+    sh.sel_mask = above;
+    sh.sel_krem = kk;
+    sh.sel_done = 0;
+    sh.sel_top = top0;
+  }
+  __syncthreads();
+  for (;;) {
+    const int top = sh.sel_top;
+    if (sh.sel_done || top < 0) break;
+    const int w = top + 1 < 12 ? top + 1 : 12;
+    const int s = top + 1 - w;
+    const uint32_t wmask = (1u << w) - 1u;
     for (int i = tid; i < 4096; i += nth) sh.hist[i] = 0;
     __syncthreads();
     const uint64_t pre = sh.sel_prefix, pm = sh.sel_mask;
@@ -47,7 +99,7 @@ __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk)
       if ((key & pm) == pre) atomicAdd(&sh.hist[(uint32_t)(key >> s) & wmask], 1u);
     }
     __syncthreads();
-    // Suffix sums: thread t owns bins [BPT t, BPT t + BPT); `above` = count in
+    // Suffix sums: thread t owns bins [BPT t, BPT t + BPT); `cnt_above` = count in
     // the bins of all higher threads (lanes scan within the wave, then the
     // waves' totals are summed from LDS).
     uint32_t mine = 0;
@@ -60,12 +112,12 @@ __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk)
     if (lane == 0) sh.part[wid] = incl;
     __syncthreads();
     uint32_t later = 0;
-    for (int w = wid + 1; w < nth / kWaveSize; ++w) later += sh.part[w];
+    for (int q = wid + 1; q < nth / kWaveSize; ++q) later += sh.part[q];
     const uint32_t krem = sh.sel_krem;
-    const uint32_t above = later + incl - mine;
+    const uint32_t cnt_above = later + incl - mine;
     __syncthreads();
-    if (above < krem && krem <= above + mine) {
-      uint32_t cum = above;
+    if (cnt_above < krem && krem <= cnt_above + mine) {
+      uint32_t cum = cnt_above;
       for (int jb = BPT - 1; jb >= 0; --jb) {
         const uint32_t h = sh.hist[tid * BPT + jb];
         if (cum + h >= krem) {
@@ -73,6 +125,7 @@ __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk)
           sh.sel_prefix = pre | ((uint64_t)dg << s);
           sh.sel_mask = pm | ((uint64_t)wmask << s);
           sh.sel_krem = krem - cum;
+          sh.sel_top = s - 1;
           if (h == krem - cum) sh.sel_done = 1u;  // the whole bin is in
           break;
         }
@@ -122,7 +175,7 @@ __device__ inline void write_result(const MergeParams &p, int b, const uint64_t 
 //    largest of the lists' known best keys -- k distinct listed keys reach
 //    each, and the answer is among the listed keys.
 // 2. Candidates: listed keys at or above the bound; lists whose best key is
-//    below it are not opened, sorted lists stop at their first key under it.
+//    below it are not opened.  All kept lists' keys are loaded at once.
 // 3. The k best candidates: one wave sorts them when few, else a radix
 //    select finds the k-th and the keys at or above it are sorted.
 __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
@@ -130,6 +183,7 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int nth = blockDim.x;
+  const int lane = tid & (kWaveSize - 1), wid = tid / kWaveSize;
   const int G = p.G;
   const uint32_t *lcnt = p.lcnt + (size_t)b * G;
   const uint64_t *lkth = p.lkth + (size_t)b * G;
@@ -140,51 +194,81 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
     sh.bound = 0;
     sh.ncand = 0;
     sh.win_cnt = 0;
-  }
-  // (a) and the known best keys (0 for empty lists and unknown ones)
-  uint64_t mb = 0;
-  const bool first_in_lds = G <= kMergeCap;
-  for (int w = tid; w < G; w += nth) {
-    const uint64_t v = lkth[w];
-    mb = v > mb ? v : mb;
-    if (first_in_lds) {
-      const uint64_t f = lfirst[w];
-      sh.cache[w] = (f == ~0ull) ? 0ull : f;
-    }
+    sh.any_known = 0;
   }
   __syncthreads();
-  if (mb) atomicMax((unsigned long long *)&sh.bound, (unsigned long long)mb);
-  // (b)
-  if (G >= p.k) {
-    uint64_t t1;
-    if (first_in_lds) {
-      t1 = radix_kth(sh, [&](uint32_t i) { return sh.cache[i]; }, (uint32_t)G, (uint32_t)p.k);
-    } else {
-      t1 = radix_kth(
-          sh, [&](uint32_t i) { const uint64_t f = lfirst[i]; return f == ~0ull ? 0ull : f; },
-          (uint32_t)G, (uint32_t)p.k);
+  // Thread t owns lists [L t, L t + L), L = kListsPerThread.
+  uint32_t cnt[kListsPerThread];
+  uint64_t first[kListsPerThread];
+  uint64_t mb = 0;
+  bool known = false;
+#pragma unroll
+  for (int j = 0; j < kListsPerThread; ++j) {
+    const int w = tid * kListsPerThread + j;
+    cnt[j] = 0;
+    first[j] = 0;
+    if (w < G) {
+      cnt[j] = lcnt[w] & ~kSortedFlag;
+      first[j] = lfirst[w];
+      const uint64_t v = lkth[w];
+      mb = v > mb ? v : mb;
+      const uint64_t f = first[j];
+      sh.cache[w] = (f == ~0ull) ? 0ull : f;
+      known |= (f != ~0ull && f != 0ull);
     }
+  }
+  mb = wave_max(mb);
+  if (lane == 0 && mb) atomicMax((unsigned long long *)&sh.bound, (unsigned long long)mb);
+  if (known) sh.any_known = 1u;
+  __syncthreads();
+  // (b), worth a selection only when some list's best key is known
+  if (sh.any_known && G >= p.k) {
+    const uint64_t t1 =
+        radix_kth(sh, [&](uint32_t i) { return sh.cache[i]; }, (uint32_t)G, (uint32_t)p.k);
     if (tid == 0 && t1 > sh.bound) sh.bound = t1;
   }
   __syncthreads();
   const uint64_t bnd = sh.bound;
 
-  // 2. gather the candidates
-  for (int w = tid; w < G; w += nth) {
-    if (lfirst[w] < bnd) continue;
-    uint32_t c = lcnt[w];
-    const bool sorted = (c & kSortedFlag) != 0;
-    c &= ~kSortedFlag;
-    const uint64_t *l = lists + (size_t)w * p.C;
-    for (uint32_t e = 0; e < c; ++e) {
-      const uint64_t key = l[e];
-      if (key >= bnd) {
-        const uint32_t at = atomicAdd(&sh.ncand, 1u);
-        if (at < (uint32_t)kMergeCap) sh.cache[at] = key;
-        else if ((int64_t)(at - kMergeCap) < p.spill_cap) spill[at - kMergeCap] = key;
-      } else if (sorted) {
-        break;
-      }
+  // 2. offsets of the kept lists' keys (lists at or above the bound), then
+  //    every key loaded by its own thread
+  uint32_t mine = 0;
+#pragma unroll
+  for (int j = 0; j < kListsPerThread; ++j) {
+    if (first[j] < bnd) cnt[j] = 0;
+    mine += cnt[j];
+  }
+  uint32_t incl = mine;
+  for (int off = 1; off < kWaveSize; off <<= 1) {
+    const uint32_t v = __shfl_up(incl, off, kWaveSize);
+    if (lane >= off) incl += v;
+  }
+  if (lane == kWaveSize - 1) sh.part[wid] = incl;
+  __syncthreads();
+  uint32_t base = incl - mine;
+  for (int q = 0; q < wid; ++q) base += sh.part[q];
+#pragma unroll
+  for (int j = 0; j < kListsPerThread; ++j) {
+    sh.hist[tid * kListsPerThread + j] = base;
+    base += cnt[j];
+  }
+  if (tid == nth - 1) sh.total = base;
+  __syncthreads();
+  const uint32_t total = sh.total;
+  const int nl = G;
+  for (uint32_t i = tid; i < total; i += nth) {
+    // the last list whose offset is <= i holds key i
+    int lo = 0, hi = nl;  // answer in [lo, hi)
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (sh.hist[mid] <= i) lo = mid;
+      else hi = mid;
+    }
+    const uint64_t key = lists[(size_t)lo * p.C + (i - sh.hist[lo])];
+    if (key >= bnd) {
+      const uint32_t at = atomicAdd(&sh.ncand, 1u);
+      if (at < (uint32_t)kMergeCap) sh.cache[at] = key;
+      else if ((int64_t)(at - kMergeCap) < p.spill_cap) spill[at - kMergeCap] = key;
     }
   }
   __threadfence_block();

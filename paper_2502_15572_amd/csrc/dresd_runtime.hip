@@ -182,8 +182,11 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
   // HBM busy, and few enough per-wave lists for the merge to keep their
   // best keys in LDS.
   pl.wg_max = ix->cus * std::min(occ, kMaxScanWgPerCu);
-  // lists per query: one per wave, or one per workgroup for the shared-key scan
-  pl.G_max = pl.mq ? pl.wg_max : pl.wg_max * (kScanThreads / kWaveSize);
+  // lists per query: one per wave, or one per workgroup for the shared-key
+  // scan; at most kMergeLists
+  const int lists_per_wg = pl.mq ? 1 : kScanThreads / kWaveSize;
+  pl.wg_max = std::min(pl.wg_max, kMergeLists / lists_per_wg);
+  pl.G_max = pl.wg_max * lists_per_wg;
   // Small batches: every wave keeps its own running top-k and sorts it at
   // the end; the merge then prunes with the best per-wave k-th key.  Larger
   // batches first set per-query thresholds from sampled passes over tiles

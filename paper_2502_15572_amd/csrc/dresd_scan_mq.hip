@@ -41,21 +41,34 @@ struct MfmaMQ<kBF16> {
 
 // A-operand chunk of column `col` for dims [dim0, dim0+8): CPQ = 1 rounds the
 // query once to the key type; CPQ = 4 gives three parts summing to it exactly
-// (f16 lower parts scaled by 2^11, 2^22) and a zero column.
+// (f16 lower parts scaled by 2^11, 2^22) and a zero column.  `vec`: rows of
+// q start 16-byte aligned, so a whole chunk is two 16-byte loads.
 template <int DT, int CPQ>
-__device__ __forceinline__ u4 query_chunk_mq(const float *q, int d, int B, int col, int dim0) {
+__device__ __forceinline__ u4 query_chunk_mq(const float *q, int d, int B, int col, int dim0,
+                                             bool vec) {
   const int b = col / CPQ;
   const int h = col % CPQ;
+  float x[8];
+  if (vec && b < B && dim0 + 8 <= d) {
+    const float4 *src = reinterpret_cast<const float4 *>(q + (int64_t)b * d + dim0);
+    const float4 lo4 = src[0], hi4 = src[1];
+    x[0] = lo4.x, x[1] = lo4.y, x[2] = lo4.z, x[3] = lo4.w;
+    x[4] = hi4.x, x[5] = hi4.y, x[6] = hi4.z, x[7] = hi4.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int dim = dim0 + e;
+      x[e] = (b < B && dim < d) ? q[(int64_t)b * d + dim] : 0.0f;
+    }
+  }
   uint16_t v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const int dim = dim0 + e;
-    const float x = (b < B && dim < d) ? q[(int64_t)b * d + dim] : 0.0f;
     if (DT == kF16) {
-      _Float16 hi = (_Float16)x;
+      _Float16 hi = (_Float16)x[e];
       _Float16 r = hi;
       if (CPQ == 4) {
-        float r1 = x - (float)hi;
+        float r1 = x[e] - (float)hi;
         _Float16 mid = (_Float16)(r1 * 2048.0f);
         float r2 = r1 - (float)mid * (1.0f / 2048.0f);
         _Float16 lo = (_Float16)(r2 * 4194304.0f);
@@ -63,8 +76,8 @@ __device__ __forceinline__ u4 query_chunk_mq(const float *q, int d, int B, int c
       }
       v[e] = __builtin_bit_cast(uint16_t, r);
     } else {
-      __bf16 hi = (__bf16)x;
-      float r1 = x - (float)hi;
+      __bf16 hi = (__bf16)x[e];
+      float r1 = x[e] - (float)hi;
       __bf16 mid = (__bf16)r1;
       __bf16 lo = (__bf16)(r1 - (float)mid);
       __bf16 r = (h == 0) ? hi : (h == 1) ? mid : (h == 2) ? lo : (__bf16)0.0f;
@@ -133,19 +146,21 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   uint64_t *ck = reinterpret_cast<uint64_t *>(w0);  // buffered keys [CB]
   uint64_t *scr = ck + CB;                          // sort scratch [C]
   uint64_t *st_key = scr + C;                       // keep keys > st_key [NQW]
-  uint16_t *cq = reinterpret_cast<uint16_t *>(st_key + NQW);  // query of ck[e] [CB]
+  uint8_t *cq = reinterpret_cast<uint8_t *>(st_key + NQW);    // query of ck[e] [CB]
   uint32_t *st_cnt = reinterpret_cast<uint32_t *>(cq + CB);   // HBM list length [NQW]
   float *st_thr = reinterpret_cast<float *>(st_cnt + NQW);    // float threshold [NQW]
+  uint64_t *st_max = reinterpret_cast<uint64_t *>(st_thr + NQW);  // best listed key [NQW]
 
   // Queries of this wave: tiles [wv*QTW, wv*QTW + QTW) of the batch.
   const int q0 = wv * NQW;
+  const bool qvec = (((uintptr_t)p.queries & 15u) == 0) && ((p.d & 3) == 0);
   u4 qreg[QTW][KBT];
 #pragma unroll
   for (int t = 0; t < QTW; ++t)
 #pragma unroll
     for (int kb = 0; kb < KBT; ++kb)
       qreg[t][kb] = query_chunk_mq<DT, CPQ>(p.queries, p.d, B, (wv * QTW + t) * 16 + m,
-                                            kb * 32 + g * 8);
+                                            kb * 32 + g * 8, qvec);
   for (int i = lane; i < NQW; i += kWaveSize) {
     uint64_t tk = 0;
     float tf = -__builtin_inff();
@@ -159,6 +174,7 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     st_key[i] = tk;
     st_cnt[i] = 0;
     st_thr[i] = tf;
+    st_max[i] = 0;
   }
   wave_sync_lds();
   // Score slot j = t * NS + s of a lane belongs to query t * QPT + g * NS + s.
@@ -204,7 +220,10 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
       while (__ballot(has)) {
         const uint32_t pos = has ? atomicAdd(&st_cnt[q], 1u) : 0u;
         const bool over = has && pos >= (uint32_t)C;
-        if (has && !over) list_of(q)[pos] = key;
+        if (has && !over) {
+          list_of(q)[pos] = key;
+          atomicMax((unsigned long long *)&st_max[q], (unsigned long long)key);
+        }
         uint64_t om = __ballot(over);
         if (om == 0) break;
         if (over) st_cnt[q] = (uint32_t)C;
@@ -228,36 +247,67 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   const int64_t ntile = v1 - v0;
   f4 acc[QTW];
 
+  // Lanes below this one holding a set bit of mask `mk`.
+  auto rank_in = [&](uint64_t mk) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u));
+  };
+
   // Buffer the candidates of key tile `tile` (rows tile*16 .. +15); rare.
-  auto candidates = [&](int64_t tile, const float (&sc)[NP]) {
+  // Bit t of hit_t: some score of query tile t reached its threshold.
+  auto candidates = [&](int64_t tile, const float (&sc)[NP], uint32_t hit_t) {
     const int64_t row64 = tile * kTileRows + m;
     const bool row_ok = row64 < p.N;
     const uint32_t row = (uint32_t)row64;
-    const uint64_t below = (1ull << lane) - 1ull;
-    uint32_t done = 0;  // slots already buffered
-    for (;;) {
-      bool stalled = false;
+    // Count first, so that at most one flush makes room for the whole tile.
+    auto count = [&]() {
+      int n = 0;
+#pragma unroll
+      for (int j = 0; j < NP; ++j)
+        if (hit_t & (1u << (j / NS))) n += __popcll(__ballot(row_ok && sc[j] >= thr[j]));
+      return n;
+    };
+    int n = count();
+    if (cnt + n > CB) {
+      flush();
+      n = count();
+    }
+    if (cnt + n <= CB) {
 #pragma unroll
       for (int j = 0; j < NP; ++j) {
-        if (!(done & (1u << j))) {
-          const bool h = row_ok && sc[j] >= thr[j];
-          const uint64_t mk = __ballot(h);
-          const int n = __popcll(mk);
-          if (cnt + n <= CB) {
-            if (h) {
-              const int at = cnt + __popcll(mk & below);
-              ck[at] = make_key(sc[j], row);
-              cq[at] = (uint16_t)((j / NS) * QPT + g * NS + (j % NS));
-            }
-            cnt += n;
-            done |= 1u << j;
-          } else {
-            stalled = true;
-          }
+        if (!(hit_t & (1u << (j / NS)))) continue;
+        const bool h = row_ok && sc[j] >= thr[j];
+        const uint64_t mk = __ballot(h);
+        if (mk == 0) continue;
+        if (h) {
+          const int at = cnt + rank_in(mk);
+          ck[at] = make_key(sc[j], row);
+          cq[at] = (uint8_t)((j / NS) * QPT + g * NS + (j % NS));
         }
+        cnt += __popcll(mk);
       }
-      if (!stalled) break;
-      flush();  // at least one more slot fits afterwards
+    } else {
+      // More candidates than the buffer holds (thresholds still low): one
+      // slot at a time with a flush whenever the next one does not fit.
+      // Slot j's score is rotated into cur[0] (no indexed register access).
+      float cur[NP];
+#pragma unroll
+      for (int j = 0; j < NP; ++j) cur[j] = sc[j];
+#pragma unroll 1
+      for (int j = 0; j < NP; ++j) {
+        const int qi = (j / NS) * QPT + g * NS + (j % NS);
+        if (cnt + __popcll(__ballot(row_ok && cur[0] >= st_thr[qi])) > CB) flush();
+        const bool h = row_ok && cur[0] >= st_thr[qi];
+        const uint64_t mk = __ballot(h);
+        if (h) {
+          const int at = cnt + rank_in(mk);
+          ck[at] = make_key(cur[0], row);
+          cq[at] = (uint8_t)qi;
+        }
+        cnt += __popcll(mk);
+#pragma unroll
+        for (int i = 0; i + 1 < NP; ++i) cur[i] = cur[i + 1];
+      }
     }
   };
 
@@ -276,10 +326,23 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
         sc[t * NS + s] = v;
       }
     // v >= thr exactly when v - thr >= 0 (round-to-nearest keeps the sign).
-    float mx = sc[0] - thr[0];
+    float mt[QTW];
 #pragma unroll
-    for (int j = 1; j < NP; ++j) mx = fmaxf(mx, sc[j] - thr[j]);
-    if (__ballot(mx >= 0.0f)) candidates((v0 + vt) * p.stride, sc);
+    for (int t = 0; t < QTW; ++t) {
+      mt[t] = sc[t * NS] - thr[t * NS];
+#pragma unroll
+      for (int s = 1; s < NS; ++s) mt[t] = fmaxf(mt[t], sc[t * NS + s] - thr[t * NS + s]);
+    }
+    float mx = mt[0];
+#pragma unroll
+    for (int t = 1; t < QTW; ++t) mx = fmaxf(mx, mt[t]);
+    if (__ballot(mx >= 0.0f)) {
+      uint32_t hit_t = 0;
+#pragma unroll
+      for (int t = 0; t < QTW; ++t)
+        if (__ballot(mt[t] >= 0.0f)) hit_t |= 1u << t;
+      candidates((v0 + vt) * p.stride, sc, hit_t);
+    }
   };
 
   if (ntile > 0) {
@@ -341,37 +404,44 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     wait_vmcnt<0>();  // no LDS copy may land after the workgroup ends
   }
 
-  // Publish this wave's lists (one per query per workgroup): cut lists
-  // longer than k to their k best (sorting every list when sort_lists), and
-  // record per list its length (kSortedFlag when sorted), best key (~0 when
-  // unknown, 0 when empty) and k-th key (0 unless it holds k sorted keys).
+  // Publish this wave's lists (one per query per workgroup) and per list its
+  // length (kSortedFlag when sorted), best key (0 when empty) and k-th key (0
+  // unless it holds k sorted keys).  Lane i takes query i; lists longer than
+  // k (every non-empty list when sort_lists) are sorted and cut to k first.
   if (cnt > 0) flush();
-  for (int i = 0; i < NQW && q0 + i < B; ++i) {
-    uint64_t *list = list_of(i);
-    const int n = (int)st_cnt[i];
-    uint64_t first = (n == 0) ? 0ull : ~0ull;
-    uint64_t kth = 0ull;
-    uint32_t flag = (n == 1) ? kSortedFlag : 0u;
-    int keep = n;
-    if (n > k || (p.sort_lists && n > 0)) {
+  static_assert(NQW <= kWaveSize, "one lane per query");
+  {
+    const int i = lane;
+    const bool valid = i < NQW && q0 + i < B;
+    const int n = valid ? (int)st_cnt[i] : 0;
+    const bool sort_me = valid && (n > k || (p.sort_lists && n > 0));
+    if (valid && !sort_me) {
+      const size_t o = (size_t)(q0 + i) * G + wg;
+      p.lcnt[o] = (uint32_t)n | ((n == 1) ? kSortedFlag : 0u);
+      p.lfirst[o] = (n == 0) ? 0ull : st_max[i];
+      p.lkth[o] = 0ull;
+    }
+    uint64_t todo = __ballot(sort_me);
+    while (todo) {
+      const int qi = __ffsll((long long)todo) - 1;
+      todo &= todo - 1;
+      uint64_t *list = list_of(qi);
+      const int nq = __builtin_amdgcn_readlane(n, qi);
       __threadfence_block();
       int np2 = 2;
-      while (np2 < n) np2 <<= 1;
-      for (int e = lane; e < np2; e += kWaveSize) scr[e] = (e < n) ? list[e] : 0ull;
+      while (np2 < nq) np2 <<= 1;
+      for (int e = lane; e < np2; e += kWaveSize) scr[e] = (e < nq) ? list[e] : 0ull;
       wave_sync_lds();
       wave_bitonic_desc(scr, np2, lane);
-      keep = n < k ? n : k;
+      const int keep = nq < k ? nq : k;
       for (int e = lane; e < keep; e += kWaveSize) list[e] = scr[e];
-      first = scr[0];
-      kth = (keep == k) ? scr[k - 1] : 0ull;
-      flag = kSortedFlag;
+      if (lane == 0) {
+        const size_t o = (size_t)(q0 + qi) * G + wg;
+        p.lcnt[o] = (uint32_t)keep | kSortedFlag;
+        p.lfirst[o] = scr[0];
+        p.lkth[o] = (keep == k) ? scr[k - 1] : 0ull;
+      }
       wave_sync_lds();
-    }
-    if (lane == 0) {
-      const size_t o = (size_t)(q0 + i) * G + wg;
-      p.lcnt[o] = (uint32_t)keep | flag;
-      p.lfirst[o] = first;
-      p.lkth[o] = kth;
     }
   }
 }
