@@ -36,6 +36,16 @@ struct ScanParams {
   int B, d, KB, k, C, G;     // batch, dims, blocks per tile, k, list capacity, lists
   int CL;                    // per-query LDS stage in front of each HBM list
   int sort_lists;            // sort every list at the end (small batches)
+  const void *qop;           // shared-key scan: query operands [tiles][KB][64] x 16 B
+};
+
+// Query operands of the shared-key scan, built once per search: chunk
+// (t, kb, lane) is the MFMA A operand of lane `lane` for query tile t and
+// 32-dim block kb (columns past the batch are zero).
+struct QopParams {
+  const float *queries;      // [B, d] fp32
+  void *out;                 // [ntile][KB][64] x 16 B
+  int B, d, KB, ntile;
 };
 
 // LDS bytes of one wave's candidate state in the single-tile scan: staged
@@ -99,6 +109,13 @@ inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, in
   if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass, stages);
   if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass, stages);
   return nullptr;
+}
+// Query-operand kernel of the shared-key scan for a key type (launch with
+// 256 threads, one thread per 16-byte chunk).
+void *qop_kernel_f16();
+void *qop_kernel_bf16();
+inline void *qop_kernel(int dtype) {
+  return dtype == kF16 ? qop_kernel_f16() : dtype == kBF16 ? qop_kernel_bf16() : nullptr;
 }
 void *merge_kernel_ptr();
 void *layout_kernel_ptr(int dtype);

@@ -83,6 +83,7 @@ struct Plan {
   int64_t spill_cap = 0;        // merge candidates per query beyond its LDS cache
   bool sort_lists = false;
   size_t off_tau = 0, off_lcnt = 0, off_lkth = 0, off_lfirst = 0, off_lists = 0, off_spill = 0;
+  size_t off_qop = 0;               // shared-key scan: query operands of a group
   size_t bytes = 0;
 };
 
@@ -190,14 +191,21 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
   // Small batches: every wave keeps its own running top-k and sorts it at
   // the end; the merge then prunes with the best per-wave k-th key.  Larger
   // batches first set per-query thresholds from sampled passes over tiles
-  // j*P (kept when they hold at least 4k rows and are at most a quarter of
-  // the tiles), so the main pass lists only a few candidates per wave.
+  // j*P, sparsest first (kept when they hold at least 4k rows and are at
+  // most a quarter of the tiles).  A pass at stride P leaves about P*k
+  // candidates per query for the next one, so batches with many
+  // (query, rank) pairs add a denser level: its extra sampled scan costs less
+  // than the candidates it removes from the full pass.
   pl.sort_lists = B <= 8;
-  if (!pl.sort_lists)
-    for (int64_t P : {(int64_t)4096, (int64_t)64}) {
+  if (!pl.sort_lists) {
+    const bool dense = (int64_t)B * k >= 8192;
+    const std::vector<int64_t> ladder =
+        dense ? std::vector<int64_t>{4096, 256, 16} : std::vector<int64_t>{4096, 64};
+    for (int64_t P : ladder) {
       int64_t nv = ceil_div(ix->T, P);
       if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides.push_back(P);
     }
+  }
   // Lists end with at most k keys each, so a query never has more than
   // G_max * k merge candidates.
   pl.spill_cap = std::max<int64_t>(0, (int64_t)pl.G_max * k - kMergeCap);
@@ -209,7 +217,8 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
   pl.off_lfirst = pl.off_lkth + up(nb * pl.G_max * 8);
   pl.off_lists = pl.off_lfirst + up(nb * pl.G_max * 8);
   pl.off_spill = pl.off_lists + up(nb * pl.G_max * pl.C * 8);
-  pl.bytes = pl.off_spill + up(nb * (size_t)std::max<int64_t>(1, pl.spill_cap) * 8);
+  pl.off_qop = pl.off_spill + up(nb * (size_t)std::max<int64_t>(1, pl.spill_cap) * 8);
+  pl.bytes = pl.off_qop + (pl.mq ? up((size_t)pl.qt * ix->KB * kBlockBytes) : 0);
   return DRESD_OK;
 }
 
@@ -428,6 +437,21 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
     sp.k = k;
     sp.C = pl.C;
     sp.CL = pl.CL;
+    sp.qop = nullptr;
+    if (pl.mq) {
+      QopParams qp;
+      qp.queries = sp.queries;
+      qp.out = ix->ws + pl.off_qop;
+      qp.B = gr.nb;
+      qp.d = ix->d;
+      qp.KB = ix->KB;
+      qp.ntile = pl.qt;
+      void *qargs[] = {&qp};
+      const int64_t chunks = (int64_t)pl.qt * ix->KB * 64;
+      DRESD_HIP(hipLaunchKernel(qop_kernel(ix->dtype), dim3((unsigned)ceil_div(chunks, 256)),
+                                dim3(256), qargs, 0, st));
+      sp.qop = qp.out;
+    }
     MergeParams mp;
     mp.lists = lists;
     mp.lcnt = lcnt;

@@ -108,6 +108,10 @@ __device__ __forceinline__ void copy2_to_lds(const void *src, uint32_t voff0, ui
       : "memory");
 }
 
+// s_waitcnt immediate that waits for vmcnt == 0 only (gfx9 encoding: vmcnt
+// bits [3:0] and [15:14], expcnt [6:4] and lgkmcnt [11:8] at their maxima).
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 // Wait until at most N of this wave's vector memory operations are pending
 // (they complete in issue order).
 template <int N>
@@ -153,14 +157,16 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
 
   // Queries of this wave: tiles [wv*QTW, wv*QTW + QTW) of the batch.
   const int q0 = wv * NQW;
-  const bool qvec = (((uintptr_t)p.queries & 15u) == 0) && ((p.d & 3) == 0);
+  const u4 *qop = static_cast<const u4 *>(p.qop) + lane;
   u4 qreg[QTW][KBT];
 #pragma unroll
   for (int t = 0; t < QTW; ++t)
 #pragma unroll
-    for (int kb = 0; kb < KBT; ++kb)
-      qreg[t][kb] = query_chunk_mq<DT, CPQ>(p.queries, p.d, B, (wv * QTW + t) * 16 + m,
-                                            kb * 32 + g * 8, qvec);
+    for (int kb = 0; kb < KBT; ++kb) qreg[t][kb] = qop[((wv * QTW + t) * KBT + kb) * 64];
+  // Wait for these loads here: left to the compiler, the wait lands at their
+  // first use inside the stream loop, where (not knowing the LDS copies are
+  // younger) it would drain the whole copy ring on every stage.
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   for (int i = lane; i < NQW; i += kWaveSize) {
     uint64_t tk = 0;
     float tf = -__builtin_inff();
@@ -456,6 +462,19 @@ __global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_sample(ScanParam
   scan_mq_body<DT, QTW, KBT, CPQ, S>(p);
 }
 
+// One thread per 16-byte chunk (t, kb, lane) of the query operands.
+template <int DT, int CPQ>
+__global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= (int64_t)p.ntile * p.KB * 64) return;
+  const int lane = (int)(c & 63);
+  const int kb = (int)((c >> 6) % p.KB);
+  const int t = (int)((c >> 6) / p.KB);
+  const bool vec = (((uintptr_t)p.queries & 15u) == 0) && ((p.d & 3) == 0);
+  static_cast<u4 *>(p.out)[c] = query_chunk_mq<DT, CPQ>(p.queries, p.d, p.B, t * 16 + (lane & 15),
+                                                        kb * 32 + (lane >> 4) * 8, vec);
+}
+
 // (QTW, KBT) pairs with QTW * KBT <= 32 (query operands <= 128 VGPRs), each
 // with its ring depth S.
 #define DRESD_MQ_CASE(DT, CPQ, QTW, KBT, S)                                      \
@@ -476,12 +495,14 @@ ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, int *stages) {
   DRESD_MQ_ALL(kF16, 1)
   return nullptr;
 }
+void *qop_kernel_f16() { return (void *)dresd_query_operand<kF16, 1>; }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
 ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, int *stages) {
   DRESD_MQ_ALL(kBF16, 4)
   return nullptr;
 }
+void *qop_kernel_bf16() { return (void *)dresd_query_operand<kBF16, 4>; }
 #endif
 
 }  // namespace dresd
