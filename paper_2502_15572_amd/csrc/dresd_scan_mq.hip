@@ -391,16 +391,34 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
                                          (size_t)((TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * KBT) *
                                              kBlockBytes) +
             lane;
-        u4 kv[BPT];
+        // Two blocks at a time, the next two read from LDS while the
+        // matrix cores work on these (the read latency is exposed once per
+        // stage instead of once per pair).
+        u4 kv0 = blk[0], kv1 = blk[64];
 #pragma unroll
-        for (int i = 0; i < BPT; ++i) kv[i] = blk[i * 64];
-#pragma unroll
-        for (int i = 0; i < BPT; ++i) {
+        for (int i = 0; i < BPT; i += 2) {
+          u4 nx0 = kv0, nx1 = kv1;
+          if (i + 2 < BPT) {
+            nx0 = blk[(i + 2) * 64];
+            nx1 = blk[(i + 3) * 64];
+          }
           const int kb = c * SB + i;
 #pragma unroll
           for (int t = 0; t < QTW; ++t)
-            acc[t] = MfmaMQ<DT>::run(qreg[t][kb], kv[i],
-                                     kb == 0 ? f4{0.f, 0.f, 0.f, 0.f} : acc[t]);
+            acc[t] = MfmaMQ<DT>::run(qreg[t][kb], kv0, kb == 0 ? f4{0.f, 0.f, 0.f, 0.f} : acc[t]);
+#pragma unroll
+          for (int t = 0; t < QTW; ++t) acc[t] = MfmaMQ<DT>::run(qreg[t][kb + 1], kv1, acc[t]);
+          kv0 = nx0;
+          kv1 = nx1;
+        }
+        // Keep that order through instruction scheduling: the first two
+        // reads, then per pair of blocks the next two reads and the pair's
+        // matrix instructions.
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+        for (int i = 0; i < BPT; i += 2) {
+          if (i + 2 < BPT) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * QTW, 0);
         }
         if (TPS == 1 || (vt & (TPS - 1)) == TPS - 1)  // stage end
           cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
