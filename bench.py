@@ -25,7 +25,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}
-KERNEL_SRC = os.path.join(ROOT, "paper_2502_15572_amd", "csrc", "dresd_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2502_15572_amd", "csrc")
 DEFAULT_WORKLOAD = "hidden1m_d4096_bf16"
 
 
@@ -34,7 +34,13 @@ def log(*a):
 
 
 def kernel_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    """Hash of every kernel source and header (a counter summary is valid
+    only for the code it was taken on)."""
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode() + open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def read_traffic(workload: str, batch: int):
@@ -166,6 +172,10 @@ def main():
     achieved = scan_bytes / (scan_ms * 1e-3) / 1e9
     flops = 2.0 * w.N * w.d * B
     plan = ix.plan(B, k)
+    kname = "dresd_scanmq_main" if plan["scan_kernel"] == "shared_key" else "dresd_scan_main"
+    # The scan's floor is the larger of its HBM time and its matrix-core time.
+    mfma_peak = MFMA_PEAK_TFLOPS[w.dtype] * 1e12
+    mfma_bound = flops / mfma_peak > scan_bytes / (HBM_PEAK_GBPS * 1e9)
     traffic = read_traffic(w.name, B) if not args.n else None
 
     res = {
@@ -183,22 +193,27 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "d": w.d, "key_dtype": w.dtype, "B": B, "k": k,
                    "L": w.L, "query_pool": int(pool.shape[0]),
-                   "sample_passes": plan["sample_passes"], "scan_waves": plan["scan_waves"]},
+                   "sample_passes": plan["sample_passes"], "scan_waves": plan["scan_waves"],
+                   "scan_kernel": plan["scan_kernel"]},
         "p50_latency_us": p50 * 1e3,
         "p90_latency_us": p90 * 1e3,
         "search_hbm_GBps_at_p50": search_bytes / (p50 * 1e-3) / 1e9,
         "index_build_s": build_s,
         "roofline": {
-            "bound": "hbm",
-            "kernel": "dresd_scan_main",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
+            "bound": "mfma" if mfma_bound else "hbm",
+            "kernel": kname,
+            "achieved": (flops / (scan_ms * 1e-3) / 1e12) if mfma_bound else achieved,
+            "peak": MFMA_PEAK_TFLOPS[w.dtype] if mfma_bound else HBM_PEAK_GBPS,
+            "unit": "TFLOP/s" if mfma_bound else "GB/s",
+            "frac": (flops / (scan_ms * 1e-3) / mfma_peak) if mfma_bound
+                    else achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": scan_bytes,
+            "algorithmic_flops_per_launch": flops,
             "avg_launch_ms": scan_ms,
-            "mfma_util": flops / (scan_ms * 1e-3) / (MFMA_PEAK_TFLOPS[w.dtype] * 1e12),
+            "hbm_GBps": achieved,
+            "hbm_frac": achieved / HBM_PEAK_GBPS,
+            "mfma_util": flops / (scan_ms * 1e-3) / mfma_peak,
         },
     }
     if not args.no_cpu_baseline and not args.n and B == 1:

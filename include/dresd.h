@@ -139,12 +139,15 @@ dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms,
 /*
  * Describe how the next search of this shape would run (host outputs, NULL
  * allowed): the number of passes over sampled keys before the main pass, the
- * number of waves of the main scan, and the bytes of workspace it needs.
+ * number of waves of the main scan, the bytes of workspace it needs, and
+ * which scan kernel runs it: 0 = single-tile scan (batches within one
+ * 16-column query tile group, queries staged in LDS), 1 = shared-key scan
+ * (queries held in registers, keys staged through LDS).
  * Errors: EINVAL for the same argument errors as dresd_search.
  */
 dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,
                                int32_t *sample_passes, int32_t *scan_waves,
-                               int64_t *workspace_bytes);
+                               int64_t *workspace_bytes, int32_t *scan_kind);
 
 #ifdef __cplusplus
 }

@@ -84,10 +84,12 @@ class Index:
         return idx, score, tok
 
     def plan(self, B: int, k: int):
-        sp, w, ws = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+        sp, w, ws, kind = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int32()
         _lib.check(self._lib.dresd_search_plan(self._h, int(B), int(k), ctypes.byref(sp),
-                                               ctypes.byref(w), ctypes.byref(ws)))
-        return {"sample_passes": sp.value, "scan_waves": w.value, "workspace_bytes": ws.value}
+                                               ctypes.byref(w), ctypes.byref(ws),
+                                               ctypes.byref(kind)))
+        return {"sample_passes": sp.value, "scan_waves": w.value, "workspace_bytes": ws.value,
+                "scan_kernel": "shared_key" if kind.value else "single_tile"}
 
     def profile(self, on: bool = True):
         _lib.check(self._lib.dresd_profile_enable(self._h, 1 if on else 0))

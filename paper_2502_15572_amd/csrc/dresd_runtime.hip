@@ -373,24 +373,24 @@ void dresd_index_destroy(dresd_index *ix) {
 }
 
 dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int32_t *sample_passes,
-                               int32_t *scan_waves, int64_t *workspace_bytes) {
+                               int32_t *scan_waves, int64_t *workspace_bytes, int32_t *scan_kind) {
   dresd_status s = validate_search(cix, B, k);
   if (s != DRESD_OK) return s;
   dresd_index *ix = const_cast<dresd_index *>(cix);
-  if (B == 0) {
-    if (sample_passes) *sample_passes = 0;
-    if (scan_waves) *scan_waves = 0;
-    if (workspace_bytes) *workspace_bytes = 0;
-    return DRESD_OK;
-  }
+  if (sample_passes) *sample_passes = 0;
+  if (scan_waves) *scan_waves = 0;
+  if (workspace_bytes) *workspace_bytes = 0;
+  if (scan_kind) *scan_kind = 0;
+  if (B == 0) return DRESD_OK;
   Plan pl;
   s = make_plan(ix, B, k, pl);
   if (s != DRESD_OK) return s;
+  const int wpg = kScanThreads / kWaveSize;
   if (sample_passes) *sample_passes = (int32_t)pl.strides.size();
   if (scan_waves)
-    *scan_waves = (int32_t)std::min<int64_t>(pl.wg_max, ceil_div(ix->T, kScanThreads / kWaveSize)) *
-                  (kScanThreads / kWaveSize);
+    *scan_waves = (int32_t)std::min<int64_t>(pl.wg_max, ceil_div(ix->T, pl.mq ? 1 : wpg)) * wpg;
   if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
+  if (scan_kind) *scan_kind = pl.mq ? 1 : 0;
   return DRESD_OK;
 }
 
