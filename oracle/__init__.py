@@ -10,7 +10,9 @@ rounded once to fp32; ranking by score descending then lowest row index).
 It follows DReSD Section 3.5, Eq. 3 (cosine similarity argmax over a
 key -> next-tokens store) with unit-norm keys and queries (Section 3.4,
 Eq. 2), generalised to the k best keys that batch verification consumes
-(Section 3.6).  This module only marshals numpy arrays into that library and
+(Section 3.6); ``topk(..., next_tok=...)`` adds the next-token filter of
+Section 3.5 (only rows whose value starts with the query's next token
+compete).  This module only marshals numpy arrays into that library and
 builds it with gcc when it is missing.
 """
 from __future__ import annotations
@@ -53,6 +55,10 @@ def _load():
                                         P, ctypes.c_int32, ctypes.c_int32, P, ctypes.c_int32,
                                         P, P, P, P, ctypes.c_int32]
             lib.oracle_topk.restype = ctypes.c_int
+            lib.oracle_topk_filtered.argtypes = [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
+                                                 P, ctypes.c_int32, ctypes.c_int32, P,
+                                                 ctypes.c_int32, P, P, P, P, P, ctypes.c_int32]
+            lib.oracle_topk_filtered.restype = ctypes.c_int
             lib.oracle_score_rows.argtypes = [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
                                               P, P, ctypes.c_int64, P]
             lib.oracle_score_rows.restype = ctypes.c_int
@@ -80,12 +86,14 @@ def _emb_bits(emb: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def topk(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
-         cont: np.ndarray | None = None, threads: int = 0):
+         cont: np.ndarray | None = None, threads: int = 0, next_tok=None):
     """Exact top-k by inner product.
 
     Returns ``(idx[B,k] int64, score[B,k] f32, tokens[B,k,L] int32 or None,
     next_score[B] f32)`` where ``next_score`` is the (k+1)-th best score
-    (NaN when k == N).
+    (NaN when there is none).  With ``next_tok`` ([B] ints) only rows whose
+    continuation starts with that query's next token compete (Section 3.5);
+    ranks past the matching rows hold index -1, score -inf and zero tokens.
     """
     e = _emb_bits(emb, dtype)
     q = np.ascontiguousarray(queries, dtype=np.float32)
@@ -108,12 +116,21 @@ def topk(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
         L = c.shape[1]
         tok = np.empty((B, k, L), np.int32)
         cptr = c.ctypes.data
-    rc = _load().oracle_topk(e.ctypes.data, DTYPE_CODES[dtype], N, d, q.ctypes.data, B, k,
-                             cptr, L, idx.ctypes.data, score.ctypes.data,
-                             tok.ctypes.data if tok is not None else None,
+    lib = _load()
+    tptr = tok.ctypes.data if tok is not None else None
+    if next_tok is None:
+        rc = lib.oracle_topk(e.ctypes.data, DTYPE_CODES[dtype], N, d, q.ctypes.data, B, k,
+                             cptr, L, idx.ctypes.data, score.ctypes.data, tptr,
                              nxt.ctypes.data, int(threads))
+    else:
+        nt = np.ascontiguousarray(next_tok, dtype=np.int32).reshape(-1)
+        if nt.shape[0] != B or cont is None or L < 1:
+            raise ValueError("next_tok needs one token per query and continuations")
+        rc = lib.oracle_topk_filtered(e.ctypes.data, DTYPE_CODES[dtype], N, d, q.ctypes.data,
+                                      B, k, cptr, L, nt.ctypes.data, idx.ctypes.data,
+                                      score.ctypes.data, tptr, nxt.ctypes.data, int(threads))
     if rc != 0:
-        raise RuntimeError("oracle_topk failed")
+        raise RuntimeError("oracle top-k failed")
     return idx, score, tok, nxt
 
 

@@ -24,6 +24,14 @@
  * beyond that definition; queries are looped inside rows only so that the
  * datastore is read once per batch, which does not change any value.
  *
+ * Filtered retrieval (Section 3.5, with Section 3.1): the next token x_{t+1}
+ * that the LLM produced alongside the query embedding removes every draft
+ * that does not start with it.  oracle_topk_filtered reads this as
+ * filter-then-select: for query b only rows i whose value starts with
+ * next_tok[b] (cont[i, 0] == next_tok[b]) compete, and the k best of them are
+ * returned; ranks past the number of matching rows hold index -1, score
+ * -inf and zero tokens.
+ *
  * Parity pins live in the CPU tests (closed forms, exact brute force,
  * invariants, duplicates, self-retrieval MRR of Eq. 4, planted mutations).
  */
@@ -139,23 +147,36 @@ static void offer(item *best, int64_t *count, int64_t m, item x) {
   if (c < m) *count = c + 1;
 }
 
+/* Row i takes part for query b: every row without a filter; with one, the
+ * rows whose value starts with that query's next token. */
+static int admitted(const int32_t *cont, int32_t L, const int32_t *next_tok, int64_t i,
+                    int32_t b) {
+  if (!next_tok) return 1;
+  /* mutation 8: the filter reads the value's second token */
+  int32_t first = cont[i * L + ((g_mutation == 8 && L > 1) ? 1 : 0)];
+  return first == next_tok[b];
+}
+
 /*
- * Exact top-k for B queries over N keys.
+ * Exact top-k for B queries over N keys (the rows admitted by next_tok when
+ * it is not NULL).
  *   emb   [N, d] row-major, dtype ORACLE_F32 / ORACLE_F16 / ORACLE_BF16
  *   Q     [B, d] fp32 row-major
- *   cont  [N, L] int32 (may be NULL when L == 0)
+ *   cont  [N, L] int32 (may be NULL when L == 0 and next_tok is NULL)
  * Outputs (caller-owned):
  *   idx [B, k] int64, score [B, k] fp32, tokens [B, k, L] int32 (NULL ok),
- *   next_score [B] fp32: the (k+1)-th best score, NaN when k == N (NULL ok).
+ *   next_score [B] fp32: the (k+1)-th best score, NaN when there is none
+ *   (NULL ok).  Ranks past the admitted rows: idx -1, score -inf, tokens 0.
  * Returns 0, or -1 on invalid arguments / allocation failure.
  */
-int oracle_topk(const void *emb, int dtype, int64_t N, int32_t d,
-                const float *Q, int32_t B, int32_t k, const int32_t *cont,
-                int32_t L, int64_t *idx, float *score, int32_t *tokens,
-                float *next_score, int32_t nthreads) {
+static int topk_impl(const void *emb, int dtype, int64_t N, int32_t d, const float *Q, int32_t B,
+                     int32_t k, const int32_t *cont, int32_t L, const int32_t *next_tok,
+                     int64_t *idx, float *score, int32_t *tokens, float *next_score,
+                     int32_t nthreads) {
   if (!emb || !Q || !idx || !score || N < 1 || d < 1 || B < 0 || k < 1 ||
       k > N || dtype < 0 || dtype > 2)
     return -1;
+  if (next_tok && (!cont || L < 1)) return -1;
   if (B == 0) return 0;
   int64_t m = (k < N) ? (int64_t)k + 1 : (int64_t)k;
   int nt = 1;
@@ -185,6 +206,7 @@ int oracle_topk(const void *emb, int dtype, int64_t N, int32_t d,
     for (int64_t i = lo; e && i < hi; ++i) {
       decode_row(emb, dtype, d, i, e);
       for (int32_t b = 0; b < B; ++b) {
+        if (!admitted(cont, L, next_tok, i, b)) continue;
         item x;
         x.s = score_row(e, d, Q + (int64_t)b * d);
         x.i = i;
@@ -213,21 +235,46 @@ int oracle_topk(const void *emb, int dtype, int64_t N, int32_t d,
     }
     qsort(merged, (size_t)tot, sizeof(item), cmp_items);
     for (int32_t r = 0; r < k; ++r) {
-      idx[(int64_t)b * k + r] = merged[r].i;
-      score[(int64_t)b * k + r] = merged[r].s;
+      const int64_t o = (int64_t)b * k + r;
+      if (r >= tot) { /* fewer admitted rows than k */
+        idx[o] = -1;
+        score[o] = -INFINITY;
+        if (tokens && L > 0) memset(tokens + o * L, 0, sizeof(int32_t) * (size_t)L);
+        continue;
+      }
+      idx[o] = merged[r].i;
+      score[o] = merged[r].s;
       if (tokens && cont && L > 0) {
         int64_t src = merged[r].i;
         if (g_mutation == 7 && src + 1 < N) ++src; /* mutation 7: off-by-one */
-        memcpy(tokens + ((int64_t)b * k + r) * L, cont + src * L,
-               sizeof(int32_t) * (size_t)L);
+        memcpy(tokens + o * L, cont + src * L, sizeof(int32_t) * (size_t)L);
       }
     }
-    if (next_score) next_score[b] = (k < N) ? merged[k].s : NAN;
+    if (next_score) next_score[b] = (k < tot) ? merged[k].s : NAN;
   }
   free(merged);
   free(all);
   free(cnt);
   return 0;
+}
+
+int oracle_topk(const void *emb, int dtype, int64_t N, int32_t d,
+                const float *Q, int32_t B, int32_t k, const int32_t *cont,
+                int32_t L, int64_t *idx, float *score, int32_t *tokens,
+                float *next_score, int32_t nthreads) {
+  return topk_impl(emb, dtype, N, d, Q, B, k, cont, L, NULL, idx, score, tokens, next_score,
+                   nthreads);
+}
+
+/* Filtered retrieval of Section 3.5: next_tok [B] int32, the token each
+ * query's drafts must start with. */
+int oracle_topk_filtered(const void *emb, int dtype, int64_t N, int32_t d, const float *Q,
+                         int32_t B, int32_t k, const int32_t *cont, int32_t L,
+                         const int32_t *next_tok, int64_t *idx, float *score, int32_t *tokens,
+                         float *next_score, int32_t nthreads) {
+  if (!next_tok) return -1;
+  return topk_impl(emb, dtype, N, d, Q, B, k, cont, L, next_tok, idx, score, tokens, next_score,
+                   nthreads);
 }
 
 /* Scores of the given rows for one query (the same arithmetic as above);

@@ -21,6 +21,7 @@ import oracle
 from datagen import WORKLOADS, generate, to_numpy_bits
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "closed_forms.json")
+GOLDEN_FILTERED = os.path.join(os.path.dirname(__file__), "golden", "filtered_closed_forms.json")
 
 
 def _identity_keys(n, dtype):
@@ -186,6 +187,83 @@ def pin_full_sort_permutation():
         assert idx[b, -1] == int(np.lexsort((-np.arange(w.N), s_all))[0])
 
 
+# --- pins of the next-token filter (Section 3.5) ------------------------------
+
+def _fval(v):
+    return np.float32(-np.inf) if v == "-inf" else np.float32(v)
+
+
+def pin_filtered_golden_closed_forms():
+    g = json.load(open(GOLDEN_FILTERED))
+    n = len(g["first_tokens"])
+    cont = np.stack([np.asarray(g["first_tokens"], np.int32),
+                     np.arange(n, dtype=np.int32) + 100], axis=1)
+    q = np.asarray([g["query"]], np.float32)
+    for c in g["cases"]:
+        for dt in ("f32", "f16", "bf16"):
+            keys = _identity_keys(n, dt)
+            idx, score, tok, _ = oracle.topk(keys, dt, q, c["k"], cont, next_tok=[c["next_tok"]])
+            assert idx[0].tolist() == c["idx"], (c["name"], dt, idx[0].tolist())
+            want = np.asarray([_fval(v) for v in c["score"]], np.float32)
+            assert np.array_equal(score[0], want), (c["name"], dt, score[0])
+            for r, i in enumerate(c["idx"]):
+                want_tok = cont[i] if i >= 0 else np.zeros(2, np.int32)
+                assert np.array_equal(tok[0, r], want_tok), (c["name"], dt, r)
+
+
+def pin_filtered_bruteforce():
+    """Exact rational scores on tiny inputs; only rows whose continuation
+    starts with the query's token compete, ranked by (-score, index); ranks
+    past them are (-1, -inf, zeros)."""
+    rng = np.random.default_rng(777)
+    N, d, B, k, L = 41, 6, 4, 7, 3
+    x = rng.standard_normal((N, d))
+    x /= np.linalg.norm(x, axis=1, keepdims=True)
+    keys = x.astype(np.float32)
+    q = rng.standard_normal((B, d)).astype(np.float32)
+    cont = rng.integers(0, 4, (N, L)).astype(np.int32)
+    nt = np.asarray([0, 1, 2, 9], np.int32)  # the last token matches no row
+    idx, score, tok, nxt = oracle.topk(keys, "f32", q, k, cont, next_tok=nt)
+    for b in range(B):
+        rows = [i for i in range(N) if cont[i, 0] == nt[b]]
+        s = {i: _exact_fp32_score(q[b], keys[i]) for i in rows}
+        order = sorted(rows, key=lambda i: (-float(s[i]), i))
+        for r in range(k):
+            if r < len(order):
+                assert idx[b, r] == order[r] and score[b, r] == s[order[r]], (b, r)
+                assert np.array_equal(tok[b, r], cont[order[r]])
+            else:
+                assert idx[b, r] == -1 and score[b, r] == -np.inf and not tok[b, r].any()
+        if len(order) > k:
+            assert nxt[b] == s[order[k]]
+        else:
+            assert np.isnan(nxt[b])
+
+
+def pin_filter_admitting_all_rows_is_unfiltered():
+    """A token every continuation starts with filters nothing: the result is
+    the unfiltered top-k, bit for bit."""
+    w = WORKLOADS["flat16k_d256_f32"].scaled(3000)
+    g = generate(w, "cpu")
+    keys, dt = to_numpy_bits(g["keys"])
+    cont = g["cont"].numpy().copy()
+    cont[:, 0] = 31
+    q = g["queries"][:5].numpy()
+    a = oracle.topk(keys, dt, q, 12, cont)
+    b = oracle.topk(keys, dt, q, 12, cont, next_tok=np.full(5, 31))
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y, equal_nan=True)
+
+
+FILTER_PINS = [pin_filtered_golden_closed_forms, pin_filtered_bruteforce,
+               pin_filter_admitting_all_rows_is_unfiltered]
+
+
+@pytest.mark.parametrize("pin", FILTER_PINS, ids=[p.__name__ for p in FILTER_PINS])
+def test_filter_pin(pin):
+    pin()
+
+
 PINS = [pin_golden_closed_forms, pin_exact_bruteforce, pin_decode_f16_all_patterns,
         pin_decode_bf16_all_patterns, pin_invariants_and_self_match, pin_self_match_16bit,
         pin_duplicates_and_mrr, pin_structural_continuations, pin_full_sort_permutation]
@@ -231,6 +309,7 @@ MUTATIONS = {
     5: "ranks ascending",
     6: "truncates scores to 16 bits",
     7: "gathers the continuation of the next row",
+    8: "filters on the continuation's second token",
 }
 
 
@@ -238,7 +317,7 @@ MUTATIONS = {
 def test_planted_mistakes(m):
     failed = []
     with oracle.mutation(m):
-        for pin in PINS:
+        for pin in PINS + FILTER_PINS:
             try:
                 pin()
             except AssertionError:
