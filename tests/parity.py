@@ -15,6 +15,11 @@ are bit-exact for the returned indices.
       (identical sets whenever the rank-k / rank-(k+1) gap is >= tol)
   R7  tokens[r, :] == cont[g_idx[r], :] bit for bit
 Also reported (not gating): exact-order agreement and max |g - exact|.
+
+Next-token-filtered searches (Section 3.5) add: every returned row is
+admitted (its continuation starts with the query's token), and ranks past
+the admitted rows -- exactly where the oracle's are -- hold index -1, score
+-inf and zero tokens; the rules above apply to the ranks before them.
 """
 from __future__ import annotations
 
@@ -85,15 +90,49 @@ def check_query(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont
     }
 
 
+def check_query_filtered(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont,
+                         first_token, tol=1e-5):
+    """One query of a next-token-filtered search: ``first_token`` is the
+    token its drafts must start with."""
+    g_idx = np.asarray(g_idx, np.int64)
+    g_score = np.asarray(g_score, np.float32)
+    o_idx = np.asarray(o_idx, np.int64)
+    k = o_idx.size
+    pad = np.nonzero(o_idx < 0)[0]
+    m = int(pad[0]) if pad.size else k
+    if np.any(o_idx[m:] >= 0):
+        raise ParityError("oracle padding is not a suffix")
+    if g_idx.shape != (k,):
+        raise ParityError("shape mismatch")
+    if np.any(g_idx[m:] != -1) or np.any(g_score[m:] != -np.inf):
+        raise ParityError("padding: ranks >= %d must be (-1, -inf)" % m)
+    if g_tok is not None and np.any(np.asarray(g_tok)[m:] != 0):
+        raise ParityError("padding: tokens of ranks >= %d must be zero" % m)
+    if m == 0:
+        return {"exact_order": True, "max_abs_vs_exact": 0.0, "max_abs_vs_oracle": 0.0}
+    if np.any(g_idx[:m] < 0) or np.any(g_idx[:m] >= N):
+        raise ParityError("R4: index out of range")
+    if np.any(np.asarray(cont)[g_idx[:m], 0] != first_token):
+        raise ParityError("filter: returned a row whose continuation does not start with %d"
+                          % first_token)
+    return check_query(g_idx[:m], g_score[:m], None if g_tok is None else np.asarray(g_tok)[:m],
+                       o_idx[:m], np.asarray(o_score)[:m], o_next, exact_of, N, cont, tol)
+
+
 def check_batch(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of_b, N, cont=None,
-                tol=1e-5):
-    """``exact_of_b(b, rows)`` re-scores rows for query b."""
+                tol=1e-5, next_tok=None):
+    """``exact_of_b(b, rows)`` re-scores rows for query b; ``next_tok`` [B]
+    marks a next-token-filtered search."""
     reps = []
     for b in range(o_idx.shape[0]):
         try:
-            reps.append(check_query(g_idx[b], g_score[b], None if g_tok is None else g_tok[b],
-                                    o_idx[b], o_score[b], None if o_next is None else o_next[b],
-                                    lambda rows, b=b: exact_of_b(b, rows), N, cont, tol))
+            args = (g_idx[b], g_score[b], None if g_tok is None else g_tok[b], o_idx[b],
+                    o_score[b], None if o_next is None else o_next[b],
+                    lambda rows, b=b: exact_of_b(b, rows), N, cont)
+            if next_tok is None:
+                reps.append(check_query(*args, tol))
+            else:
+                reps.append(check_query_filtered(*args, int(next_tok[b]), tol))
         except ParityError as e:
             raise ParityError("query %d: %s" % (b, e)) from None
     return {

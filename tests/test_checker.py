@@ -101,3 +101,47 @@ def test_near_tie_swap_at_boundary_is_allowed(case):
     tok = c["tok"].copy()
     tok[b, -1] = c["cont"][idx_k1[0, -1]]
     _run(c, idx=idx, score=s, tok=tok)
+
+
+# --- next-token-filtered searches -------------------------------------------
+
+def _filtered_case():
+    rng = np.random.default_rng(5)
+    N, d, B, k = 300, 16, 3, 8
+    x = rng.standard_normal((N, d))
+    x = (x / np.linalg.norm(x, axis=1, keepdims=True)).astype(np.float32)
+    q = rng.standard_normal((B, d)).astype(np.float32)
+    cont = rng.integers(0, 6, (N, 2)).astype(np.int32)
+    cont[:5, 0] = 40  # token 40: exactly five rows, fewer than k
+    nt = np.asarray([1, 40, 77], np.int32)  # 77 matches no row
+    o = oracle.topk(x, "f32", q, k, cont, next_tok=nt)
+    ex = lambda b, rows: oracle.score_rows(x, "f32", q[b], rows)
+    return x, cont, nt, o, ex, N
+
+
+def test_filtered_oracle_result_passes():
+    x, cont, nt, (oi, os_, ot, on), ex, N = _filtered_case()
+    assert (oi[1, 5:] == -1).all() and (oi[2] == -1).all()
+    check_batch(oi, os_, ot, oi, os_, on, ex, N, cont, 1e-5, next_tok=nt)
+
+
+def test_filtered_unadmitted_row_fails():
+    x, cont, nt, (oi, os_, ot, on), ex, N = _filtered_case()
+    gi, gs, gt = oi.copy(), os_.copy(), ot.copy()
+    bad = int(np.nonzero(cont[:, 0] != nt[0])[0][0])
+    gi[0, -1] = bad  # score left as the oracle's: only the filter rule can reject it
+    gt[0, -1] = cont[bad]
+    with pytest.raises(ParityError):
+        check_batch(gi, gs, gt, oi, os_, on, ex, N, cont, 1e-5, next_tok=nt)
+
+
+def test_filtered_padding_must_match():
+    x, cont, nt, (oi, os_, ot, on), ex, N = _filtered_case()
+    gi, gs, gt = oi.copy(), os_.copy(), ot.copy()
+    gi[1, 5], gs[1, 5] = 7, 0.0  # a real row where the oracle pads
+    with pytest.raises(ParityError):
+        check_batch(gi, gs, gt, oi, os_, on, ex, N, cont, 1e-5, next_tok=nt)
+    gi, gs, gt = oi.copy(), os_.copy(), ot.copy()
+    gt[2, 0, 0] = 1  # padding tokens must be zero
+    with pytest.raises(ParityError):
+        check_batch(gi, gs, gt, oi, os_, on, ex, N, cont, 1e-5, next_tok=nt)
