@@ -102,6 +102,10 @@ def main():
     ap.add_argument("--k", type=int, default=0, help="default: the workload's k")
     ap.add_argument("--n", type=int, default=0, help="override N (reduced runs; not a bench line)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--filtered", action="store_true",
+                    help="next-token-filtered search: each query's next token is the first "
+                         "token of its source row's continuation (the most frequent first "
+                         "token for queries without a source row)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -137,13 +141,21 @@ def main():
     pool = g["queries"]
     nb = max(1, pool.shape[0] // B)
     batches = [pool[(i % nb) * B:(i % nb) * B + B].contiguous() for i in range(nb)]
+    tok_batches = [None] * nb
+    if args.filtered:
+        c0 = g["cont"][:, 0]
+        frequent = int(torch.mode(c0[: min(w.N, 1 << 20)]).values)
+        src = g["query_src"]
+        nt = torch.where(src >= 0, c0[src.clamp(min=0)], torch.full_like(src, frequent))
+        nt = nt.to(torch.int32)
+        tok_batches = [nt[(i % nb) * B:(i % nb) * B + B].contiguous() for i in range(nb)]
     idx = torch.empty((B, k), dtype=torch.int64, device=dev)
     score = torch.empty((B, k), dtype=torch.float32, device=dev)
     tok = torch.empty((B, k, w.L), dtype=torch.int32, device=dev)
     out = (idx, score, tok)
 
     for i in range(args.warmup):
-        ix.search(batches[i % nb], k, out=out)
+        ix.search(batches[i % nb], k, out=out, next_tok=tok_batches[i % nb])
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
@@ -155,7 +167,7 @@ def main():
     t0 = time.perf_counter()
     for i in range(args.steps):
         ev[i][0].record(stream)
-        ix.search(batches[i % nb], k, out=out)
+        ix.search(batches[i % nb], k, out=out, next_tok=tok_batches[i % nb])
         ev[i][1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -167,6 +179,8 @@ def main():
 
     s = w.elem_bytes
     scan_bytes = w.N * w.d * s + B * w.d * 4           # keys once + queries
+    if args.filtered:
+        scan_bytes += w.N * 4 + B * 4                  # first-token column + next tokens
     search_bytes = scan_bytes + B * k * (8 + 4 + 4 * w.L)
     scan_ms = prof["scan_ms"] / max(1, prof["searches"])
     achieved = scan_bytes / (scan_ms * 1e-3) / 1e9
@@ -192,6 +206,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "d": w.d, "key_dtype": w.dtype, "B": B, "k": k,
+                   "filtered": bool(args.filtered),
                    "L": w.L, "query_pool": int(pool.shape[0]),
                    "sample_passes": plan["sample_passes"], "scan_waves": plan["scan_waves"],
                    "scan_kernel": plan["scan_kernel"]},
@@ -216,7 +231,7 @@ def main():
             "mfma_util": flops / (scan_ms * 1e-3) / mfma_peak,
         },
     }
-    if not args.no_cpu_baseline and not args.n and B == 1:
+    if not args.no_cpu_baseline and not args.n and B == 1 and not args.filtered:
         log("timing the oracle on the host ...")
         res["cpu_baseline"] = cpu_baseline(g["keys"], pool, k)
     ix.close()

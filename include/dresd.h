@@ -111,6 +111,26 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B,
                           int32_t k, int64_t *idx, float *score,
                           int32_t *tokens, dresd_stream stream);
 
+/*
+ * Next-token-filtered retrieval (Section 3.5, with Section 3.1): the token
+ * x_{t+1} that the LLM produced with the query embedding removes every draft
+ * that does not start with it.  Read as filter-then-select: for query b only
+ * rows whose continuation starts with next_tok[b] (continuations[i][0] ==
+ * next_tok[b]) compete, and the k best of them are returned exactly as by
+ * dresd_search.  When fewer than k rows match, the ranks past them hold
+ * idx -1, score -inf and zero tokens.
+ *
+ *   next_tok  device, [B] int32: the next token of each query.
+ *   Other arguments, order, determinism, ownership and errors as for
+ *   dresd_search (EINVAL also for a null next_tok when B > 0).  The first
+ *   token of every row is kept by the index (4 bytes per row, built by
+ *   dresd_index_create), so a filtered scan reads 64 more bytes per 16 rows.
+ */
+dresd_status dresd_search_filtered(dresd_index *ix, const float *queries,
+                                   const int32_t *next_tok, int32_t B, int32_t k,
+                                   int64_t *idx, float *score, int32_t *tokens,
+                                   dresd_stream stream);
+
 /* Describe an index.  Any output pointer (host) may be NULL.
  * Errors: EINVAL when ix is NULL. */
 dresd_status dresd_index_info(const dresd_index *ix, int64_t *N, int32_t *d,

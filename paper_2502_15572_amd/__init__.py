@@ -61,9 +61,12 @@ class Index:
             ctypes.c_void_p(keys.data_ptr()), ctypes.c_void_p(cont.data_ptr()), self.N, self.d,
             self.L, _dtype_code(keys), _stream_handle(stream), ctypes.byref(self._h)))
 
-    def search(self, queries, k: int, tokens: bool = True, out=None, stream=None):
+    def search(self, queries, k: int, tokens: bool = True, out=None, stream=None, next_tok=None):
         """Top-k by inner product.  Returns ``(idx int64[B,k], score f32[B,k],
-        tokens int32[B,k,L] or None)``."""
+        tokens int32[B,k,L] or None)``.  With ``next_tok`` (int32 GPU tensor
+        [B]) only rows whose continuation starts with the query's next token
+        compete (Section 3.5); ranks past the matching rows hold idx -1,
+        score -inf and zero tokens."""
         import torch
         if not queries.is_cuda or queries.dtype != torch.float32:
             raise TypeError("queries must be a float32 GPU tensor")
@@ -71,16 +74,27 @@ class Index:
             raise ValueError("queries must be [B, %d]" % self.d)
         q = queries.contiguous()
         B = int(q.shape[0])
+        if next_tok is not None:
+            if not next_tok.is_cuda or next_tok.dtype != torch.int32 or next_tok.numel() != B:
+                raise TypeError("next_tok must be an int32 GPU tensor with one token per query")
+            next_tok = next_tok.contiguous()
         if out is None:
             idx = torch.empty((B, k), dtype=torch.int64, device=q.device)
             score = torch.empty((B, k), dtype=torch.float32, device=q.device)
             tok = torch.empty((B, k, self.L), dtype=torch.int32, device=q.device) if tokens else None
         else:
             idx, score, tok = out
-        _lib.check(self._lib.dresd_search(
-            self._h, ctypes.c_void_p(q.data_ptr()), B, int(k), ctypes.c_void_p(idx.data_ptr()),
-            ctypes.c_void_p(score.data_ptr()),
-            ctypes.c_void_p(tok.data_ptr()) if tok is not None else None, _stream_handle(stream)))
+        tptr = ctypes.c_void_p(tok.data_ptr()) if tok is not None else None
+        if next_tok is None:
+            _lib.check(self._lib.dresd_search(
+                self._h, ctypes.c_void_p(q.data_ptr()), B, int(k),
+                ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(score.data_ptr()), tptr,
+                _stream_handle(stream)))
+        else:
+            _lib.check(self._lib.dresd_search_filtered(
+                self._h, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(next_tok.data_ptr()), B,
+                int(k), ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(score.data_ptr()), tptr,
+                _stream_handle(stream)))
         return idx, score, tok
 
     def plan(self, B: int, k: int):

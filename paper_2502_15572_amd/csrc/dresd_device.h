@@ -41,6 +41,31 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Asynchronous copies global -> LDS (global_load_lds_*), issued from inline
+// assembly so that the compiler's wait-count model, which cannot tell which
+// LDS bytes such a copy writes, adds no waits for them before unrelated LDS
+// reads.  Callers wait with wait_vmcnt before reading the destination.
+__device__ __forceinline__ void copy1_to_lds(const void *src, uint32_t lds) {
+  // one dword per lane from its own address; lane l lands at lds + 4 l
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "global_load_lds_dword %0, off"
+      :
+      : "v"(src), "s"(lds)
+      : "memory");
+}
+
+// s_waitcnt immediate that waits for vmcnt == 0 only (gfx9 encoding: vmcnt
+// bits [3:0] and [15:14], expcnt [6:4] and lgkmcnt [11:8] at their maxima).
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Wait until at most N of this wave's vector memory operations are pending
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
 // Sort n (power of two, >= 2) keys in LDS, descending, by one wave.
 __device__ inline void wave_bitonic_desc(uint64_t *s, int n, int lane) {
   for (int size = 2; size <= n; size <<= 1) {

@@ -37,6 +37,10 @@ struct ScanParams {
   int CL;                    // per-query LDS stage in front of each HBM list
   int sort_lists;            // sort every list at the end (small batches)
   const void *qop;           // shared-key scan: query operands [tiles][KB][64] x 16 B
+  // Next-token-filtered search (both null otherwise): only rows whose value
+  // starts with the query's next token compete.
+  const int32_t *ftok;       // [tiles * 16] first token of each row's value
+  const int32_t *next_tok;   // [B] next token of each query
 };
 
 // Query operands of the shared-key scan, built once per search: chunk
@@ -53,6 +57,17 @@ struct QopParams {
 // per query, rounded up to 16 bytes.
 __host__ __device__ inline size_t scan_wave_bytes(int nq, int cl, int C) {
   return ((size_t)nq * cl * 8 + (size_t)C * 8 + (size_t)nq * 8 + (size_t)nq * 12 + 15) / 16 * 16;
+}
+
+// Single-tile scan: next tokens of the launch's queries, shared by the waves,
+// and per wave two slots of first tokens (four tiles' rows each).
+__host__ __device__ inline size_t scan_ntok_bytes(int nq) { return ((size_t)nq * 4 + 15) / 16 * 16; }
+constexpr int kScanFtokBytes = 2 * 64 * 4;
+
+// Shared-key scan, filtered search: per wave, the next token of each score
+// slot [4 lane groups][np] and a ring of first-token copies [stages][64].
+__host__ __device__ inline size_t scan_mq_filter_bytes(int stages, int np) {
+  return (size_t)16 * np + (size_t)stages * 256;
 }
 
 // Shared-key scan: a wave's candidate buffer holds kMqCandBuf (key, query)
@@ -102,12 +117,14 @@ struct LayoutParams {
 typedef void (*ScanKernel)(ScanParams);
 ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass);  // cpq: columns per query
 // Shared-key scan (dresd_scan_mq.hip): qtw query tiles per wave, kbt blocks
-// per key tile; *stages receives the depth of its LDS ring of key stages.
-ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, int *stages);
-ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, int *stages);
-inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, int *stages) {
-  if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass, stages);
-  if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass, stages);
+// per key tile, filtered = next-token-filtered search; *stages receives the
+// depth of its LDS ring of key stages.
+ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, bool filtered, int *stages);
+ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, bool filtered, int *stages);
+inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, bool filtered,
+                                 int *stages) {
+  if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass, filtered, stages);
+  if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass, filtered, stages);
   return nullptr;
 }
 // Query-operand kernel of the shared-key scan for a key type (launch with

@@ -139,13 +139,15 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   const int ncols = B * CPQ;
   const int g = lane >> 4, m = lane & 15;
 
-  // LDS carve-up: query operand | zero chunk | one candidate region per wave
-  // (staged keys, sort scratch, thresholds, counters)
+  // LDS carve-up: query operand | zero chunk | next tokens of the queries |
+  // one candidate region per wave (staged keys, sort scratch, thresholds,
+  // counters)
   const int qop_bytes = ncols * KB * 64;
   const int zero_off = qop_bytes;
   const int CL = p.CL;
+  int32_t *nt_lds = reinterpret_cast<int32_t *>(smem + qop_bytes + 16);
   CandSink sink;
-  sink.stg = reinterpret_cast<uint64_t *>(smem + qop_bytes + 16 +
+  sink.stg = reinterpret_cast<uint64_t *>(smem + qop_bytes + 16 + scan_ntok_bytes(NQ) +
                                           (size_t)wv * scan_wave_bytes(NQ, CL, C));
   sink.scr = sink.stg + (size_t)NQ * CL;
   sink.st_key = sink.scr + C;
@@ -173,6 +175,8 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
           query_chunk<DT, CPQ>(p.queries, p.d, B, c, kb * 4 * EPC + gg * EPC);
     }
     if (threadIdx.x == 0) *reinterpret_cast<u4 *>(smem + zero_off) = u4{0, 0, 0, 0};
+    if (p.next_tok)
+      for (int q = threadIdx.x; q < NQ; q += blockDim.x) nt_lds[q] = q < B ? p.next_tok[q] : 0;
   }
   // 2. Per-wave state: thresholds start at the pass's tau (or none).
   sink_init(sink, NQ, B, p.tau);
@@ -227,6 +231,31 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   int64_t ctile = v0 * p.stride;
   int ckb = 0;
 
+  // Filtered search (Section 3.5): the first tokens of a group of four
+  // tiles (64 rows, lane l: row l % 16 of tile 4 i + l / 16) are copied into
+  // one of two per-wave LDS slots by an LDS-DMA copy issued a whole group
+  // ahead of use.  Every block load issued since is younger, so waiting for
+  // at most U pending loads covers the copy (all of them in the last,
+  // partial group of blocks, which issues no loads).
+  const bool filt = p.ftok != nullptr;
+  const int64_t ntw = v1 - v0;  // tiles of this wave
+  int64_t tdone = 0;            // tiles finished (wave-uniform)
+  // two 64-entry slots per wave, after the waves' candidate regions
+  int32_t *ftbuf = reinterpret_cast<int32_t *>(smem + qop_bytes + 16 + scan_ntok_bytes(NQ) +
+                                               (size_t)4 * scan_wave_bytes(NQ, CL, C)) +
+                   wv * 128;
+  const uint32_t ftbuf_lds = (uint32_t)(uintptr_t)ftbuf;  // low half of an LDS address
+  auto ftok_group = [&](int64_t grp) {
+    int64_t vt = grp * 4 + (lane >> 4);
+    vt = vt < ntw ? vt : ntw - 1;
+    copy1_to_lds(p.ftok + (v0 + vt) * p.stride * kTileRows + (lane & 15),
+                 ftbuf_lds + (uint32_t)(grp & 1) * 256u);
+  };
+  if (filt && ntw > 0) {
+    ftok_group(0);
+    ftok_group(1);
+  }
+
   auto mfma_block = [&](const u4 &blk) {
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
@@ -235,7 +264,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
     }
   };
   // Tile epilogue: threshold filter, rare slow path, reset for the next tile.
-  auto tile_end = [&]() {
+  auto tile_end = [&](bool tail) {
     const int64_t row64 = ctile * kTileRows + m;
     const bool row_ok = row64 < p.N;
     const uint32_t row = (uint32_t)row64;
@@ -252,8 +281,29 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
           v = (v + acc[t][s * CPQ + 1] * s1) + acc[t][s * CPQ + 2] * s2;
         }
         sc[t][s] = v;
-        any |= row_ok && sc[t][s] >= thr[t][s];
       }
+    if (filt) {
+      // Rows whose value does not start with the query's next token drop
+      // out: their score becomes NaN, which fails every threshold test
+      // (even a threshold of -inf).
+      const int tg = (int)(tdone & 3);
+      if (tg == 0) {
+        if (tail) wait_vmcnt<0>();
+        else wait_vmcnt<U>();
+      }
+      const int f = ftbuf[(int)((tdone >> 2) & 1) * 64 + tg * 16 + m];
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+          if (f != nt_lds[t * QPT + g * NS + s]) sc[t][s] = __builtin_nanf("");
+      if (tg == 3) ftok_group((tdone >> 2) + 2);  // the slot just finished
+    }
+    ++tdone;
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+#pragma unroll
+      for (int s = 0; s < NS; ++s) any |= row_ok && sc[t][s] >= thr[t][s];
     if (__ballot(any)) {
       bool spilled = false;
 #pragma unroll
@@ -291,7 +341,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
     for (int u = 0; u < U; ++u) {
       mfma_block(ring[u]);
       ring[u] = __builtin_nontemporal_load(block(jj + u + U));
-      if (++ckb == KB) tile_end();
+      if (++ckb == KB) tile_end(false);
     }
   }
   // The last partial group: its blocks are already in the ring.
@@ -299,9 +349,11 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   for (int u = 0; u < U; ++u) {
     if (j + u < J) {
       mfma_block(ring[u]);
-      if (++ckb == KB) tile_end();
+      if (++ckb == KB) tile_end(true);
     }
   }
+
+  if (filt) wait_vmcnt<0>();  // no LDS copy may land after the workgroup ends
 
   // 4. Publish the lists: lists holding more than k keys are cut to their k
   // best (every list is sorted with sort_lists); each publishes its length,

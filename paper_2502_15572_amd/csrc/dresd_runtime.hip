@@ -20,6 +20,7 @@ struct dresd_index {
   int64_t T = 0;       // tiles
   void *data = nullptr;
   int32_t *cont = nullptr;
+  int32_t *ftok = nullptr;  // first token of each row's value [T * 16] (filtered search)
   int cus = 0;
   size_t lds_max = 0;
   // workspace
@@ -82,6 +83,7 @@ struct Plan {
   int G_max = 0;
   int64_t spill_cap = 0;        // merge candidates per query beyond its LDS cache
   bool sort_lists = false;
+  bool filt = false;            // next-token-filtered search
   size_t off_tau = 0, off_lcnt = 0, off_lkth = 0, off_lfirst = 0, off_lists = 0, off_spill = 0;
   size_t off_qop = 0;               // shared-key scan: query operands of a group
   size_t bytes = 0;
@@ -89,7 +91,8 @@ struct Plan {
 
 // Single-tile scan: query operand | zero chunk | candidate region per wave.
 size_t scan_lds(int ncols, int KB, int nq, int cl, int C) {
-  return (size_t)ncols * KB * 64 + 16 + (size_t)4 * scan_wave_bytes(nq, cl, C);
+  return (size_t)ncols * KB * 64 + 16 + scan_ntok_bytes(nq) + (size_t)4 * scan_wave_bytes(nq, cl, C) +
+         (size_t)4 * kScanFtokBytes;
 }
 
 // Per-query LDS stage in front of each HBM list: larger when few queries share the wave.
@@ -116,8 +119,9 @@ dresd_status validate_search(const dresd_index *ix, int32_t B, int32_t k) {
   return DRESD_OK;
 }
 
-dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
+dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = false) {
   pl = Plan();
+  pl.filt = filt;
   // The query enters the matrix cores as three 16-bit parts that sum to it
   // exactly (four columns per query) for bf16 keys and for small f16 batches;
   // larger f16 batches round it once to f16.
@@ -139,10 +143,12 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl) {
     pl.qt = 4 * qtw;
     pl.bmax = std::min(B, pl.qt * pl.qpt);
     int stages = 0;
-    pl.kmain = scan_mq_kernel(ix->dtype, qtw, ix->KB, true, &stages);
-    pl.ksample = scan_mq_kernel(ix->dtype, qtw, ix->KB, false, &stages);
+    pl.kmain = scan_mq_kernel(ix->dtype, qtw, ix->KB, true, filt, &stages);
+    pl.ksample = scan_mq_kernel(ix->dtype, qtw, ix->KB, false, filt, &stages);
     pl.CL = 0;
-    pl.lds = scan_mq_lds_bytes(stages, qtw * pl.qpt, pl.C);
+    pl.lds = scan_mq_lds_bytes(stages, qtw * pl.qpt, pl.C) +
+             (filt ? (size_t)(kScanThreads / kWaveSize) * scan_mq_filter_bytes(stages, qtw * (4 / pl.terms))
+                   : 0);
   } else {
     // Largest group (power-of-two number of query tiles, at most 16) whose
     // query operand and per-wave state fit in the workgroup's LDS.
@@ -257,6 +263,11 @@ hipEvent_t take_event(dresd_index *ix) {
   return e;
 }
 
+// One search; next_tok (device [B]) selects the next-token-filtered form.
+dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *next_tok, int32_t B,
+                         int32_t k, int64_t *idx, float *score, int32_t *tokens,
+                         dresd_stream stream);
+
 }  // namespace
 
 extern "C" {
@@ -277,6 +288,7 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
   auto cleanup = [&](dresd_status s) {
     if (ix->data) hipFree(ix->data);
     if (ix->cont) hipFree(ix->cont);
+    if (ix->ftok) hipFree(ix->ftok);
     delete ix;
     return s;
   };
@@ -305,13 +317,19 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
     ix->cont = nullptr;
     return cleanup(fail(DRESD_ENOMEM, "continuation storage allocation failed"));
   }
+  const size_t ftok_bytes = (size_t)ix->T * kTileRows * sizeof(int32_t);
+  if (hipMalloc((void **)&ix->ftok, ftok_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    ix->ftok = nullptr;
+    return cleanup(fail(DRESD_ENOMEM, "first-token column allocation failed"));
+  }
   // Raise the dynamic-LDS limit of every scan kernel to the device's.
   for (int v = 0; v < 3; ++v)
     for (int qtw : {1, 2, 4})
       for (int kbt : {4, 8, 16, 32})
-        for (int mp = 0; mp < 2; ++mp) {
+        for (int mp = 0; mp < 4; ++mp) {
           int stages = 0;
-          ScanKernel kf = scan_mq_kernel(v, qtw, kbt, mp != 0, &stages);
+          ScanKernel kf = scan_mq_kernel(v, qtw, kbt, (mp & 1) != 0, mp >= 2, &stages);
           if (kf)
             (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
                                       (int)ix->lds_max);
@@ -339,6 +357,12 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
                                  0, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(ix->cont, continuations, cont_bytes, hipMemcpyDeviceToDevice, st);
+  // First-token column: value[i][0] for every row, zero past N.
+  if (e == hipSuccess)
+    e = hipMemsetAsync(ix->ftok, 0, ftok_bytes, st);
+  if (e == hipSuccess)
+    e = hipMemcpy2DAsync(ix->ftok, sizeof(int32_t), continuations, (size_t)L * sizeof(int32_t),
+                         sizeof(int32_t), (size_t)N, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess)
     return cleanup(fail(DRESD_EDEVICE, std::string("index build failed: ") + hipGetErrorString(e)));
@@ -364,6 +388,7 @@ void dresd_index_destroy(dresd_index *ix) {
   (void)hipDeviceSynchronize();
   if (ix->data) hipFree(ix->data);
   if (ix->cont) hipFree(ix->cont);
+  if (ix->ftok) hipFree(ix->ftok);
   if (ix->ws) hipFree(ix->ws);
   for (auto e : ix->ev_free) hipEventDestroy(e);
   for (auto e : ix->ev_scan) hipEventDestroy(e);
@@ -400,9 +425,30 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
   if (s != DRESD_OK) return s;
   if (B > 0 && (!queries || !idx || !score)) return fail(DRESD_EINVAL, "NULL pointer argument");
   if (B == 0) return DRESD_OK;
+  return search_impl(ix, queries, nullptr, B, k, idx, score, tokens, stream);
+}
+
+dresd_status dresd_search_filtered(dresd_index *ix, const float *queries, const int32_t *next_tok,
+                                   int32_t B, int32_t k, int64_t *idx, float *score,
+                                   int32_t *tokens, dresd_stream stream) {
+  dresd_status s = validate_search(ix, B, k);
+  if (s != DRESD_OK) return s;
+  if (B > 0 && (!queries || !next_tok || !idx || !score))
+    return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (B == 0) return DRESD_OK;
+  return search_impl(ix, queries, next_tok, B, k, idx, score, tokens, stream);
+}
+
+}  // extern "C"
+
+namespace {
+dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *next_tok, int32_t B,
+                         int32_t k, int64_t *idx, float *score, int32_t *tokens,
+                         dresd_stream stream) {
+  dresd_status s = DRESD_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Plan pl;
-  s = make_plan(ix, B, k, pl);
+  s = make_plan(ix, B, k, pl, next_tok != nullptr);
   if (s != DRESD_OK) return s;
   s = ensure_workspace(ix, pl.bytes);
   if (s != DRESD_OK) return s;
@@ -437,6 +483,8 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
     sp.k = k;
     sp.C = pl.C;
     sp.CL = pl.CL;
+    sp.ftok = next_tok ? ix->ftok : nullptr;
+    sp.next_tok = next_tok ? next_tok + gr.b0 : nullptr;
     sp.qop = nullptr;
     if (pl.mq) {
       QopParams qp;
@@ -514,6 +562,10 @@ dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B, int3
   }
   return DRESD_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 dresd_status dresd_profile_enable(dresd_index *ix, int32_t on) {
   if (!ix) return fail(DRESD_EINVAL, "index is NULL");

@@ -108,22 +108,13 @@ __device__ __forceinline__ void copy2_to_lds(const void *src, uint32_t voff0, ui
       : "memory");
 }
 
-// s_waitcnt immediate that waits for vmcnt == 0 only (gfx9 encoding: vmcnt
-// bits [3:0] and [15:14], expcnt [6:4] and lgkmcnt [11:8] at their maxima).
-constexpr int kWaitVmcnt0 = 0x0F70;
-
-// Wait until at most N of this wave's vector memory operations are pending
-// (they complete in issue order).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
-
 }  // namespace
 
 // QTW query tiles per wave, KBT 32-dim blocks per key tile (must equal the
-// index's blocks per tile), CPQ operand columns per query, S LDS stages.
-template <int DT, int QTW, int KBT, int CPQ, int S>
+// index's blocks per tile), CPQ operand columns per query, S LDS stages;
+// FILT: next-token-filtered search (a separate instantiation, so the
+// unfiltered stream loop carries none of its code).
+template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
 __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   constexpr int QPT = 16 / CPQ;   // queries per tile
   constexpr int NS = 4 / CPQ;     // scores per lane per query tile
@@ -154,6 +145,13 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   uint32_t *st_cnt = reinterpret_cast<uint32_t *>(cq + CB);   // HBM list length [NQW]
   float *st_thr = reinterpret_cast<float *>(st_cnt + NQW);    // float threshold [NQW]
   uint64_t *st_max = reinterpret_cast<uint64_t *>(st_thr + NQW);  // best listed key [NQW]
+  // Filtered search (Section 3.5): next token of each score slot, and a
+  // ring of first-token copies, one per stage (its tiles' 16 rows each).
+  constexpr bool filt = FILT;
+  int32_t *nt_slot = reinterpret_cast<int32_t *>(
+      smem + (size_t)S * SB * kBlockBytes + (size_t)(kScanThreads / kWaveSize) * wreg +
+      (size_t)wv * scan_mq_filter_bytes(S, NP));  // [4 lane groups][NP]
+  int32_t *fring = nt_slot + 4 * NP;              // [S][64]
 
   // Queries of this wave: tiles [wv*QTW, wv*QTW + QTW) of the batch.
   const int q0 = wv * NQW;
@@ -182,6 +180,12 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     st_thr[i] = tf;
     st_max[i] = 0;
   }
+  if (filt)
+    for (int i = lane; i < 4 * NP; i += kWaveSize) {
+      const int gg = i / NP, j = i % NP;
+      const int q = q0 + (j / NS) * QPT + gg * NS + (j % NS);
+      nt_slot[i] = q < B ? p.next_tok[q] : 0;
+    }
   wave_sync_lds();
   // Score slot j = t * NS + s of a lane belongs to query t * QPT + g * NS + s.
   float thr[NP];
@@ -317,6 +321,14 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     }
   };
 
+  int tslot = 0;  // ring slot of the stage that holds the current tile's last blocks
+  // Filtered search with few score slots: their next tokens stay in VGPRs.
+  int ntr[NP <= 8 ? NP : 1];
+  if (filt && NP <= 8) {
+    wave_sync_lds();
+#pragma unroll
+    for (int j = 0; j < (NP <= 8 ? NP : 1); ++j) ntr[j] = nt_slot[g * NP + j];
+  }
   auto tile_end = [&](int64_t vt) {
     float sc[NP];
 #pragma unroll
@@ -331,6 +343,14 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
         }
         sc[t * NS + s] = v;
       }
+    if (filt) {
+      // Rows whose value does not start with the slot's next token drop out:
+      // NaN fails every threshold test and is ignored by fmaxf.
+      const int f = fring[tslot * 64 + (TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * 16 + m];
+#pragma unroll
+      for (int j = 0; j < NP; ++j)
+        if (f != (NP <= 8 ? ntr[j] : nt_slot[g * NP + j])) sc[j] = __builtin_nanf("");
+    }
     // v >= thr exactly when v - thr >= 0 (round-to-nearest keeps the sign).
     float mt[QTW];
 #pragma unroll
@@ -356,8 +376,9 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     const int64_t tstep = p.stride * KBT * kBlockBytes;  // bytes between visited tiles
     const unsigned char *dbase = static_cast<const unsigned char *>(p.data) + v0 * tstep;
     const uint32_t voff0 = (uint32_t)lane * 16u, voff1 = voff0 + kBlockBytes;
-    // LDS offset of the ring: the low half of a generic LDS address.
+    // LDS offsets: the low half of a generic LDS address.
     const uint32_t ring = (uint32_t)(uintptr_t)smem;
+    const uint32_t fring_lds = (uint32_t)(uintptr_t)fring;
     // Copy this wave's 2 blocks of stage `st` into ring slot `slot`.
     auto issue = [&](int64_t st, int slot) {
       int64_t j = st * SB + wv * 2;
@@ -366,6 +387,14 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
       const unsigned char *src = dbase + vt * tstep + (j - vt * KBT) * kBlockBytes;
       copy2_to_lds(src, voff0, voff1,
                    ring + (uint32_t)(slot * SB + wv * 2) * (uint32_t)kBlockBytes);
+      if (filt) {
+        // first tokens of the stage's tiles: lane l takes row l % 16 of the
+        // stage's (l / 16)-th tile (clamped to the last tile)
+        int64_t ft = (TPS > 1 ? st * TPS : st / SPT) + (lane >> 4);
+        ft = ft < ntile ? ft : ntile - 1;
+        copy1_to_lds(p.ftok + (v0 + ft) * p.stride * kTileRows + (lane & 15),
+                     fring_lds + (uint32_t)slot * 256u);
+      }
     };
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) issue(st, st);
@@ -380,7 +409,8 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
           // Stage start: this wave's copies of it have landed; after the
           // barrier so have every wave's, and the slot consumed last is free
           // for the copy S - 1 stages ahead.
-          wait_vmcnt<WAIT>();
+          if (filt) wait_vmcnt<WAIT + (S - 2)>();  // one more copy per stage
+          else wait_vmcnt<WAIT>();
           __syncthreads();
           issue(next_st, next_slot);
           ++next_st;
@@ -420,6 +450,7 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
           if (i + 2 < BPT) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
           __builtin_amdgcn_sched_group_barrier(0x008, 2 * QTW, 0);
         }
+        tslot = cur_slot;
         if (TPS == 1 || (vt & (TPS - 1)) == TPS - 1)  // stage end
           cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
       }
@@ -470,14 +501,14 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   }
 }
 
-template <int DT, int QTW, int KBT, int CPQ, int S>
+template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
 __global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_main(ScanParams p) {
-  scan_mq_body<DT, QTW, KBT, CPQ, S>(p);
+  scan_mq_body<DT, QTW, KBT, CPQ, S, FILT>(p);
 }
 
-template <int DT, int QTW, int KBT, int CPQ, int S>
+template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
 __global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_sample(ScanParams p) {
-  scan_mq_body<DT, QTW, KBT, CPQ, S>(p);
+  scan_mq_body<DT, QTW, KBT, CPQ, S, FILT>(p);
 }
 
 // One thread per 16-byte chunk (t, kb, lane) of the query operands.
@@ -495,11 +526,14 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
 
 // (QTW, KBT) pairs with QTW * KBT <= 32 (query operands <= 128 VGPRs), each
 // with its ring depth S.
-#define DRESD_MQ_CASE(DT, CPQ, QTW, KBT, S)                                      \
-  if (qtw == QTW && kbt == KBT) {                                                \
-    *stages = S;                                                                 \
-    return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S>       \
-                     : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S>;    \
+#define DRESD_MQ_CASE(DT, CPQ, QTW, KBT, S)                                               \
+  if (qtw == QTW && kbt == KBT) {                                                         \
+    *stages = S;                                                                          \
+    if (filtered)                                                                         \
+      return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S, true>        \
+                       : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S, true>;     \
+    return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S, false>         \
+                     : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S, false>;      \
   }
 #define DRESD_MQ_ALL(DT, CPQ)                                                     \
   DRESD_MQ_CASE(DT, CPQ, 1, 4, 4) DRESD_MQ_CASE(DT, CPQ, 1, 8, 4)                 \
@@ -509,14 +543,14 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
   DRESD_MQ_CASE(DT, CPQ, 4, 8, 6)
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
-ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, int *stages) {
+ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, bool filtered, int *stages) {
   DRESD_MQ_ALL(kF16, 1)
   return nullptr;
 }
 void *qop_kernel_f16() { return (void *)dresd_query_operand<kF16, 1>; }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
-ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, int *stages) {
+ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, bool filtered, int *stages) {
   DRESD_MQ_ALL(kBF16, 4)
   return nullptr;
 }

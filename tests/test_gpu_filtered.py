@@ -1,0 +1,133 @@
+"""Parity of next-token-filtered retrieval (DReSD Section 3.5: drafts that do
+not start with the LLM's next token x_{t+1} are dropped; read as
+filter-then-select) between the HIP path and the CPU oracle.
+
+Each batch mixes the realistic case (the next token of the query's source
+row, so the source row competes), a frequent token, a token matching fewer
+rows than k (the result is padded with -1 / -inf / zero tokens) and a token
+matching no row.  Covers both scan kernels (single-tile and shared-key) and
+the sampled threshold passes.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from datagen import WORKLOADS, generate, to_numpy_bits
+from parity import TOL, check_batch
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "filtered_closed_forms.json")
+_TD = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+NO_ROW_TOKEN = 1 << 30  # no continuation starts with it
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_filtered(keys, cont, queries, next_tok, k, dtype):
+    from paper_2502_15572_amd import Index
+    ix = Index(keys.to(DEV), cont.to(DEV))
+    nt = torch.as_tensor(np.asarray(next_tok, np.int32)).to(DEV)
+    idx, score, tok = ix.search(queries.to(DEV, torch.float32), k, next_tok=nt)
+    torch.cuda.synchronize()
+    ix.close()
+    kb, dt = to_numpy_bits(keys)
+    qn = queries.cpu().numpy().astype(np.float32)
+    cn = cont.cpu().numpy()
+    o_idx, o_score, _, o_next = oracle.topk(kb, dt, qn, k, cn, next_tok=next_tok)
+    return check_batch(idx.cpu().numpy(), score.cpu().numpy(), tok.cpu().numpy(), o_idx, o_score,
+                       o_next, lambda b, rows: oracle.score_rows(kb, dt, qn[b], rows), kb.shape[0],
+                       cn, TOL[dt], next_tok=next_tok)
+
+
+def mixed_tokens(cont, src, B, k, seed):
+    """Per query: its source row's next token, or a frequent one, a rare one
+    (fewer than k matching rows) or none at all."""
+    c0 = cont[:, 0].numpy()
+    vals, counts = np.unique(c0, return_counts=True)
+    frequent = int(vals[np.argmax(counts)])
+    rare = vals[counts < k]
+    rare_tok = int(rare[0]) if rare.size else frequent
+    rng = np.random.default_rng(seed)
+    out = []
+    for b in range(B):
+        r = b % 4
+        if r == 0:
+            out.append(int(c0[int(src[b])]) if int(src[b]) >= 0 else frequent)
+        elif r == 1:
+            out.append(frequent)
+        elif r == 2:
+            out.append(rare_tok)
+        else:
+            out.append(NO_ROW_TOKEN)
+    return np.asarray(out, np.int32)
+
+
+def test_filtered_golden_on_gpu(gpu_lib):
+    g = json.load(open(GOLDEN))
+    n = len(g["first_tokens"])
+    cont = torch.stack([torch.tensor(g["first_tokens"], dtype=torch.int32),
+                        torch.arange(n, dtype=torch.int32) + 100], dim=1)
+    q = torch.tensor([g["query"]], dtype=torch.float32)
+    from paper_2502_15572_amd import Index
+    for dt in ("f32", "f16", "bf16"):
+        ix = Index(torch.eye(n, dtype=_TD[dt], device=DEV), cont.to(DEV))
+        for c in g["cases"]:
+            say("filtered golden", dt, c["name"])
+            nt = torch.tensor([c["next_tok"]], dtype=torch.int32, device=DEV)
+            idx, score, tok = ix.search(q.to(DEV), c["k"], next_tok=nt)
+            assert idx[0].tolist() == c["idx"], (dt, c["name"], idx[0].tolist())
+            want = [float("-inf") if v == "-inf" else float(np.float32(v)) for v in c["score"]]
+            assert score[0].cpu().tolist() == want, (dt, c["name"], score[0].tolist())
+            for r, i in enumerate(c["idx"]):
+                want_tok = cont[i].tolist() if i >= 0 else [0, 0]
+                assert tok[0, r].cpu().tolist() == want_tok
+        ix.close()
+
+
+FILTERED = [
+    # (workload, reduced N, batches)
+    ("flat16k_d256_f32", 16384, (8,)),
+    ("hidden1m_d4096_bf16", 6000 + 5, (1, 4)),
+    ("pca4m_d1024_f16", 40000 + 3, (1, 16)),
+    ("batch10m_d256_f16", 120000 + 9, (64, 256)),
+    ("zipf33m_d128_f16", 200000 + 11, (1, 128)),
+]
+
+
+@pytest.mark.parametrize("name,N,batches", FILTERED, ids=[f[0] for f in FILTERED])
+def test_filtered_parity_reduced(gpu_lib, name, N, batches):
+    w = WORKLOADS[name].scaled(N)
+    g = generate(w, "cpu")
+    for B in batches:
+        nt = mixed_tokens(g["cont"], g["query_src"], B, w.k, seed=B)
+        say("filtered", name, "N=%d B=%d k=%d tokens %s" % (N, B, w.k, nt[:4].tolist()))
+        rep = run_filtered(g["keys"], g["cont"], g["queries"][:B], nt, w.k, w.dtype)
+        say("  exact-order rate %.3f" % rep["exact_order_rate"])
+
+
+def test_filtered_all_rows_match_equals_unfiltered(gpu_lib):
+    """A token every row starts with filters nothing: same result as the
+    unfiltered search, bit for bit (shared-key scan and sampled passes)."""
+    say("filtered all-match")
+    w = WORKLOADS["batch10m_d256_f16"].scaled(60000)
+    g = generate(w, "cpu")
+    cont = g["cont"].clone()
+    cont[:, 0] = 5
+    from paper_2502_15572_amd import Index
+    ix = Index(g["keys"].to(DEV), cont.to(DEV))
+    q = g["queries"][:100].to(DEV)
+    a = ix.search(q, w.k)
+    b = ix.search(q, w.k, next_tok=torch.full((100,), 5, dtype=torch.int32, device=DEV))
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    ix.close()
