@@ -160,3 +160,27 @@ class mutation:
     def __exit__(self, *exc):
         _load().oracle_set_mutation(0)
         return False
+
+
+def transform(x: np.ndarray, mean: np.ndarray, var: np.ndarray, W: np.ndarray,
+              eps_z: float = 1e-5, eps_n: float = 1e-12) -> np.ndarray:
+    """Query-side transform of Algorithm 1 steps 4-6, in fp64, in the paper's
+    order: z-score normalisation with the datastore's per-dimension mean and
+    variance (Section 3.2, Eq. 1: (v - E[V]) / sqrt(Var[V] + eps)), projection
+    onto the first l principal components (Section 3.3: v W_l), and L2
+    normalisation (Section 3.4, Eq. 2: v_l / max(||v_l||_2, eps)).
+
+    x [M, D], mean [D], var [D], W [D, l]; returns [M, l] float64.
+    """
+    x = np.asarray(x, np.float64)
+    mu = np.asarray(mean, np.float64)
+    vr = np.asarray(var, np.float64)
+    Wl = np.asarray(W, np.float64)
+    if x.ndim != 2 or Wl.ndim != 2 or Wl.shape[0] != x.shape[1]:
+        raise ValueError("x must be [M, D] and W [D, l]")
+    if mu.shape != (x.shape[1],) or vr.shape != (x.shape[1],):
+        raise ValueError("mean and var must be [D]")
+    z = (x - mu) / np.sqrt(vr + eps_z)                                   # Eq. 1
+    v = z @ Wl                                                           # Section 3.3
+    n = np.sqrt(np.sum(v * v, axis=1, keepdims=True))
+    return v / np.maximum(n, eps_n)                                      # Eq. 2
