@@ -92,6 +92,39 @@ def cpu_baseline(keys_dev, queries, k, budget_s=12.0):
                       "pool) in %.1f s, after one untimed warm-up search" % (done, el)}
 
 
+def time_transform(args):
+    """Time the query-side transform (z-score, projection, L2) of B rows."""
+    import torch
+    from datagen import WORKLOADS
+    from paper_2502_15572_amd import transform
+    w = WORKLOADS[args.workload]
+    B, D, l = args.batch, args.transform, w.d
+    g = torch.Generator(device="cuda").manual_seed(0)
+    x = torch.randn(B, D, device="cuda", generator=g)
+    mean = torch.randn(D, device="cuda", generator=g)
+    var = torch.rand(D, device="cuda", generator=g) + 0.5
+    W = torch.randn(D, l, device="cuda", generator=g) / D ** 0.5
+    y = torch.empty(B, l, device="cuda")
+    for _ in range(args.warmup):
+        transform(x, mean, var, W, out=y)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:
+        a.record()
+        transform(x, mean, var, W, out=y)
+        b.record()
+    torch.cuda.synchronize()
+    per = sorted(a.elapsed_time(b) for a, b in ev)
+    p50 = statistics.median(per)
+    flops = 2.0 * B * D * l
+    byts = 4.0 * (B * D + D * l + 2 * D + 2 * B * l)
+    print(json.dumps({"transform": {"B": B, "D": D, "l": l, "p50_us": p50 * 1e3,
+                                    "TFLOPs": flops / (p50 * 1e-3) / 1e12,
+                                    "frac_fp32_mfma_peak": flops / (p50 * 1e-3) / 157.3e12,
+                                    "GBps": byts / (p50 * 1e-3) / 1e9}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -106,6 +139,9 @@ def main():
                     help="next-token-filtered search: each query's next token is the first "
                          "token of its source row's continuation (the most frequent first "
                          "token for queries without a source row)")
+    ap.add_argument("--transform", type=int, default=0, metavar="D",
+                    help="only time the query-side transform: B rows of D fp32 dims projected "
+                         "to the workload's d (Eq. 1, Section 3.3, Eq. 2)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -116,6 +152,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.transform:
+        time_transform(args)
         return
 
     import torch

@@ -157,6 +157,39 @@ dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms,
                                 double *search_ms, int64_t *searches);
 
 /*
+ * Query-side transform of Algorithm 1 steps 4-6, for decode-step queries (or,
+ * once, for the datastore rows that become keys):
+ *   z   = (x - mean) / sqrt(var + eps_z)        z-score normalisation, Eq. 1
+ *   v   = z W                                   first l principal components,
+ *                                               Section 3.3
+ *   y   = v / max(||v||_2, eps_n)               L2 normalisation, Eq. 2
+ *
+ *   x       device, [M, D] fp32 row-major (e.g. last hidden states).
+ *   M       0 <= M < 2^31; M == 0 is a no-op.
+ *   D       1 <= D <= 2^20.
+ *   mean    device, [D] fp32: E[V] of the datastore sample.
+ *   var     device, [D] fp32: Var[V] of the datastore sample (>= 0).
+ *   eps_z   finite, >= 0 (the paper's eps of Eq. 1; 1e-5 is a common choice).
+ *   W       device, [D, l] fp32 row-major: the principal components W_l.
+ *   l       1 <= l <= 16384.
+ *   eps_n   finite, >= 0 (the eps of Eq. 2; 1e-12 is a common choice).
+ *   y       device, [M, l] fp32 row-major output (ready for dresd_search).
+ *   stream  stream the transform runs on (asynchronous).
+ * Arithmetic: fp32, the projection on the fp32 matrix cores; batches with
+ * few output tiles split D across workgroups and add the partial sums in a
+ * fixed order, so results are deterministic.  Ownership: all buffers are
+ * caller-owned and must stay alive until `stream` completes; the partial sums
+ * use a per-device library buffer that is allocated (synchronously) on the
+ * first call that needs a larger one and kept until the process ends, so
+ * calls that overlap on one device must be serialised by the caller.
+ * Errors: EINVAL (null pointer with M > 0, sizes or eps out of range),
+ * ENOMEM, EDEVICE.
+ */
+dresd_status dresd_transform(const float *x, int64_t M, int32_t D, const float *mean,
+                             const float *var, float eps_z, const float *W, int32_t l,
+                             float eps_n, float *y, dresd_stream stream);
+
+/*
  * Describe how the next search of this shape would run (host outputs, NULL
  * allowed): the number of passes over sampled keys before the main pass, the
  * number of waves of the main scan, the bytes of workspace it needs, and

@@ -124,3 +124,29 @@ class Index:
             self.close()
         except Exception:
             pass
+
+
+def transform(x, mean, var, W, eps_z: float = 1e-5, eps_n: float = 1e-12, out=None, stream=None):
+    """Query-side transform of Algorithm 1 steps 4-6 on the GPU: z-score
+    normalisation (Eq. 1), projection onto the principal components W
+    ([D, l], Section 3.3) and L2 normalisation (Eq. 2).  All tensors are
+    float32 on the GPU; returns y [M, l]."""
+    import torch
+    for name, t in (("x", x), ("mean", mean), ("var", var), ("W", W)):
+        if not t.is_cuda or t.dtype != torch.float32:
+            raise TypeError("%s must be a float32 GPU tensor" % name)
+    if x.dim() != 2 or W.dim() != 2 or W.shape[0] != x.shape[1]:
+        raise ValueError("x must be [M, D] and W [D, l]")
+    M, D = int(x.shape[0]), int(x.shape[1])
+    l = int(W.shape[1])
+    if mean.numel() != D or var.numel() != D:
+        raise ValueError("mean and var must hold D values")
+    x, mean, var, W = x.contiguous(), mean.contiguous(), var.contiguous(), W.contiguous()
+    y = torch.empty((M, l), dtype=torch.float32, device=x.device) if out is None else out
+    lib = _lib.load()
+    _lib.check(lib.dresd_transform(ctypes.c_void_p(x.data_ptr()), M, D,
+                                   ctypes.c_void_p(mean.data_ptr()),
+                                   ctypes.c_void_p(var.data_ptr()), float(eps_z),
+                                   ctypes.c_void_p(W.data_ptr()), l, float(eps_n),
+                                   ctypes.c_void_p(y.data_ptr()), _stream_handle(stream)))
+    return y

@@ -33,7 +33,8 @@ HIPCC_FLAGS = [
 UNITS = [("dresd_kernels.hip", ["-DDRESD_TU=%d" % t], "kernels%d" % t) for t in range(5)] + [
     ("dresd_scan_mq.hip", ["-DDRESD_MQ_TU=0"], "scanmq0"),
     ("dresd_scan_mq.hip", ["-DDRESD_MQ_TU=1"], "scanmq1"),
-    ("dresd_merge.hip", [], "merge"), ("dresd_runtime.hip", [], "runtime")]
+    ("dresd_merge.hip", [], "merge"), ("dresd_transform.hip", [], "transform"),
+    ("dresd_runtime.hip", [], "runtime")]
 
 
 def _compile(hipcc, src, defs, obj, verbose):

@@ -113,6 +113,23 @@ struct LayoutParams {
   int d, KB;
 };
 
+// Query-side transform (dresd_transform.hip): y = unit rows of
+// ((x - mean) / sqrt(var + eps_z)) W.
+struct TransformParams {
+  const float *x;            // [M, D]
+  const float *mean, *var;   // [D]
+  const float *W;            // [D, l] row-major
+  float *y;                  // [M, l]
+  float *part;               // [splits][M][l] partial sums (splits > 1)
+  int64_t M;
+  int D, l;
+  int splits, dslice;        // D split into `splits` slices of `dslice` dims
+  float eps_z, eps_n;
+};
+// Splits of D for an M x l output on a device with `cus` compute units.
+int transform_splits(int64_t M, int D, int l, int cus);
+hipError_t launch_transform(const TransformParams &p, hipStream_t st);
+
 // Kernel launch entry points (defined in dresd_kernels.hip).
 typedef void (*ScanKernel)(ScanParams);
 ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass);  // cpq: columns per query

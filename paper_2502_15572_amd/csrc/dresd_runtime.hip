@@ -8,6 +8,8 @@
 #include <vector>
 
 #include "dresd.h"
+#include <math.h>
+
 #include "dresd_internal.h"
 
 using namespace dresd;
@@ -566,6 +568,61 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
 }  // namespace
 
 extern "C" {
+
+dresd_status dresd_transform(const float *x, int64_t M, int32_t D, const float *mean,
+                             const float *var, float eps_z, const float *W, int32_t l, float eps_n,
+                             float *y, dresd_stream stream) {
+  if (M < 0 || M > (int64_t)0x7fffffff) return fail(DRESD_EINVAL, "M out of range");
+  if (D < 1 || D > (1 << 20)) return fail(DRESD_EINVAL, "D out of range");
+  if (l < 1 || l > 16384) return fail(DRESD_EINVAL, "l out of range");
+  if (!(eps_z >= 0.f) || !(eps_n >= 0.f) || eps_z == HUGE_VALF || eps_n == HUGE_VALF)
+    return fail(DRESD_EINVAL, "eps must be finite and >= 0");
+  if (M == 0) return DRESD_OK;
+  if (!x || !mean || !var || !W || !y) return fail(DRESD_EINVAL, "NULL pointer argument");
+  int dev = 0;
+  DRESD_HIP(hipGetDevice(&dev));
+  int cus = 0;
+  DRESD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  TransformParams p;
+  p.splits = transform_splits(M, D, l, cus);
+  p.dslice = (int)ceil_div(D, p.splits);
+  p.part = nullptr;
+  if (p.splits > 1) {
+    // Partial sums of the D slices: a per-device buffer kept for the life of
+    // the process, grown (synchronously) when a larger one is needed.
+    static std::mutex mu;
+    static std::vector<std::pair<void *, size_t>> bufs;
+    const size_t need = (size_t)p.splits * (size_t)M * (size_t)l * sizeof(float);
+    std::lock_guard<std::mutex> lock(mu);
+    if (bufs.size() <= (size_t)dev) bufs.resize((size_t)dev + 1, {nullptr, 0});
+    if (bufs[dev].second < need) {
+      if (bufs[dev].first) {
+        DRESD_HIP(hipDeviceSynchronize());
+        (void)hipFree(bufs[dev].first);
+        bufs[dev] = {nullptr, 0};
+      }
+      void *b = nullptr;
+      if (hipMalloc(&b, need) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(DRESD_ENOMEM, "transform workspace allocation failed");
+      }
+      bufs[dev] = {b, need};
+    }
+    p.part = static_cast<float *>(bufs[dev].first);
+  }
+  p.x = x;
+  p.mean = mean;
+  p.var = var;
+  p.W = W;
+  p.y = y;
+  p.M = M;
+  p.D = D;
+  p.l = l;
+  p.eps_z = eps_z;
+  p.eps_n = eps_n;
+  DRESD_HIP(launch_transform(p, static_cast<hipStream_t>(stream)));
+  return DRESD_OK;
+}
 
 dresd_status dresd_profile_enable(dresd_index *ix, int32_t on) {
   if (!ix) return fail(DRESD_EINVAL, "index is NULL");
