@@ -184,3 +184,45 @@ def transform(x: np.ndarray, mean: np.ndarray, var: np.ndarray, W: np.ndarray,
     v = z @ Wl                                                           # Section 3.3
     n = np.sqrt(np.sum(v * v, axis=1, keepdims=True))
     return v / np.maximum(n, eps_n)                                      # Eq. 2
+
+
+def pack_drafts(tokens: np.ndarray, r: int, length: int, eos: int = 0):
+    """Draft assembly for batch verification (Section 3.6): drafts are rows of
+    a [r, length] matrix padded with the EOS id.
+
+    For each query, walk its retrieved continuations in rank order; a draft is
+    the first ``length`` tokens with every token after the first EOS replaced
+    by EOS (the sequence has ended); drafts that start with EOS (nothing to
+    propose, e.g. the padding ranks of a filtered search) and drafts equal to
+    an earlier one are dropped; the first ``r`` remaining drafts fill the rows
+    and missing rows are all EOS.
+
+    tokens [B, k, L] int; returns (drafts [B, r, length] int32, count [B] int32).
+    """
+    t = np.asarray(tokens)
+    B, k, L = t.shape
+    if not (1 <= length <= L) or r < 1:
+        raise ValueError("need 1 <= length <= L and r >= 1")
+    out = np.full((B, r, length), eos, np.int32)
+    cnt = np.zeros(B, np.int32)
+    for b in range(B):
+        kept = []
+        for rank in range(k):
+            d = []
+            ended = False
+            for j in range(length):
+                v = int(t[b, rank, j])
+                if ended:
+                    v = eos
+                elif v == eos:
+                    ended = True
+                d.append(v)
+            if d[0] == eos or d in kept:
+                continue
+            kept.append(d)
+            if len(kept) == r:
+                break
+        for i, d in enumerate(kept):
+            out[b, i] = d
+        cnt[b] = len(kept)
+    return out, cnt
