@@ -190,6 +190,28 @@ dresd_status dresd_transform(const float *x, int64_t M, int32_t D, const float *
                              float eps_n, float *y, dresd_stream stream);
 
 /*
+ * Draft assembly for batch verification (Section 3.6): the retrieved
+ * continuations become the rows of an EOS-padded draft matrix.  For each
+ * query, in rank order: a draft is the first `length` tokens of a
+ * continuation with every token after its first EOS replaced by EOS; drafts
+ * that start with EOS (nothing to propose, e.g. the padding ranks of
+ * dresd_search_filtered) and repeats of an earlier draft are dropped; the
+ * first r remaining drafts fill the rows, and rows past them are all EOS.
+ *
+ *   tokens  device, [B, k, L] int32 (as written by dresd_search).
+ *   B >= 0 (0 is a no-op); 1 <= k <= DRESD_K_MAX; 1 <= L <= 4096;
+ *   1 <= r <= k drafts; 1 <= length <= L tokens per draft; eos: the EOS id.
+ *   drafts  device, [B, r, length] int32 output.
+ *   count   device, [B] int32 output: drafts kept per query (<= r).
+ *   stream  stream it runs on (asynchronous).
+ * Deterministic; allocates nothing; buffers are caller-owned.
+ * Errors: EINVAL (null pointer with B > 0, sizes out of range), EDEVICE.
+ */
+dresd_status dresd_pack_drafts(const int32_t *tokens, int32_t B, int32_t k, int32_t L,
+                               int32_t r, int32_t length, int32_t eos, int32_t *drafts,
+                               int32_t *count, dresd_stream stream);
+
+/*
  * Describe how the next search of this shape would run (host outputs, NULL
  * allowed): the number of passes over sampled keys before the main pass, the
  * number of waves of the main scan, the bytes of workspace it needs, and

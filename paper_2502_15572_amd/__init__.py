@@ -150,3 +150,25 @@ def transform(x, mean, var, W, eps_z: float = 1e-5, eps_n: float = 1e-12, out=No
                                    ctypes.c_void_p(W.data_ptr()), l, float(eps_n),
                                    ctypes.c_void_p(y.data_ptr()), _stream_handle(stream)))
     return y
+
+
+def pack_drafts(tokens, r: int, length: int, eos: int = 0, out=None, stream=None):
+    """Draft assembly for batch verification (Section 3.6) on the GPU: tokens
+    [B, k, L] int32 (from ``Index.search``) -> (drafts [B, r, length] int32,
+    count [B] int32): EOS-padded rows, drafts starting with EOS and repeats
+    dropped in rank order."""
+    import torch
+    if not tokens.is_cuda or tokens.dtype != torch.int32 or tokens.dim() != 3:
+        raise TypeError("tokens must be an int32 GPU tensor [B, k, L]")
+    B, k, L = (int(s) for s in tokens.shape)
+    t = tokens.contiguous()
+    if out is None:
+        drafts = torch.empty((B, r, length), dtype=torch.int32, device=t.device)
+        count = torch.empty((B,), dtype=torch.int32, device=t.device)
+    else:
+        drafts, count = out
+    lib = _lib.load()
+    _lib.check(lib.dresd_pack_drafts(ctypes.c_void_p(t.data_ptr()), B, k, L, int(r), int(length),
+                                     int(eos), ctypes.c_void_p(drafts.data_ptr()),
+                                     ctypes.c_void_p(count.data_ptr()), _stream_handle(stream)))
+    return drafts, count

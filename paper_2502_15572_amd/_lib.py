@@ -19,7 +19,8 @@ F32, F16, BF16 = 0, 1, 2
 
 EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_index_destroy",
            "dresd_last_error", "dresd_profile_enable", "dresd_profile_read",
-           "dresd_search_plan", "dresd_search_filtered", "dresd_transform"]
+           "dresd_search_plan", "dresd_search_filtered", "dresd_transform",
+           "dresd_pack_drafts"]
 
 _lock = threading.Lock()
 _lib = None
@@ -42,6 +43,8 @@ def _declare(lib):
     F = ctypes.c_float
     lib.dresd_transform.argtypes = [P, I64, I32, P, P, F, P, I32, F, P, P]
     lib.dresd_transform.restype = ctypes.c_int
+    lib.dresd_pack_drafts.argtypes = [P, I32, I32, I32, I32, I32, I32, P, P, P]
+    lib.dresd_pack_drafts.restype = ctypes.c_int
     lib.dresd_index_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I32),
                                      ctypes.POINTER(I32), ctypes.POINTER(I32)]
     lib.dresd_index_info.restype = ctypes.c_int

@@ -130,6 +130,15 @@ struct TransformParams {
 int transform_splits(int64_t M, int D, int l, int cus);
 hipError_t launch_transform(const TransformParams &p, hipStream_t st);
 
+// Draft assembly (dresd_drafts.hip): tokens [B, k, L] -> drafts [B, r, length],
+// count [B].
+struct DraftParams {
+  const int32_t *tokens;
+  int32_t *drafts, *count;
+  int B, k, L, r, length, eos;
+};
+hipError_t launch_pack_drafts(const DraftParams &p, hipStream_t st);
+
 // Kernel launch entry points (defined in dresd_kernels.hip).
 typedef void (*ScanKernel)(ScanParams);
 ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass);  // cpq: columns per query

@@ -624,6 +624,30 @@ dresd_status dresd_transform(const float *x, int64_t M, int32_t D, const float *
   return DRESD_OK;
 }
 
+dresd_status dresd_pack_drafts(const int32_t *tokens, int32_t B, int32_t k, int32_t L, int32_t r,
+                               int32_t length, int32_t eos, int32_t *drafts, int32_t *count,
+                               dresd_stream stream) {
+  if (B < 0) return fail(DRESD_EINVAL, "B must be >= 0");
+  if (k < 1 || k > DRESD_K_MAX) return fail(DRESD_EINVAL, "k must be in [1, DRESD_K_MAX]");
+  if (L < 1 || L > 4096) return fail(DRESD_EINVAL, "L out of range");
+  if (length < 1 || length > L) return fail(DRESD_EINVAL, "length must be in [1, L]");
+  if (r < 1 || r > k) return fail(DRESD_EINVAL, "r must be in [1, k]");
+  if (B == 0) return DRESD_OK;
+  if (!tokens || !drafts || !count) return fail(DRESD_EINVAL, "NULL pointer argument");
+  DraftParams p;
+  p.tokens = tokens;
+  p.drafts = drafts;
+  p.count = count;
+  p.B = B;
+  p.k = k;
+  p.L = L;
+  p.r = r;
+  p.length = length;
+  p.eos = eos;
+  DRESD_HIP(launch_pack_drafts(p, static_cast<hipStream_t>(stream)));
+  return DRESD_OK;
+}
+
 dresd_status dresd_profile_enable(dresd_index *ix, int32_t on) {
   if (!ix) return fail(DRESD_EINVAL, "index is NULL");
   ix->prof = on != 0;
