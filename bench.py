@@ -33,26 +33,36 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
-    """Hash of every kernel source and header (a counter summary is valid
-    only for the code it was taken on)."""
+SCAN_UNIT = {"single_tile": "dresd_kernels.hip", "shared_key": "dresd_scan_mq.hip"}
+
+
+def kernel_hash(unit: str) -> str:
+    """Hash of one kernel source file and every header it includes (a counter
+    summary is valid only for the code it was taken on)."""
+    seen, todo = [], [unit]
+    while todo:
+        f = todo.pop()
+        if f in seen or not os.path.exists(os.path.join(CSRC, f)):
+            continue
+        seen.append(f)
+        todo += re.findall(r'^#include "([^"]+)"', open(os.path.join(CSRC, f)).read(), re.M)
     h = hashlib.sha256()
-    for f in sorted(os.listdir(CSRC)):
-        if f.endswith((".hip", ".h")):
-            h.update(f.encode() + open(os.path.join(CSRC, f), "rb").read())
+    for f in sorted(seen):
+        h.update(f.encode() + open(os.path.join(CSRC, f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload: str, batch: int):
+def read_traffic(workload: str, batch: int, scan_kernel: str):
     """HBM bytes per main-scan launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None."""
+    summary, if it was taken on the current source of that scan kernel; else
+    None."""
     path = os.path.join(ROOT, "profiles", "traffic_scan_%s_B%d.md" % (workload, batch))
     if not os.path.exists(path):
         return None
     txt = open(path).read()
     m = re.search(r"^kernel_source_sha256_16:\s*(\S+)", txt, re.M)
     b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt, re.M)
-    if not m or not b or m.group(1) != kernel_hash():
+    if not m or not b or m.group(1) != kernel_hash(SCAN_UNIT[scan_kernel]):
         return None
     return float(b.group(1))
 
@@ -229,7 +239,7 @@ def main():
     # The scan's floor is the larger of its HBM time and its matrix-core time.
     mfma_peak = MFMA_PEAK_TFLOPS[w.dtype] * 1e12
     mfma_bound = flops / mfma_peak > scan_bytes / (HBM_PEAK_GBPS * 1e9)
-    traffic = read_traffic(w.name, B) if not args.n else None
+    traffic = read_traffic(w.name, B, plan["scan_kernel"]) if not args.n else None
 
     res = {
         "metric": "retrieval queries/s + p50 latency at B=1; achieved HBM GB/s vs peak",
