@@ -12,8 +12,13 @@ key -> next-tokens store) with unit-norm keys and queries (Section 3.4,
 Eq. 2), generalised to the k best keys that batch verification consumes
 (Section 3.6); ``topk(..., next_tok=...)`` adds the next-token filter of
 Section 3.5 (only rows whose value starts with the query's next token
-compete).  This module only marshals numpy arrays into that library and
-builds it with gcc when it is missing.
+compete); ``topk_partitioned`` is the partitioned (inverted-file) reading
+of the paper's approximate search: the exact k best rows among the
+partitions each query probes.  This module marshals numpy arrays into that
+library (building it with gcc when it is missing) and holds the fp64 numpy
+oracles of the steps around the search: the query-side transform (Eqs. 1-2,
+Section 3.3), spherical k-means (the partitioning of the partitioned search)
+and draft assembly (Section 3.6).
 """
 from __future__ import annotations
 
@@ -59,6 +64,10 @@ def _load():
                                                  P, ctypes.c_int32, ctypes.c_int32, P,
                                                  ctypes.c_int32, P, P, P, P, P, ctypes.c_int32]
             lib.oracle_topk_filtered.restype = ctypes.c_int
+            I32 = ctypes.c_int32
+            lib.oracle_topk_partitioned.argtypes = [P, ctypes.c_int, ctypes.c_int64, I32, P, I32,
+                                                    I32, P, I32, P, I32, P, I32, P, P, P, P, I32]
+            lib.oracle_topk_partitioned.restype = ctypes.c_int
             lib.oracle_score_rows.argtypes = [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
                                               P, P, ctypes.c_int64, P]
             lib.oracle_score_rows.restype = ctypes.c_int
@@ -132,6 +141,93 @@ def topk(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
     if rc != 0:
         raise RuntimeError("oracle top-k failed")
     return idx, score, tok, nxt
+
+
+def topk_partitioned(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
+                     assign, P: int, probes, cont: np.ndarray | None = None, threads: int = 0):
+    """Partitioned retrieval (the approximate search of Section 3.5, read as
+    an inverted file): row i belongs to partition ``assign[i]`` in [0, P);
+    query b returns the exact k best rows among the partitions listed in
+    ``probes[b]`` (entries outside [0, P) ignored, repeats counted once).
+    Same outputs and padding as ``topk(..., next_tok=...)``."""
+    e = _emb_bits(emb, dtype)
+    q = np.ascontiguousarray(queries, dtype=np.float32)
+    if q.ndim != 2 or q.shape[1] != e.shape[1]:
+        raise ValueError("queries must be [B, d]")
+    N, d = e.shape
+    B = q.shape[0]
+    if not (1 <= k <= N):
+        raise ValueError("need 1 <= k <= N")
+    a = np.ascontiguousarray(assign, dtype=np.int32).reshape(-1)
+    if a.shape[0] != N:
+        raise ValueError("assign must hold one partition per row")
+    pr = np.ascontiguousarray(probes, dtype=np.int32)
+    if pr.ndim != 2 or pr.shape[0] != B:
+        raise ValueError("probes must be [B, S]")
+    idx = np.empty((B, k), np.int64)
+    score = np.empty((B, k), np.float32)
+    nxt = np.empty((B,), np.float32)
+    tok, L, cptr = None, 0, None
+    if cont is not None:
+        c = np.ascontiguousarray(cont, dtype=np.int32)
+        if c.ndim != 2 or c.shape[0] != N:
+            raise ValueError("continuations must be [N, L]")
+        L = c.shape[1]
+        tok = np.empty((B, k, L), np.int32)
+        cptr = c.ctypes.data
+    rc = _load().oracle_topk_partitioned(
+        e.ctypes.data, DTYPE_CODES[dtype], N, d, q.ctypes.data, B, k, cptr, L, a.ctypes.data,
+        int(P), pr.ctypes.data, pr.shape[1], idx.ctypes.data, score.ctypes.data,
+        tok.ctypes.data if tok is not None else None, nxt.ctypes.data, int(threads))
+    if rc != 0:
+        raise RuntimeError("oracle partitioned top-k failed (assignment out of range?)")
+    return idx, score, tok, nxt
+
+
+def decode_keys(emb: np.ndarray, dtype: str) -> np.ndarray:
+    """Key rows as float64 (exact for f32, f16 and bf16 bits)."""
+    e = _emb_bits(emb, dtype)
+    if dtype == "bf16":
+        return (e.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if dtype == "f16" and e.dtype == np.uint16:
+        return e.view(np.float16).astype(np.float64)
+    return e.astype(np.float64)
+
+
+def kmeans_assign(x: np.ndarray, centroids: np.ndarray):
+    """Assignment step of spherical k-means, the partitioning behind the
+    partitioned search: each row goes to the centroid with the largest inner
+    product (cosine for unit rows, Eq. 3), ties to the lowest centroid id.
+    x [n, d] float64 (``decode_keys``), centroids [P, d]; returns
+    (assign [n] int32, best score [n] float64, all scores [n, P] float64)."""
+    s = np.asarray(x, np.float64) @ np.asarray(centroids, np.float64).T
+    a = np.argmax(s, axis=1)  # first maximum = lowest id
+    return a.astype(np.int32), s[np.arange(s.shape[0]), a], s
+
+
+def kmeans_update(x: np.ndarray, assign, centroids: np.ndarray) -> np.ndarray:
+    """Update step of spherical k-means: each centroid becomes the unit
+    vector along the sum of its rows; a partition with no rows (or a zero
+    sum) keeps its previous centroid.  Returns [P, d] float64."""
+    x = np.asarray(x, np.float64)
+    c = np.array(centroids, np.float64)
+    a = np.asarray(assign).reshape(-1)
+    P = c.shape[0]
+    if a.shape[0] != x.shape[0] or (a.size and (a.min() < 0 or a.max() >= P)):
+        raise ValueError("assign must hold one partition in [0, P) per row")
+    sums = np.zeros_like(c)
+    np.add.at(sums, a, x)
+    n = np.sqrt(np.sum(sums * sums, axis=1))
+    ok = n > 0
+    c[ok] = sums[ok] / n[ok, None]
+    return c
+
+
+def kmeans_objective(x: np.ndarray, centroids: np.ndarray) -> float:
+    """Sum over rows of the best inner product with a centroid: the quantity
+    spherical k-means never decreases."""
+    return float(np.sum(np.max(np.asarray(x, np.float64) @ np.asarray(centroids, np.float64).T,
+                               axis=1)))
 
 
 def score_rows(emb: np.ndarray, dtype: str, query: np.ndarray, rows) -> np.ndarray:

@@ -32,6 +32,13 @@
  * returned; ranks past the number of matching rows hold index -1, score
  * -inf and zero tokens.
  *
+ * Partitioned retrieval (the approximate search the paper runs through its
+ * ANN library, Section 3.5, read as an inverted file): every row belongs to
+ * one partition (assign[i] in [0, P)), each query probes a set of
+ * partitions, and oracle_topk_partitioned returns the exact k best rows among
+ * the rows of the probed partitions, with the same padding as the filter.
+ * Probe entries outside [0, P) are ignored and repeated entries count once.
+ *
  * Parity pins live in the CPU tests (closed forms, exact brute force,
  * invariants, duplicates, self-retrieval MRR of Eq. 4, planted mutations).
  */
@@ -147,10 +154,18 @@ static void offer(item *best, int64_t *count, int64_t m, item x) {
   if (c < m) *count = c + 1;
 }
 
+/* Partitioned retrieval: probed[b * P + p] != 0 when query b probes
+ * partition p; assign[i] is row i's partition.  NULL when not partitioned. */
+static const int32_t *g_assign = NULL;
+static const unsigned char *g_probed = NULL;
+static int32_t g_parts = 0;
+
 /* Row i takes part for query b: every row without a filter; with one, the
- * rows whose value starts with that query's next token. */
+ * rows whose value starts with that query's next token; in a partitioned
+ * search, the rows of the partitions the query probes. */
 static int admitted(const int32_t *cont, int32_t L, const int32_t *next_tok, int64_t i,
                     int32_t b) {
+  if (g_probed && !g_probed[(int64_t)b * g_parts + g_assign[i]]) return 0;
   if (!next_tok) return 1;
   /* mutation 8: the filter reads the value's second token */
   int32_t first = cont[i * L + ((g_mutation == 8 && L > 1) ? 1 : 0)];
@@ -275,6 +290,38 @@ int oracle_topk_filtered(const void *emb, int dtype, int64_t N, int32_t d, const
   if (!next_tok) return -1;
   return topk_impl(emb, dtype, N, d, Q, B, k, cont, L, next_tok, idx, score, tokens, next_score,
                    nthreads);
+}
+
+/* Partitioned retrieval: assign [N] int32 in [0, P); probes [B, S] int32
+ * (entries outside [0, P) ignored).  Not reentrant (the probe sets live in
+ * file-scope state for the duration of the call). */
+int oracle_topk_partitioned(const void *emb, int dtype, int64_t N, int32_t d, const float *Q,
+                            int32_t B, int32_t k, const int32_t *cont, int32_t L,
+                            const int32_t *assign, int32_t P, const int32_t *probes, int32_t S,
+                            int64_t *idx, float *score, int32_t *tokens, float *next_score,
+                            int32_t nthreads) {
+  if (!assign || P < 1 || S < 0 || (S > 0 && !probes) || B < 0) return -1;
+  for (int64_t i = 0; i < N; ++i)
+    if (assign[i] < 0 || assign[i] >= P) return -1;
+  unsigned char *probed = (unsigned char *)calloc((size_t)(B > 0 ? B : 1) * (size_t)P, 1);
+  if (!probed) return -1;
+  /* mutation 9: the last probe of every query is lost */
+  const int32_t used = (g_mutation == 9 && S > 0) ? S - 1 : S;
+  for (int32_t b = 0; b < B; ++b)
+    for (int32_t j = 0; j < used; ++j) {
+      const int32_t p = probes[(int64_t)b * S + j];
+      if (p >= 0 && p < P) probed[(int64_t)b * P + p] = 1;
+    }
+  g_assign = assign;
+  g_probed = probed;
+  g_parts = P;
+  const int rc = topk_impl(emb, dtype, N, d, Q, B, k, cont, L, NULL, idx, score, tokens,
+                           next_score, nthreads);
+  g_assign = NULL;
+  g_probed = NULL;
+  g_parts = 0;
+  free(probed);
+  return rc;
 }
 
 /* Scores of the given rows for one query (the same arithmetic as above);
