@@ -36,6 +36,7 @@ extern "C" {
 #endif
 
 typedef struct dresd_index dresd_index; /* opaque, library-owned */
+typedef struct dresd_ivf dresd_ivf;     /* opaque: partitioned index */
 typedef void *dresd_stream;             /* a hipStream_t */
 
 /* Storage type of the keys.  Queries are always fp32; scores are fp32. */
@@ -53,6 +54,8 @@ typedef enum {
 #define DRESD_K_MAX 1024
 /* Largest datastore: row indices are carried in 32 bits inside the kernels. */
 #define DRESD_N_MAX 4294967040LL
+/* Most partitions of a partitioned index. */
+#define DRESD_PARTS_MAX (1 << 24)
 
 /*
  * Build an index over N keys (Section 3.5: keys are token embeddings, values
@@ -223,6 +226,55 @@ dresd_status dresd_pack_drafts(const int32_t *tokens, int32_t B, int32_t k, int3
 dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,
                                int32_t *sample_passes, int32_t *scan_waves,
                                int64_t *workspace_bytes, int32_t *scan_kind);
+
+/*
+ * Partitioned (approximate) search.  The paper retrieves with an approximate
+ * nearest-neighbour library (Section 3.5); this is its partitioned reading,
+ * an inverted file: every key belongs to one of P partitions, each with a
+ * centroid, and a search scores only the keys of the nprobe partitions whose
+ * centroids score highest for the query.  The result is the exact top-k over
+ * those keys (same ranking, scores and tie rule as dresd_search), so it
+ * differs from dresd_search only where a true top-k key lies in a partition
+ * that was not probed.
+ *
+ * dresd_ivf_create: embeddings / continuations / N / d / L / dtype as in
+ *   dresd_index_create; centroids device [P, d] fp32 (unit rows, e.g. from
+ *   dresd_kmeans_*), 1 <= P <= DRESD_PARTS_MAX; assign device [N] int32, the
+ *   partition of each key, in [0, P).  Keys are stored grouped by partition
+ *   (each partition padded to a 16-row tile); continuations stay in row
+ *   order.  Copies everything, synchronises `stream`; the caller may free its
+ *   buffers afterwards.  One-time cost: the grouping is a counting sort on
+ *   the host.  Errors: EINVAL (nulls, ranges, an assignment outside [0, P)),
+ *   ENOMEM, EDEVICE.
+ * dresd_ivf_search: like dresd_search, probing 1 <= nprobe <= min(P,
+ *   DRESD_K_MAX) partitions per query (the nprobe best centroids by inner
+ *   product, ties to the lower id).  Ranks past the keys of the probed
+ *   partitions hold index -1, score -inf and zero tokens.  One search at a
+ *   time per index.
+ * dresd_ivf_search_probes: the same with caller-chosen partitions: probes
+ *   device [B, S] int32, 1 <= S <= DRESD_K_MAX; entries outside [0, P) are
+ *   ignored and repeats count once.
+ * dresd_ivf_info: host outputs (NULL allowed); tiles = 16-row tiles of the
+ *   partitioned layout (padding included).
+ * dresd_ivf_profile_enable / _read: as dresd_profile_*, for the scan of the
+ *   probed partitions and the whole search.
+ */
+dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuations, int64_t N,
+                              int32_t d, int32_t L, int32_t dtype, const float *centroids,
+                              int32_t P, const int32_t *assign, dresd_stream stream,
+                              dresd_ivf **out);
+void dresd_ivf_destroy(dresd_ivf *ivf);
+dresd_status dresd_ivf_info(const dresd_ivf *ivf, int64_t *N, int32_t *d, int32_t *L,
+                            int32_t *dtype, int32_t *P, int64_t *tiles);
+dresd_status dresd_ivf_search(dresd_ivf *ivf, const float *queries, int32_t B, int32_t k,
+                              int32_t nprobe, int64_t *idx, float *score, int32_t *tokens,
+                              dresd_stream stream);
+dresd_status dresd_ivf_search_probes(dresd_ivf *ivf, const float *queries, const int32_t *probes,
+                                     int32_t S, int32_t B, int32_t k, int64_t *idx, float *score,
+                                     int32_t *tokens, dresd_stream stream);
+dresd_status dresd_ivf_profile_enable(dresd_ivf *ivf, int32_t on);
+dresd_status dresd_ivf_profile_read(dresd_ivf *ivf, double *scan_ms, double *search_ms,
+                                    int64_t *searches);
 
 #ifdef __cplusplus
 }

@@ -14,7 +14,7 @@ import ctypes
 from . import _lib
 from ._lib import DresdError, K_MAX  # noqa: F401
 
-__all__ = ["Index", "DresdError", "K_MAX"]
+__all__ = ["Index", "PartitionedIndex", "DresdError", "K_MAX", "transform", "pack_drafts"]
 
 _DTYPES = None
 
@@ -117,6 +117,118 @@ class Index:
     def close(self):
         if getattr(self, "_h", None) and self._h.value:
             self._lib.dresd_index_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _search_out(B, k, L, tokens, device, out):
+    import torch
+    if out is not None:
+        return out
+    idx = torch.empty((B, k), dtype=torch.int64, device=device)
+    score = torch.empty((B, k), dtype=torch.float32, device=device)
+    tok = torch.empty((B, k, L), dtype=torch.int32, device=device) if tokens else None
+    return idx, score, tok
+
+
+class PartitionedIndex:
+    """Partitioned (approximate) inner-product index: ``keys[N, d]`` with
+    values ``cont[N, L]``, grouped into the partitions ``assign[N]`` (int32 in
+    [0, P)) whose unit centroids are ``centroids[P, d]`` (float32).  A search
+    probes the ``nprobe`` partitions with the best centroids and returns the
+    exact top-k over their keys (the paper's approximate search, Section 3.5,
+    read as an inverted file).  Everything is copied at construction."""
+
+    def __init__(self, keys, cont, centroids, assign, stream=None):
+        import torch
+        for t in (keys, cont, centroids, assign):
+            if not t.is_cuda:
+                raise ValueError("all inputs must be GPU tensors")
+        if keys.dim() != 2 or cont.dim() != 2 or cont.shape[0] != keys.shape[0]:
+            raise ValueError("keys must be [N, d] and continuations [N, L]")
+        if centroids.dtype != torch.float32 or centroids.dim() != 2 or \
+                centroids.shape[1] != keys.shape[1]:
+            raise TypeError("centroids must be float32 [P, d]")
+        if cont.dtype != torch.int32 or assign.dtype != torch.int32 or \
+                assign.numel() != keys.shape[0]:
+            raise TypeError("continuations and assign must be int32; assign holds one id per key")
+        keys, cont = keys.contiguous(), cont.contiguous()
+        centroids, assign = centroids.contiguous(), assign.contiguous()
+        self._lib = _lib.load()
+        self._h = ctypes.c_void_p()
+        self.N, self.d = int(keys.shape[0]), int(keys.shape[1])
+        self.L = int(cont.shape[1])
+        self.P = int(centroids.shape[0])
+        _lib.check(self._lib.dresd_ivf_create(
+            ctypes.c_void_p(keys.data_ptr()), ctypes.c_void_p(cont.data_ptr()), self.N, self.d,
+            self.L, _dtype_code(keys), ctypes.c_void_p(centroids.data_ptr()), self.P,
+            ctypes.c_void_p(assign.data_ptr()), _stream_handle(stream), ctypes.byref(self._h)))
+
+    def _check_q(self, queries):
+        import torch
+        if not queries.is_cuda or queries.dtype != torch.float32:
+            raise TypeError("queries must be a float32 GPU tensor")
+        if queries.dim() != 2 or queries.shape[1] != self.d:
+            raise ValueError("queries must be [B, %d]" % self.d)
+        return queries.contiguous()
+
+    def search(self, queries, k: int, nprobe: int, tokens: bool = True, out=None, stream=None):
+        """Top-k over the keys of the ``nprobe`` best partitions.  Returns
+        ``(idx, score, tokens)`` as ``Index.search``; ranks past the probed
+        keys hold idx -1, score -inf and zero tokens."""
+        q = self._check_q(queries)
+        B = int(q.shape[0])
+        idx, score, tok = _search_out(B, k, self.L, tokens, q.device, out)
+        _lib.check(self._lib.dresd_ivf_search(
+            self._h, ctypes.c_void_p(q.data_ptr()), B, int(k), int(nprobe),
+            ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(score.data_ptr()),
+            ctypes.c_void_p(tok.data_ptr()) if tok is not None else None, _stream_handle(stream)))
+        return idx, score, tok
+
+    def search_probes(self, queries, probes, k: int, tokens: bool = True, out=None, stream=None):
+        """Top-k over the keys of the partitions in ``probes`` (int32 GPU
+        tensor [B, S]; ids outside [0, P) ignored, repeats counted once)."""
+        import torch
+        q = self._check_q(queries)
+        B = int(q.shape[0])
+        if not probes.is_cuda or probes.dtype != torch.int32 or probes.dim() != 2 or \
+                probes.shape[0] != B:
+            raise TypeError("probes must be an int32 GPU tensor [B, S]")
+        pr = probes.contiguous()
+        idx, score, tok = _search_out(B, k, self.L, tokens, q.device, out)
+        _lib.check(self._lib.dresd_ivf_search_probes(
+            self._h, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(pr.data_ptr()),
+            int(pr.shape[1]), B, int(k), ctypes.c_void_p(idx.data_ptr()),
+            ctypes.c_void_p(score.data_ptr()),
+            ctypes.c_void_p(tok.data_ptr()) if tok is not None else None, _stream_handle(stream)))
+        return idx, score, tok
+
+    def info(self):
+        N, d, L, dt, P, T = (ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(),
+                             ctypes.c_int32(), ctypes.c_int64())
+        _lib.check(self._lib.dresd_ivf_info(self._h, ctypes.byref(N), ctypes.byref(d),
+                                            ctypes.byref(L), ctypes.byref(dt), ctypes.byref(P),
+                                            ctypes.byref(T)))
+        return {"N": N.value, "d": d.value, "L": L.value, "dtype": dt.value, "P": P.value,
+                "tiles": T.value}
+
+    def profile(self, on: bool = True):
+        _lib.check(self._lib.dresd_ivf_profile_enable(self._h, 1 if on else 0))
+
+    def profile_read(self):
+        a, b, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+        _lib.check(self._lib.dresd_ivf_profile_read(self._h, ctypes.byref(a), ctypes.byref(b),
+                                                    ctypes.byref(n)))
+        return {"scan_ms": a.value, "search_ms": b.value, "searches": n.value}
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            self._lib.dresd_ivf_destroy(self._h)
             self._h = ctypes.c_void_p()
 
     def __del__(self):

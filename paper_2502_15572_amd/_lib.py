@@ -20,7 +20,9 @@ F32, F16, BF16 = 0, 1, 2
 EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_index_destroy",
            "dresd_last_error", "dresd_profile_enable", "dresd_profile_read",
            "dresd_search_plan", "dresd_search_filtered", "dresd_transform",
-           "dresd_pack_drafts"]
+           "dresd_pack_drafts", "dresd_ivf_create", "dresd_ivf_destroy", "dresd_ivf_info",
+           "dresd_ivf_search", "dresd_ivf_search_probes", "dresd_ivf_profile_enable",
+           "dresd_ivf_profile_read"]
 
 _lock = threading.Lock()
 _lib = None
@@ -45,6 +47,23 @@ def _declare(lib):
     lib.dresd_transform.restype = ctypes.c_int
     lib.dresd_pack_drafts.argtypes = [P, I32, I32, I32, I32, I32, I32, P, P, P]
     lib.dresd_pack_drafts.restype = ctypes.c_int
+    lib.dresd_ivf_create.argtypes = [P, P, I64, I32, I32, I32, P, I32, P, P, ctypes.POINTER(P)]
+    lib.dresd_ivf_create.restype = ctypes.c_int
+    lib.dresd_ivf_destroy.argtypes = [P]
+    lib.dresd_ivf_destroy.restype = None
+    lib.dresd_ivf_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I32),
+                                   ctypes.POINTER(I32), ctypes.POINTER(I32), ctypes.POINTER(I32),
+                                   ctypes.POINTER(I64)]
+    lib.dresd_ivf_info.restype = ctypes.c_int
+    lib.dresd_ivf_search.argtypes = [P, P, I32, I32, I32, P, P, P, P]
+    lib.dresd_ivf_search.restype = ctypes.c_int
+    lib.dresd_ivf_search_probes.argtypes = [P, P, P, I32, I32, I32, P, P, P, P]
+    lib.dresd_ivf_search_probes.restype = ctypes.c_int
+    lib.dresd_ivf_profile_enable.argtypes = [P, I32]
+    lib.dresd_ivf_profile_enable.restype = ctypes.c_int
+    lib.dresd_ivf_profile_read.argtypes = [P, ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]
+    lib.dresd_ivf_profile_read.restype = ctypes.c_int
     lib.dresd_index_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I32),
                                      ctypes.POINTER(I32), ctypes.POINTER(I32)]
     lib.dresd_index_info.restype = ctypes.c_int

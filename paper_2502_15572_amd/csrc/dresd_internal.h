@@ -41,7 +41,16 @@ struct ScanParams {
   // starts with the query's next token compete.
   const int32_t *ftok;       // [tiles * 16] first token of each row's value
   const int32_t *next_tok;   // [B] next token of each query
+  // Partitioned search (dresd_scan_parts): slot table and each query's
+  // probed segments; wgq workgroups per query, G lists per query.
+  const uint32_t *slot_row;  // [tiles * 16] row of each slot, kPadRow for padding
+  const int32_t *seg_off;    // [B][S + 1] cumulative tiles of the probed partitions
+  const int32_t *seg_tile;   // [B][S] first tile of each probed partition
+  int S, wgq;
 };
+
+// Slot of the partitioned layout that holds no row.
+constexpr uint32_t kPadRow = 0xFFFFFFFFu;
 
 // Query operands of the shared-key scan, built once per search: chunk
 // (t, kb, lane) is the MFMA A operand of lane `lane` for query tile t and
@@ -108,6 +117,7 @@ struct MergeParams {
 struct LayoutParams {
   const void *src;           // [N, d] row-major
   void *dst;                 // tiles
+  const uint32_t *slot_row;  // partitioned layout: row of each slot (null: slot = row)
   int64_t N;
   int64_t chunks;            // total 16-byte chunks of the tiled layout
   int d, KB;
@@ -160,6 +170,17 @@ void *qop_kernel_bf16();
 inline void *qop_kernel(int dtype) {
   return dtype == kF16 ? qop_kernel_f16() : dtype == kBF16 ? qop_kernel_bf16() : nullptr;
 }
+ScanKernel scan_parts_kernel(int dtype);  // partitioned search, one query per workgroup
+// Probed segments of a partitioned search (dresd_parts.hip): one workgroup
+// per query turns its probe list into seg_off / seg_tile.
+struct SegParams {
+  const int64_t *probes64;   // [B][S] partition ids (one of the two is set)
+  const int32_t *probes32;
+  const int32_t *part_tile;  // [P + 1] first tile of each partition
+  int32_t *seg_off, *seg_tile;
+  int B, S, P;
+};
+hipError_t launch_segments(const SegParams &p, hipStream_t st);
 void *merge_kernel_ptr();
 void *layout_kernel_ptr(int dtype);
 int qt_index(int qt);  // 1,2,4,8,16 -> 0..4, else -1

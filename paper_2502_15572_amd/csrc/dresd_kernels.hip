@@ -27,6 +27,10 @@ __global__ void __launch_bounds__(256) dresd_layout(LayoutParams p) {
     int r = (int)(c - tile * per_tile);
     int kb = r >> 6, ln = r & 63;
     int64_t row = tile * kTileRows + (ln & 15);
+    if (p.slot_row) {  // partitioned layout: the slot's row, or padding
+      const uint32_t r = p.slot_row[row];
+      row = r == kPadRow ? p.N : (int64_t)r;
+    }
     int dim0 = kb * 4 * EPC + (ln >> 4) * EPC;
     union {
       T e[EPC];
@@ -123,8 +127,18 @@ __device__ __forceinline__ u4 query_chunk(const float *q, int d, int B, int col,
   return out;
 }
 
-template <int DT, int QT, int CPQ, bool MAIN>
-__device__ __forceinline__ void scan_body(const ScanParams &p) {
+// Scan modes: the main pass over every tile, a sampled threshold pass over
+// every stride-th tile, and the partitioned search (each workgroup serves one
+// query and walks the tiles of the partitions that query probes).
+constexpr int kModeMain = 0, kModeSample = 1, kModeParts = 2;
+
+// `gw` is the wave's list within its query (or batch); seg_off / seg_tile
+// are the query's probed segments in the partitioned search.
+template <int DT, int QT, int CPQ, int MODE>
+__device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
+                                          const int32_t *seg_off, const int32_t *seg_tile) {
+  constexpr bool MAIN = MODE == kModeMain;
+  constexpr bool PARTS = MODE == kModeParts;
   constexpr int QPT = 16 / CPQ;  // queries per 16-column tile
   constexpr int NS = 4 / CPQ;    // scores per lane per tile
   constexpr int NQ = QT * QPT;   // queries held by one launch
@@ -134,7 +148,6 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int nwv = blockDim.x >> 6;
-  const int gw = blockIdx.x * nwv + wv;
   const int G = p.G, C = p.C, KB = p.KB, B = p.B;
   const int ncols = B * CPQ;
   const int g = lane >> 4, m = lane & 15;
@@ -210,11 +223,54 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   // served from cache) instead of branching.  The main pass visits every
   // tile, so its blocks are one contiguous run; a sampled pass jumps
   // `stride` tiles after each visited one.
-  const int64_t v0 = wave_uniform(p.nvisit * gw / G);
-  const int64_t v1 = wave_uniform(p.nvisit * (gw + 1) / G);
+  // Partitioned search: the probed partitions' tiles, in probe order, form
+  // the query's virtual tile sequence [0, seg_off[S]); segment j (partition
+  // probe j) is virtual tiles [seg_off[j], seg_off[j+1]) starting at physical
+  // tile seg_tile[j].  The waves of the query split the sequence evenly.
+  const int64_t vtot = PARTS ? (int64_t)seg_off[p.S] : p.nvisit;
+  const int64_t v0 = wave_uniform(vtot * gw / G);
+  const int64_t v1 = wave_uniform(vtot * (gw + 1) / G);
   const int64_t J = (v1 - v0) * KB;
   const u4 *base = static_cast<const u4 *>(p.data) + lane;
+  // Two cursors walk the segments: one for block loads (ahead of use), one
+  // for the tile being finished.  Each holds its segment, its position and
+  // what is left of the segment.
+  int lseg = 0, cseg = 0;
+  int64_t lrem = 0, crem = 0;  // blocks (loads) / tiles (finish) left in the segment
+  const u4 *lptr = base;
+  int64_t lnext = 0;           // index of the block the load cursor points at
+  auto seg_len = [&](int j) -> int64_t { return (int64_t)seg_off[j + 1] - seg_off[j]; };
+  auto next_seg = [&](int j) -> int {
+    do ++j;
+    while (seg_len(j) == 0);
+    return j;
+  };
+  if constexpr (PARTS) {
+    if (J > 0) {
+      int j = 0;
+      while ((int64_t)seg_off[j + 1] <= v0) ++j;
+      lseg = cseg = j;
+      lptr = base + ((int64_t)seg_tile[j] + (v0 - seg_off[j])) * KB * 64;
+      lrem = ((int64_t)seg_off[j + 1] - v0) * KB;
+      crem = (int64_t)seg_off[j + 1] - v0;
+    }
+  }
   auto block = [&](int64_t i) -> const u4 * {
+    if constexpr (PARTS) {
+      // Calls come in order i = 0, 1, 2, ...; past the last block the
+      // cursor stays on it (an in-bounds re-read, served from cache).
+      const u4 *r = lptr;
+      if (lnext + 1 < J) {
+        ++lnext;
+        lptr += 64;
+        if (--lrem == 0) {
+          lseg = next_seg(lseg);
+          lptr = base + (int64_t)seg_tile[lseg] * KB * 64;
+          lrem = seg_len(lseg) * KB;
+        }
+      }
+      return r;
+    }
     i = i < J ? i : J - 1;
     if (MAIN) return base + (v0 * KB + i) * 64;
     const int64_t vt = i / KB;
@@ -228,7 +284,8 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   f4 acc[QT];
 #pragma unroll
   for (int t = 0; t < QT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-  int64_t ctile = v0 * p.stride;
+  int64_t ctile = PARTS ? (J > 0 ? (int64_t)seg_tile[cseg] + (v0 - seg_off[cseg]) : 0)
+                        : v0 * p.stride;
   int ckb = 0;
 
   // Filtered search (Section 3.5): the first tokens of a group of four
@@ -237,7 +294,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   // ahead of use.  Every block load issued since is younger, so waiting for
   // at most U pending loads covers the copy (all of them in the last,
   // partial group of blocks, which issues no loads).
-  const bool filt = p.ftok != nullptr;
+  const bool filt = !PARTS && p.ftok != nullptr;
   const int64_t ntw = v1 - v0;  // tiles of this wave
   int64_t tdone = 0;            // tiles finished (wave-uniform)
   // two 64-entry slots per wave, after the waves' candidate regions
@@ -265,9 +322,11 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
   };
   // Tile epilogue: threshold filter, rare slow path, reset for the next tile.
   auto tile_end = [&](bool tail) {
+    // Partitioned layout: a slot's row is known only from the slot table,
+    // read when a score passes (padding slots hold kPadRow).
     const int64_t row64 = ctile * kTileRows + m;
-    const bool row_ok = row64 < p.N;
-    const uint32_t row = (uint32_t)row64;
+    bool row_ok = PARTS || row64 < p.N;
+    uint32_t row = (uint32_t)row64;
     float sc[QT][NS];
     bool any = false;
 #pragma unroll
@@ -305,6 +364,10 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
 #pragma unroll
       for (int s = 0; s < NS; ++s) any |= row_ok && sc[t][s] >= thr[t][s];
     if (__ballot(any)) {
+      if constexpr (PARTS) {
+        row = p.slot_row[ctile * kTileRows + m];
+        row_ok = row != kPadRow;
+      }
       bool spilled = false;
 #pragma unroll
       for (int t = 0; t < QT; ++t)
@@ -330,7 +393,16 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
 #pragma unroll
     for (int t = 0; t < QT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
     ckb = 0;
-    ctile += p.stride;
+    if constexpr (PARTS) {
+      ++ctile;
+      if (--crem == 0 && tdone < ntw) {
+        cseg = next_seg(cseg);
+        ctile = seg_tile[cseg];
+        crem = seg_len(cseg);
+      }
+    } else {
+      ctile += p.stride;
+    }
   };
   // Whole groups of U blocks: every step issues exactly one load, so the
   // wait before each MFMA is a fixed count on every path.
@@ -368,12 +440,33 @@ __device__ __forceinline__ void scan_body(const ScanParams &p) {
 // sampled passes that only set thresholds.
 template <int DT, int QT, int CPQ>
 __global__ void __launch_bounds__(kScanThreads) dresd_scan_main(ScanParams p) {
-  scan_body<DT, QT, CPQ, true>(p);
+  scan_body<DT, QT, CPQ, kModeMain>(p, blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
+                                    nullptr, nullptr);
 }
 
 template <int DT, int QT, int CPQ>
 __global__ void __launch_bounds__(kScanThreads) dresd_scan_sample(ScanParams p) {
-  scan_body<DT, QT, CPQ, false>(p);
+  scan_body<DT, QT, CPQ, kModeSample>(p, blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
+                                      nullptr, nullptr);
+}
+
+// Partitioned search (its own kernel name, so that profiles separate it from
+// the exact search): workgroup blockIdx.x serves query blockIdx.x / wgq, and
+// its waves own lists [G] of that query; otherwise it is a one-query scan.
+template <int DT, int CPQ>
+__global__ void __launch_bounds__(kScanThreads) dresd_scan_parts(ScanParams p) {
+  const int qb = blockIdx.x / p.wgq;
+  const int gw = (blockIdx.x - qb * p.wgq) * (blockDim.x >> 6) +
+                 __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  ScanParams q = p;
+  q.queries += (size_t)qb * p.d;
+  q.lists += (size_t)qb * p.G * p.C;
+  q.lcnt += (size_t)qb * p.G;
+  q.lkth += (size_t)qb * p.G;
+  q.lfirst += (size_t)qb * p.G;
+  q.B = 1;
+  scan_body<DT, 1, CPQ, kModeParts>(q, gw, p.seg_off + (size_t)qb * (p.S + 1),
+                                    p.seg_tile + (size_t)qb * p.S);
 }
 
 // ---------------------------------------------------------------- tables ---
@@ -435,6 +528,13 @@ ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass) {
   if (dtype == kF16 && cpq == 1) return scan_kernel_variant1(qi, main_pass);
   if (dtype == kF16 && cpq == 4) return scan_kernel_variant2(qi, main_pass);
   if (dtype == kBF16 && cpq == 4) return scan_kernel_variant3(qi, main_pass);
+  return nullptr;
+}
+
+ScanKernel scan_parts_kernel(int dtype) {
+  if (dtype == kF32) return (ScanKernel)dresd_scan_parts<kF32, 1>;
+  if (dtype == kF16) return (ScanKernel)dresd_scan_parts<kF16, 4>;
+  if (dtype == kBF16) return (ScanKernel)dresd_scan_parts<kBF16, 4>;
   return nullptr;
 }
 

@@ -1,0 +1,65 @@
+// Partitioned search (the approximate search of DReSD Section 3.5 read as an
+// inverted file): turn each query's probe list into the segments its scan
+// walks.  One workgroup per query, one thread per probe: ids outside [0, P)
+// and repeats of an earlier probe get an empty segment; a workgroup prefix
+// sum of the partitions' tile counts gives the segment offsets.
+#include "dresd_device.h"
+
+namespace dresd {
+
+namespace {
+
+constexpr int kSegThreads = 1024;
+
+__global__ void __launch_bounds__(kSegThreads) dresd_segments(SegParams p) {
+  __shared__ int32_t pid[kSegThreads];
+  __shared__ int32_t wsum[kSegThreads / kWaveSize];
+  const int b = blockIdx.x;
+  const int i = threadIdx.x, lane = i & 63, wid = i >> 6;
+  int32_t id = -1;
+  if (i < p.S) {
+    const size_t o = (size_t)b * p.S + i;
+    const int64_t v = p.probes64 ? p.probes64[o] : (int64_t)p.probes32[o];
+    id = (v >= 0 && v < p.P) ? (int32_t)v : -1;
+  }
+  pid[i] = id;
+  __syncthreads();
+  if (id >= 0)
+    for (int j = 0; j < i; ++j)
+      if (pid[j] == id) {
+        id = -1;
+        break;
+      }
+  int32_t start = 0, len = 0;
+  if (id >= 0) {
+    start = p.part_tile[id];
+    len = p.part_tile[id + 1] - start;
+  }
+  // inclusive prefix sum of len over the workgroup
+  int32_t x = len;
+#pragma unroll
+  for (int off = 1; off < kWaveSize; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, kWaveSize);
+    if (lane >= off) x += y;
+  }
+  if (lane == kWaveSize - 1) wsum[wid] = x;
+  __syncthreads();
+  for (int w = 0; w < wid; ++w) x += wsum[w];
+  if (i < p.S) {
+    p.seg_off[(size_t)b * (p.S + 1) + i + 1] = x;
+    p.seg_tile[(size_t)b * p.S + i] = start;
+  }
+  if (i == 0) p.seg_off[(size_t)b * (p.S + 1)] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_segments(const SegParams &p, hipStream_t st) {
+  if (p.B == 0) return hipSuccess;
+  SegParams q = p;
+  void *args[] = {&q};
+  return hipLaunchKernel((const void *)dresd_segments, dim3((unsigned)p.B), dim3(kSegThreads), args,
+                         0, st);
+}
+
+}  // namespace dresd

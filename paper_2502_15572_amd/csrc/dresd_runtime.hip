@@ -97,8 +97,10 @@ size_t scan_lds(int ncols, int KB, int nq, int cl, int C) {
          (size_t)4 * kScanFtokBytes;
 }
 
-// Per-query LDS stage in front of each HBM list: larger when few queries share the wave.
-int stage_cap(int nq) { return nq >= 64 ? 8 : nq >= 16 ? 16 : 32; }
+// Per-query LDS stage in front of each HBM list: larger when few queries
+// share the wave.  One tile can pass all 16 of its rows for a query at once
+// (after a spill has emptied the stage), so the stage holds at least a tile.
+int stage_cap(int nq) { return nq >= 16 ? kTileRows : 2 * kTileRows; }
 
 int occupancy(dresd_index *ix, ScanKernel k, size_t lds) {
   for (size_t i = 0; i < ix->occ_key.size(); ++i)
@@ -265,6 +267,10 @@ hipEvent_t take_event(dresd_index *ix) {
   return e;
 }
 
+dresd_status index_build(const void *embeddings, const int32_t *continuations, int64_t N,
+                         int32_t d, int32_t L, int32_t dtype, const uint32_t *slot_row,
+                         int64_t T, dresd_stream stream, dresd_index **out);
+
 // One search; next_tok (device [B]) selects the next-token-filtered form.
 dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *next_tok, int32_t B,
                          int32_t k, int64_t *idx, float *score, int32_t *tokens,
@@ -284,6 +290,19 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
   if (d < 1 || d > 16384) return fail(DRESD_EINVAL, "d out of range");
   if (L < 1 || L > 4096) return fail(DRESD_EINVAL, "L out of range");
   if (dtype < DRESD_F32 || dtype > DRESD_BF16) return fail(DRESD_EINVAL, "unknown dtype");
+  return index_build(embeddings, continuations, N, d, L, dtype, nullptr, 0, stream, out);
+}
+
+}  // extern "C"
+
+namespace {
+// Build an index (arguments already checked).  With a slot table (device
+// [T * 16], the row of each slot or kPadRow) the keys are laid out in slot
+// order over T tiles -- the partitioned layout -- and no first-token column
+// is built; without one, slot = row.
+dresd_status index_build(const void *embeddings, const int32_t *continuations, int64_t N,
+                         int32_t d, int32_t L, int32_t dtype, const uint32_t *slot_row,
+                         int64_t T, dresd_stream stream, dresd_index **out) {
   hipStream_t st = static_cast<hipStream_t>(stream);
   dresd_index *ix = new (std::nothrow) dresd_index();
   if (!ix) return fail(DRESD_ENOMEM, "host allocation failed");
@@ -306,7 +325,7 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
   ix->dtype = dtype;
   const int bd = block_dims(dtype);
   ix->KB = (int)ceil_div(d, bd);
-  ix->T = ceil_div(N, kTileRows);
+  ix->T = slot_row ? T : ceil_div(N, kTileRows);
   const size_t data_bytes = (size_t)ix->T * ix->KB * kBlockBytes;
   const size_t cont_bytes = (size_t)N * L * sizeof(int32_t);
   if (hipMalloc(&ix->data, data_bytes) != hipSuccess) {
@@ -320,7 +339,7 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
     return cleanup(fail(DRESD_ENOMEM, "continuation storage allocation failed"));
   }
   const size_t ftok_bytes = (size_t)ix->T * kTileRows * sizeof(int32_t);
-  if (hipMalloc((void **)&ix->ftok, ftok_bytes) != hipSuccess) {
+  if (!slot_row && hipMalloc((void **)&ix->ftok, ftok_bytes) != hipSuccess) {
     (void)hipGetLastError();
     ix->ftok = nullptr;
     return cleanup(fail(DRESD_ENOMEM, "first-token column allocation failed"));
@@ -345,10 +364,15 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
             (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
                                       (int)ix->lds_max);
         }
+  for (int v = 0; v < 3; ++v)
+    if (ScanKernel kf = scan_parts_kernel(v))
+      (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)ix->lds_max);
   (void)hipGetLastError();
   LayoutParams lp;
   lp.src = embeddings;
   lp.dst = ix->data;
+  lp.slot_row = slot_row;
   lp.N = N;
   lp.chunks = (int64_t)ix->T * ix->KB * 64;
   lp.d = d;
@@ -360,9 +384,9 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
   if (e == hipSuccess)
     e = hipMemcpyAsync(ix->cont, continuations, cont_bytes, hipMemcpyDeviceToDevice, st);
   // First-token column: value[i][0] for every row, zero past N.
-  if (e == hipSuccess)
+  if (e == hipSuccess && ix->ftok)
     e = hipMemsetAsync(ix->ftok, 0, ftok_bytes, st);
-  if (e == hipSuccess)
+  if (e == hipSuccess && ix->ftok)
     e = hipMemcpy2DAsync(ix->ftok, sizeof(int32_t), continuations, (size_t)L * sizeof(int32_t),
                          sizeof(int32_t), (size_t)N, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
@@ -371,6 +395,9 @@ dresd_status dresd_index_create(const void *embeddings, const int32_t *continuat
   *out = ix;
   return DRESD_OK;
 }
+}  // namespace
+
+extern "C" {
 
 dresd_status dresd_index_info(const dresd_index *ix, int64_t *N, int32_t *d, int32_t *L,
                               int32_t *dtype) {
@@ -488,6 +515,9 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     sp.ftok = next_tok ? ix->ftok : nullptr;
     sp.next_tok = next_tok ? next_tok + gr.b0 : nullptr;
     sp.qop = nullptr;
+    sp.slot_row = nullptr;
+    sp.seg_off = sp.seg_tile = nullptr;
+    sp.S = sp.wgq = 0;
     if (pl.mq) {
       QopParams qp;
       qp.queries = sp.queries;
@@ -679,6 +709,321 @@ dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms, double *search
   ix->ev_scan.clear();
   ix->ev_all.clear();
   return DRESD_OK;
+}
+
+
+// ------------------------------------------------------ partitioned search ---
+
+}  // extern "C"
+
+struct dresd_ivf {
+  dresd_index *ix = nullptr;     // keys in partition order, continuations by row
+  dresd_index *cix = nullptr;    // the centroids (fp32 keys, exact probing)
+  uint32_t *slot_row = nullptr;  // [T * 16] row of each slot, kPadRow for padding
+  int32_t *part_tile = nullptr;  // [P + 1] first tile of each partition
+  int32_t P = 0;
+  int64_t probe_bytes = 0;       // probe results of the last search: ids + scores
+  unsigned char *probe = nullptr;
+};
+
+namespace {
+
+void ivf_free(dresd_ivf *v) {
+  if (!v) return;
+  if (v->ix) dresd_index_destroy(v->ix);
+  if (v->cix) dresd_index_destroy(v->cix);
+  if (v->slot_row) hipFree(v->slot_row);
+  if (v->part_tile) hipFree(v->part_tile);
+  if (v->probe) hipFree(v->probe);
+  delete v;
+}
+
+// Scan of the probed partitions + merge.  probes64 (from the centroid
+// search) or probes32 (caller's) is [B][S] on the device.
+dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *probes64,
+                          const int32_t *probes32, int32_t S, int32_t B, int32_t k, int64_t *idx,
+                          float *score, int32_t *tokens, hipStream_t st) {
+  dresd_index *ix = v->ix;
+  const int terms = ix->dtype == kF32 ? 1 : 4;  // the query as three exact 16-bit parts
+  const int nq = 16 / terms;
+  const int C = next_pow2(std::max(k + 64, 128));
+  const int CL = stage_cap(nq);
+  const size_t lds = scan_lds(terms, ix->KB, nq, CL, C);
+  if (lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS for this d and k");
+  ScanKernel kern = scan_parts_kernel(ix->dtype);
+  if (!kern) return fail(DRESD_EUNSUPPORTED, "no partitioned scan kernel for this key type");
+  // Workgroups per query: enough for ~4 per CU over the batch, but no more
+  // than one per 32 tiles of an average probe set.
+  const int64_t avg_tiles = std::max<int64_t>(1, (int64_t)S * ix->T / v->P);
+  int64_t wgq = std::min<int64_t>(ceil_div(4LL * ix->cus, B), ceil_div(avg_tiles, 32));
+  wgq = std::max<int64_t>(1, std::min<int64_t>(wgq, kMergeLists / 4));
+  const int G = (int)wgq * (kScanThreads / kWaveSize);
+  const int64_t spill_cap = std::max<int64_t>(0, (int64_t)G * k - kMergeCap);
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  const size_t nb = (size_t)B;
+  const size_t off_seg = 0;
+  const size_t off_tile = off_seg + up(nb * (S + 1) * 4);
+  const size_t off_lcnt = off_tile + up(nb * S * 4);
+  const size_t off_lkth = off_lcnt + up(nb * G * 4);
+  const size_t off_lfirst = off_lkth + up(nb * G * 8);
+  const size_t off_lists = off_lfirst + up(nb * G * 8);
+  const size_t off_spill = off_lists + up(nb * G * (size_t)C * 8);
+  const size_t bytes = off_spill + up(nb * (size_t)std::max<int64_t>(1, spill_cap) * 8);
+  dresd_status s = ensure_workspace(ix, bytes);
+  if (s != DRESD_OK) return s;
+  unsigned char *ws = ix->ws;
+
+  SegParams gp;
+  gp.probes64 = probes64;
+  gp.probes32 = probes32;
+  gp.part_tile = v->part_tile;
+  gp.seg_off = reinterpret_cast<int32_t *>(ws + off_seg);
+  gp.seg_tile = reinterpret_cast<int32_t *>(ws + off_tile);
+  gp.B = B;
+  gp.S = S;
+  gp.P = v->P;
+  DRESD_HIP(launch_segments(gp, st));
+
+  ScanParams sp;
+  sp.data = ix->data;
+  sp.queries = queries;
+  sp.N = ix->N;
+  sp.nvisit = 0;
+  sp.stride = 1;
+  sp.tau = nullptr;
+  sp.lists = reinterpret_cast<uint64_t *>(ws + off_lists);
+  sp.lcnt = reinterpret_cast<uint32_t *>(ws + off_lcnt);
+  sp.lkth = reinterpret_cast<uint64_t *>(ws + off_lkth);
+  sp.lfirst = reinterpret_cast<uint64_t *>(ws + off_lfirst);
+  sp.B = B;
+  sp.d = ix->d;
+  sp.KB = ix->KB;
+  sp.k = k;
+  sp.C = C;
+  sp.G = G;
+  sp.CL = CL;
+  sp.sort_lists = 1;
+  sp.qop = nullptr;
+  sp.ftok = nullptr;
+  sp.next_tok = nullptr;
+  sp.slot_row = v->slot_row;
+  sp.seg_off = gp.seg_off;
+  sp.seg_tile = gp.seg_tile;
+  sp.S = S;
+  sp.wgq = (int)wgq;
+  void *sargs[] = {&sp};
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (ix->prof) {
+    e0 = take_event(ix);
+    e1 = take_event(ix);
+    if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
+    DRESD_HIP(hipEventRecord(e0, st));
+  }
+  DRESD_HIP(hipLaunchKernel((const void *)kern, dim3((unsigned)(B * wgq)), dim3(kScanThreads),
+                            sargs, lds, st));
+  if (ix->prof) {
+    DRESD_HIP(hipEventRecord(e1, st));
+    ix->ev_scan.push_back(e0);
+    ix->ev_scan.push_back(e1);
+  }
+  MergeParams mp;
+  mp.lists = sp.lists;
+  mp.lcnt = sp.lcnt;
+  mp.lkth = sp.lkth;
+  mp.lfirst = sp.lfirst;
+  mp.spill = reinterpret_cast<uint64_t *>(ws + off_spill);
+  mp.spill_cap = spill_cap;
+  mp.B = B;
+  mp.k = k;
+  mp.C = C;
+  mp.G = G;
+  mp.tau_out = nullptr;
+  mp.idx = idx;
+  mp.score = score;
+  mp.tokens = tokens;
+  mp.cont = ix->cont;
+  mp.L = ix->L;
+  mp.final_mode = 1;
+  void *margs[] = {&mp};
+  DRESD_HIP(hipLaunchKernel(merge_kernel_ptr(), dim3((unsigned)B), dim3(kMergeThreads), margs, 0,
+                            st));
+  return DRESD_OK;
+}
+
+dresd_status validate_ivf_search(const dresd_ivf *v, int32_t B, int32_t k) {
+  if (!v) return fail(DRESD_EINVAL, "partitioned index is NULL");
+  return validate_search(v->ix, B, k);
+}
+
+}  // namespace
+
+extern "C" {
+
+dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuations, int64_t N,
+                              int32_t d, int32_t L, int32_t dtype, const float *centroids,
+                              int32_t P, const int32_t *assign, dresd_stream stream,
+                              dresd_ivf **out) {
+  if (!embeddings || !continuations || !centroids || !assign || !out)
+    return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (N < 1 || N > DRESD_N_MAX) return fail(DRESD_EINVAL, "N out of range");
+  if (d < 1 || d > 16384) return fail(DRESD_EINVAL, "d out of range");
+  if (L < 1 || L > 4096) return fail(DRESD_EINVAL, "L out of range");
+  if (dtype < DRESD_F32 || dtype > DRESD_BF16) return fail(DRESD_EINVAL, "unknown dtype");
+  if (P < 1 || P > DRESD_PARTS_MAX) return fail(DRESD_EINVAL, "P out of range");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // Slot table: partitions in id order, each padded to whole tiles, rows of
+  // a partition in row order (a stable counting sort of the assignment).
+  std::vector<int32_t> a((size_t)N);
+  DRESD_HIP(hipMemcpyAsync(a.data(), assign, (size_t)N * 4, hipMemcpyDeviceToHost, st));
+  DRESD_HIP(hipStreamSynchronize(st));
+  std::vector<int64_t> cnt((size_t)P, 0);
+  for (int64_t i = 0; i < N; ++i) {
+    if (a[i] < 0 || a[i] >= P) return fail(DRESD_EINVAL, "assignment outside [0, P)");
+    ++cnt[a[i]];
+  }
+  std::vector<int32_t> pt((size_t)P + 1);
+  int64_t T = 0;
+  for (int32_t p = 0; p < P; ++p) {
+    pt[p] = (int32_t)T;
+    T += ceil_div(cnt[p], kTileRows);
+  }
+  pt[P] = (int32_t)T;
+  std::vector<uint32_t> slot((size_t)T * kTileRows, kPadRow);
+  std::vector<int64_t> next((size_t)P);
+  for (int32_t p = 0; p < P; ++p) next[p] = (int64_t)pt[p] * kTileRows;
+  for (int64_t i = 0; i < N; ++i) slot[next[a[i]]++] = (uint32_t)i;
+  a.clear();
+  a.shrink_to_fit();
+
+  dresd_ivf *v = new (std::nothrow) dresd_ivf();
+  if (!v) return fail(DRESD_ENOMEM, "host allocation failed");
+  v->P = P;
+  auto bail = [&](dresd_status s) {
+    ivf_free(v);
+    return s;
+  };
+  if (hipMalloc((void **)&v->slot_row, slot.size() * 4) != hipSuccess ||
+      hipMalloc((void **)&v->part_tile, pt.size() * 4) != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(fail(DRESD_ENOMEM, "slot table allocation failed"));
+  }
+  if (hipMemcpy(v->slot_row, slot.data(), slot.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(v->part_tile, pt.data(), pt.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return bail(fail(DRESD_EDEVICE, "slot table upload failed"));
+  dresd_status s = index_build(embeddings, continuations, N, d, L, dtype, v->slot_row, T, stream,
+                               &v->ix);
+  if (s != DRESD_OK) return bail(s);
+  // Centroid index: fp32 keys, value = the partition id.
+  std::vector<int32_t> ids((size_t)P);
+  for (int32_t p = 0; p < P; ++p) ids[p] = p;
+  int32_t *ids_dev = nullptr;
+  if (hipMalloc((void **)&ids_dev, (size_t)P * 4) != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(fail(DRESD_ENOMEM, "allocation failed"));
+  }
+  if (hipMemcpy(ids_dev, ids.data(), (size_t)P * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    hipFree(ids_dev);
+    return bail(fail(DRESD_EDEVICE, "partition id upload failed"));
+  }
+  s = index_build(centroids, ids_dev, P, d, 1, DRESD_F32, nullptr, 0, stream, &v->cix);
+  hipFree(ids_dev);
+  if (s != DRESD_OK) return bail(s);
+  *out = v;
+  return DRESD_OK;
+}
+
+void dresd_ivf_destroy(dresd_ivf *v) {
+  if (!v) return;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  if (v->ix) {
+    (void)hipSetDevice(v->ix->device);
+    (void)hipDeviceSynchronize();
+  }
+  ivf_free(v);
+  (void)hipSetDevice(cur);
+}
+
+dresd_status dresd_ivf_info(const dresd_ivf *v, int64_t *N, int32_t *d, int32_t *L, int32_t *dtype,
+                            int32_t *P, int64_t *tiles) {
+  if (!v) return fail(DRESD_EINVAL, "partitioned index is NULL");
+  dresd_status s = dresd_index_info(v->ix, N, d, L, dtype);
+  if (s != DRESD_OK) return s;
+  if (P) *P = v->P;
+  if (tiles) *tiles = v->ix->T;
+  return DRESD_OK;
+}
+
+dresd_status dresd_ivf_search(dresd_ivf *v, const float *queries, int32_t B, int32_t k,
+                              int32_t nprobe, int64_t *idx, float *score, int32_t *tokens,
+                              dresd_stream stream) {
+  dresd_status s = validate_ivf_search(v, B, k);
+  if (s != DRESD_OK) return s;
+  if (nprobe < 1 || nprobe > std::min<int32_t>(v->P, DRESD_K_MAX))
+    return fail(DRESD_EINVAL, "nprobe must be in [1, min(P, DRESD_K_MAX)]");
+  if (B > 0 && (!queries || !idx || !score)) return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (B == 0) return DRESD_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t need = (int64_t)B * nprobe * 12;
+  if (v->probe_bytes < need) {
+    if (v->probe) {
+      DRESD_HIP(hipDeviceSynchronize());
+      hipFree(v->probe);
+      v->probe = nullptr;
+      v->probe_bytes = 0;
+    }
+    if (hipMalloc((void **)&v->probe, (size_t)need) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(DRESD_ENOMEM, "probe buffer allocation failed");
+    }
+    v->probe_bytes = need;
+  }
+  int64_t *pid = reinterpret_cast<int64_t *>(v->probe);
+  float *psc = reinterpret_cast<float *>(v->probe + (size_t)B * nprobe * 8);
+  hipEvent_t a0 = nullptr, a1 = nullptr;
+  dresd_index *ix = v->ix;
+  if (ix->prof) {
+    a0 = take_event(ix);
+    a1 = take_event(ix);
+    if (!a0 || !a1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
+    DRESD_HIP(hipEventRecord(a0, st));
+  }
+  // 1. probe: the nprobe best centroids of each query (exact search)
+  s = search_impl(v->cix, queries, nullptr, B, nprobe, pid, psc, nullptr, stream);
+  if (s != DRESD_OK) return s;
+  // 2. exact top-k over the probed partitions
+  s = parts_search(v, queries, pid, nullptr, nprobe, B, k, idx, score, tokens, st);
+  if (s != DRESD_OK) return s;
+  if (ix->prof) {
+    DRESD_HIP(hipEventRecord(a1, st));
+    ix->ev_all.push_back(a0);
+    ix->ev_all.push_back(a1);
+  }
+  return DRESD_OK;
+}
+
+dresd_status dresd_ivf_search_probes(dresd_ivf *v, const float *queries, const int32_t *probes,
+                                     int32_t S, int32_t B, int32_t k, int64_t *idx, float *score,
+                                     int32_t *tokens, dresd_stream stream) {
+  dresd_status s = validate_ivf_search(v, B, k);
+  if (s != DRESD_OK) return s;
+  if (S < 1 || S > DRESD_K_MAX) return fail(DRESD_EINVAL, "S must be in [1, DRESD_K_MAX]");
+  if (B > 0 && (!queries || !probes || !idx || !score))
+    return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (B == 0) return DRESD_OK;
+  return parts_search(v, queries, nullptr, probes, S, B, k, idx, score, tokens,
+                      static_cast<hipStream_t>(stream));
+}
+
+dresd_status dresd_ivf_profile_enable(dresd_ivf *v, int32_t on) {
+  if (!v) return fail(DRESD_EINVAL, "partitioned index is NULL");
+  return dresd_profile_enable(v->ix, on);
+}
+
+dresd_status dresd_ivf_profile_read(dresd_ivf *v, double *scan_ms, double *search_ms,
+                                    int64_t *searches) {
+  if (!v) return fail(DRESD_EINVAL, "partitioned index is NULL");
+  return dresd_profile_read(v->ix, scan_ms, search_ms, searches);
 }
 
 }  // extern "C"

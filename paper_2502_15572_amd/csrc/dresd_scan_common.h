@@ -78,8 +78,9 @@ __device__ inline void sink_spill(const CandSink &s, int i, uint64_t *list) {
 }
 
 // Offer this lane's key to query i (wave-uniform i).  `mine` marks the
-// lanes holding a score of query i that passed the fast filter.  Returns
-// true when the stage was spilled (vector memory was used).
+// lanes holding a score of query i that passed the fast filter -- at most
+// one tile's 16 rows, which an emptied stage always holds (cl >= 16).
+// Returns true when the stage was spilled (vector memory was used).
 __device__ inline bool sink_offer(const CandSink &s, int i, bool mine, uint64_t key,
                                   uint64_t *list) {
   bool spilled = false;

@@ -16,10 +16,11 @@ are bit-exact for the returned indices.
   R7  tokens[r, :] == cont[g_idx[r], :] bit for bit
 Also reported (not gating): exact-order agreement and max |g - exact|.
 
-Next-token-filtered searches (Section 3.5) add: every returned row is
-admitted (its continuation starts with the query's token), and ranks past
-the admitted rows -- exactly where the oracle's are -- hold index -1, score
--inf and zero tokens; the rules above apply to the ranks before them.
+Searches over a subset of the rows -- next-token-filtered (Section 3.5) or
+partitioned (the probed partitions) -- add: every returned row is in the
+subset, and ranks past the subset's rows -- exactly where the oracle's are --
+hold index -1, score -inf and zero tokens; the rules above apply to the ranks
+before them.
 """
 from __future__ import annotations
 
@@ -90,10 +91,13 @@ def check_query(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont
     }
 
 
-def check_query_filtered(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont,
-                         first_token, tol=1e-5):
-    """One query of a next-token-filtered search: ``first_token`` is the
-    token its drafts must start with."""
+def check_query_padded(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont,
+                       admitted, what, tol=1e-5):
+    """One query of a search over a subset of the rows (next-token filter,
+    probed partitions): ranks past the subset -- exactly where the oracle's
+    are -- hold (-1, -inf, zero tokens); every returned row is in the subset
+    (``admitted(rows) -> bool array``, ``what`` names the rule); the rules
+    above apply to the ranks before the padding."""
     g_idx = np.asarray(g_idx, np.int64)
     g_score = np.asarray(g_score, np.float32)
     o_idx = np.asarray(o_idx, np.int64)
@@ -112,24 +116,38 @@ def check_query_filtered(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of
         return {"exact_order": True, "max_abs_vs_exact": 0.0, "max_abs_vs_oracle": 0.0}
     if np.any(g_idx[:m] < 0) or np.any(g_idx[:m] >= N):
         raise ParityError("R4: index out of range")
-    if np.any(np.asarray(cont)[g_idx[:m], 0] != first_token):
-        raise ParityError("filter: returned a row whose continuation does not start with %d"
-                          % first_token)
+    if not np.all(admitted(g_idx[:m])):
+        raise ParityError(what)
     return check_query(g_idx[:m], g_score[:m], None if g_tok is None else np.asarray(g_tok)[:m],
                        o_idx[:m], np.asarray(o_score)[:m], o_next, exact_of, N, cont, tol)
 
 
+def check_query_filtered(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont,
+                         first_token, tol=1e-5):
+    """One query of a next-token-filtered search: ``first_token`` is the
+    token its drafts must start with."""
+    return check_query_padded(
+        g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of, N, cont,
+        lambda rows: np.asarray(cont)[rows, 0] == first_token,
+        "filter: returned a row whose continuation does not start with %d" % first_token, tol)
+
+
 def check_batch(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of_b, N, cont=None,
-                tol=1e-5, next_tok=None):
+                tol=1e-5, next_tok=None, admitted_b=None):
     """``exact_of_b(b, rows)`` re-scores rows for query b; ``next_tok`` [B]
-    marks a next-token-filtered search."""
+    marks a next-token-filtered search; ``admitted_b(b, rows)`` a search over
+    a per-query subset of the rows (probed partitions)."""
     reps = []
     for b in range(o_idx.shape[0]):
         try:
             args = (g_idx[b], g_score[b], None if g_tok is None else g_tok[b], o_idx[b],
                     o_score[b], None if o_next is None else o_next[b],
                     lambda rows, b=b: exact_of_b(b, rows), N, cont)
-            if next_tok is None:
+            if admitted_b is not None:
+                reps.append(check_query_padded(*args, lambda rows, b=b: admitted_b(b, rows),
+                                               "partitions: returned a row of a partition that "
+                                               "was not probed", tol))
+            elif next_tok is None:
                 reps.append(check_query(*args, tol))
             else:
                 reps.append(check_query_filtered(*args, int(next_tok[b]), tol))

@@ -109,6 +109,12 @@ EDGE = [
     ("f32", 2000, 256, 4, 1),
     ("f16", 70000, 128, 1, 1000),    # large k
     ("bf16", 9000, 256, 32, 16),
+    # many queries per single-tile launch: up to 16 passing rows of a tile
+    # for one query must fit the query's LDS stage
+    ("f32", 50, 256, 33, 4),         # fp32, three query tiles
+    ("f32", 5000, 64, 100, 20),      # fp32, seven query tiles
+    ("f16", 3000, 2048, 40, 10),     # f16 blocks per tile outside the shared-key scan
+    ("bf16", 2000, 2048, 64, 8),     # bf16 (three-part queries), sixteen query tiles
 ]
 
 
