@@ -272,6 +272,36 @@ dresd_status dresd_ivf_search(dresd_ivf *ivf, const float *queries, int32_t B, i
 dresd_status dresd_ivf_search_probes(dresd_ivf *ivf, const float *queries, const int32_t *probes,
                                      int32_t S, int32_t B, int32_t k, int64_t *idx, float *score,
                                      int32_t *tokens, dresd_stream stream);
+/*
+ * Spherical k-means, the partitioning of the partitioned search (the
+ * centroids and assignment that dresd_ivf_create takes).  Cosine similarity
+ * of unit vectors (Eq. 3) is the inner product.
+ *
+ * dresd_kmeans_assign: assign[i] = the centroid with the largest inner
+ *   product with row i, ties to the lower id; score[i] (NULL allowed) = that
+ *   inner product (fp32 accumulation of exact products).
+ *   x device [n, d] row-major in dtype; 0 <= n <= DRESD_N_MAX (0: no-op);
+ *   1 <= d <= 16384; centroids device [P, d] fp32, 1 <= P <= DRESD_PARTS_MAX;
+ *   assign device [n] int32 out; score device [n] fp32 out.
+ * dresd_kmeans_update: each centroid becomes the unit vector along the sum of
+ *   the rows assigned to it; a centroid with no rows (or a zero sum) is left
+ *   as it is.  Sums are exact to 2^-30 per element and independent of the
+ *   order of the rows (deterministic).  x as above with n < 2^31; assign
+ *   device [n] int32, each in [0, P) (not checked: the caller's contract);
+ *   centroids device [P, d] fp32 in/out; counts device [P] int32 out (rows per
+ *   centroid, NULL allowed).  Uses a per-device workspace of P*d*8 + P*4
+ *   bytes, allocated (synchronously) on first use and kept; calls that
+ *   overlap on one device race on it.
+ * Both are asynchronous on `stream`.  Errors: EINVAL (ranges, nulls), ENOMEM,
+ * EDEVICE.
+ */
+dresd_status dresd_kmeans_assign(const void *x, int64_t n, int32_t d, int32_t dtype,
+                                 const float *centroids, int32_t P, int32_t *assign,
+                                 float *score, dresd_stream stream);
+dresd_status dresd_kmeans_update(const void *x, int64_t n, int32_t d, int32_t dtype,
+                                 const int32_t *assign, int32_t P, float *centroids,
+                                 int32_t *counts, dresd_stream stream);
+
 dresd_status dresd_ivf_profile_enable(dresd_ivf *ivf, int32_t on);
 dresd_status dresd_ivf_profile_read(dresd_ivf *ivf, double *scan_ms, double *search_ms,
                                     int64_t *searches);

@@ -14,7 +14,8 @@ import ctypes
 from . import _lib
 from ._lib import DresdError, K_MAX  # noqa: F401
 
-__all__ = ["Index", "PartitionedIndex", "DresdError", "K_MAX", "transform", "pack_drafts"]
+__all__ = ["Index", "PartitionedIndex", "DresdError", "K_MAX", "transform", "pack_drafts",
+           "kmeans_assign", "kmeans_update", "train_partitions"]
 
 _DTYPES = None
 
@@ -284,3 +285,69 @@ def pack_drafts(tokens, r: int, length: int, eos: int = 0, out=None, stream=None
                                      int(eos), ctypes.c_void_p(drafts.data_ptr()),
                                      ctypes.c_void_p(count.data_ptr()), _stream_handle(stream)))
     return drafts, count
+
+
+def _rows(x):
+    if not x.is_cuda or x.dim() != 2:
+        raise TypeError("rows must be a GPU tensor [n, d]")
+    return x.contiguous()
+
+
+def kmeans_assign(x, centroids, with_score: bool = False, stream=None):
+    """Nearest centroid by inner product for every row of ``x`` ([n, d],
+    float32/float16/bfloat16 on the GPU; ``centroids`` float32 [P, d]), ties
+    to the lower id.  Returns assign int32 [n] (and the fp32 scores)."""
+    import torch
+    x = _rows(x)
+    c = centroids.contiguous()
+    if c.dtype != torch.float32 or c.dim() != 2 or c.shape[1] != x.shape[1]:
+        raise TypeError("centroids must be float32 [P, d]")
+    n, d = int(x.shape[0]), int(x.shape[1])
+    a = torch.empty((n,), dtype=torch.int32, device=x.device)
+    sc = torch.empty((n,), dtype=torch.float32, device=x.device) if with_score else None
+    _lib.check(_lib.load().dresd_kmeans_assign(
+        ctypes.c_void_p(x.data_ptr()), n, d, _dtype_code(x), ctypes.c_void_p(c.data_ptr()),
+        int(c.shape[0]), ctypes.c_void_p(a.data_ptr()),
+        ctypes.c_void_p(sc.data_ptr()) if sc is not None else None, _stream_handle(stream)))
+    return (a, sc) if with_score else a
+
+
+def kmeans_update(x, assign, centroids, stream=None):
+    """Spherical k-means update in place: each centroid (float32 [P, d],
+    contiguous) becomes the unit vector along the sum of its rows (unchanged
+    without rows).  Returns the rows per centroid (int32 [P])."""
+    import torch
+    x = _rows(x)
+    if not centroids.is_contiguous() or centroids.dtype != torch.float32:
+        raise TypeError("centroids must be a contiguous float32 tensor [P, d]")
+    if assign.dtype != torch.int32 or assign.numel() != x.shape[0]:
+        raise TypeError("assign must be int32 with one entry per row")
+    a = assign.contiguous()
+    P = int(centroids.shape[0])
+    counts = torch.empty((P,), dtype=torch.int32, device=x.device)
+    _lib.check(_lib.load().dresd_kmeans_update(
+        ctypes.c_void_p(x.data_ptr()), int(x.shape[0]), int(x.shape[1]), _dtype_code(x),
+        ctypes.c_void_p(a.data_ptr()), P, ctypes.c_void_p(centroids.data_ptr()),
+        ctypes.c_void_p(counts.data_ptr()), _stream_handle(stream)))
+    return counts
+
+
+def train_partitions(x, P: int, iters: int = 10, seed: int = 0, stream=None):
+    """Spherical k-means on the GPU: P centroids started from P distinct rows
+    of ``x`` chosen by a seeded permutation, then ``iters`` assign + update
+    steps.  Returns (centroids float32 [P, d], assign int32 [n])."""
+    import torch
+    x = _rows(x)
+    n, d = int(x.shape[0]), int(x.shape[1])
+    if not (1 <= P <= n):
+        raise ValueError("need 1 <= P <= n")
+    pick = torch.randperm(n, generator=torch.Generator().manual_seed(seed))[:P].to(x.device)
+    centroids = torch.zeros((P, d), dtype=torch.float32, device=x.device)
+    # each picked row alone in its partition: the update makes it a unit centroid
+    kmeans_update(x[pick], torch.arange(P, dtype=torch.int32, device=x.device), centroids,
+                  stream)
+    assign = None
+    for _ in range(iters):
+        assign = kmeans_assign(x, centroids, stream=stream)
+        kmeans_update(x, assign, centroids, stream)
+    return centroids, kmeans_assign(x, centroids, stream=stream)

@@ -22,7 +22,7 @@ EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_inde
            "dresd_search_plan", "dresd_search_filtered", "dresd_transform",
            "dresd_pack_drafts", "dresd_ivf_create", "dresd_ivf_destroy", "dresd_ivf_info",
            "dresd_ivf_search", "dresd_ivf_search_probes", "dresd_ivf_profile_enable",
-           "dresd_ivf_profile_read"]
+           "dresd_ivf_profile_read", "dresd_kmeans_assign", "dresd_kmeans_update"]
 
 _lock = threading.Lock()
 _lib = None
@@ -64,6 +64,10 @@ def _declare(lib):
     lib.dresd_ivf_profile_read.argtypes = [P, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]
     lib.dresd_ivf_profile_read.restype = ctypes.c_int
+    lib.dresd_kmeans_assign.argtypes = [P, I64, I32, I32, P, I32, P, P, P]
+    lib.dresd_kmeans_assign.restype = ctypes.c_int
+    lib.dresd_kmeans_update.argtypes = [P, I64, I32, I32, P, I32, P, P, P]
+    lib.dresd_kmeans_update.restype = ctypes.c_int
     lib.dresd_index_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I32),
                                      ctypes.POINTER(I32), ctypes.POINTER(I32)]
     lib.dresd_index_info.restype = ctypes.c_int

@@ -181,6 +181,23 @@ struct SegParams {
   int B, S, P;
 };
 hipError_t launch_segments(const SegParams &p, hipStream_t st);
+// Spherical k-means (dresd_kmeans.hip).
+struct KmeansParams {
+  const void *x;             // [n, d] rows, storage type dtype
+  int64_t n;
+  int d, dtype, P;
+  const float *centroids;    // [P, d] (assign)
+  int32_t *assign;           // [n] out (assign)
+  float *score;              // [n] out, may be null (assign)
+  const int32_t *assign_in;  // [n] (update)
+  float *centroids_out;      // [P, d] in/out (update)
+  int32_t *counts;           // [P] out, may be null (update)
+  long long *sums;           // [P, d] fixed-point workspace (update)
+  int32_t *cnt;              // [P] workspace (update)
+};
+hipError_t launch_kmeans_assign(const KmeansParams &p, hipStream_t st);
+hipError_t launch_kmeans_update(const KmeansParams &p, int cus, hipStream_t st);
+
 void *merge_kernel_ptr();
 void *layout_kernel_ptr(int dtype);
 int qt_index(int qt);  // 1,2,4,8,16 -> 0..4, else -1

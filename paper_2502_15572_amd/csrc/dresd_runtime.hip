@@ -1015,6 +1015,76 @@ dresd_status dresd_ivf_search_probes(dresd_ivf *v, const float *queries, const i
                       static_cast<hipStream_t>(stream));
 }
 
+dresd_status dresd_kmeans_assign(const void *x, int64_t n, int32_t d, int32_t dtype,
+                                 const float *centroids, int32_t P, int32_t *assign, float *score,
+                                 dresd_stream stream) {
+  if (n < 0 || n > DRESD_N_MAX) return fail(DRESD_EINVAL, "n out of range");
+  if (d < 1 || d > 16384) return fail(DRESD_EINVAL, "d out of range");
+  if (dtype < DRESD_F32 || dtype > DRESD_BF16) return fail(DRESD_EINVAL, "unknown dtype");
+  if (P < 1 || P > DRESD_PARTS_MAX) return fail(DRESD_EINVAL, "P out of range");
+  if (n == 0) return DRESD_OK;
+  if (!x || !centroids || !assign) return fail(DRESD_EINVAL, "NULL pointer argument");
+  KmeansParams p = {};
+  p.x = x;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.P = P;
+  p.centroids = centroids;
+  p.assign = assign;
+  p.score = score;
+  DRESD_HIP(launch_kmeans_assign(p, static_cast<hipStream_t>(stream)));
+  return DRESD_OK;
+}
+
+dresd_status dresd_kmeans_update(const void *x, int64_t n, int32_t d, int32_t dtype,
+                                 const int32_t *assign, int32_t P, float *centroids,
+                                 int32_t *counts, dresd_stream stream) {
+  if (n < 0 || n > (int64_t)1 << 31) return fail(DRESD_EINVAL, "n out of range");
+  if (d < 1 || d > 16384) return fail(DRESD_EINVAL, "d out of range");
+  if (dtype < DRESD_F32 || dtype > DRESD_BF16) return fail(DRESD_EINVAL, "unknown dtype");
+  if (P < 1 || P > DRESD_PARTS_MAX) return fail(DRESD_EINVAL, "P out of range");
+  if (!centroids || (n > 0 && (!x || !assign))) return fail(DRESD_EINVAL, "NULL pointer argument");
+  int dev = 0;
+  DRESD_HIP(hipGetDevice(&dev));
+  int cus = 0;
+  DRESD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  // Fixed-point sums and counts: a per-device buffer kept for the life of
+  // the process, grown (synchronously) when a larger one is needed.
+  static std::mutex mu;
+  static std::vector<std::pair<void *, size_t>> bufs;
+  const size_t need = (size_t)P * d * 8 + (size_t)P * 4;
+  std::lock_guard<std::mutex> lock(mu);
+  if (bufs.size() <= (size_t)dev) bufs.resize((size_t)dev + 1, {nullptr, 0});
+  if (bufs[dev].second < need) {
+    if (bufs[dev].first) {
+      DRESD_HIP(hipDeviceSynchronize());
+      hipFree(bufs[dev].first);
+      bufs[dev] = {nullptr, 0};
+    }
+    void *b = nullptr;
+    if (hipMalloc(&b, need) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(DRESD_ENOMEM, "k-means workspace allocation failed");
+    }
+    bufs[dev] = {b, need};
+  }
+  KmeansParams p = {};
+  p.x = x;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.P = P;
+  p.assign_in = assign;
+  p.centroids_out = centroids;
+  p.counts = counts;
+  p.sums = static_cast<long long *>(bufs[dev].first);
+  p.cnt = reinterpret_cast<int32_t *>(static_cast<unsigned char *>(bufs[dev].first) +
+                                      (size_t)P * d * 8);
+  DRESD_HIP(launch_kmeans_update(p, cus, static_cast<hipStream_t>(stream)));
+  return DRESD_OK;
+}
+
 dresd_status dresd_ivf_profile_enable(dresd_ivf *v, int32_t on) {
   if (!v) return fail(DRESD_EINVAL, "partitioned index is NULL");
   return dresd_profile_enable(v->ix, on);
