@@ -135,6 +135,101 @@ def time_transform(args):
                                     "GBps": byts / (p50 * 1e-3) / 1e9}}), flush=True)
 
 
+def time_partitioned(args):
+    """Partitioned (inverted-file) search of the workload: spherical k-means
+    on a seeded sample of the keys, every key assigned, then B-query searches
+    at each nprobe.  Recall@k is measured against the exact search on the
+    same queries; the scan's bandwidth counts the bytes of the probed
+    partitions' keys (padding rows included)."""
+    import torch
+    from datagen import WORKLOADS, generate
+    from paper_2502_15572_amd import Index, PartitionedIndex, kmeans_assign, train_partitions
+    w = WORKLOADS[args.workload]
+    if args.n:
+        w = w.scaled(args.n)
+    k = args.k or w.k
+    B, P = args.batch, args.ivf
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = generate(w, dev)
+    keys, cont, pool = g["keys"], g["cont"], g["queries"]
+    torch.cuda.synchronize()
+    t0 = time.time()
+    ns = min(w.N, args.train_rows_per_part * P)
+    pick = torch.randperm(w.N, generator=torch.Generator().manual_seed(1))[:ns].to(dev)
+    sample = keys[pick].contiguous()
+    cents, _ = train_partitions(sample, P, iters=args.train_iters, seed=2)
+    del sample
+    assign = kmeans_assign(keys, cents)
+    torch.cuda.synchronize()
+    train_s = time.time() - t0
+    t0 = time.time()
+    ivf = PartitionedIndex(keys, cont, cents, assign)
+    build_s = time.time() - t0
+    info = ivf.info()
+    log("partitions: P=%d trained on %d rows in %.2fs, index built in %.2fs, %d tiles"
+        % (P, ns, train_s, build_s, info["tiles"]))
+    nb = max(1, pool.shape[0] // B)
+    batches = [pool[i * B:(i + 1) * B].contiguous() for i in range(nb)]
+    exact = Index(keys, cont)
+    ref = [exact.search(b, k, tokens=False)[0] for b in batches]
+    exact.close()
+    # probed rows per query, from the same exact probing over the centroids
+    cix = Index(cents, torch.arange(P, dtype=torch.int32, device=dev).view(P, 1))
+    sizes = torch.bincount(assign.long(), minlength=P)
+    padded = (sizes + 15) // 16 * 16
+    for nprobe in args.nprobe:
+        idx = torch.empty((B, k), dtype=torch.int64, device=dev)
+        score = torch.empty((B, k), dtype=torch.float32, device=dev)
+        tok = torch.empty((B, k, w.L), dtype=torch.int32, device=dev)
+        out = (idx, score, tok)
+        hits = 0
+        for i, b in enumerate(batches):
+            ivf.search(b, k, nprobe, out=out)
+            r = ref[i]
+            hits += sum(len(set(idx[j].tolist()) & set(r[j].tolist())) for j in range(B))
+        recall = hits / (nb * B * k)
+        probe_rows = 0
+        for b in batches:
+            pr = cix.search(b, nprobe, tokens=False)[0]
+            probe_rows += int(padded[pr].sum())
+        probe_rows /= nb * B
+        for i in range(args.warmup):
+            ivf.search(batches[i % nb], k, nprobe, out=out)
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        ivf.profile(True)
+        ivf.profile_read()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            ev[i][0].record(stream)
+            ivf.search(batches[i % nb], k, nprobe, out=out)
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        prof = ivf.profile_read()
+        ivf.profile(False)
+        per = sorted(a.elapsed_time(b) for a, b in ev)
+        p50 = statistics.median(per)
+        scan_ms = prof["scan_ms"] / max(1, prof["searches"])
+        scan_bytes = probe_rows * B * w.d * w.elem_bytes
+        print(json.dumps({
+            "partitioned": {"workload": w.name, "N": w.N, "d": w.d, "key_dtype": w.dtype,
+                            "B": B, "k": k, "P": P, "nprobe": nprobe,
+                            "queries_per_s": args.steps * B / el, "p50_latency_us": p50 * 1e3,
+                            "recall_at_k": recall, "probed_rows_per_query": probe_rows,
+                            "probed_fraction": probe_rows / w.N,
+                            "scan_kernel": "dresd_scan_parts", "scan_ms": scan_ms,
+                            "scan_GBps": scan_bytes / (scan_ms * 1e-3) / 1e9,
+                            "scan_hbm_frac": scan_bytes / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                            "train_rows": ns, "train_iters": args.train_iters,
+                            "train_s": train_s, "index_build_s": build_s}}), flush=True)
+    cix.close()
+    ivf.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -152,6 +247,13 @@ def main():
     ap.add_argument("--transform", type=int, default=0, metavar="D",
                     help="only time the query-side transform: B rows of D fp32 dims projected "
                          "to the workload's d (Eq. 1, Section 3.3, Eq. 2)")
+    ap.add_argument("--ivf", type=int, default=0, metavar="P",
+                    help="only time the partitioned search with P k-means partitions")
+    ap.add_argument("--nprobe", type=int, nargs="+", default=[16, 64, 256],
+                    help="partitions probed per query (--ivf)")
+    ap.add_argument("--train-rows-per-part", type=int, default=64,
+                    help="k-means sample: this many keys per partition (--ivf)")
+    ap.add_argument("--train-iters", type=int, default=10, help="k-means iterations (--ivf)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -162,6 +264,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.ivf:
+        time_partitioned(args)
         return
     if args.transform:
         time_transform(args)
