@@ -135,6 +135,39 @@ def time_transform(args):
                                     "GBps": byts / (p50 * 1e-3) / 1e9}}), flush=True)
 
 
+def time_drafts(args):
+    """Time draft assembly (Section 3.6) of B queries' k retrieved
+    continuations into r EOS-padded drafts of `length` tokens.  Tokens are
+    drawn from a 64-token vocabulary so repeated drafts and EOS are common."""
+    import torch
+    from datagen import WORKLOADS
+    from paper_2502_15572_amd import pack_drafts
+    w = WORKLOADS[args.workload]
+    k = args.k or w.k
+    B, L = args.batch, w.L
+    r, length = min(args.drafts, k), L
+    g = torch.Generator(device="cuda").manual_seed(0)
+    tok = torch.randint(0, 64, (B, k, L), device="cuda", generator=g, dtype=torch.int32)
+    drafts = torch.empty((B, r, length), dtype=torch.int32, device="cuda")
+    count = torch.empty((B,), dtype=torch.int32, device="cuda")
+    for _ in range(args.warmup):
+        pack_drafts(tok, r, length, out=(drafts, count))
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:
+        a.record()
+        pack_drafts(tok, r, length, out=(drafts, count))
+        b.record()
+    torch.cuda.synchronize()
+    per = sorted(a.elapsed_time(b) for a, b in ev)
+    p50 = statistics.median(per)
+    byts = 4.0 * (B * k * L + B * r * length + B)
+    print(json.dumps({"drafts": {"B": B, "k": k, "L": L, "r": r, "length": length,
+                                 "p50_us": p50 * 1e3, "GBps": byts / (p50 * 1e-3) / 1e9,
+                                 "mean_kept": float(count.float().mean())}}), flush=True)
+
+
 def time_partitioned(args):
     """Partitioned (inverted-file) search of the workload: spherical k-means
     on a seeded sample of the keys, every key assigned, then B-query searches
@@ -254,6 +287,9 @@ def main():
     ap.add_argument("--train-rows-per-part", type=int, default=64,
                     help="k-means sample: this many keys per partition (--ivf)")
     ap.add_argument("--train-iters", type=int, default=10, help="k-means iterations (--ivf)")
+    ap.add_argument("--drafts", type=int, default=0, metavar="R",
+                    help="only time draft assembly of the workload's k continuations into R "
+                         "drafts (Section 3.6)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -267,6 +303,9 @@ def main():
         return
     if args.ivf:
         time_partitioned(args)
+        return
+    if args.drafts:
+        time_drafts(args)
         return
     if args.transform:
         time_transform(args)

@@ -47,6 +47,12 @@ struct ScanParams {
   const int32_t *seg_off;    // [B][S + 1] cumulative tiles of the probed partitions
   const int32_t *seg_tile;   // [B][S] first tile of each probed partition
   int S, wgq;
+  // ... or, when probes64 is set, each workgroup builds its query's segments
+  // in LDS at byte offset seg_lds from the exact probe search's output
+  // ([B][S] distinct ids in [0, P)) and the partitions' first tiles.
+  const int64_t *probes64;
+  const int32_t *part_tile;  // [P + 1]
+  int seg_lds, P;
 };
 
 // Slot of the partitioned layout that holds no row.

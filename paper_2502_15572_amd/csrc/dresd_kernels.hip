@@ -450,11 +450,53 @@ __global__ void __launch_bounds__(kScanThreads) dresd_scan_sample(ScanParams p) 
                                       nullptr, nullptr);
 }
 
+// Segments of one query from its probe list (S <= 1024 distinct ids in
+// [0, P), in probe order): off[j + 1] = tiles of probes 0..j, tile[j] = first
+// tile of probe j.  All threads of the workgroup take part.
+__device__ void parts_segments(const int64_t *probes, const int32_t *part_tile, int S, int P,
+                               int32_t *off, int32_t *tile) {
+  constexpr int E = 4;  // entries per thread: S <= E * kScanThreads
+  __shared__ int32_t wsum[kScanThreads / kWaveSize];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int32_t start[E], len[E], sum = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int j = t * E + e;
+    const int64_t id = j < S ? probes[j] : -1;
+    const bool ok = id >= 0 && id < P;
+    start[e] = ok ? part_tile[id] : 0;
+    len[e] = ok ? part_tile[id + 1] - start[e] : 0;
+    sum += len[e];
+  }
+  int32_t x = sum;  // inclusive scan over the wave
+#pragma unroll
+  for (int o = 1; o < kWaveSize; o <<= 1) {
+    const int32_t y = __shfl_up(x, o, kWaveSize);
+    if (lane >= o) x += y;
+  }
+  if (lane == kWaveSize - 1) wsum[w] = x;
+  __syncthreads();
+  int32_t run = x - sum;
+  for (int v = 0; v < w; ++v) run += wsum[v];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int j = t * E + e;
+    run += len[e];
+    if (j < S) {
+      off[j + 1] = run;
+      tile[j] = start[e];
+    }
+  }
+  if (t == 0) off[0] = 0;
+  __syncthreads();
+}
+
 // Partitioned search (its own kernel name, so that profiles separate it from
 // the exact search): workgroup blockIdx.x serves query blockIdx.x / wgq, and
 // its waves own lists [G] of that query; otherwise it is a one-query scan.
 template <int DT, int CPQ>
 __global__ void __launch_bounds__(kScanThreads) dresd_scan_parts(ScanParams p) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int qb = blockIdx.x / p.wgq;
   const int gw = (blockIdx.x - qb * p.wgq) * (blockDim.x >> 6) +
                  __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -465,8 +507,15 @@ __global__ void __launch_bounds__(kScanThreads) dresd_scan_parts(ScanParams p) {
   q.lkth += (size_t)qb * p.G;
   q.lfirst += (size_t)qb * p.G;
   q.B = 1;
-  scan_body<DT, 1, CPQ, kModeParts>(q, gw, p.seg_off + (size_t)qb * (p.S + 1),
-                                    p.seg_tile + (size_t)qb * p.S);
+  if (p.probes64) {
+    int32_t *off = reinterpret_cast<int32_t *>(smem + p.seg_lds);
+    int32_t *tile = off + p.S + 1;
+    parts_segments(p.probes64 + (size_t)qb * p.S, p.part_tile, p.S, p.P, off, tile);
+    scan_body<DT, 1, CPQ, kModeParts>(q, gw, off, tile);
+  } else {
+    scan_body<DT, 1, CPQ, kModeParts>(q, gw, p.seg_off + (size_t)qb * (p.S + 1),
+                                      p.seg_tile + (size_t)qb * p.S);
+  }
 }
 
 // ---------------------------------------------------------------- tables ---

@@ -518,6 +518,9 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     sp.slot_row = nullptr;
     sp.seg_off = sp.seg_tile = nullptr;
     sp.S = sp.wgq = 0;
+    sp.probes64 = nullptr;
+    sp.part_tile = nullptr;
+    sp.seg_lds = sp.P = 0;
     if (pl.mq) {
       QopParams qp;
       qp.queries = sp.queries;
@@ -748,14 +751,21 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   const int nq = 16 / terms;
   const int C = next_pow2(std::max(k + 64, 128));
   const int CL = stage_cap(nq);
-  const size_t lds = scan_lds(terms, ix->KB, nq, CL, C);
+  // Probes from the exact centroid search: each workgroup builds its
+  // query's segments in LDS behind the scan's own state.
+  const bool fused = probes64 != nullptr;
+  const size_t lds_scan = scan_lds(terms, ix->KB, nq, CL, C);
+  const size_t lds = lds_scan + (fused ? ((size_t)(2 * S + 1) * 4 + 15) / 16 * 16 : 0);
   if (lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS for this d and k");
   ScanKernel kern = scan_parts_kernel(ix->dtype);
   if (!kern) return fail(DRESD_EUNSUPPORTED, "no partitioned scan kernel for this key type");
-  // Workgroups per query: enough for ~4 per CU over the batch, but no more
-  // than one per 32 tiles of an average probe set.
+  // Workgroups per query: enough for ~4 per CU over the batch, but no fewer
+  // than 4 tiles per wave of an average probe set.  A probe set is small
+  // (tens of MB), and one wave streams it slowly (its loads in flight bound
+  // it), so short waves in large numbers finish first; the merge of their
+  // lists costs less than longer waves do.
   const int64_t avg_tiles = std::max<int64_t>(1, (int64_t)S * ix->T / v->P);
-  int64_t wgq = std::min<int64_t>(ceil_div(4LL * ix->cus, B), ceil_div(avg_tiles, 32));
+  int64_t wgq = std::min<int64_t>(ceil_div(4LL * ix->cus, B), ceil_div(avg_tiles, 16));
   wgq = std::max<int64_t>(1, std::min<int64_t>(wgq, kMergeLists / 4));
   const int G = (int)wgq * (kScanThreads / kWaveSize);
   const int64_t spill_cap = std::max<int64_t>(0, (int64_t)G * k - kMergeCap);
@@ -774,7 +784,7 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   unsigned char *ws = ix->ws;
 
   SegParams gp;
-  gp.probes64 = probes64;
+  gp.probes64 = nullptr;
   gp.probes32 = probes32;
   gp.part_tile = v->part_tile;
   gp.seg_off = reinterpret_cast<int32_t *>(ws + off_seg);
@@ -782,7 +792,7 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   gp.B = B;
   gp.S = S;
   gp.P = v->P;
-  DRESD_HIP(launch_segments(gp, st));
+  if (!fused) DRESD_HIP(launch_segments(gp, st));
 
   ScanParams sp;
   sp.data = ix->data;
@@ -811,6 +821,10 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   sp.seg_tile = gp.seg_tile;
   sp.S = S;
   sp.wgq = (int)wgq;
+  sp.probes64 = probes64;
+  sp.part_tile = v->part_tile;
+  sp.seg_lds = (int)lds_scan;
+  sp.P = v->P;
   void *sargs[] = {&sp};
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (ix->prof) {
