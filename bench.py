@@ -222,11 +222,13 @@ def time_partitioned(args):
             r = ref[i]
             hits += sum(len(set(idx[j].tolist()) & set(r[j].tolist())) for j in range(B))
         recall = hits / (nb * B * k)
-        probe_rows = 0
+        probe_rows, union_rows = 0, 0
         for b in batches:
             pr = cix.search(b, nprobe, tokens=False)[0]
             probe_rows += int(padded[pr].sum())
+            union_rows += int(padded[torch.unique(pr)].sum())
         probe_rows /= nb * B
+        union_rows /= nb
         for i in range(args.warmup):
             ivf.search(batches[i % nb], k, nprobe, out=out)
         torch.cuda.synchronize()
@@ -254,6 +256,7 @@ def time_partitioned(args):
                             "queries_per_s": args.steps * B / el, "p50_latency_us": p50 * 1e3,
                             "recall_at_k": recall, "probed_rows_per_query": probe_rows,
                             "probed_fraction": probe_rows / w.N,
+                            "batch_union_rows": union_rows,
                             "scan_kernel": "dresd_scan_parts", "scan_ms": scan_ms,
                             "scan_GBps": scan_bytes / (scan_ms * 1e-3) / 1e9,
                             "scan_hbm_frac": scan_bytes / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
