@@ -66,7 +66,8 @@ def _load():
             lib.oracle_topk_filtered.restype = ctypes.c_int
             I32 = ctypes.c_int32
             lib.oracle_topk_partitioned.argtypes = [P, ctypes.c_int, ctypes.c_int64, I32, P, I32,
-                                                    I32, P, I32, P, I32, P, I32, P, P, P, P, I32]
+                                                    I32, P, I32, P, I32, P, I32, P, P, P, P, P,
+                                                    I32]
             lib.oracle_topk_partitioned.restype = ctypes.c_int
             lib.oracle_score_rows.argtypes = [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
                                               P, P, ctypes.c_int64, P]
@@ -144,12 +145,15 @@ def topk(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
 
 
 def topk_partitioned(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
-                     assign, P: int, probes, cont: np.ndarray | None = None, threads: int = 0):
+                     assign, P: int, probes, cont: np.ndarray | None = None, threads: int = 0,
+                     next_tok=None):
     """Partitioned retrieval (the approximate search of Section 3.5, read as
     an inverted file): row i belongs to partition ``assign[i]`` in [0, P);
     query b returns the exact k best rows among the partitions listed in
-    ``probes[b]`` (entries outside [0, P) ignored, repeats counted once).
-    Same outputs and padding as ``topk(..., next_tok=...)``."""
+    ``probes[b]`` (entries outside [0, P) ignored, repeats counted once) --
+    with ``next_tok`` only those whose value starts with the query's next
+    token (Section 3.5's filter).  Same outputs and padding as
+    ``topk(..., next_tok=...)``."""
     e = _emb_bits(emb, dtype)
     q = np.ascontiguousarray(queries, dtype=np.float32)
     if q.ndim != 2 or q.shape[1] != e.shape[1]:
@@ -175,9 +179,15 @@ def topk_partitioned(emb: np.ndarray, dtype: str, queries: np.ndarray, k: int,
         L = c.shape[1]
         tok = np.empty((B, k, L), np.int32)
         cptr = c.ctypes.data
+    ntp = None
+    if next_tok is not None:
+        nt = np.ascontiguousarray(next_tok, dtype=np.int32).reshape(-1)
+        if nt.shape[0] != B or cont is None or L < 1:
+            raise ValueError("next_tok needs one token per query and continuations")
+        ntp = nt.ctypes.data
     rc = _load().oracle_topk_partitioned(
         e.ctypes.data, DTYPE_CODES[dtype], N, d, q.ctypes.data, B, k, cptr, L, a.ctypes.data,
-        int(P), pr.ctypes.data, pr.shape[1], idx.ctypes.data, score.ctypes.data,
+        int(P), pr.ctypes.data, pr.shape[1], ntp, idx.ctypes.data, score.ctypes.data,
         tok.ctypes.data if tok is not None else None, nxt.ctypes.data, int(threads))
     if rc != 0:
         raise RuntimeError("oracle partitioned top-k failed (assignment out of range?)")

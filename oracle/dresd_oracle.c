@@ -293,14 +293,17 @@ int oracle_topk_filtered(const void *emb, int dtype, int64_t N, int32_t d, const
 }
 
 /* Partitioned retrieval: assign [N] int32 in [0, P); probes [B, S] int32
- * (entries outside [0, P) ignored).  Not reentrant (the probe sets live in
- * file-scope state for the duration of the call). */
+ * (entries outside [0, P) ignored); next_tok [B] (NULL: no filter) adds the
+ * next-token filter: a row takes part when its partition is probed and its
+ * value starts with the query's next token.  Not reentrant (the probe sets
+ * live in file-scope state for the duration of the call). */
 int oracle_topk_partitioned(const void *emb, int dtype, int64_t N, int32_t d, const float *Q,
                             int32_t B, int32_t k, const int32_t *cont, int32_t L,
                             const int32_t *assign, int32_t P, const int32_t *probes, int32_t S,
-                            int64_t *idx, float *score, int32_t *tokens, float *next_score,
-                            int32_t nthreads) {
+                            const int32_t *next_tok, int64_t *idx, float *score, int32_t *tokens,
+                            float *next_score, int32_t nthreads) {
   if (!assign || P < 1 || S < 0 || (S > 0 && !probes) || B < 0) return -1;
+  if (next_tok && (!cont || L < 1)) return -1;
   for (int64_t i = 0; i < N; ++i)
     if (assign[i] < 0 || assign[i] >= P) return -1;
   unsigned char *probed = (unsigned char *)calloc((size_t)(B > 0 ? B : 1) * (size_t)P, 1);
@@ -315,7 +318,7 @@ int oracle_topk_partitioned(const void *emb, int dtype, int64_t N, int32_t d, co
   g_assign = assign;
   g_probed = probed;
   g_parts = P;
-  const int rc = topk_impl(emb, dtype, N, d, Q, B, k, cont, L, NULL, idx, score, tokens,
+  const int rc = topk_impl(emb, dtype, N, d, Q, B, k, cont, L, next_tok, idx, score, tokens,
                            next_score, nthreads);
   g_assign = NULL;
   g_probed = NULL;

@@ -168,3 +168,34 @@ def test_kmeans_separated_clusters_and_monotone_objective():
         obj = oracle.kmeans_objective(y, c)
         assert obj >= prev - 1e-9
         prev = obj
+
+
+def test_partitioned_filtered_reductions_and_brute_force():
+    """With the next-token filter: every partition probed is the filtered
+    exact search; a tiny brute force of filter-and-probe; one token that no
+    probed row starts with pads every rank."""
+    rng = np.random.default_rng(9)
+    N, d, P, k = 400, 12, 5, 15
+    x = unit_rows(rng, N, d)
+    cont = rng.integers(0, 4, (N, 3)).astype(np.int32)
+    assign = rng.integers(0, P, N).astype(np.int32)
+    q = unit_rows(rng, 4, d)
+    nt = np.array([0, 1, 3, 7], np.int32)
+    allp = np.tile(np.arange(P, dtype=np.int32), (4, 1))
+    want = oracle.topk(x, "f32", q, k, cont, next_tok=nt)
+    got = oracle.topk_partitioned(x, "f32", q, k, assign, P, allp, cont, next_tok=nt)
+    for w, g in zip(want, got):
+        assert np.array_equal(w, g, equal_nan=True)
+    probes = np.array([[0, 2], [1, 1], [4, -1], [0, 3]], np.int32)
+    idx, sc, _, _ = oracle.topk_partitioned(x, "f32", q, k, assign, P, probes, cont, next_tok=nt)
+    x64 = x.astype(np.float64)
+    for b in range(4):
+        ps = {int(p) for p in probes[b] if 0 <= p < P}
+        rows = np.array([i for i in range(N) if assign[i] in ps and cont[i, 0] == nt[b]], np.int64)
+        s = (x64[rows] @ q[b].astype(np.float64)).astype(np.float32) if rows.size else \
+            np.zeros(0, np.float32)
+        order = np.lexsort((rows, -s.astype(np.float64)))[:k]
+        m = order.size
+        assert np.array_equal(idx[b, :m], rows[order]) and np.array_equal(sc[b, :m], s[order])
+        assert (idx[b, m:] == -1).all() and np.isinf(sc[b, m:]).all()
+    assert (idx[3] == -1).all()  # token 7 starts no value
