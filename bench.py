@@ -184,18 +184,23 @@ def time_partitioned(args):
     B, P = args.batch, args.ivf
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    t0 = time.time()
     g = generate(w, dev)
     keys, cont, pool = g["keys"], g["cont"], g["queries"]
     torch.cuda.synchronize()
+    log("generated %s N=%d d=%d %s in %.1fs" % (w.name, w.N, w.d, w.dtype, time.time() - t0))
     t0 = time.time()
     ns = min(w.N, args.train_rows_per_part * P)
     pick = torch.randperm(w.N, generator=torch.Generator().manual_seed(1))[:ns].to(dev)
     sample = keys[pick].contiguous()
     cents, _ = train_partitions(sample, P, iters=args.train_iters, seed=2)
     del sample
+    torch.cuda.synchronize()
+    log("k-means on %d keys in %.1fs" % (ns, time.time() - t0))
     assign = kmeans_assign(keys, cents)
     torch.cuda.synchronize()
     train_s = time.time() - t0
+    log("all keys assigned at %.1fs" % train_s)
     t0 = time.time()
     ivf = PartitionedIndex(keys, cont, cents, assign)
     build_s = time.time() - t0
@@ -204,8 +209,16 @@ def time_partitioned(args):
         % (P, ns, train_s, build_s, info["tiles"]))
     nb = max(1, pool.shape[0] // B)
     batches = [pool[i * B:(i + 1) * B].contiguous() for i in range(nb)]
+    nts = [None] * nb
+    if args.filtered:  # as in the exact bench: the source row's first token
+        c0 = cont[:, 0]
+        frequent = int(torch.mode(c0[: min(w.N, 1 << 20)]).values)
+        src = g["query_src"]
+        nt = torch.where(src >= 0, c0[src.clamp(min=0)], torch.full_like(src, frequent))
+        nt = nt.to(torch.int32)
+        nts = [nt[i * B:(i + 1) * B].contiguous() for i in range(nb)]
     exact = Index(keys, cont)
-    ref = [exact.search(b, k, tokens=False)[0] for b in batches]
+    ref = [exact.search(b, k, tokens=False, next_tok=nts[i])[0] for i, b in enumerate(batches)]
     exact.close()
     # probed rows per query, from the same exact probing over the centroids
     cix = Index(cents, torch.arange(P, dtype=torch.int32, device=dev).view(P, 1))
@@ -216,12 +229,15 @@ def time_partitioned(args):
         score = torch.empty((B, k), dtype=torch.float32, device=dev)
         tok = torch.empty((B, k, w.L), dtype=torch.int32, device=dev)
         out = (idx, score, tok)
-        hits = 0
+        hits, total = 0, 0
         for i, b in enumerate(batches):
-            ivf.search(b, k, nprobe, out=out)
+            ivf.search(b, k, nprobe, out=out, next_tok=nts[i])
             r = ref[i]
-            hits += sum(len(set(idx[j].tolist()) & set(r[j].tolist())) for j in range(B))
-        recall = hits / (nb * B * k)
+            for j in range(B):
+                want = set(r[j].tolist()) - {-1}
+                hits += len(set(idx[j].tolist()) & want)
+                total += len(want)
+        recall = hits / max(1, total)
         probe_rows, union_rows = 0, 0
         for b in batches:
             pr = cix.search(b, nprobe, tokens=False)[0]
@@ -229,8 +245,9 @@ def time_partitioned(args):
             union_rows += int(padded[torch.unique(pr)].sum())
         probe_rows /= nb * B
         union_rows /= nb
+        log("nprobe %d: recall %.3f, timing ..." % (nprobe, recall))
         for i in range(args.warmup):
-            ivf.search(batches[i % nb], k, nprobe, out=out)
+            ivf.search(batches[i % nb], k, nprobe, out=out, next_tok=nts[i % nb])
         torch.cuda.synchronize()
         stream = torch.cuda.current_stream()
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -240,7 +257,7 @@ def time_partitioned(args):
         t0 = time.perf_counter()
         for i in range(args.steps):
             ev[i][0].record(stream)
-            ivf.search(batches[i % nb], k, nprobe, out=out)
+            ivf.search(batches[i % nb], k, nprobe, out=out, next_tok=nts[i % nb])
             ev[i][1].record(stream)
         torch.cuda.synchronize()
         el = time.perf_counter() - t0
@@ -253,6 +270,7 @@ def time_partitioned(args):
         print(json.dumps({
             "partitioned": {"workload": w.name, "N": w.N, "d": w.d, "key_dtype": w.dtype,
                             "B": B, "k": k, "P": P, "nprobe": nprobe,
+                            "filtered": bool(args.filtered),
                             "queries_per_s": args.steps * B / el, "p50_latency_us": p50 * 1e3,
                             "recall_at_k": recall, "probed_rows_per_query": probe_rows,
                             "probed_fraction": probe_rows / w.N,

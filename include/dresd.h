@@ -251,9 +251,14 @@ dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,
  *   product, ties to the lower id).  Ranks past the keys of the probed
  *   partitions hold index -1, score -inf and zero tokens.  One search at a
  *   time per index.
- * dresd_ivf_search_probes: the same with caller-chosen partitions: probes
+ * dresd_ivf_search_filtered: dresd_ivf_search with the next-token filter of
+ *   dresd_search_filtered (next_tok device [B] int32): among the keys of the
+ *   probed partitions only those whose continuation starts with the query's
+ *   next token compete; ranks past them are padded the same way.
+ * dresd_ivf_search_probes: the search with caller-chosen partitions: probes
  *   device [B, S] int32, 1 <= S <= DRESD_K_MAX; entries outside [0, P) are
- *   ignored and repeats count once.
+ *   ignored and repeats count once; next_tok: NULL, or device [B] int32 for
+ *   the next-token filter.
  * dresd_ivf_info: host outputs (NULL allowed); tiles = 16-row tiles of the
  *   partitioned layout (padding included).
  * dresd_ivf_profile_enable / _read: as dresd_profile_*, for the scan of the
@@ -269,9 +274,14 @@ dresd_status dresd_ivf_info(const dresd_ivf *ivf, int64_t *N, int32_t *d, int32_
 dresd_status dresd_ivf_search(dresd_ivf *ivf, const float *queries, int32_t B, int32_t k,
                               int32_t nprobe, int64_t *idx, float *score, int32_t *tokens,
                               dresd_stream stream);
+dresd_status dresd_ivf_search_filtered(dresd_ivf *ivf, const float *queries,
+                                       const int32_t *next_tok, int32_t B, int32_t k,
+                                       int32_t nprobe, int64_t *idx, float *score,
+                                       int32_t *tokens, dresd_stream stream);
 dresd_status dresd_ivf_search_probes(dresd_ivf *ivf, const float *queries, const int32_t *probes,
-                                     int32_t S, int32_t B, int32_t k, int64_t *idx, float *score,
-                                     int32_t *tokens, dresd_stream stream);
+                                     int32_t S, const int32_t *next_tok, int32_t B, int32_t k,
+                                     int64_t *idx, float *score, int32_t *tokens,
+                                     dresd_stream stream);
 /*
  * Spherical k-means, the partitioning of the partitioned search (the
  * centroids and assignment that dresd_ivf_create takes).  Cosine similarity

@@ -178,22 +178,43 @@ class PartitionedIndex:
             raise ValueError("queries must be [B, %d]" % self.d)
         return queries.contiguous()
 
-    def search(self, queries, k: int, nprobe: int, tokens: bool = True, out=None, stream=None):
-        """Top-k over the keys of the ``nprobe`` best partitions.  Returns
-        ``(idx, score, tokens)`` as ``Index.search``; ranks past the probed
-        keys hold idx -1, score -inf and zero tokens."""
+    @staticmethod
+    def _next_tok(next_tok, B):
+        import torch
+        if next_tok is None:
+            return None
+        if not next_tok.is_cuda or next_tok.dtype != torch.int32 or next_tok.numel() != B:
+            raise TypeError("next_tok must be an int32 GPU tensor with one token per query")
+        return next_tok.contiguous()
+
+    def search(self, queries, k: int, nprobe: int, tokens: bool = True, out=None, stream=None,
+               next_tok=None):
+        """Top-k over the keys of the ``nprobe`` best partitions (with
+        ``next_tok``, int32 GPU tensor [B], only keys whose continuation starts
+        with the query's next token).  Returns ``(idx, score, tokens)`` as
+        ``Index.search``; ranks past the admitted keys hold idx -1, score -inf
+        and zero tokens."""
         q = self._check_q(queries)
         B = int(q.shape[0])
+        nt = self._next_tok(next_tok, B)
         idx, score, tok = _search_out(B, k, self.L, tokens, q.device, out)
-        _lib.check(self._lib.dresd_ivf_search(
-            self._h, ctypes.c_void_p(q.data_ptr()), B, int(k), int(nprobe),
-            ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(score.data_ptr()),
-            ctypes.c_void_p(tok.data_ptr()) if tok is not None else None, _stream_handle(stream)))
+        args = (ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(score.data_ptr()),
+                ctypes.c_void_p(tok.data_ptr()) if tok is not None else None,
+                _stream_handle(stream))
+        if nt is None:
+            _lib.check(self._lib.dresd_ivf_search(
+                self._h, ctypes.c_void_p(q.data_ptr()), B, int(k), int(nprobe), *args))
+        else:
+            _lib.check(self._lib.dresd_ivf_search_filtered(
+                self._h, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(nt.data_ptr()), B, int(k),
+                int(nprobe), *args))
         return idx, score, tok
 
-    def search_probes(self, queries, probes, k: int, tokens: bool = True, out=None, stream=None):
+    def search_probes(self, queries, probes, k: int, tokens: bool = True, out=None, stream=None,
+                      next_tok=None):
         """Top-k over the keys of the partitions in ``probes`` (int32 GPU
-        tensor [B, S]; ids outside [0, P) ignored, repeats counted once)."""
+        tensor [B, S]; ids outside [0, P) ignored, repeats counted once),
+        optionally next-token filtered."""
         import torch
         q = self._check_q(queries)
         B = int(q.shape[0])
@@ -201,11 +222,12 @@ class PartitionedIndex:
                 probes.shape[0] != B:
             raise TypeError("probes must be an int32 GPU tensor [B, S]")
         pr = probes.contiguous()
+        nt = self._next_tok(next_tok, B)
         idx, score, tok = _search_out(B, k, self.L, tokens, q.device, out)
         _lib.check(self._lib.dresd_ivf_search_probes(
             self._h, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(pr.data_ptr()),
-            int(pr.shape[1]), B, int(k), ctypes.c_void_p(idx.data_ptr()),
-            ctypes.c_void_p(score.data_ptr()),
+            int(pr.shape[1]), ctypes.c_void_p(nt.data_ptr()) if nt is not None else None, B,
+            int(k), ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(score.data_ptr()),
             ctypes.c_void_p(tok.data_ptr()) if tok is not None else None, _stream_handle(stream)))
         return idx, score, tok
 

@@ -39,7 +39,7 @@ struct ScanParams {
   const void *qop;           // shared-key scan: query operands [tiles][KB][64] x 16 B
   // Next-token-filtered search (both null otherwise): only rows whose value
   // starts with the query's next token compete.
-  const int32_t *ftok;       // [tiles * 16] first token of each row's value
+  const int32_t *ftok;       // [tiles * 16] first token of each slot's value
   const int32_t *next_tok;   // [B] next token of each query
   // Partitioned search (dresd_scan_parts): slot table and each query's
   // probed segments; wgq workgroups per query, G lists per query.
@@ -187,6 +187,9 @@ struct SegParams {
   int B, S, P;
 };
 hipError_t launch_segments(const SegParams &p, hipStream_t st);
+// ftok[s] = first token of slot s's value (0 for padding slots).
+hipError_t launch_slot_first_tokens(const uint32_t *slot_row, const int32_t *cont, int L,
+                                    int64_t nslot, int32_t *ftok, hipStream_t st);
 // Spherical k-means (dresd_kmeans.hip).
 struct KmeansParams {
   const void *x;             // [n, d] rows, storage type dtype

@@ -365,8 +365,11 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
       for (int s = 0; s < NS; ++s) any |= row_ok && sc[t][s] >= thr[t][s];
     if (__ballot(any)) {
       if constexpr (PARTS) {
-        row = p.slot_row[ctile * kTileRows + m];
-        row_ok = row != kPadRow;
+        // the slot's row; with the next-token filter (Section 3.5), only a
+        // row whose value starts with the query's next token
+        const int64_t slot = ctile * kTileRows + m;
+        row = p.slot_row[slot];
+        row_ok = row != kPadRow && (p.ftok == nullptr || p.ftok[slot] == nt_lds[0]);
       }
       bool spilled = false;
 #pragma unroll
@@ -507,6 +510,7 @@ __global__ void __launch_bounds__(kScanThreads) dresd_scan_parts(ScanParams p) {
   q.lkth += (size_t)qb * p.G;
   q.lfirst += (size_t)qb * p.G;
   q.B = 1;
+  if (p.next_tok) q.next_tok += qb;
   if (p.probes64) {
     int32_t *off = reinterpret_cast<int32_t *>(smem + p.seg_lds);
     int32_t *tile = off + p.S + 1;

@@ -52,7 +52,28 @@ __global__ void __launch_bounds__(kSegThreads) dresd_segments(SegParams p) {
   if (i == 0) p.seg_off[(size_t)b * (p.S + 1)] = 0;
 }
 
+// First token of each slot's value in the partitioned layout (0 for
+// padding): ftok[s] = cont[slot_row[s]][0].
+__global__ void __launch_bounds__(256) dresd_slot_first_tokens(const uint32_t *slot_row,
+                                                               const int32_t *cont, int L,
+                                                               int64_t nslot, int32_t *ftok) {
+  for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < nslot;
+       s += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t r = slot_row[s];
+    ftok[s] = r == kPadRow ? 0 : cont[(int64_t)r * L];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_slot_first_tokens(const uint32_t *slot_row, const int32_t *cont, int L,
+                                    int64_t nslot, int32_t *ftok, hipStream_t st) {
+  const int64_t want = (nslot + 255) / 256;
+  const unsigned blocks = (unsigned)(want < 65536 ? (want > 0 ? want : 1) : 65536);
+  hipLaunchKernelGGL(dresd_slot_first_tokens, dim3(blocks), dim3(256), 0, st, slot_row, cont, L,
+                     nslot, ftok);
+  return hipGetLastError();
+}
 
 hipError_t launch_segments(const SegParams &p, hipStream_t st) {
   if (p.B == 0) return hipSuccess;

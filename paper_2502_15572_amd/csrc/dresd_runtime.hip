@@ -723,6 +723,7 @@ struct dresd_ivf {
   dresd_index *ix = nullptr;     // keys in partition order, continuations by row
   dresd_index *cix = nullptr;    // the centroids (fp32 keys, exact probing)
   uint32_t *slot_row = nullptr;  // [T * 16] row of each slot, kPadRow for padding
+  int32_t *ftok_slot = nullptr;  // [T * 16] first token of each slot's value (0: padding)
   int32_t *part_tile = nullptr;  // [P + 1] first tile of each partition
   int32_t P = 0;
   int64_t probe_bytes = 0;       // probe results of the last search: ids + scores
@@ -736,6 +737,7 @@ void ivf_free(dresd_ivf *v) {
   if (v->ix) dresd_index_destroy(v->ix);
   if (v->cix) dresd_index_destroy(v->cix);
   if (v->slot_row) hipFree(v->slot_row);
+  if (v->ftok_slot) hipFree(v->ftok_slot);
   if (v->part_tile) hipFree(v->part_tile);
   if (v->probe) hipFree(v->probe);
   delete v;
@@ -744,8 +746,8 @@ void ivf_free(dresd_ivf *v) {
 // Scan of the probed partitions + merge.  probes64 (from the centroid
 // search) or probes32 (caller's) is [B][S] on the device.
 dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *probes64,
-                          const int32_t *probes32, int32_t S, int32_t B, int32_t k, int64_t *idx,
-                          float *score, int32_t *tokens, hipStream_t st) {
+                          const int32_t *probes32, int32_t S, const int32_t *next_tok, int32_t B,
+                          int32_t k, int64_t *idx, float *score, int32_t *tokens, hipStream_t st) {
   dresd_index *ix = v->ix;
   const int terms = ix->dtype == kF32 ? 1 : 4;  // the query as three exact 16-bit parts
   const int nq = 16 / terms;
@@ -814,8 +816,8 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   sp.CL = CL;
   sp.sort_lists = 1;
   sp.qop = nullptr;
-  sp.ftok = nullptr;
-  sp.next_tok = nullptr;
+  sp.ftok = next_tok ? v->ftok_slot : nullptr;
+  sp.next_tok = next_tok;
   sp.slot_row = v->slot_row;
   sp.seg_off = gp.seg_off;
   sp.seg_tile = gp.seg_tile;
@@ -917,6 +919,7 @@ dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuatio
     return s;
   };
   if (hipMalloc((void **)&v->slot_row, slot.size() * 4) != hipSuccess ||
+      hipMalloc((void **)&v->ftok_slot, slot.size() * 4) != hipSuccess ||
       hipMalloc((void **)&v->part_tile, pt.size() * 4) != hipSuccess) {
     (void)hipGetLastError();
     return bail(fail(DRESD_ENOMEM, "slot table allocation failed"));
@@ -924,6 +927,11 @@ dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuatio
   if (hipMemcpy(v->slot_row, slot.data(), slot.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(v->part_tile, pt.data(), pt.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
     return bail(fail(DRESD_EDEVICE, "slot table upload failed"));
+  // First token of each slot's value (the next-token filter).
+  if (launch_slot_first_tokens(v->slot_row, continuations, L, (int64_t)slot.size(), v->ftok_slot,
+                               st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return bail(fail(DRESD_EDEVICE, "first-token column build failed"));
   dresd_status s = index_build(embeddings, continuations, N, d, L, dtype, v->slot_row, T, stream,
                                &v->ix);
   if (s != DRESD_OK) return bail(s);
@@ -968,9 +976,12 @@ dresd_status dresd_ivf_info(const dresd_ivf *v, int64_t *N, int32_t *d, int32_t 
   return DRESD_OK;
 }
 
-dresd_status dresd_ivf_search(dresd_ivf *v, const float *queries, int32_t B, int32_t k,
-                              int32_t nprobe, int64_t *idx, float *score, int32_t *tokens,
-                              dresd_stream stream) {
+}  // extern "C"
+
+namespace {
+dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *next_tok,
+                             int32_t B, int32_t k, int32_t nprobe, int64_t *idx, float *score,
+                             int32_t *tokens, dresd_stream stream) {
   dresd_status s = validate_ivf_search(v, B, k);
   if (s != DRESD_OK) return s;
   if (nprobe < 1 || nprobe > std::min<int32_t>(v->P, DRESD_K_MAX))
@@ -1006,7 +1017,7 @@ dresd_status dresd_ivf_search(dresd_ivf *v, const float *queries, int32_t B, int
   s = search_impl(v->cix, queries, nullptr, B, nprobe, pid, psc, nullptr, stream);
   if (s != DRESD_OK) return s;
   // 2. exact top-k over the probed partitions
-  s = parts_search(v, queries, pid, nullptr, nprobe, B, k, idx, score, tokens, st);
+  s = parts_search(v, queries, pid, nullptr, nprobe, next_tok, B, k, idx, score, tokens, st);
   if (s != DRESD_OK) return s;
   if (ix->prof) {
     DRESD_HIP(hipEventRecord(a1, st));
@@ -1015,17 +1026,35 @@ dresd_status dresd_ivf_search(dresd_ivf *v, const float *queries, int32_t B, int
   }
   return DRESD_OK;
 }
+}  // namespace
+
+extern "C" {
+
+dresd_status dresd_ivf_search(dresd_ivf *v, const float *queries, int32_t B, int32_t k,
+                              int32_t nprobe, int64_t *idx, float *score, int32_t *tokens,
+                              dresd_stream stream) {
+  return ivf_search_impl(v, queries, nullptr, B, k, nprobe, idx, score, tokens, stream);
+}
+
+dresd_status dresd_ivf_search_filtered(dresd_ivf *v, const float *queries,
+                                       const int32_t *next_tok, int32_t B, int32_t k,
+                                       int32_t nprobe, int64_t *idx, float *score,
+                                       int32_t *tokens, dresd_stream stream) {
+  if (B > 0 && !next_tok) return fail(DRESD_EINVAL, "NULL pointer argument");
+  return ivf_search_impl(v, queries, next_tok, B, k, nprobe, idx, score, tokens, stream);
+}
 
 dresd_status dresd_ivf_search_probes(dresd_ivf *v, const float *queries, const int32_t *probes,
-                                     int32_t S, int32_t B, int32_t k, int64_t *idx, float *score,
-                                     int32_t *tokens, dresd_stream stream) {
+                                     int32_t S, const int32_t *next_tok, int32_t B, int32_t k,
+                                     int64_t *idx, float *score, int32_t *tokens,
+                                     dresd_stream stream) {
   dresd_status s = validate_ivf_search(v, B, k);
   if (s != DRESD_OK) return s;
   if (S < 1 || S > DRESD_K_MAX) return fail(DRESD_EINVAL, "S must be in [1, DRESD_K_MAX]");
   if (B > 0 && (!queries || !probes || !idx || !score))
     return fail(DRESD_EINVAL, "NULL pointer argument");
   if (B == 0) return DRESD_OK;
-  return parts_search(v, queries, nullptr, probes, S, B, k, idx, score, tokens,
+  return parts_search(v, queries, nullptr, probes, S, next_tok, B, k, idx, score, tokens,
                       static_cast<hipStream_t>(stream));
 }
 

@@ -53,13 +53,20 @@ def make(name, n, P, seed=0):
     return keys, cont, q, kb, dt, c, a
 
 
-def check(g, kb, dt, qn, cn, a, probes, k, P):
+def check(g, kb, dt, qn, cn, a, probes, k, P, next_tok=None):
     g_idx, g_score, g_tok = (t.cpu().numpy() for t in g)
-    o_idx, o_score, _, o_next = oracle.topk_partitioned(kb, dt, qn, k, a, P, probes, cn)
+    o_idx, o_score, _, o_next = oracle.topk_partitioned(kb, dt, qn, k, a, P, probes, cn,
+                                                        next_tok=next_tok)
     sets = [set(int(p) for p in row if 0 <= p < P) for row in probes]
+
+    def admitted(b, rows):
+        ok = np.isin(a[rows], list(sets[b]))
+        if next_tok is not None:
+            ok &= cn[rows, 0] == next_tok[b]
+        return ok
     return check_batch(g_idx, g_score, g_tok, o_idx, o_score, o_next,
                        lambda b, rows: oracle.score_rows(kb, dt, qn[b], rows), kb.shape[0], cn,
-                       TOL[dt], admitted_b=lambda b, rows: np.isin(a[rows], list(sets[b])))
+                       TOL[dt], admitted_b=admitted)
 
 
 CASES = [
@@ -166,4 +173,40 @@ def test_ivf_edges(gpu_lib):
     g = ix.search_probes(torch.from_numpy(q[:1]).to(DEV), torch.from_numpy(probes[3:4]).to(DEV), 5)
     torch.cuda.synchronize()
     check(g, kb, dt, q[:1], cont.numpy(), a, probes[3:4], 5, P)
+    ix.close()
+
+
+@pytest.mark.parametrize("name,n,P,B,k,S", CASES[:3], ids=[c[0] for c in CASES[:3]])
+def test_ivf_filtered(gpu_lib, name, n, P, B, k, S):
+    """Next-token filter over the probed partitions (Section 3.5): each
+    query's next token is its source row's first token, a frequent token, or
+    one that starts no value; caller probes and internal probing."""
+    from paper_2502_15572_amd import PartitionedIndex
+    say("ivf filtered", name, n, P, B, k, S)
+    keys, cont, q, kb, dt, c, a = make(name, n, P)
+    g = generate(WORKLOADS[name].scaled(n), "cpu", seed=0)
+    cn = cont.numpy()
+    src = g["query_src"][:B].numpy()
+    freq = int(np.bincount(cn[:, 0]).argmax())
+    nt = np.where(src >= 0, cn[np.maximum(src, 0), 0], freq).astype(np.int32)
+    nt[1] = freq
+    nt[2] = 10 ** 6
+    qn = q[:B].numpy()
+    ix = PartitionedIndex(keys.to(DEV), cont.to(DEV), torch.from_numpy(c).to(DEV),
+                          torch.from_numpy(a).to(DEV))
+    rng = np.random.default_rng(3)
+    probes = rng.integers(0, P, (B, S)).astype(np.int32)
+    ntd = torch.from_numpy(nt).to(DEV)
+    gq = ix.search_probes(q[:B].to(DEV), torch.from_numpy(probes).to(DEV), k, next_tok=ntd)
+    torch.cuda.synchronize()
+    check(gq, kb, dt, qn, cn, a, probes, k, P, next_tok=nt)
+    assert (gq[0][2] == -1).all()
+    # internal probing, on queries whose probed set is unique
+    p_idx, p_sc, _, _ = oracle.topk(c, "f32", qn, min(S + 1, P))
+    unique = p_sc[:, S - 1] - p_sc[:, S] >= 1e-5
+    gs = ix.search(q[:B].to(DEV), k, S, next_tok=ntd)
+    torch.cuda.synchronize()
+    sel = np.nonzero(unique)[0]
+    check(tuple(t[torch.from_numpy(sel)] for t in gs), kb, dt, qn[sel], cn, a,
+          p_idx[sel, :S].astype(np.int32), k, P, next_tok=nt[sel])
     ix.close()
