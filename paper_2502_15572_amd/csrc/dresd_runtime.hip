@@ -69,7 +69,12 @@ struct Group {
 };
 
 constexpr size_t kMaxGroup = 256;  // 16 query tiles x 16 columns
-constexpr int kMaxScanWgPerCu = 4;
+constexpr int kMaxScanWgPerCu = 4;  // shared-key scan (its LDS allows two)
+// Single-tile scan: one workgroup (4 waves, one per SIMD) per CU.  Each wave
+// streams one contiguous range; fewer, longer streams keep HBM rows open
+// longer (measured on 1M x 4096, 10M x 256 and 33.5M x 128 keys at B = 1:
+// +1.5-3.5% over two to four workgroups per CU).
+constexpr int kMaxTileWgPerCu = 1;
 
 struct Plan {
   int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
@@ -189,10 +194,9 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
   if (pl.lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS");
   int occ = std::min(occupancy(ix, pl.kmain, pl.lds), occupancy(ix, pl.ksample, pl.lds));
-  // At most 4 workgroups (16 waves) per CU: enough loads in flight to keep
-  // HBM busy, and few enough per-wave lists for the merge to keep their
-  // best keys in LDS.
-  pl.wg_max = ix->cus * std::min(occ, kMaxScanWgPerCu);
+  // Few enough workgroups per CU that the merge keeps the lists' best keys
+  // in LDS: one for the single-tile scan, up to four for the shared-key scan.
+  pl.wg_max = ix->cus * std::min(occ, pl.mq ? kMaxScanWgPerCu : kMaxTileWgPerCu);
   // lists per query: one per wave, or one per workgroup for the shared-key
   // scan; at most kMergeLists
   const int lists_per_wg = pl.mq ? 1 : kScanThreads / kWaveSize;
