@@ -313,11 +313,32 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
     ftok_group(1);
   }
 
-  auto mfma_block = [&](const u4 &blk) {
+  // A operands from LDS.  Up to 4 query tiles they are read one block ahead
+  // (the next block's reads are in flight while this block's matrix
+  // instructions run), so the LDS latency is not paid once per tile per
+  // block; more tiles read them just in time (registers).
+  constexpr bool PIPE = QT <= 4;
+  auto read_a = [&](int kb, u4 (&a)[PIPE ? QT : 1]) {
 #pragma unroll
-    for (int t = 0; t < QT; ++t) {
-      u4 a = *reinterpret_cast<const u4 *>(smem + qa0[t] + ckb * qstep[t]);
-      acc[t] = Mfma<DT>::run(a, blk, acc[t]);
+    for (int t = 0; t < (PIPE ? QT : 1); ++t)
+      a[t] = *reinterpret_cast<const u4 *>(smem + qa0[t] + kb * qstep[t]);
+  };
+  u4 a_cur[PIPE ? QT : 1];
+  if (PIPE) read_a(0, a_cur);
+  auto mfma_block = [&](const u4 &blk) {
+    if constexpr (PIPE) {
+      u4 a_nxt[QT];
+      read_a(ckb + 1 == KB ? 0 : ckb + 1, a_nxt);
+#pragma unroll
+      for (int t = 0; t < QT; ++t) acc[t] = Mfma<DT>::run(a_cur[t], blk, acc[t]);
+#pragma unroll
+      for (int t = 0; t < QT; ++t) a_cur[t] = a_nxt[t];
+    } else {
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        u4 a = *reinterpret_cast<const u4 *>(smem + qa0[t] + ckb * qstep[t]);
+        acc[t] = Mfma<DT>::run(a, blk, acc[t]);
+      }
     }
   };
   // Tile epilogue: threshold filter, rare slow path, reset for the next tile.

@@ -69,11 +69,13 @@ struct Group {
 };
 
 constexpr size_t kMaxGroup = 256;  // 16 query tiles x 16 columns
-constexpr int kMaxScanWgPerCu = 4;  // shared-key scan (its LDS allows two)
-// Single-tile scan: one workgroup (4 waves, one per SIMD) per CU.  Each wave
-// streams one contiguous range; fewer, longer streams keep HBM rows open
-// longer (measured on 1M x 4096, 10M x 256 and 33.5M x 128 keys at B = 1:
-// +1.5-3.5% over two to four workgroups per CU).
+constexpr int kMaxScanWgPerCu = 4;
+// One workgroup (4 waves, one per SIMD) per CU where it measured faster:
+// each wave (or workgroup) streams one contiguous range, and fewer, longer
+// streams keep HBM rows open longer (single-tile scan with one query tile on
+// 1M x 4096, 10M x 256 and 33.5M x 128 keys at B = 1: +1.5-3.5%; shared-key
+// scan on 4M x 1024 keys at B = 64-256: +3%).  Scans whose per-block work is
+// larger need the extra waves to hide latency.
 constexpr int kMaxTileWgPerCu = 1;
 
 struct Plan {
@@ -132,20 +134,24 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   pl = Plan();
   pl.filt = filt;
   // The query enters the matrix cores as three 16-bit parts that sum to it
-  // exactly (four columns per query) for bf16 keys and for small f16 batches;
-  // larger f16 batches round it once to f16.
+  // exactly (four columns per query) for bf16 keys and for f16 batches that
+  // fit one 16-column tile that way (B <= 4); larger f16 batches round it
+  // once to f16.
   if (ix->dtype == kBF16) pl.terms = 4;
-  else if (ix->dtype == kF16) pl.terms = (B <= 8) ? 4 : 1;
+  else if (ix->dtype == kF16) pl.terms = (B <= 4) ? 4 : 1;
   else pl.terms = 1;
   pl.qpt = 16 / pl.terms;
   pl.C = next_pow2(std::max(k + 64, 128));
   const int qt_all = (int)ceil_div((int64_t)B * pl.terms, 16);  // query tiles of the batch
   const bool mq_type = (ix->dtype == kF16 && pl.terms == 1) || ix->dtype == kBF16;
   const bool mq_kb = ix->KB == 4 || ix->KB == 8 || ix->KB == 16 || ix->KB == 32;
-  if (mq_type && mq_kb && qt_all >= 4) {
-    // Several query tiles: queries stationary in registers, keys shared
+  if (mq_type && mq_kb && (qt_all >= 2 || pl.terms == 1)) {
+    // Several query tiles, or one of f16-rounded queries (four scores per
+    // lane per key tile): queries stationary in registers, keys shared
     // through LDS.  Each of the 4 waves holds qtw tiles (operands for all
-    // KB blocks: qtw * KB <= 32 chunks of 16 bytes).
+    // KB blocks: qtw * KB <= 32 chunks of 16 bytes); one to three tiles are
+    // padded to four.  The single-tile scan re-reads every query operand
+    // from LDS per block and runs such batches 2-3x slower.
     pl.mq = true;
     int qtw = 1;
     while (qtw < 4 && 4 * qtw < qt_all && 2 * qtw * ix->KB <= 32) qtw <<= 1;
@@ -194,24 +200,31 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
   if (pl.lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS");
   int occ = std::min(occupancy(ix, pl.kmain, pl.lds), occupancy(ix, pl.ksample, pl.lds));
-  // Few enough workgroups per CU that the merge keeps the lists' best keys
-  // in LDS: one for the single-tile scan, up to four for the shared-key scan.
-  pl.wg_max = ix->cus * std::min(occ, pl.mq ? kMaxScanWgPerCu : kMaxTileWgPerCu);
+  // At most four workgroups per CU (few enough lists for the merge to keep
+  // their best keys in LDS); one where fewer, longer HBM streams measured
+  // faster: the single-tile scan with one query tile, and the shared-key
+  // scan over 32-block (1 KiB-row) key tiles.
+  const bool one_per_cu = pl.mq ? ix->KB >= 32 : pl.qt == 1;
+  pl.wg_max = ix->cus * std::min(occ, one_per_cu ? kMaxTileWgPerCu : kMaxScanWgPerCu);
   // lists per query: one per wave, or one per workgroup for the shared-key
   // scan; at most kMergeLists
   const int lists_per_wg = pl.mq ? 1 : kScanThreads / kWaveSize;
   pl.wg_max = std::min(pl.wg_max, kMergeLists / lists_per_wg);
   pl.G_max = pl.wg_max * lists_per_wg;
-  // Small batches: every wave keeps its own running top-k and sorts it at
-  // the end; the merge then prunes with the best per-wave k-th key.  Larger
-  // batches first set per-query thresholds from sampled passes over tiles
+  // Small batches (B <= 8): every wave keeps its own running top-k and sorts
+  // it at the end; the merge then prunes with the best per-wave k-th key.
+  // Batches past 8 queries, and smaller ones with k >= 16 and B * k >= 64
+  // (query, rank) pairs (measured: +5% at 5-8 queries, k = 16; +28-60% at
+  // 4-8 queries, k = 100; fewer (query, rank) pairs leave the main pass few
+  // candidates anyway), first set per-query thresholds from sampled passes
+  // over tiles
   // j*P, sparsest first (kept when they hold at least 4k rows and are at
   // most a quarter of the tiles).  A pass at stride P leaves about P*k
   // candidates per query for the next one, so batches with many
   // (query, rank) pairs add a denser level: its extra sampled scan costs less
   // than the candidates it removes from the full pass.
   pl.sort_lists = B <= 8;
-  if (!pl.sort_lists) {
+  if (!pl.sort_lists || (k >= 16 && (int64_t)B * k >= 64)) {
     const bool dense = (int64_t)B * k >= 8192;
     const std::vector<int64_t> ladder =
         dense ? std::vector<int64_t>{4096, 256, 16} : std::vector<int64_t>{4096, 64};

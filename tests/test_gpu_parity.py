@@ -91,7 +91,7 @@ def test_workload_parity_reduced(gpu_lib, name, N, _):
         say("  exact-order rate %.3f, max |g-exact| %.2e" % (rep["exact_order_rate"],
                                                            rep["max_abs_vs_exact"]))
         # split-query paths are within summation error of the oracle
-        if w.dtype in ("f32", "bf16") or B <= 8:
+        if w.dtype in ("f32", "bf16") or B <= 4:
             assert rep["max_abs_vs_exact"] <= 1e-5, rep
 
 
@@ -102,7 +102,10 @@ EDGE = [
     ("bf16", 17, 64, 2, 17),         # two tiles, k == N
     ("f32", 33, 20, 5, 7),           # fp32 keys with ragged dims
     ("f16", 1000, 128, 17, 63),      # B past one query tile (single f16 rounding)
-    ("f16", 1000, 128, 8, 64),       # largest split batch
+    ("f16", 1000, 128, 4, 64),       # largest split batch
+    ("f16", 1000, 128, 8, 64),       # rounded queries, one tile
+    ("f16", 3000, 1024, 32, 16),     # two query tiles padded into the shared-key scan
+    ("bf16", 2000, 256, 7, 12),      # bf16 over two query tiles: shared-key scan
     ("f16", 5000, 64, 16, 65),
     ("bf16", 3000, 96, 9, 100),      # bf16 split over two query tiles
     ("f16", 4096, 128, 64, 128),
