@@ -63,3 +63,49 @@ def test_last_error_is_thread_local():
     t.start()
     t.join()
     assert seen == [b""]
+
+
+def test_new_entry_points_reject_bad_arguments_before_device_work():
+    """Search variants, the transform, draft assembly, the partitioned index
+    and k-means validate their arguments before any HIP call."""
+    lib = _lib.load()
+    E = _lib.EINVAL
+    fake = ctypes.c_void_p(16)  # never dereferenced: arguments are checked first
+    out = ctypes.c_void_p()
+    assert lib.dresd_search_filtered(None, None, None, 1, 1, None, None, None, None) == E
+    # transform: ranges, then null pointers; M = 0 is a no-op
+    assert lib.dresd_transform(fake, -1, 4, fake, fake, 1e-5, fake, 2, 1e-12, fake, None) == E
+    assert lib.dresd_transform(fake, 1, 0, fake, fake, 1e-5, fake, 2, 1e-12, fake, None) == E
+    assert lib.dresd_transform(fake, 1, 4, fake, fake, -1.0, fake, 2, 1e-12, fake, None) == E
+    assert lib.dresd_transform(None, 1, 4, None, None, 1e-5, None, 2, 1e-12, None, None) == E
+    assert lib.dresd_transform(None, 0, 4, None, None, 1e-5, None, 2, 1e-12, None, None) == 0
+    # drafts: B, k, L, length, r ranges; nulls with B > 0; B = 0 is a no-op
+    for B, k, L, r, ln in [(-1, 4, 4, 2, 2), (1, 0, 4, 1, 2), (1, 2000, 4, 1, 2), (1, 4, 4, 5, 2),
+                           (1, 4, 4, 0, 2), (1, 4, 4, 2, 5), (1, 4, 4, 2, 0), (1, 4, 0, 2, 1)]:
+        assert lib.dresd_pack_drafts(fake, B, k, L, r, ln, 0, fake, fake, None) == E, (B, k, L, r)
+    assert lib.dresd_pack_drafts(None, 1, 4, 4, 2, 2, 0, None, None, None) == E
+    assert lib.dresd_pack_drafts(None, 0, 4, 4, 2, 2, 0, None, None, None) == 0
+    # partitioned index
+    assert lib.dresd_ivf_create(None, None, 10, 8, 4, 0, None, 2, None, None,
+                                ctypes.byref(out)) == E
+    for N, d, L, dt, P in [(0, 8, 4, 0, 2), (10, 0, 4, 0, 2), (10, 8, 0, 0, 2), (10, 8, 4, 3, 2),
+                           (10, 8, 4, 0, 0), (10, 8, 4, 0, (1 << 24) + 1)]:
+        assert lib.dresd_ivf_create(fake, fake, N, d, L, dt, fake, P, fake, None,
+                                    ctypes.byref(out)) == E, (N, d, L, dt, P)
+        assert out.value is None
+    assert lib.dresd_ivf_search(None, None, 1, 1, 1, None, None, None, None) == E
+    assert lib.dresd_ivf_search_filtered(None, None, None, 1, 1, 1, None, None, None, None) == E
+    assert lib.dresd_ivf_search_probes(None, None, None, 1, None, 1, 1, None, None, None,
+                                       None) == E
+    assert lib.dresd_ivf_info(None, None, None, None, None, None, None) == E
+    assert lib.dresd_ivf_profile_enable(None, 1) == E
+    assert lib.dresd_ivf_profile_read(None, None, None, None) == E
+    lib.dresd_ivf_destroy(None)  # ignored
+    # k-means
+    for n, d, dt, P in [(-1, 8, 0, 2), (10, 0, 0, 2), (10, 20000, 0, 2), (10, 8, 3, 2),
+                        (10, 8, 0, 0)]:
+        assert lib.dresd_kmeans_assign(fake, n, d, dt, fake, P, fake, None, None) == E
+        assert lib.dresd_kmeans_update(fake, n, d, dt, fake, P, fake, None, None) == E
+    assert lib.dresd_kmeans_assign(None, 10, 8, 0, None, 2, None, None, None) == E
+    assert lib.dresd_kmeans_assign(None, 0, 8, 0, None, 2, None, None, None) == 0
+    assert lib.dresd_kmeans_update(None, 10, 8, 0, None, 2, None, None, None) == E

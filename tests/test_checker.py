@@ -145,3 +145,38 @@ def test_filtered_padding_must_match():
     gt[2, 0, 0] = 1  # padding tokens must be zero
     with pytest.raises(ParityError):
         check_batch(gi, gs, gt, oi, os_, on, ex, N, cont, 1e-5, next_tok=nt)
+
+
+def _partitioned_case():
+    rng = np.random.default_rng(21)
+    N, d, P = 600, 16, 6
+    x = rng.standard_normal((N, d))
+    x = (x / np.linalg.norm(x, axis=1, keepdims=True)).astype(np.float32)
+    cont = rng.integers(0, 50, (N, 2)).astype(np.int32)
+    assign = rng.integers(0, P, N).astype(np.int32)
+    q = rng.standard_normal((3, d)).astype(np.float32)
+    probes = np.array([[0, 1], [2, 2], [5, -1]], np.int32)
+    o = oracle.topk_partitioned(x, "f32", q, 12, assign, P, probes, cont)
+    sets = [set(p for p in row if 0 <= p < P) for row in probes]
+
+    def ex(b, rows):
+        return oracle.score_rows(x, "f32", q[b], rows)
+
+    def adm(b, rows):
+        return np.isin(assign[rows], list(sets[b]))
+    return x, cont, assign, probes, o, ex, adm, N
+
+
+def test_partitioned_oracle_result_passes():
+    x, cont, assign, probes, (oi, os_, ot, on), ex, adm, N = _partitioned_case()
+    check_batch(oi, os_, ot, oi, os_, on, ex, N, cont, 1e-5, admitted_b=adm)
+
+
+def test_partitioned_row_outside_probes_fails():
+    x, cont, assign, probes, (oi, os_, ot, on), ex, adm, N = _partitioned_case()
+    gi, gs, gt = oi.copy(), os_.copy(), ot.copy()
+    bad = int(np.nonzero(~np.isin(assign, [0, 1]))[0][0])
+    gi[0, -1] = bad  # score left as the oracle's: only the partition rule can reject it
+    gt[0, -1] = cont[bad]
+    with pytest.raises(ParityError):
+        check_batch(gi, gs, gt, oi, os_, on, ex, N, cont, 1e-5, admitted_b=adm)
