@@ -164,7 +164,7 @@ def generate(w: Workload, device="cpu", seed: int = 0, with_queries: bool = True
         c1 = min(N, c0 + _CHUNK)
         t = _zipf_draw(tcdf, (c1 - c0) * w.L, _gen(device, seed, w.wid, 4, c0 // _CHUNK))
         cont[c0:c1] = t.view(c1 - c0, w.L).to(torch.int32)
-    out = {"keys": keys, "cont": cont, "assign": assign, "duplicates": dups}
+    out = {"keys": keys, "cont": cont, "assign": assign, "centres": centres, "duplicates": dups}
     if with_queries:
         out.update(_queries(w, keys, centres, scales, device, seed))
     return out
