@@ -98,7 +98,7 @@ dresd_status dresd_index_create(const void *embeddings,
  *
  * Order: rank r holds the r-th largest score; equal scores are ordered by
  * ascending row index.  Scores are accumulated in fp32.  For bf16 keys, and
- * for f16 keys while B <= 8, the query enters the matrix cores as three
+ * for f16 keys while B <= 4, the query enters the matrix cores as three
  * 16-bit parts that sum to it exactly (scores within fp32 summation error of
  * the exact inner product); larger f16 batches round the query once to f16
  * (score error below 5e-4, inside the 2e-3 parity bound for 16-bit keys).
