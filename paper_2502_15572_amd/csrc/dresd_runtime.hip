@@ -175,7 +175,8 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
     }
     int bmax = std::min(B, qt * pl.qpt);
     pl.CL = stage_cap(qt * pl.qpt);
-    if (scan_lds(std::min(bmax, pl.qpt) * pl.terms, ix->KB, pl.qpt, pl.CL, pl.C) > ix->lds_max)
+    // the smallest group (one query) must fit; larger batches shrink to fit
+    if (scan_lds(pl.terms, ix->KB, pl.qpt, pl.CL, pl.C) > ix->lds_max)
       return fail(DRESD_EUNSUPPORTED, "query tile does not fit in LDS for this d and k");
     // shrink bmax until it fits (qt == 1 case)
     while (bmax > 1 &&

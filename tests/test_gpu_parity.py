@@ -118,6 +118,11 @@ EDGE = [
     ("f32", 5000, 64, 100, 20),      # fp32, seven query tiles
     ("f16", 3000, 2048, 40, 10),     # f16 blocks per tile outside the shared-key scan
     ("bf16", 2000, 2048, 64, 8),     # bf16 (three-part queries), sixteen query tiles
+    # the largest d (16384): one query operand nearly fills the LDS, so
+    # batches split into groups of one or two queries
+    ("bf16", 300, 16384, 1, 5),
+    ("f16", 300, 16384, 2, 5),
+    ("f32", 200, 16384, 3, 4),
 ]
 
 
@@ -255,3 +260,16 @@ def test_argument_errors_on_device(gpu_lib):
     out = ix.search(q[:0], 5)  # B == 0 is a no-op
     assert out[0].shape == (0, 5)
     ix.close()
+
+
+def test_longest_values(gpu_lib):
+    """L = 4096 tokens per value (the largest): gathered bit for bit."""
+    say("max L")
+    gen = torch.Generator().manual_seed(17)
+    N, d, L = 200, 64, 4096
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float16)
+    q = torch.randn(3, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 2 ** 31 - 1, (N, L), generator=gen, dtype=torch.int32)
+    run_case(gpu_lib, x, cont, q, 7, "f16")
