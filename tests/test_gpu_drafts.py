@@ -37,6 +37,8 @@ CASES = [
     (3, 1024, 6, 300, 3, 5, 1),
     (2, 33, 20, 3, 20, 2, 0),
     (64, 32, 10, 32, 10, 50, 0),
+    (5, 16, 1, 16, 1, 3, 0),          # one-token values
+    (2, 1, 4, 1, 4, 2, 1),            # one retrieved continuation
 ]
 
 

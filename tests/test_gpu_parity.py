@@ -152,6 +152,9 @@ MQ_EDGE = [
     ("bf16", 15013, 256, 64, 40),     # three-part bf16 queries, 4 tiles per wave
     ("bf16", 7001, 128, 13, 9),       # smallest bf16 batch that fills 4 query tiles
     ("f16", 40009, 256, 200, 1000),   # large k: lists cut to k many times
+    ("f16", 100, 128, 40, 100),       # k == N: every row returned, in order
+    ("bf16", 999, 64, 8, 999),        # k == N, two padded query tiles
+    ("f16", 5000, 128, 600, 20),      # three groups of 256 queries
 ]
 
 
