@@ -97,11 +97,13 @@ dresd_status dresd_index_create(const void *embeddings,
  *   stream    stream the search runs on.
  *
  * Order: rank r holds the r-th largest score; equal scores are ordered by
- * ascending row index.  Scores are accumulated in fp32.  For bf16 keys, and
- * for f16 keys while B <= 4, the query enters the matrix cores as three
- * 16-bit parts that sum to it exactly (scores within fp32 summation error of
- * the exact inner product); larger f16 batches round the query once to f16
- * (score error below 5e-4, inside the 2e-3 parity bound for 16-bit keys).
+ * ascending row index.  Scores are accumulated in fp32.  For 16-bit keys and
+ * B <= 4 the query enters the matrix cores as three 16-bit parts that sum to
+ * it exactly (scores within fp32 summation error of the exact inner
+ * product); larger bf16 batches take two parts (their sum within 2^-17
+ * relative of the query: score error below 8e-6) and larger f16 batches the
+ * query rounded once to f16 (score error below 5e-4); both are inside the
+ * 2e-3 parity bound for 16-bit keys.
  * Determinism: identical inputs give bitwise identical outputs.
  * Ownership: outputs are caller-owned and must stay alive until `stream`
  * completes.  The index owns a workspace that grows on first use with a new

@@ -1,6 +1,6 @@
 """Build the HIP retrieval library (gfx950) in-tree: libdresd.so.
 
-The scan file is compiled as five translation units in parallel (one per
+The scan file is compiled as six translation units in parallel (one per
 scan variant, one for layout/dispatch), beside the merge and the runtime.
 Usage: python -m paper_2502_15572_amd.build [-v]
 """
@@ -30,7 +30,7 @@ HIPCC_FLAGS = [
 ]
 
 # (source, extra defines, object name)
-UNITS = [("dresd_kernels.hip", ["-DDRESD_TU=%d" % t], "kernels%d" % t) for t in range(5)] + [
+UNITS = [("dresd_kernels.hip", ["-DDRESD_TU=%d" % t], "kernels%d" % t) for t in range(6)] + [
     ("dresd_scan_mq.hip", ["-DDRESD_MQ_TU=0"], "scanmq0"),
     ("dresd_scan_mq.hip", ["-DDRESD_MQ_TU=1"], "scanmq1"),
     ("dresd_merge.hip", [], "merge"), ("dresd_transform.hip", [], "transform"),

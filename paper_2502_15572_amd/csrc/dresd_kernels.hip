@@ -79,6 +79,8 @@ struct Mfma<kBF16> {
 
 // Query operand: CPQ consecutive columns of the A operand hold one query.
 // CPQ = 1: the query itself (fp32 keys) or rounded once to f16;
+// CPQ = 2: bf16 keys, two parts: high and the rounded remainder (their sum
+//          is the query within 2^-17 relative);
 // CPQ = 4: three parts whose sum is the fp32 query exactly, plus a zero
 //          column.  bf16: high, middle, low.  f16: high, then the remainders
 //          scaled by 2^11 and 2^22 so they stay in f16's normal range (the
@@ -118,7 +120,7 @@ __device__ __forceinline__ u4 query_chunk(const float *q, int d, int B, int col,
       float r1 = x - (float)hi;
       __bf16 mid = (__bf16)r1;
       __bf16 lo = (__bf16)(r1 - (float)mid);
-      __bf16 r = (h == 0) ? hi : (h == 1) ? mid : (h == 2) ? lo : (__bf16)0.0f;
+      __bf16 r = (h == 0) ? hi : (h == 1) ? mid : (CPQ == 4 && h == 2) ? lo : (__bf16)0.0f;
       v[e] = __builtin_bit_cast(uint16_t, r);
     }
   }
@@ -359,6 +361,8 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
           const float s1 = (DT == kF16) ? (1.0f / 2048.0f) : 1.0f;
           const float s2 = (DT == kF16) ? (1.0f / 4194304.0f) : 1.0f;
           v = (v + acc[t][s * CPQ + 1] * s1) + acc[t][s * CPQ + 2] * s2;
+        } else if (CPQ == 2) {
+          v = v + acc[t][s * CPQ + 1];
         }
         sc[t][s] = v;
       }
@@ -564,7 +568,8 @@ __global__ void __launch_bounds__(kScanThreads) dresd_scan_parts(ScanParams p) {
     return table[main_pass ? 0 : 1][qi];                             \
   }
 
-// variants: 0 = f32 keys, 1 = f16 keys x1, 2 = f16 keys x4, 3 = bf16 keys x4
+// variants: 0 = f32 keys, 1 = f16 keys x1, 2 = f16 keys x4, 3 = bf16 keys x4,
+// 4 = bf16 keys x2
 #if !defined(DRESD_TU) || DRESD_TU == 1
 DRESD_VARIANT(0, kF32, 1)
 #endif
@@ -577,12 +582,16 @@ DRESD_VARIANT(2, kF16, 4)
 #if !defined(DRESD_TU) || DRESD_TU == 4
 DRESD_VARIANT(3, kBF16, 4)
 #endif
+#if !defined(DRESD_TU) || DRESD_TU == 5
+DRESD_VARIANT(4, kBF16, 2)
+#endif
 
 #if !defined(DRESD_TU) || DRESD_TU == 0
 ScanKernel scan_kernel_variant0(int, bool);
 ScanKernel scan_kernel_variant1(int, bool);
 ScanKernel scan_kernel_variant2(int, bool);
 ScanKernel scan_kernel_variant3(int, bool);
+ScanKernel scan_kernel_variant4(int, bool);
 
 int qt_index(int qt) {
   switch (qt) {
@@ -602,6 +611,7 @@ ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass) {
   if (dtype == kF16 && cpq == 1) return scan_kernel_variant1(qi, main_pass);
   if (dtype == kF16 && cpq == 4) return scan_kernel_variant2(qi, main_pass);
   if (dtype == kBF16 && cpq == 4) return scan_kernel_variant3(qi, main_pass);
+  if (dtype == kBF16 && cpq == 2) return scan_kernel_variant4(qi, main_pass);
   return nullptr;
 }
 

@@ -134,10 +134,11 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   pl = Plan();
   pl.filt = filt;
   // The query enters the matrix cores as three 16-bit parts that sum to it
-  // exactly (four columns per query) for bf16 keys and for f16 batches that
-  // fit one 16-column tile that way (B <= 4); larger f16 batches round it
-  // once to f16.
-  if (ix->dtype == kBF16) pl.terms = 4;
+  // exactly (four columns per query) for batches that fit one 16-column tile
+  // that way (B <= 4); larger batches take fewer columns: bf16 keys two
+  // parts (high + rounded remainder, within 2^-17 relative of the query),
+  // f16 keys the query rounded once to f16.
+  if (ix->dtype == kBF16) pl.terms = (B <= 4) ? 4 : 2;
   else if (ix->dtype == kF16) pl.terms = (B <= 4) ? 4 : 1;
   else pl.terms = 1;
   pl.qpt = 16 / pl.terms;
@@ -145,9 +146,10 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   const int qt_all = (int)ceil_div((int64_t)B * pl.terms, 16);  // query tiles of the batch
   const bool mq_type = (ix->dtype == kF16 && pl.terms == 1) || ix->dtype == kBF16;
   const bool mq_kb = ix->KB == 4 || ix->KB == 8 || ix->KB == 16 || ix->KB == 32;
-  if (mq_type && mq_kb && (qt_all >= 2 || pl.terms == 1)) {
-    // Several query tiles, or one of f16-rounded queries (four scores per
-    // lane per key tile): queries stationary in registers, keys shared
+  if (mq_type && mq_kb && (qt_all >= 2 || pl.terms < 4)) {
+    // Several query tiles, or one of one- or two-column queries (four or
+    // two scores per lane per key tile): queries stationary in registers,
+    // keys shared
     // through LDS.  Each of the 4 waves holds qtw tiles (operands for all
     // KB blocks: qtw * KB <= 32 chunks of 16 bytes); one to three tiles are
     // padded to four.  The single-tile scan re-reads every query operand

@@ -40,8 +40,10 @@ struct MfmaMQ<kBF16> {
 };
 
 // A-operand chunk of column `col` for dims [dim0, dim0+8): CPQ = 1 rounds the
-// query once to the key type; CPQ = 4 gives three parts summing to it exactly
-// (f16 lower parts scaled by 2^11, 2^22) and a zero column.  `vec`: rows of
+// query once to the key type; CPQ = 2 (bf16) gives the high part and the
+// rounded remainder (sum within 2^-17 relative of the query); CPQ = 4 gives
+// three parts summing to it exactly (f16 lower parts scaled by 2^11, 2^22)
+// and a zero column.  `vec`: rows of
 // q start 16-byte aligned, so a whole chunk is two 16-byte loads.
 template <int DT, int CPQ>
 __device__ __forceinline__ u4 query_chunk_mq(const float *q, int d, int B, int col, int dim0,
@@ -80,7 +82,7 @@ __device__ __forceinline__ u4 query_chunk_mq(const float *q, int d, int B, int c
       float r1 = x[e] - (float)hi;
       __bf16 mid = (__bf16)r1;
       __bf16 lo = (__bf16)(r1 - (float)mid);
-      __bf16 r = (h == 0) ? hi : (h == 1) ? mid : (h == 2) ? lo : (__bf16)0.0f;
+      __bf16 r = (h == 0) ? hi : (h == 1) ? mid : (CPQ == 4 && h == 2) ? lo : (__bf16)0.0f;
       v[e] = __builtin_bit_cast(uint16_t, r);
     }
   }
@@ -340,6 +342,8 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
           const float s1 = (DT == kF16) ? (1.0f / 2048.0f) : 1.0f;
           const float s2 = (DT == kF16) ? (1.0f / 4194304.0f) : 1.0f;
           v = (v + acc[t][s * CPQ + 1] * s1) + acc[t][s * CPQ + 2] * s2;
+        } else if (CPQ == 2) {
+          v = v + acc[t][s * CPQ + 1];
         }
         sc[t * NS + s] = v;
       }
@@ -551,10 +555,10 @@ void *qop_kernel_f16() { return (void *)dresd_query_operand<kF16, 1>; }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
 ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, bool filtered, int *stages) {
-  DRESD_MQ_ALL(kBF16, 4)
+  DRESD_MQ_ALL(kBF16, 2)
   return nullptr;
 }
-void *qop_kernel_bf16() { return (void *)dresd_query_operand<kBF16, 4>; }
+void *qop_kernel_bf16() { return (void *)dresd_query_operand<kBF16, 2>; }
 #endif
 
 }  // namespace dresd
