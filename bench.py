@@ -168,6 +168,81 @@ def time_drafts(args):
                                  "mean_kept": float(count.float().mean())}}), flush=True)
 
 
+def time_pipeline(args):
+    """One decode step of retrieval (Algorithm 1 steps 4-8) on one stream:
+    B hidden states of D fp32 dims -> transform (Eq. 1, a D x d projection
+    standing in for the PCA basis, Eq. 2) -> next-token-filtered search of
+    the workload's datastore (exact, or partitioned with --ivf P) -> draft
+    assembly into 10 EOS-padded drafts.  Times the whole step."""
+    import torch
+    from datagen import WORKLOADS, generate
+    from paper_2502_15572_amd import (Index, PartitionedIndex, kmeans_assign, pack_drafts,
+                                      train_partitions, transform)
+    w = WORKLOADS[args.workload]
+    if args.n:
+        w = w.scaled(args.n)
+    k, B, D = args.k or w.k, args.batch, args.pipeline
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = generate(w, dev, with_queries=False)
+    keys, cont = g["keys"], g["cont"]
+    nprobe = args.nprobe[0]
+    if args.ivf:
+        pick = torch.randperm(w.N, generator=torch.Generator().manual_seed(1))
+        sample = keys[pick[: min(w.N, args.train_rows_per_part * args.ivf)].to(dev)].contiguous()
+        cents, _ = train_partitions(sample, args.ivf, iters=args.train_iters, seed=2)
+        ix = PartitionedIndex(keys, cont, cents, kmeans_assign(keys, cents))
+        search = lambda y, nt, out: ix.search(y, k, nprobe, out=out, next_tok=nt)
+    else:
+        ix = Index(keys, cont)
+        search = lambda y, nt, out: ix.search(y, k, out=out, next_tok=nt)
+    torch.cuda.synchronize()
+    log("index ready: %s, %s" % (w.name, "partitioned P=%d nprobe=%d" % (args.ivf, nprobe)
+                                  if args.ivf else "exact"))
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    xs = torch.randn(64, B, D, device=dev, generator=gen)
+    mean = torch.randn(D, device=dev, generator=gen)
+    var = torch.rand(D, device=dev, generator=gen) + 0.5
+    W = torch.randn(D, w.d, device=dev, generator=gen) / D ** 0.5
+    # next token: the most frequent first token other than the EOS id (0)
+    c0 = cont[: min(w.N, 1 << 20), 0]
+    frequent = int(torch.mode(c0[c0 != 0]).values)
+    nt = torch.full((B,), frequent, dtype=torch.int32, device=dev)
+    y = torch.empty(B, w.d, device=dev)
+    out = (torch.empty((B, k), dtype=torch.int64, device=dev),
+           torch.empty((B, k), dtype=torch.float32, device=dev),
+           torch.empty((B, k, w.L), dtype=torch.int32, device=dev))
+    r = min(10, k)
+    dout = (torch.empty((B, r, w.L), dtype=torch.int32, device=dev),
+            torch.empty((B,), dtype=torch.int32, device=dev))
+
+    def step(i):
+        transform(xs[i % 64], mean, var, W, out=y)
+        search(y, nt, out)
+        pack_drafts(out[2], r, w.L, out=dout)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record()
+        step(i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    per = sorted(a.elapsed_time(b) for a, b in ev)
+    print(json.dumps({"pipeline": {
+        "workload": w.name, "N": w.N, "d": w.d, "D": D, "B": B, "k": k, "drafts": r,
+        "search": ("partitioned P=%d nprobe=%d" % (args.ivf, nprobe)) if args.ivf else "exact",
+        "steps_per_s": args.steps / el, "queries_per_s": args.steps * B / el,
+        "p50_us": statistics.median(per) * 1e3,
+        "mean_drafts_kept": float(dout[1].float().mean())}}), flush=True)
+    ix.close()
+
+
 def time_partitioned(args):
     """Partitioned (inverted-file) search of the workload: spherical k-means
     on a seeded sample of the keys, every key assigned, then B-query searches
@@ -308,6 +383,10 @@ def main():
     ap.add_argument("--train-rows-per-part", type=int, default=64,
                     help="k-means sample: this many keys per partition (--ivf)")
     ap.add_argument("--train-iters", type=int, default=10, help="k-means iterations (--ivf)")
+    ap.add_argument("--pipeline", type=int, default=0, metavar="D",
+                    help="only time one decode step of retrieval: B hidden states of D dims -> "
+                         "transform -> filtered search (exact, or partitioned with --ivf) -> "
+                         "10 drafts")
     ap.add_argument("--drafts", type=int, default=0, metavar="R",
                     help="only time draft assembly of the workload's k continuations into R "
                          "drafts (Section 3.6)")
@@ -321,6 +400,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.pipeline:
+        time_pipeline(args)
         return
     if args.ivf:
         time_partitioned(args)
