@@ -35,6 +35,13 @@
 extern "C" {
 #endif
 
+/*
+ * Streams and graphs.  Every search, transform and draft call only enqueues
+ * kernels on the given stream once a first call of the same shapes has sized
+ * the workspaces it uses (that first call may allocate and synchronise).
+ * After such a warm-up call these calls can be captured in a HIP graph:
+ * they issue no allocation, no synchronisation and no memset while running.
+ */
 typedef struct dresd_index dresd_index; /* opaque, library-owned */
 typedef struct dresd_ivf dresd_ivf;     /* opaque: partitioned index */
 typedef void *dresd_stream;             /* a hipStream_t */

@@ -1,0 +1,70 @@
+"""A decode step (transform -> filtered search -> drafts) captured in a HIP
+graph after one warm-up call of the same shapes: every replay, with other
+work and synchronisations between replays, equals the eager step bit for bit
+(exact and partitioned search)."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+@pytest.mark.parametrize("partitioned", [False, True], ids=["exact", "partitioned"])
+def test_captured_step_replays_match_eager(gpu_lib, partitioned):
+    from paper_2502_15572_amd import (Index, PartitionedIndex, kmeans_assign, pack_drafts,
+                                      train_partitions, transform)
+    dev = torch.device(DEV)
+    gen = torch.Generator(device="cuda").manual_seed(3)
+    N, d, D, L, B, k = 30000, 64, 512, 5, 3, 20
+    keys = torch.randn(N, d, device=dev, generator=gen)
+    keys = (keys / keys.norm(dim=1, keepdim=True)).to(torch.float16)
+    cont = torch.randint(0, 6, (N, L), device=dev, generator=gen, dtype=torch.int32)
+    if partitioned:
+        cents, _ = train_partitions(keys, 32, iters=3, seed=1)
+        ix = PartitionedIndex(keys, cont, cents, kmeans_assign(keys, cents))
+        search = lambda y, o, s: ix.search(y, k, 6, out=o, next_tok=nt, stream=s)
+    else:
+        ix = Index(keys, cont)
+        search = lambda y, o, s: ix.search(y, k, out=o, next_tok=nt, stream=s)
+    xs = torch.randn(8, B, D, device=dev, generator=gen)
+    mean = torch.randn(D, device=dev, generator=gen)
+    var = torch.rand(D, device=dev, generator=gen) + 0.5
+    W = torch.randn(D, d, device=dev, generator=gen) / D ** 0.5
+    nt = torch.tensor([1, 2, 3], dtype=torch.int32, device=dev)
+    x_in = torch.empty(B, D, device=dev)
+    y = torch.empty(B, d, device=dev)
+    out = (torch.empty((B, k), dtype=torch.int64, device=dev),
+           torch.empty((B, k), dtype=torch.float32, device=dev),
+           torch.empty((B, k, L), dtype=torch.int32, device=dev))
+    dout = (torch.empty((B, 4, L), dtype=torch.int32, device=dev),
+            torch.empty((B,), dtype=torch.int32, device=dev))
+    s = torch.cuda.Stream()
+
+    def step():
+        transform(x_in, mean, var, W, out=y, stream=s)
+        search(y, out, s)
+        pack_drafts(out[2], 4, L, out=dout, stream=s)
+
+    with torch.cuda.stream(s):
+        x_in.copy_(xs[0])
+        step()  # warm-up: workspaces reach their size
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        step()
+    torch.cuda.synchronize()
+    for i in range(6):
+        x_in.copy_(xs[i % 8])
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        replayed = [t.clone() for t in out + dout]
+        torch.randn(4096, device=dev).sum().item()  # other work between replays
+        with torch.cuda.stream(s):
+            step()
+        torch.cuda.synchronize()
+        for a, b in zip(replayed, out + dout):
+            assert torch.equal(a, b), i
+    assert (out[0] >= -1).all() and int(dout[1].max()) >= 1
+    ix.close()
