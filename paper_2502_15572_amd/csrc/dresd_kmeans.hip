@@ -6,9 +6,10 @@
 //   assign : every row goes to the centroid with the largest inner product,
 //            ties to the lower centroid id.  An LDS-tiled fp32 contraction on
 //            the fp32 matrix cores (v_mfma_f32_16x16x4_f32): a workgroup owns
-//            64 rows and walks all centroids in tiles of 64, staging 128 dims
-//            of rows (decoded from their storage type) and centroids per step;
-//            the argmax is fused into the epilogue of each centroid tile.
+//            64 rows (decoded from their storage type, staged once when they
+//            have at most 128 dims) and walks all centroids in tiles of 64 x
+//            128 dims, loading the next tile while it multiplies this one; the
+//            argmax is fused into the epilogue of each centroid tile.
 //   update : each centroid becomes the unit vector along the sum of its
 //            rows (unchanged when it has none).  Rows are added into 64-bit
 //            fixed point (2^-30 units) with integer atomics, so the sums, and
@@ -41,6 +42,57 @@ __device__ __forceinline__ bool beats(float s, int id, float bs, int bid) {
   return s > bs || (s == bs && id < bid);
 }
 
+// Rows [r0, r0 + 64) x dims [k0, k0 + 128) of x, decoded to fp32, into xs
+// (zero past n and d): thread t takes row t / 4, dims 32 (t % 4) .. + 32,
+// with 16-byte loads when the rows allow them (`vec`).
+template <int DT>
+__device__ __forceinline__ void stage_rows(const KmeansParams &p, int64_t r0, int k0,
+                                           float (*xs)[kKK + 1], bool vec) {
+  const int tid = threadIdx.x;
+  const int r = tid >> 2, kk = (tid & 3) * 32;
+  const int64_t row = r0 + r;
+  const int d = p.d;
+  if (vec && row < p.n && k0 + kk + 32 <= d) {
+    if constexpr (DT == kF32) {
+      const float4 *src =
+          reinterpret_cast<const float4 *>(static_cast<const float *>(p.x) + row * d + k0 + kk);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float4 v = src[e];
+        xs[r][kk + 4 * e] = v.x;
+        xs[r][kk + 4 * e + 1] = v.y;
+        xs[r][kk + 4 * e + 2] = v.z;
+        xs[r][kk + 4 * e + 3] = v.w;
+      }
+    } else {
+      const uint4 *src =
+          reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.x) + row * d + k0 + kk);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint4 v = src[e];
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint16_t lo = (uint16_t)(w[j] & 0xffffu), hi = (uint16_t)(w[j] >> 16);
+          if constexpr (DT == kF16) {
+            xs[r][kk + 8 * e + 2 * j] = (float)__builtin_bit_cast(_Float16, lo);
+            xs[r][kk + 8 * e + 2 * j + 1] = (float)__builtin_bit_cast(_Float16, hi);
+          } else {
+            xs[r][kk + 8 * e + 2 * j] = __uint_as_float((uint32_t)lo << 16);
+            xs[r][kk + 8 * e + 2 * j + 1] = __uint_as_float((uint32_t)hi << 16);
+          }
+        }
+      }
+    }
+  } else {
+#pragma unroll 8
+    for (int e = 0; e < 32; ++e) {
+      const int k = k0 + kk + e;
+      xs[r][kk + e] = (row < p.n && k < d) ? load_elem<DT>(p.x, row * d + k) : 0.f;
+    }
+  }
+}
+
 template <int DT>
 __global__ void __launch_bounds__(256) dresd_kmeans_assign(KmeansParams p) {
   __shared__ float xs[kKR][kKK + 1];  // rows (padded: no bank conflicts)
@@ -50,6 +102,9 @@ __global__ void __launch_bounds__(256) dresd_kmeans_assign(KmeansParams p) {
   const int g = lane >> 4, m = lane & 15;
   const int64_t r0 = (int64_t)blockIdx.x * kKR;
   const int d = p.d, P = p.P;
+  const int es = DT == kF32 ? 4 : 2;
+  const bool xvec = (((uintptr_t)p.x & 15u) == 0) && ((d * es) % 16 == 0);
+  const bool cvec = (((uintptr_t)p.centroids & 15u) == 0) && (d % 4 == 0);
   // running best of rows wv*16 + 4g + i (identical in the 16 lanes of a group)
   float best[4];
   int bid[4];
@@ -58,30 +113,54 @@ __global__ void __launch_bounds__(256) dresd_kmeans_assign(KmeansParams p) {
     best[i] = -__builtin_inff();
     bid[i] = 0x7fffffff;
   }
+  // Centroid tile (c0, k0) goes through registers: thread t loads centroid
+  // c0 + t / 4, dims k0 + 32 (t % 4) .. + 32 (one tile ahead of its use).
+  float4 creg[8];
+  auto load_c = [&](int c0, int k0) {
+    const int c = c0 + (tid >> 2), kk = k0 + (tid & 3) * 32;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = kk + 4 * e;
+      const float *src = p.centroids + (int64_t)c * d + k;
+      if (c < P && cvec && k + 4 <= d) {
+        creg[e] = *reinterpret_cast<const float4 *>(src);
+      } else {
+        creg[e].x = (c < P && k < d) ? src[0] : 0.f;
+        creg[e].y = (c < P && k + 1 < d) ? src[1] : 0.f;
+        creg[e].z = (c < P && k + 2 < d) ? src[2] : 0.f;
+        creg[e].w = (c < P && k + 3 < d) ? src[3] : 0.f;
+      }
+    }
+  };
+  auto store_c = [&]() {
+    const int cl = tid >> 2, kk = (tid & 3) * 32;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      cs[kk + 4 * e][cl] = creg[e].x;
+      cs[kk + 4 * e + 1][cl] = creg[e].y;
+      cs[kk + 4 * e + 2][cl] = creg[e].z;
+      cs[kk + 4 * e + 3][cl] = creg[e].w;
+    }
+  };
+  // Rows of at most 128 dims are staged once for all centroid tiles.
+  const bool x_once = d <= kKK;
+  if (x_once) stage_rows<DT>(p, r0, 0, xs, xvec);
+  load_c(0, 0);
   for (int c0 = 0; c0 < P; c0 += kKC) {
     f4 acc[kKC / 16];
 #pragma unroll
     for (int t = 0; t < kKC / 16; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < d; k0 += kKK) {
-      // rows: thread t stages row t/4, dims 32(t%4)..+32; centroids: thread
-      // t stages dim t/2, centroids 32(t%2)..+32; zero past n, P or d.
-      {
-        const int r = tid >> 2, kk = (tid & 3) * 32;
-        const int64_t row = r0 + r;
-#pragma unroll 8
-        for (int e = 0; e < 32; ++e) {
-          const int k = k0 + kk + e;
-          xs[r][kk + e] = (row < p.n && k < d) ? load_elem<DT>(p.x, row * d + k) : 0.f;
-        }
-        const int kc = tid >> 1, cc = (tid & 1) * 32;
-        const int k = k0 + kc;
-#pragma unroll 8
-        for (int e = 0; e < 32; ++e) {
-          const int c = c0 + cc + e;
-          cs[kc][cc + e] = (k < d && c < P) ? p.centroids[(int64_t)c * d + k] : 0.f;
-        }
-      }
+      if (!x_once) stage_rows<DT>(p, r0, k0, xs, xvec);
+      store_c();
       __syncthreads();
+      // the next centroid tile's loads overlap this tile's matrix work
+      int nk0 = k0 + kKK, nc0 = c0;
+      if (nk0 >= d) {
+        nk0 = 0;
+        nc0 = c0 + kKC;
+      }
+      if (nc0 < P) load_c(nc0, nk0);
       // lane (g, m) feeds A[row m][k g] and B[k g][centroid m]
 #pragma unroll 8
       for (int ks = 0; ks < kKK; ks += 4) {
