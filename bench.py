@@ -67,6 +67,23 @@ def read_traffic(workload: str, batch: int, scan_kernel: str):
     return float(b.group(1))
 
 
+def search_latency(run, steps: int):
+    """p50 and p90 device time of one search (ms): events on the current
+    stream around each of `steps` searches, in a loop of its own so that the
+    timed region carries no per-search events."""
+    import torch
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record(stream)
+        run(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    per = sorted(a.elapsed_time(b) for a, b in ev)
+    return statistics.median(per), per[min(len(per) - 1, int(0.9 * len(per)))]
+
+
 def copy_calibration(nbytes: int):
     """A plain device copy of known size, to scale the HBM byte counters."""
     import torch
@@ -224,21 +241,17 @@ def time_pipeline(args):
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
     t0 = time.perf_counter()
     for i in range(args.steps):
-        ev[i][0].record()
         step(i)
-        ev[i][1].record()
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
-    per = sorted(a.elapsed_time(b) for a, b in ev)
+    p50, _ = search_latency(step, args.steps)
     print(json.dumps({"pipeline": {
         "workload": w.name, "N": w.N, "d": w.d, "D": D, "B": B, "k": k, "drafts": r,
         "search": ("partitioned P=%d nprobe=%d" % (args.ivf, nprobe)) if args.ivf else "exact",
         "steps_per_s": args.steps / el, "queries_per_s": args.steps * B / el,
-        "p50_us": statistics.median(per) * 1e3,
+        "p50_us": p50 * 1e3,
         "mean_drafts_kept": float(dout[1].float().mean())}}), flush=True)
     ix.close()
 
@@ -324,22 +337,17 @@ def time_partitioned(args):
         for i in range(args.warmup):
             ivf.search(batches[i % nb], k, nprobe, out=out, next_tok=nts[i % nb])
         torch.cuda.synchronize()
-        stream = torch.cuda.current_stream()
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
         ivf.profile(True)
         ivf.profile_read()
         t0 = time.perf_counter()
         for i in range(args.steps):
-            ev[i][0].record(stream)
             ivf.search(batches[i % nb], k, nprobe, out=out, next_tok=nts[i % nb])
-            ev[i][1].record(stream)
         torch.cuda.synchronize()
         el = time.perf_counter() - t0
         prof = ivf.profile_read()
         ivf.profile(False)
-        per = sorted(a.elapsed_time(b) for a, b in ev)
-        p50 = statistics.median(per)
+        p50, _ = search_latency(lambda i: ivf.search(batches[i % nb], k, nprobe, out=out,
+                                                     next_tok=nts[i % nb]), args.steps)
         scan_ms = prof["scan_ms"] / max(1, prof["searches"])
         scan_bytes = probe_rows * B * w.d * w.elem_bytes
         print(json.dumps({
@@ -454,24 +462,20 @@ def main():
         ix.search(batches[i % nb], k, out=out, next_tok=tok_batches[i % nb])
     torch.cuda.synchronize()
 
-    stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    # Timed region: K back-to-back searches; the library times its main scan
+    # kernel with events tied to that kernel's dispatch.
     ix.profile(True)
     ix.profile_read()  # clear
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        ev[i][0].record(stream)
         ix.search(batches[i % nb], k, out=out, next_tok=tok_batches[i % nb])
-        ev[i][1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     prof = ix.profile_read()
     ix.profile(False)
-    per = sorted(a.elapsed_time(b) for a, b in ev)  # ms, device time per search
-    p50 = statistics.median(per)
-    p90 = per[min(len(per) - 1, int(0.9 * len(per)))]
+    p50, p90 = search_latency(lambda i: ix.search(batches[i % nb], k, out=out,
+                                                  next_tok=tok_batches[i % nb]), args.steps)
 
     s = w.elem_bytes
     scan_bytes = w.N * w.d * s + B * w.d * 4           # keys once + queries

@@ -157,9 +157,11 @@ void dresd_index_destroy(dresd_index *ix);
 const char *dresd_last_error(void);
 
 /*
- * Measurement support.  When enabled, every search records HIP events on its
- * stream around the main scan kernel (the full pass over the keys) and around
- * the whole search.  dresd_profile_read synchronises those events and
+ * Measurement support.  When enabled, every search ties HIP events to its
+ * kernels' own dispatches (hipExtLaunchKernel): the begin and end of the main
+ * scan kernel (the full pass over the keys), and the begin of the search's
+ * first kernel and the end of its last, so that profiling adds no packets
+ * between kernels.  dresd_profile_read synchronises those events and
  * returns the summed device milliseconds and the number of searches since
  * the last read, then clears them.  Outputs are host pointers (NULL allowed).
  * Errors: EINVAL when ix is NULL; EDEVICE.

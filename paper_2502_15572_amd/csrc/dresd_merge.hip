@@ -139,6 +139,8 @@ __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk)
 
 // Output of one query from its sorted winners win[0..kk): the k-th best key
 // (sampled pass) or indices, scores and gathered continuations (final pass).
+// Each thread issues all of its continuation loads before its first store,
+// so the gather costs one memory latency rather than one per token.
 __device__ inline void write_result(const MergeParams &p, int b, const uint64_t *win,
                                     uint32_t kk, int tid, int nth) {
   if (!p.final_mode) {
@@ -157,15 +159,24 @@ __device__ inline void write_result(const MergeParams &p, int b, const uint64_t 
     }
   }
   if (p.tokens) {
-    const int L = p.L;
-    for (int i = tid; i < p.k * L; i += nth) {
-      const int r = i / L, l = i - r * L;
-      int32_t v = 0;
-      if (r < (int)kk) {
-        const uint32_t row = ~(uint32_t)win[r];
-        v = p.cont[(size_t)row * L + l];
+    constexpr int R = 8;  // tokens per thread per round, loaded together
+    const int L = p.L, n = p.k * L;
+    int32_t *out = p.tokens + (size_t)b * p.k * L;
+    for (int i0 = tid; i0 < n; i0 += R * nth) {
+      int32_t v[R];
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int i = i0 + u * nth;
+        const int r = i / L;
+        v[u] = 0;
+        if (i < n && r < (int)kk) {
+          const uint32_t row = ~(uint32_t)win[r];
+          v[u] = p.cont[(size_t)row * L + (i - r * L)];
+        }
       }
-      p.tokens[((size_t)b * p.k + r) * L + l] = v;
+#pragma unroll
+      for (int u = 0; u < R; ++u)
+        if (i0 + u * nth < n) out[i0 + u * nth] = v[u];
     }
   }
 }
@@ -256,19 +267,31 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
   __syncthreads();
   const uint32_t total = sh.total;
   const int nl = G;
-  for (uint32_t i = tid; i < total; i += nth) {
-    // the last list whose offset is <= i holds key i
-    int lo = 0, hi = nl;  // answer in [lo, hi)
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (sh.hist[mid] <= i) lo = mid;
-      else hi = mid;
+  constexpr int R = 8;  // keys per thread per round, loaded together
+  for (uint32_t i0 = tid; i0 < total; i0 += R * nth) {
+    uint64_t key[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const uint32_t i = i0 + (uint32_t)(u * nth);
+      key[u] = 0ull;
+      if (i < total) {
+        // the last list whose offset is <= i holds key i
+        int lo = 0, hi = nl;  // answer in [lo, hi)
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (sh.hist[mid] <= i) lo = mid;
+          else hi = mid;
+        }
+        key[u] = lists[(size_t)lo * p.C + (i - sh.hist[lo])];
+      }
     }
-    const uint64_t key = lists[(size_t)lo * p.C + (i - sh.hist[lo])];
-    if (key >= bnd) {
-      const uint32_t at = atomicAdd(&sh.ncand, 1u);
-      if (at < (uint32_t)kMergeCap) sh.cache[at] = key;
-      else if ((int64_t)(at - kMergeCap) < p.spill_cap) spill[at - kMergeCap] = key;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      if (i0 + (uint32_t)(u * nth) < total && key[u] >= bnd) {
+        const uint32_t at = atomicAdd(&sh.ncand, 1u);
+        if (at < (uint32_t)kMergeCap) sh.cache[at] = key[u];
+        else if ((int64_t)(at - kMergeCap) < p.spill_cap) spill[at - kMergeCap] = key[u];
+      }
     }
   }
   __threadfence_block();
@@ -284,8 +307,9 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
       for (int i = (int)M + tid; i < n; i += kWaveSize) sh.cache[i] = 0ull;
       wave_sync_lds();
       wave_bitonic_desc(sh.cache, n, tid);
-      write_result(p, b, sh.cache, kk, tid, kWaveSize);
     }
+    __syncthreads();
+    write_result(p, b, sh.cache, kk, tid, nth);
     return;
   }
   auto cand = [&](uint32_t i) {

@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "dresd.h"
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include "dresd_internal.h"
@@ -287,14 +288,44 @@ hipEvent_t take_event(dresd_index *ix) {
   return e;
 }
 
+// Kernel launches of one search.  Profiling events are tied to kernels'
+// own dispatches (their begin and end timestamps) instead of being recorded
+// as packets of their own, which would leave the device idle between
+// kernels: `first` marks the begin of the next launch (and is cleared),
+// a launch's own start/stop pair its duration, `last` the end of the launch
+// that the caller flags as the search's last.
+struct Launcher {
+  hipStream_t st;
+  hipEvent_t first = nullptr;       // pending: begin of the next launch
+  hipEvent_t first_used = nullptr;  // the event that marked it
+  hipEvent_t last = nullptr;        // end of the flagged launch
+  hipError_t operator()(const void *f, dim3 grid, dim3 block, void **args, size_t lds,
+                        hipEvent_t start = nullptr, hipEvent_t stop = nullptr,
+                        bool is_last = false) {
+    if (first) {
+      if (!start) start = first;  // else the launch's own start marks both
+      first_used = start;
+      first = nullptr;
+    }
+    if (is_last && last) stop = stop ? stop : last;
+    if (!start && !stop) return hipLaunchKernel(f, grid, block, args, lds, st);
+    return hipExtLaunchKernel(f, grid, block, args, lds, st, start, stop, 0);
+  }
+};
+
+// Events of an index's profile, each once (a pair may share its start with
+// a scan's pair).
+std::vector<hipEvent_t> profile_events(const dresd_index *ix);
+
 dresd_status index_build(const void *embeddings, const int32_t *continuations, int64_t N,
                          int32_t d, int32_t L, int32_t dtype, const uint32_t *slot_row,
                          int64_t T, dresd_stream stream, dresd_index **out);
 
 // One search; next_tok (device [B]) selects the next-token-filtered form.
+// `outer` (optional) carries the timing events of an enclosing search.
 dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *next_tok, int32_t B,
                          int32_t k, int64_t *idx, float *score, int32_t *tokens,
-                         dresd_stream stream);
+                         dresd_stream stream, Launcher *outer = nullptr);
 
 }  // namespace
 
@@ -440,8 +471,7 @@ void dresd_index_destroy(dresd_index *ix) {
   if (ix->ftok) hipFree(ix->ftok);
   if (ix->ws) hipFree(ix->ws);
   for (auto e : ix->ev_free) hipEventDestroy(e);
-  for (auto e : ix->ev_scan) hipEventDestroy(e);
-  for (auto e : ix->ev_all) hipEventDestroy(e);
+  for (auto e : profile_events(ix)) hipEventDestroy(e);
   (void)hipSetDevice(cur);
   delete ix;
 }
@@ -491,11 +521,22 @@ dresd_status dresd_search_filtered(dresd_index *ix, const float *queries, const 
 }  // extern "C"
 
 namespace {
+std::vector<hipEvent_t> profile_events(const dresd_index *ix) {
+  std::vector<hipEvent_t> v(ix->ev_scan);
+  v.insert(v.end(), ix->ev_all.begin(), ix->ev_all.end());
+  std::sort(v.begin(), v.end());
+  v.erase(std::unique(v.begin(), v.end()), v.end());
+  return v;
+}
+
 dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *next_tok, int32_t B,
                          int32_t k, int64_t *idx, float *score, int32_t *tokens,
-                         dresd_stream stream) {
+                         dresd_stream stream, Launcher *outer) {
   dresd_status s = DRESD_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  Launcher own;
+  own.st = st;
+  Launcher &launch = outer ? *outer : own;
   Plan pl;
   s = make_plan(ix, B, k, pl, next_tok != nullptr);
   if (s != DRESD_OK) return s;
@@ -509,11 +550,12 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
   uint64_t *spill = reinterpret_cast<uint64_t *>(ix->ws + pl.off_spill);
 
   hipEvent_t e_all0 = nullptr, e_all1 = nullptr;
-  if (ix->prof) {
+  if (ix->prof && !outer) {
     e_all0 = take_event(ix);
     e_all1 = take_event(ix);
     if (!e_all0 || !e_all1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
-    DRESD_HIP(hipEventRecord(e_all0, st));
+    own.first = e_all0;
+    own.last = e_all1;
   }
   const int wpg = kScanThreads / kWaveSize;
   for (const Group &gr : pl.groups) {
@@ -551,8 +593,8 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       qp.ntile = pl.qt;
       void *qargs[] = {&qp};
       const int64_t chunks = (int64_t)pl.qt * ix->KB * 64;
-      DRESD_HIP(hipLaunchKernel(qop_kernel(ix->dtype), dim3((unsigned)ceil_div(chunks, 256)),
-                                dim3(256), qargs, 0, st));
+      DRESD_HIP(launch(qop_kernel(ix->dtype), dim3((unsigned)ceil_div(chunks, 256)), dim3(256),
+                       qargs, 0));
       sp.qop = qp.out;
     }
     MergeParams mp;
@@ -581,12 +623,10 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
         e0 = take_event(ix);
         e1 = take_event(ix);
         if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
-        DRESD_HIP(hipEventRecord(e0, st));
       }
-      DRESD_HIP(hipLaunchKernel((const void *)(main_pass ? pl.kmain : pl.ksample),
-                                dim3((unsigned)wgs), dim3(kScanThreads), sargs, pl.lds, st));
+      DRESD_HIP(launch((const void *)(main_pass ? pl.kmain : pl.ksample), dim3((unsigned)wgs),
+                       dim3(kScanThreads), sargs, pl.lds, e0, e1));
       if (main_pass && ix->prof) {
-        DRESD_HIP(hipEventRecord(e1, st));
         ix->ev_scan.push_back(e0);
         ix->ev_scan.push_back(e1);
       }
@@ -597,8 +637,8 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       mp.score = score + (size_t)gr.b0 * k;
       mp.tokens = tokens ? tokens + (size_t)gr.b0 * k * ix->L : nullptr;
       void *margs[] = {&mp};
-      DRESD_HIP(hipLaunchKernel(merge_kernel_ptr(), dim3((unsigned)gr.nb), dim3(kMergeThreads),
-                                margs, 0, st));
+      DRESD_HIP(launch(merge_kernel_ptr(), dim3((unsigned)gr.nb), dim3(kMergeThreads), margs, 0,
+                       nullptr, nullptr, main_pass && &gr == &pl.groups.back()));
       tau_in = mp.tau_out;
       ++level;
       return DRESD_OK;
@@ -610,9 +650,10 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     s = run_pass(1, true);
     if (s != DRESD_OK) return s;
   }
-  if (ix->prof) {
-    DRESD_HIP(hipEventRecord(e_all1, st));
-    ix->ev_all.push_back(e_all0);
+  if (e_all0) {
+    // the search's first kernel may have been the timed scan itself
+    if (own.first_used != e_all0) ix->ev_free.push_back(e_all0);
+    ix->ev_all.push_back(own.first_used);
     ix->ev_all.push_back(e_all1);
   }
   return DRESD_OK;
@@ -727,8 +768,7 @@ dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms, double *search
   if (scan_ms) *scan_ms = a;
   if (search_ms) *search_ms = b;
   if (searches) *searches = (int64_t)(ix->ev_all.size() / 2);
-  for (auto e : ix->ev_scan) ix->ev_free.push_back(e);
-  for (auto e : ix->ev_all) ix->ev_free.push_back(e);
+  for (auto e : profile_events(ix)) ix->ev_free.push_back(e);
   ix->ev_scan.clear();
   ix->ev_all.clear();
   return DRESD_OK;
@@ -767,8 +807,9 @@ void ivf_free(dresd_ivf *v) {
 // search) or probes32 (caller's) is [B][S] on the device.
 dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *probes64,
                           const int32_t *probes32, int32_t S, const int32_t *next_tok, int32_t B,
-                          int32_t k, int64_t *idx, float *score, int32_t *tokens, hipStream_t st) {
+                          int32_t k, int64_t *idx, float *score, int32_t *tokens, Launcher &launch) {
   dresd_index *ix = v->ix;
+  hipStream_t st = launch.st;
   const int terms = ix->dtype == kF32 ? 1 : 4;  // the query as three exact 16-bit parts
   const int nq = 16 / terms;
   const int C = next_pow2(std::max(k + 64, 128));
@@ -853,12 +894,10 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
     e0 = take_event(ix);
     e1 = take_event(ix);
     if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
-    DRESD_HIP(hipEventRecord(e0, st));
   }
-  DRESD_HIP(hipLaunchKernel((const void *)kern, dim3((unsigned)(B * wgq)), dim3(kScanThreads),
-                            sargs, lds, st));
+  DRESD_HIP(launch((const void *)kern, dim3((unsigned)(B * wgq)), dim3(kScanThreads), sargs, lds,
+                   e0, e1));
   if (ix->prof) {
-    DRESD_HIP(hipEventRecord(e1, st));
     ix->ev_scan.push_back(e0);
     ix->ev_scan.push_back(e1);
   }
@@ -881,8 +920,8 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   mp.L = ix->L;
   mp.final_mode = 1;
   void *margs[] = {&mp};
-  DRESD_HIP(hipLaunchKernel(merge_kernel_ptr(), dim3((unsigned)B), dim3(kMergeThreads), margs, 0,
-                            st));
+  DRESD_HIP(launch(merge_kernel_ptr(), dim3((unsigned)B), dim3(kMergeThreads), margs, 0, nullptr,
+                   nullptr, true));
   return DRESD_OK;
 }
 
@@ -1027,21 +1066,24 @@ dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *
   float *psc = reinterpret_cast<float *>(v->probe + (size_t)B * nprobe * 8);
   hipEvent_t a0 = nullptr, a1 = nullptr;
   dresd_index *ix = v->ix;
+  Launcher launch;
+  launch.st = st;
   if (ix->prof) {
     a0 = take_event(ix);
     a1 = take_event(ix);
     if (!a0 || !a1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
-    DRESD_HIP(hipEventRecord(a0, st));
+    launch.first = a0;  // the begin of the probe's first kernel
   }
   // 1. probe: the nprobe best centroids of each query (exact search)
-  s = search_impl(v->cix, queries, nullptr, B, nprobe, pid, psc, nullptr, stream);
+  s = search_impl(v->cix, queries, nullptr, B, nprobe, pid, psc, nullptr, stream, &launch);
   if (s != DRESD_OK) return s;
-  // 2. exact top-k over the probed partitions
-  s = parts_search(v, queries, pid, nullptr, nprobe, next_tok, B, k, idx, score, tokens, st);
+  // 2. exact top-k over the probed partitions (its merge ends the search)
+  launch.last = a1;
+  s = parts_search(v, queries, pid, nullptr, nprobe, next_tok, B, k, idx, score, tokens, launch);
   if (s != DRESD_OK) return s;
-  if (ix->prof) {
-    DRESD_HIP(hipEventRecord(a1, st));
-    ix->ev_all.push_back(a0);
+  if (a0) {
+    if (launch.first_used != a0) ix->ev_free.push_back(a0);
+    ix->ev_all.push_back(launch.first_used);
     ix->ev_all.push_back(a1);
   }
   return DRESD_OK;
@@ -1074,8 +1116,9 @@ dresd_status dresd_ivf_search_probes(dresd_ivf *v, const float *queries, const i
   if (B > 0 && (!queries || !probes || !idx || !score))
     return fail(DRESD_EINVAL, "NULL pointer argument");
   if (B == 0) return DRESD_OK;
-  return parts_search(v, queries, nullptr, probes, S, next_tok, B, k, idx, score, tokens,
-                      static_cast<hipStream_t>(stream));
+  Launcher launch;
+  launch.st = static_cast<hipStream_t>(stream);
+  return parts_search(v, queries, nullptr, probes, S, next_tok, B, k, idx, score, tokens, launch);
 }
 
 dresd_status dresd_kmeans_assign(const void *x, int64_t n, int32_t d, int32_t dtype,
