@@ -13,16 +13,19 @@
 
 namespace dresd {
 
-// Candidate counts up to this are sorted whole by one wave.
+// Candidate counts up to this are ordered whole (no selection first).
 constexpr int kSmallMerge = 256;
+// Winner counts up to this are ordered by rank, larger ones by a bitonic
+// network over the workgroup.
+constexpr int kRankSortMax = 512;
 // Each thread owns this many lists (their offsets share the histogram).
 constexpr int kListsPerThread = kMergeLists / kMergeThreads;
 
 struct MergeShared {
   uint32_t hist[4096];  // radix histogram; list offsets during the gather
   uint32_t part[kMergeThreads / kWaveSize];
-  uint64_t cache[kMergeCap];
-  uint64_t win[DRESD_K_MAX_INTERNAL];
+  alignas(16) uint64_t cache[kMergeCap];
+  alignas(16) uint64_t win[DRESD_K_MAX_INTERNAL];
   uint64_t sel_prefix, sel_mask, bound, v_and, v_or;
   uint32_t sel_krem, sel_done, win_cnt, ncand, total, any_known;
   int sel_top;
@@ -42,6 +45,28 @@ __device__ inline uint64_t wave_max(uint64_t v) {
     v = o > v ? o : v;
   }
   return v;
+}
+
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+
+// Descending order of n distinct keys src[0..n) (every key names its own
+// row): key i goes to dst[number of keys greater than it] when that is below
+// `keep`.  Threads read all keys as LDS broadcasts, so there is no barrier
+// inside; src and dst are 16-byte aligned LDS arrays, src is not written.
+__device__ inline void rank_sort_desc(const uint64_t *src, uint32_t n, uint64_t *dst,
+                                      uint32_t keep, int tid, int nth) {
+  const uint32_t n2 = n & ~1u;
+  for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nth) {
+    const uint64_t x = src[i];
+    uint32_t r = 0;
+#pragma unroll 4
+    for (uint32_t j = 0; j < n2; j += 2) {
+      const u64x2 v = *reinterpret_cast<const u64x2 *>(src + j);
+      r += (uint32_t)(v.x > x) + (uint32_t)(v.y > x);
+    }
+    if (n & 1u) r += (uint32_t)(src[n - 1] > x);
+    if (r < keep) dst[r] = x;
+  }
 }
 
 // Largest value v such that at least kk of the M values src(i) are >= v
@@ -187,8 +212,8 @@ __device__ inline void write_result(const MergeParams &p, int b, const uint64_t 
 //    each, and the answer is among the listed keys.
 // 2. Candidates: listed keys at or above the bound; lists whose best key is
 //    below it are not opened.  All kept lists' keys are loaded at once.
-// 3. The k best candidates: one wave sorts them when few, else a radix
-//    select finds the k-th and the keys at or above it are sorted.
+// 3. The k best candidates: ordered by rank when few, else a radix select
+//    finds the k-th and the keys at or above it are ordered.
 __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
   __shared__ MergeShared sh;
   const int b = blockIdx.x;
@@ -301,15 +326,9 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
 
   // 3. the k best
   if (M <= (uint32_t)kSmallMerge) {
-    if (tid < kWaveSize) {
-      int n = 2;
-      while (n < (int)M) n <<= 1;
-      for (int i = (int)M + tid; i < n; i += kWaveSize) sh.cache[i] = 0ull;
-      wave_sync_lds();
-      wave_bitonic_desc(sh.cache, n, tid);
-    }
+    rank_sort_desc(sh.cache, M, sh.win, kk, tid, nth);
     __syncthreads();
-    write_result(p, b, sh.cache, kk, tid, nth);
+    write_result(p, b, sh.win, kk, tid, nth);
     return;
   }
   auto cand = [&](uint32_t i) {
@@ -324,11 +343,17 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
     }
   }
   __syncthreads();
+  if (kk <= (uint32_t)kRankSortMax) {  // the winners, ordered into the free cache
+    rank_sort_desc(sh.win, kk, sh.cache, kk, tid, nth);
+    __syncthreads();
+    write_result(p, b, sh.cache, kk, tid, nth);
+    return;
+  }
   int n = 1;
   while (n < (int)kk) n <<= 1;
   for (int i = (int)kk + tid; i < n; i += nth) sh.win[i] = 0ull;
   __syncthreads();
-  if (n >= 2) block_bitonic_desc(sh.win, n);
+  block_bitonic_desc(sh.win, n);
   write_result(p, b, sh.win, kk, tid, nth);
 }
 
