@@ -85,6 +85,47 @@ __device__ inline void wave_bitonic_desc(uint64_t *s, int n, int lane) {
   }
 }
 
+// Sets of keys up to this size are ordered by wave_rank_top.
+constexpr int kWaveRankMax = 256;
+
+// The keys of rank 0 and keep - 1 of an ordering (0 when absent).
+struct RankEnds {
+  uint64_t first, last;
+};
+
+// Top `keep` of n distinct keys src[0..n) (LDS; every key names its own row)
+// in descending order, by one wave: the key of rank r < keep goes to dst[r]
+// (LDS or global memory, not src).  Each lane counts, for each of its keys,
+// the greater keys over broadcast LDS reads.  Every lane returns the keys of
+// rank 0 and keep - 1.
+__device__ inline RankEnds wave_rank_top(const uint64_t *src, int n, uint64_t *dst, int keep,
+                                         int lane) {
+  const int n2 = n & ~1;
+  uint64_t f = 0ull, l = 0ull;
+  bool hf = false, hl = false;
+  for (int i = lane; i < n; i += kWaveSize) {
+    const uint64_t x = src[i];
+    int r = 0;
+#pragma unroll 4
+    for (int j = 0; j < n2; j += 2) r += (int)(src[j] > x) + (int)(src[j + 1] > x);
+    if (n & 1) r += (int)(src[n - 1] > x);
+    if (r < keep) dst[r] = x;
+    if (r == 0) {
+      f = x;
+      hf = true;
+    }
+    if (r == keep - 1) {
+      l = x;
+      hl = true;
+    }
+  }
+  const uint64_t mf = __ballot(hf), ml = __ballot(hl);
+  RankEnds e;
+  e.first = mf ? __shfl(f, __ffsll((long long)mf) - 1, kWaveSize) : 0ull;
+  e.last = ml ? __shfl(l, __ffsll((long long)ml) - 1, kWaveSize) : 0ull;
+  return e;
+}
+
 // Same, by a whole workgroup.
 __device__ inline void block_bitonic_desc(uint64_t *s, int n) {
   for (int size = 2; size <= n; size <<= 1) {

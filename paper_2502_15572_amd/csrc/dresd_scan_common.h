@@ -115,15 +115,23 @@ __device__ inline void sink_publish(const CandSink &s, int i, uint64_t *list, bo
   uint32_t flag = 0u;
   if (cnt > s.k || (sort_all && cnt > 0)) {
     __threadfence_block();
-    int n = 2;
-    while (n < cnt) n <<= 1;
-    for (int e = s.lane; e < n; e += kWaveSize) s.scr[e] = (e < cnt) ? list[e] : 0ull;
-    wave_sync_lds();
-    wave_bitonic_desc(s.scr, n, s.lane);
     const int keep = cnt < s.k ? cnt : s.k;
-    for (int e = s.lane; e < keep; e += kWaveSize) list[e] = s.scr[e];
-    first = s.scr[0];
-    kth = (keep == s.k) ? s.scr[s.k - 1] : 0ull;
+    if (cnt <= kWaveRankMax) {
+      for (int e = s.lane; e < cnt; e += kWaveSize) s.scr[e] = list[e];
+      wave_sync_lds();
+      const RankEnds r = wave_rank_top(s.scr, cnt, list, keep, s.lane);
+      first = r.first;
+      kth = (keep == s.k) ? r.last : 0ull;
+    } else {
+      int n = 2;
+      while (n < cnt) n <<= 1;
+      for (int e = s.lane; e < n; e += kWaveSize) s.scr[e] = (e < cnt) ? list[e] : 0ull;
+      wave_sync_lds();
+      wave_bitonic_desc(s.scr, n, s.lane);
+      for (int e = s.lane; e < keep; e += kWaveSize) list[e] = s.scr[e];
+      first = s.scr[0];
+      kth = (keep == s.k) ? s.scr[s.k - 1] : 0ull;
+    }
     flag = kSortedFlag;
     s.st_cnt[i] = (uint32_t)keep;
     wave_sync_lds();

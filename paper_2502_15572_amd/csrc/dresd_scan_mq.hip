@@ -487,18 +487,27 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
       uint64_t *list = list_of(qi);
       const int nq = __builtin_amdgcn_readlane(n, qi);
       __threadfence_block();
-      int np2 = 2;
-      while (np2 < nq) np2 <<= 1;
-      for (int e = lane; e < np2; e += kWaveSize) scr[e] = (e < nq) ? list[e] : 0ull;
-      wave_sync_lds();
-      wave_bitonic_desc(scr, np2, lane);
       const int keep = nq < k ? nq : k;
-      for (int e = lane; e < keep; e += kWaveSize) list[e] = scr[e];
+      RankEnds ends;
+      if (nq <= kWaveRankMax) {
+        for (int e = lane; e < nq; e += kWaveSize) scr[e] = list[e];
+        wave_sync_lds();
+        ends = wave_rank_top(scr, nq, list, keep, lane);
+      } else {
+        int np2 = 2;
+        while (np2 < nq) np2 <<= 1;
+        for (int e = lane; e < np2; e += kWaveSize) scr[e] = (e < nq) ? list[e] : 0ull;
+        wave_sync_lds();
+        wave_bitonic_desc(scr, np2, lane);
+        for (int e = lane; e < keep; e += kWaveSize) list[e] = scr[e];
+        ends.first = scr[0];
+        ends.last = scr[keep - 1];
+      }
       if (lane == 0) {
         const size_t o = (size_t)(q0 + qi) * G + wg;
         p.lcnt[o] = (uint32_t)keep | kSortedFlag;
-        p.lfirst[o] = scr[0];
-        p.lkth[o] = (keep == k) ? scr[k - 1] : 0ull;
+        p.lfirst[o] = ends.first;
+        p.lkth[o] = (keep == k) ? ends.last : 0ull;
       }
       wave_sync_lds();
     }
