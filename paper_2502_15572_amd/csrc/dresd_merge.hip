@@ -22,13 +22,12 @@ constexpr int kRankSortMax = 512;
 constexpr int kListsPerThread = kMergeLists / kMergeThreads;
 
 struct MergeShared {
-  uint32_t hist[4096];  // radix histogram; list offsets during the gather
+  uint32_t hist[kMergeLists];  // radix histogram (256 bins); list offsets during the gather
   uint32_t part[kMergeThreads / kWaveSize];
   alignas(16) uint64_t cache[kMergeCap];
   alignas(16) uint64_t win[DRESD_K_MAX_INTERNAL];
   uint64_t sel_prefix, sel_mask, bound, v_and, v_or;
   uint32_t sel_krem, sel_done, win_cnt, ncand, total, any_known;
-  int sel_top;
 };
 
 __device__ inline uint64_t wave_and(uint64_t v) {
@@ -71,18 +70,22 @@ __device__ inline void rank_sort_desc(const uint64_t *src, uint32_t n, uint64_t 
 
 // Largest value v such that at least kk of the M values src(i) are >= v
 // (1 <= kk <= M; the kk-th largest value, or a lower boundary of the digit
-// bin holding exactly the kk largest values).  Radix selection 12 bits at a
-// time from the highest bit in which the values differ.  Called by the whole
-// workgroup.
+// bin holding exactly the kk largest values).  Radix selection 8 bits at a
+// time from the highest bit in which the values differ: every thread adds
+// its values to the 256-bin histogram, then one wave finds the bin holding
+// the kk-th largest (and clears the histogram), two barriers per digit.
+// Called by the whole workgroup.
 template <class Src>
 __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk) {
-  constexpr int BPT = 4096 / kMergeThreads;  // histogram bins per thread
+  constexpr int kDigit = 8, kBins = 1 << kDigit, kBinsPerLane = kBins / kWaveSize;
   const int tid = threadIdx.x, nth = blockDim.x;
   const int lane = tid & (kWaveSize - 1), wid = tid / kWaveSize;
   if (tid == 0) {
     sh.v_and = ~0ull;
     sh.v_or = 0ull;
+    sh.sel_done = 0u;
   }
+  if (tid < kBins) sh.hist[tid] = 0;
   __syncthreads();
   uint64_t va = ~0ull, vo = 0ull;
   for (uint32_t i = tid; i < M; i += nth) {
@@ -99,67 +102,62 @@ __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk)
   __syncthreads();
   const uint64_t diff = sh.v_and ^ sh.v_or;
   if (diff == 0) return sh.v_or;  // one distinct value
-  const int top0 = 63 - __clzll((long long)diff);
-  const uint64_t above = (top0 == 63) ? 0ull : ~((2ull << top0) - 1ull);
-  __syncthreads();
-  if (tid == 0) {
-    sh.sel_prefix = sh.v_and & above;
-    sh.sel_mask = above;
-    sh.sel_krem = kk;
-    sh.sel_done = 0;
-    sh.sel_top = top0;
-  }
-  __syncthreads();
+  int top = 63 - __clzll((long long)diff);
+  uint64_t pm = (top == 63) ? 0ull : ~((2ull << top) - 1ull);  // bits fixed so far
+  uint64_t pre = sh.v_and & pm;                                 // their values
+  uint32_t krem = kk;  // rank of the answer among the values matching pre
+  // Every thread follows the same (pre, pm, top, krem), published by wave 0.
   for (;;) {
-    const int top = sh.sel_top;
-    if (sh.sel_done || top < 0) break;
-    const int w = top + 1 < 12 ? top + 1 : 12;
+    const int w = top + 1 < kDigit ? top + 1 : kDigit;
     const int s = top + 1 - w;
     const uint32_t wmask = (1u << w) - 1u;
-    for (int i = tid; i < 4096; i += nth) sh.hist[i] = 0;
-    __syncthreads();
-    const uint64_t pre = sh.sel_prefix, pm = sh.sel_mask;
     for (uint32_t i = tid; i < M; i += nth) {
       const uint64_t key = src(i);
       if ((key & pm) == pre) atomicAdd(&sh.hist[(uint32_t)(key >> s) & wmask], 1u);
     }
     __syncthreads();
-    // Suffix sums: thread t owns bins [BPT t, BPT t + BPT); `cnt_above` = count in
-    // the bins of all higher threads (lanes scan within the wave, then the
-    // waves' totals are summed from LDS).
-    uint32_t mine = 0;
-    for (int jb = 0; jb < BPT; ++jb) mine += sh.hist[tid * BPT + jb];
-    uint32_t incl = mine;
-    for (int off = 1; off < kWaveSize; off <<= 1) {
-      const uint32_t v = __shfl_down(incl, off, kWaveSize);
-      if (lane + off < kWaveSize) incl += v;
-    }
-    if (lane == 0) sh.part[wid] = incl;
-    __syncthreads();
-    uint32_t later = 0;
-    for (int q = wid + 1; q < nth / kWaveSize; ++q) later += sh.part[q];
-    const uint32_t krem = sh.sel_krem;
-    const uint32_t cnt_above = later + incl - mine;
-    __syncthreads();
-    if (cnt_above < krem && krem <= cnt_above + mine) {
-      uint32_t cum = cnt_above;
-      for (int jb = BPT - 1; jb >= 0; --jb) {
-        const uint32_t h = sh.hist[tid * BPT + jb];
-        if (cum + h >= krem) {
-          const uint32_t dg = (uint32_t)(tid * BPT + jb);
-          sh.sel_prefix = pre | ((uint64_t)dg << s);
-          sh.sel_mask = pm | ((uint64_t)wmask << s);
-          sh.sel_krem = krem - cum;
-          sh.sel_top = s - 1;
-          if (h == krem - cum) sh.sel_done = 1u;  // the whole bin is in
-          break;
-        }
-        cum += h;
+    if (wid == 0) {
+      // lane l owns bins [kBinsPerLane l, kBinsPerLane (l + 1)); count the
+      // values in the bins of all higher lanes
+      uint32_t h[kBinsPerLane], mine = 0;
+#pragma unroll
+      for (int j = 0; j < kBinsPerLane; ++j) {
+        h[j] = sh.hist[lane * kBinsPerLane + j];
+        mine += h[j];
       }
+      uint32_t incl = mine;
+      for (int off = 1; off < kWaveSize; off <<= 1) {
+        const uint32_t v = __shfl_down(incl, off, kWaveSize);
+        if (lane + off < kWaveSize) incl += v;
+      }
+      const uint32_t cnt_above = incl - mine;
+      if (cnt_above < krem && krem <= cnt_above + mine) {
+        uint32_t cum = cnt_above;
+        for (int j = kBinsPerLane - 1; j >= 0; --j) {
+          if (cum + h[j] >= krem) {
+            const uint32_t dg = (uint32_t)(lane * kBinsPerLane + j);
+            sh.sel_prefix = pre | ((uint64_t)dg << s);
+            sh.sel_mask = pm | ((uint64_t)wmask << s);
+            sh.sel_krem = krem - cum;
+            sh.sel_done = (h[j] == krem - cum) ? 1u : 0u;  // the whole bin is in
+            break;
+          }
+          cum += h[j];
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kBinsPerLane; ++j) sh.hist[lane * kBinsPerLane + j] = 0;
     }
     __syncthreads();
+    pre = sh.sel_prefix;
+    pm = sh.sel_mask;
+    krem = sh.sel_krem;
+    top = s - 1;
+    if (sh.sel_done || top < 0) break;
+    // wave 0 rewrites the state only after the next histogram's barrier,
+    // which every thread reaches after reading it
   }
-  return sh.sel_prefix;
+  return pre;
 }
 
 // Output of one query from its sorted winners win[0..kk): the k-th best key
