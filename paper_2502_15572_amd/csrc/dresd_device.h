@@ -93,37 +93,65 @@ struct RankEnds {
   uint64_t first, last;
 };
 
-// Top `keep` of n distinct keys src[0..n) (LDS; every key names its own row)
-// in descending order, by one wave: the key of rank r < keep goes to dst[r]
-// (LDS or global memory, not src).  Each lane counts, for each of its keys,
-// the greater keys over broadcast LDS reads.  Every lane returns the keys of
-// rank 0 and keep - 1.
+// Ranks of the n distinct keys src[0..n) (LDS), E per lane: key
+// lane + 64 e is x[e], its rank (number of greater keys) r[e].  Every key
+// read serves all E of the lane's keys.
+template <int E>
+__device__ inline void wave_ranks(const uint64_t *src, int n, int lane, uint64_t (&x)[4],
+                                  int (&r)[4]) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = lane + e * kWaveSize;
+    x[e] = i < n ? src[i] : ~0ull;  // ~0: counts nothing and is never stored
+    r[e] = 0;
+  }
+  const int n2 = n & ~1;
+#pragma unroll 2
+  for (int j = 0; j < n2; j += 2) {
+    const uint64_t a = src[j], b = src[j + 1];
+#pragma unroll
+    for (int e = 0; e < E; ++e) r[e] += (int)(a > x[e]) + (int)(b > x[e]);
+  }
+  if (n & 1) {
+    const uint64_t a = src[n - 1];
+#pragma unroll
+    for (int e = 0; e < E; ++e) r[e] += (int)(a > x[e]);
+  }
+}
+
+// Top `keep` of n <= kWaveRankMax distinct keys src[0..n) (LDS; every key
+// names its own row) in descending order, by one wave: the key of rank
+// r < keep goes to dst[r] (LDS or global memory, not src).  Every lane
+// returns the keys of rank 0 and keep - 1.
 __device__ inline RankEnds wave_rank_top(const uint64_t *src, int n, uint64_t *dst, int keep,
                                          int lane) {
-  const int n2 = n & ~1;
+  uint64_t x[4] = {0ull, 0ull, 0ull, 0ull};
+  int r[4] = {0, 0, 0, 0};
+  const int E = (n + kWaveSize - 1) / kWaveSize;
+  if (E <= 1) wave_ranks<1>(src, n, lane, x, r);
+  else if (E == 2) wave_ranks<2>(src, n, lane, x, r);
+  else if (E == 3) wave_ranks<3>(src, n, lane, x, r);
+  else wave_ranks<4>(src, n, lane, x, r);
   uint64_t f = 0ull, l = 0ull;
   bool hf = false, hl = false;
-  for (int i = lane; i < n; i += kWaveSize) {
-    const uint64_t x = src[i];
-    int r = 0;
-#pragma unroll 4
-    for (int j = 0; j < n2; j += 2) r += (int)(src[j] > x) + (int)(src[j + 1] > x);
-    if (n & 1) r += (int)(src[n - 1] > x);
-    if (r < keep) dst[r] = x;
-    if (r == 0) {
-      f = x;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (e >= E || lane + e * kWaveSize >= n) continue;
+    if (r[e] < keep) dst[r[e]] = x[e];
+    if (r[e] == 0) {
+      f = x[e];
       hf = true;
     }
-    if (r == keep - 1) {
-      l = x;
+    if (r[e] == keep - 1) {
+      l = x[e];
       hl = true;
     }
   }
   const uint64_t mf = __ballot(hf), ml = __ballot(hl);
-  RankEnds e;
-  e.first = mf ? __shfl(f, __ffsll((long long)mf) - 1, kWaveSize) : 0ull;
-  e.last = ml ? __shfl(l, __ffsll((long long)ml) - 1, kWaveSize) : 0ull;
-  return e;
+  RankEnds ends;
+  ends.first = mf ? __shfl(f, __ffsll((long long)mf) - 1, kWaveSize) : 0ull;
+  ends.last = ml ? __shfl(l, __ffsll((long long)ml) - 1, kWaveSize) : 0ull;
+  return ends;
 }
 
 // Same, by a whole workgroup.

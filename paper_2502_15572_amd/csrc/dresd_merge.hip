@@ -50,21 +50,29 @@ typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
 
 // Descending order of n distinct keys src[0..n) (every key names its own
 // row): key i goes to dst[number of keys greater than it] when that is below
-// `keep`.  Threads read all keys as LDS broadcasts, so there is no barrier
-// inside; src and dst are 16-byte aligned LDS arrays, src is not written.
+// `keep`.  T adjacent lanes (a power of two, as many as the workgroup allows
+// up to a wave) share a key's count, so every wave takes part; keys are read
+// as LDS broadcasts and there is no barrier inside.  src and dst are 16-byte
+// aligned LDS arrays; src is not written.
 __device__ inline void rank_sort_desc(const uint64_t *src, uint32_t n, uint64_t *dst,
                                       uint32_t keep, int tid, int nth) {
-  const uint32_t n2 = n & ~1u;
-  for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nth) {
-    const uint64_t x = src[i];
+  int T = 1;
+  while (T < kWaveSize && n * (uint32_t)(2 * T) <= (uint32_t)nth) T <<= 1;
+  const int sub = tid & (T - 1);
+  const uint32_t per = (uint32_t)(nth / T), n2 = n & ~1u;
+  for (uint32_t i0 = 0; i0 < n; i0 += per) {
+    const uint32_t i = i0 + (uint32_t)(tid / T);
+    const bool valid = i < n;
+    const uint64_t x = valid ? src[i] : ~0ull;
     uint32_t r = 0;
 #pragma unroll 4
-    for (uint32_t j = 0; j < n2; j += 2) {
+    for (uint32_t j = 2u * (uint32_t)sub; j < n2; j += 2u * (uint32_t)T) {
       const u64x2 v = *reinterpret_cast<const u64x2 *>(src + j);
       r += (uint32_t)(v.x > x) + (uint32_t)(v.y > x);
     }
-    if (n & 1u) r += (uint32_t)(src[n - 1] > x);
-    if (r < keep) dst[r] = x;
+    if ((n & 1u) && sub == 0) r += (uint32_t)(src[n - 1] > x);
+    for (int o = 1; o < T; o <<= 1) r += __shfl_xor(r, o, kWaveSize);
+    if (valid && sub == 0 && r < keep) dst[r] = x;
   }
 }
 
