@@ -111,6 +111,10 @@ EDGE = [
     ("f16", 4096, 128, 64, 128),
     ("f32", 2000, 256, 4, 1),
     ("f16", 70000, 128, 1, 1000),    # large k
+    # lists of 129-256 keys ordered by rank when published (up to four keys
+    # per lane), and 257-512 winners ordered by rank in the merge
+    ("f16", 150000, 128, 2, 200),
+    ("f16", 60000, 128, 3, 400),
     ("bf16", 9000, 256, 32, 16),
     # many queries per single-tile launch: up to 16 passing rows of a tile
     # for one query must fit the query's LDS stage
@@ -155,6 +159,7 @@ MQ_EDGE = [
     ("f16", 100, 128, 40, 100),       # k == N: every row returned, in order
     ("bf16", 999, 64, 8, 999),        # k == N, two padded query tiles
     ("f16", 5000, 128, 600, 20),      # three groups of 256 queries
+    ("f16", 90001, 128, 24, 300),     # published lists past 256 keys, 300 winners
 ]
 
 
