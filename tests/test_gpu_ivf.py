@@ -14,6 +14,8 @@ exact search), fewer probed rows than k, empty partitions, k = 1024, one
 query and many, d spanning several blocks with a ragged tail."""
 import sys
 
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -117,6 +119,45 @@ def test_ivf_search_oracle_probes(gpu_lib, name, n, P, B, k, S):
     sel = np.nonzero(unique)[0]
     gs = tuple(t[torch.from_numpy(sel)] for t in g)
     check(gs, kb, dt, qn[sel], cont.numpy(), a, probes[sel], k, P)
+    ix.close()
+
+
+# Internal probing (the exact search over the centroid index) at more shapes:
+# centroid sets past one workgroup's 512 rows with a ragged end, 1, 64 and 65
+# probes, and dims that are not a multiple of 4.
+PROBE_CASES = [
+    # workload, rows, partitions, batch, k, probes per query, dims (0: the workload's)
+    ("zipf33m_d128_f16", 20000 + 11, 1500, 6, 50, 64, 0),
+    ("zipf33m_d128_f16", 20000 + 11, 1500, 6, 50, 1, 0),
+    ("zipf33m_d128_f16", 20000 + 11, 1500, 6, 50, 65, 0),
+    ("batch10m_d256_f16", 9000 + 1, 700, 5, 20, 17, 50),
+]
+
+
+@pytest.mark.parametrize("name,n,P,B,k,S,d", PROBE_CASES,
+                         ids=["P%d-S%d-d%d" % (c[2], c[5], c[6]) for c in PROBE_CASES])
+def test_ivf_probe_paths(gpu_lib, name, n, P, B, k, S, d):
+    from paper_2502_15572_amd import PartitionedIndex
+    say("ivf probe path", name, n, P, B, k, S, d)
+    w = WORKLOADS[name].scaled(n)
+    if d:
+        w = dataclasses.replace(w, d=d)
+    g = generate(w, "cpu", seed=3)
+    keys, cont, q = g["keys"], g["cont"], g["queries"]
+    kb, dt = to_numpy_bits(keys)
+    c, a = partitions(kb, dt, P, 4, iters=1)
+    qn = q[:B].numpy()
+    p_idx, p_sc, _, _ = oracle.topk(c, "f32", qn, S + 1)
+    unique = p_sc[:, S - 1] - p_sc[:, S] >= 1e-5
+    assert unique.mean() >= 0.5
+    ix = PartitionedIndex(keys.to(DEV), cont.to(DEV), torch.from_numpy(c).to(DEV),
+                          torch.from_numpy(a).to(DEV))
+    for rep in range(2):  # the second search reuses the index's probe buffers
+        res = ix.search(q[:B].to(DEV), k, S)
+        torch.cuda.synchronize()
+        sel = np.nonzero(unique)[0]
+        gs = tuple(t[torch.from_numpy(sel)] for t in res)
+        check(gs, kb, dt, qn[sel], cont.numpy(), a, p_idx[sel, :S].astype(np.int32), k, P)
     ix.close()
 
 
