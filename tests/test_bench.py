@@ -1,0 +1,59 @@
+"""Host-side logic of bench.py: the one-GPU contract and the rule that a
+committed HBM-counter summary is reported only for the kernel source it was
+taken on (the scan file plus every header it includes)."""
+import os
+import shutil
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused_before_any_device_work():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def _copy_sources(tmp_path):
+    dst = tmp_path / "csrc"
+    shutil.copytree(bench.CSRC, dst)
+    return dst
+
+
+def test_kernel_hash_follows_the_included_headers(tmp_path, monkeypatch):
+    csrc = _copy_sources(tmp_path)
+    monkeypatch.setattr(bench, "CSRC", str(csrc))
+    h_tile, h_mq = bench.kernel_hash("dresd_kernels.hip"), bench.kernel_hash("dresd_scan_mq.hip")
+    assert h_tile == bench.kernel_hash("dresd_kernels.hip") and h_tile != h_mq
+    # a header both scans include changes both hashes
+    with open(csrc / "dresd_device.h", "a") as f:
+        f.write("\n// edit\n")
+    assert bench.kernel_hash("dresd_kernels.hip") != h_tile
+    assert bench.kernel_hash("dresd_scan_mq.hip") != h_mq
+    h_tile2, h_mq2 = bench.kernel_hash("dresd_kernels.hip"), bench.kernel_hash("dresd_scan_mq.hip")
+    # a source neither scan includes changes neither
+    with open(csrc / "dresd_transform.hip", "a") as f:
+        f.write("\n// edit\n")
+    assert bench.kernel_hash("dresd_kernels.hip") == h_tile2
+    assert bench.kernel_hash("dresd_scan_mq.hip") == h_mq2
+
+
+def test_traffic_is_read_only_for_the_current_source(tmp_path, monkeypatch):
+    csrc = _copy_sources(tmp_path)
+    monkeypatch.setattr(bench, "CSRC", str(csrc))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    (tmp_path / "profiles").mkdir()
+    path = tmp_path / "profiles" / "traffic_scan_w_B3.md"
+    assert bench.read_traffic("w", 3, "single_tile") is None  # no summary
+    h = bench.kernel_hash("dresd_kernels.hip")
+    path.write_text("kernel_source_sha256_16: %s\nhbm_bytes_per_launch: 1.25e+09\n" % h)
+    assert bench.read_traffic("w", 3, "single_tile") == 1.25e9
+    assert bench.read_traffic("w", 3, "shared_key") is None  # another kernel's source
+    with open(csrc / "dresd_kernels.hip", "a") as f:
+        f.write("\n// edit\n")
+    assert bench.read_traffic("w", 3, "single_tile") is None  # source changed since
