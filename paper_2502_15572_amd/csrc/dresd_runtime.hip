@@ -60,8 +60,6 @@ int next_pow2(int x) {
   return n;
 }
 
-int elem_bytes(int dtype) { return dtype == kF32 ? 4 : 2; }
-
 // Dimensions per 1 KiB block: 16 lanes' rows x 4 lane groups x (8 | 4) dims.
 int block_dims(int dtype) { return dtype == kF32 ? 16 : 32; }
 
@@ -257,7 +255,7 @@ dresd_status ensure_workspace(dresd_index *ix, size_t bytes) {
   if (ix->ws_bytes >= bytes) return DRESD_OK;
   if (ix->ws) {
     DRESD_HIP(hipDeviceSynchronize());
-    hipFree(ix->ws);
+    (void)hipFree(ix->ws);
     ix->ws = nullptr;
     ix->ws_bytes = 0;
   }
@@ -269,7 +267,7 @@ dresd_status ensure_workspace(dresd_index *ix, size_t bytes) {
   // Every region is written before it is read in each search; clearing it
   // once keeps a fresh workspace deterministic to inspect.
   if (hipMemset(p, 0, bytes) != hipSuccess) {
-    hipFree(p);
+    (void)hipFree(p);
     return fail(DRESD_EDEVICE, "workspace clear failed");
   }
   ix->ws = static_cast<unsigned char *>(p);
@@ -358,9 +356,9 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
   dresd_index *ix = new (std::nothrow) dresd_index();
   if (!ix) return fail(DRESD_ENOMEM, "host allocation failed");
   auto cleanup = [&](dresd_status s) {
-    if (ix->data) hipFree(ix->data);
-    if (ix->cont) hipFree(ix->cont);
-    if (ix->ftok) hipFree(ix->ftok);
+    if (ix->data) (void)hipFree(ix->data);
+    if (ix->cont) (void)hipFree(ix->cont);
+    if (ix->ftok) (void)hipFree(ix->ftok);
     delete ix;
     return s;
   };
@@ -466,12 +464,12 @@ void dresd_index_destroy(dresd_index *ix) {
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(ix->device);
   (void)hipDeviceSynchronize();
-  if (ix->data) hipFree(ix->data);
-  if (ix->cont) hipFree(ix->cont);
-  if (ix->ftok) hipFree(ix->ftok);
-  if (ix->ws) hipFree(ix->ws);
-  for (auto e : ix->ev_free) hipEventDestroy(e);
-  for (auto e : profile_events(ix)) hipEventDestroy(e);
+  if (ix->data) (void)hipFree(ix->data);
+  if (ix->cont) (void)hipFree(ix->cont);
+  if (ix->ftok) (void)hipFree(ix->ftok);
+  if (ix->ws) (void)hipFree(ix->ws);
+  for (auto e : ix->ev_free) (void)hipEventDestroy(e);
+  for (auto e : profile_events(ix)) (void)hipEventDestroy(e);
   (void)hipSetDevice(cur);
   delete ix;
 }
@@ -796,10 +794,10 @@ void ivf_free(dresd_ivf *v) {
   if (!v) return;
   if (v->ix) dresd_index_destroy(v->ix);
   if (v->cix) dresd_index_destroy(v->cix);
-  if (v->slot_row) hipFree(v->slot_row);
-  if (v->ftok_slot) hipFree(v->ftok_slot);
-  if (v->part_tile) hipFree(v->part_tile);
-  if (v->probe) hipFree(v->probe);
+  if (v->slot_row) (void)hipFree(v->slot_row);
+  if (v->ftok_slot) (void)hipFree(v->ftok_slot);
+  if (v->part_tile) (void)hipFree(v->part_tile);
+  if (v->probe) (void)hipFree(v->probe);
   delete v;
 }
 
@@ -1003,11 +1001,11 @@ dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuatio
     return bail(fail(DRESD_ENOMEM, "allocation failed"));
   }
   if (hipMemcpy(ids_dev, ids.data(), (size_t)P * 4, hipMemcpyHostToDevice) != hipSuccess) {
-    hipFree(ids_dev);
+    (void)hipFree(ids_dev);
     return bail(fail(DRESD_EDEVICE, "partition id upload failed"));
   }
   s = index_build(centroids, ids_dev, P, d, 1, DRESD_F32, nullptr, 0, stream, &v->cix);
-  hipFree(ids_dev);
+  (void)hipFree(ids_dev);
   if (s != DRESD_OK) return bail(s);
   *out = v;
   return DRESD_OK;
@@ -1052,7 +1050,7 @@ dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *
   if (v->probe_bytes < need) {
     if (v->probe) {
       DRESD_HIP(hipDeviceSynchronize());
-      hipFree(v->probe);
+      (void)hipFree(v->probe);
       v->probe = nullptr;
       v->probe_bytes = 0;
     }
@@ -1165,7 +1163,7 @@ dresd_status dresd_kmeans_update(const void *x, int64_t n, int32_t d, int32_t dt
   if (bufs[dev].second < need) {
     if (bufs[dev].first) {
       DRESD_HIP(hipDeviceSynchronize());
-      hipFree(bufs[dev].first);
+      (void)hipFree(bufs[dev].first);
       bufs[dev] = {nullptr, 0};
     }
     void *b = nullptr;
