@@ -44,22 +44,29 @@ __device__ inline void sink_init(const CandSink &s, int nq, int B_local, const u
 
 // Move query i's stage into its HBM list (cutting the list to its k best
 // when it would overflow).  Wave-uniform; issues vector memory operations.
-__device__ inline void sink_spill(const CandSink &s, int i, uint64_t *list) {
+// `early`: inside the stream, where a query without a threshold yet (-inf)
+// is also cut once list + stage hold 2k keys: the threshold (the median of
+// those or better) then rises after a few tiles instead of after C - cl
+// insertions, and the sort covers only the keys present.
+__device__ inline void sink_spill(const CandSink &s, int i, uint64_t *list, bool early = false) {
   const int ns = (int)s.stg_cnt[i];
   int cnt = (int)s.st_cnt[i];
   const uint64_t *stg = s.stg + (size_t)i * s.cl;
   // The HBM list holds at most C - cl keys, so list + stage fit the C-entry
   // scratch; C >= k + 2 cl leaves room for a full stage after a cut.
-  if (cnt + ns > s.C - s.cl) {
+  const int m = cnt + ns;
+  if (m > s.C - s.cl || (early && m >= 2 * s.k && s.st_thr[i] == -__builtin_inff())) {
     __threadfence_block();  // this wave's list stores are visible to its loads
-    for (int e = s.lane; e < s.C; e += kWaveSize) {
+    int n = 2;
+    while (n < m) n <<= 1;
+    for (int e = s.lane; e < n; e += kWaveSize) {
       uint64_t v = 0ull;
       if (e < cnt) v = list[e];
-      else if (e < cnt + ns) v = stg[e - cnt];
+      else if (e < m) v = stg[e - cnt];
       s.scr[e] = v;
     }
     wave_sync_lds();
-    wave_bitonic_desc(s.scr, s.C, s.lane);
+    wave_bitonic_desc(s.scr, n, s.lane);
     for (int e = s.lane; e < s.k; e += kWaveSize) list[e] = s.scr[e];
     const uint64_t kth = s.scr[s.k - 1];
     wave_sync_lds();
@@ -89,7 +96,7 @@ __device__ inline bool sink_offer(const CandSink &s, int i, bool mine, uint64_t 
   int n = __popcll(tm);
   if (n == 0) return false;
   if ((int)s.stg_cnt[i] + n > s.cl) {
-    sink_spill(s, i, list);
+    sink_spill(s, i, list, true);
     spilled = true;
     take = mine && key > s.st_key[i];
     tm = __ballot(take);
