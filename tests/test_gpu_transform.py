@@ -55,6 +55,10 @@ SHAPES = [
     (3, 17, 5),
     (300, 4096, 1024),
     (20000, 512, 128),
+    # datastore-sized passes take 128-row tiles: ragged rows, dims and
+    # columns, and dims that are not a multiple of 4 (scalar staging)
+    (1500, 1000, 130),
+    (1100, 999, 70),
 ]
 
 
