@@ -224,12 +224,18 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   // most a quarter of the tiles).  A pass at stride P leaves about P*k
   // candidates per query for the next one, so batches with many
   // (query, rank) pairs add a denser level: its extra sampled scan costs less
-  // than the candidates it removes from the full pass.
+  // than the candidates it removes from the full pass.  The single-tile
+  // scan, whose waves cut their lists early on their own, does best with
+  // one pass at stride 256 (measured: 1.5-4% faster than 4096, 64 at
+  // 1-4 queries and at d = 4096 groups; the shared-key scan is faster with
+  // the two levels).
   pl.sort_lists = B <= 8;
   if (!pl.sort_lists || (k >= 16 && (int64_t)B * k >= 64)) {
     const bool dense = (int64_t)B * k >= 8192;
     const std::vector<int64_t> ladder =
-        dense ? std::vector<int64_t>{4096, 256, 16} : std::vector<int64_t>{4096, 64};
+        dense    ? std::vector<int64_t>{4096, 256, 16}
+        : pl.mq  ? std::vector<int64_t>{4096, 64}
+                 : std::vector<int64_t>{256};
     for (int64_t P : ladder) {
       int64_t nv = ceil_div(ix->T, P);
       if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides.push_back(P);
