@@ -228,7 +228,8 @@ dresd_status dresd_pack_drafts(const int32_t *tokens, int32_t B, int32_t k, int3
 /*
  * Describe how the next search of this shape would run (host outputs, NULL
  * allowed): the number of passes over sampled keys before the main pass, the
- * number of waves of the main scan, the bytes of workspace it needs, and
+ * number of waves of the main scan (of the first launch when the batch
+ * takes several), the bytes of workspace it needs, and
  * which scan kernel runs it: 0 = single-tile scan (batches within one
  * 16-column query tile group, queries staged in LDS), 1 = shared-key scan
  * (queries held in registers, keys staged through LDS).

@@ -53,6 +53,10 @@ struct ScanParams {
   const int64_t *probes64;
   const int32_t *part_tile;  // [P + 1]
   int seg_lds, P;
+  // Single-tile scan: query groups served by one launch.  Group i holds
+  // queries [B i / ngroups, B (i + 1) / ngroups) of the launch's B; each
+  // group has its own G lists per query and gridDim.x / ngroups workgroups.
+  int ngroups = 1;
 };
 
 // Slot of the partitioned layout that holds no row.
@@ -157,7 +161,9 @@ hipError_t launch_pack_drafts(const DraftParams &p, hipStream_t st);
 
 // Kernel launch entry points (defined in dresd_kernels.hip).
 typedef void (*ScanKernel)(ScanParams);
-ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass);  // cpq: columns per query
+// cpq: columns per query; shared: the variant for launches of several query
+// groups (one query tile only, else null)
+ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass, bool shared = false);
 // Shared-key scan (dresd_scan_mq.hip): qtw query tiles per wave, kbt blocks
 // per key tile, filtered = next-token-filtered search; *stages receives the
 // depth of its LDS ring of key stages.

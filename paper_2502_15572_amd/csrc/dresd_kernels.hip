@@ -136,7 +136,12 @@ constexpr int kModeMain = 0, kModeSample = 1, kModeParts = 2;
 
 // `gw` is the wave's list within its query (or batch); seg_off / seg_tile
 // are the query's probed segments in the partitioned search.
-template <int DT, int QT, int CPQ, int MODE>
+// SHARED: a launch of several query groups whose workgroups read each key
+// range together (see scan_group_view).  Its key loads are cached, so that
+// the XCD's L2 keeps a block for the range's other readers, and 16 deep:
+// most of them wait on a line already in flight from HBM.  A lone reader
+// streams past the cache (nontemporal loads, 8 deep).
+template <int DT, int QT, int CPQ, int MODE, bool SHARED = false>
 __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
                                           const int32_t *seg_off, const int32_t *seg_tile) {
   constexpr bool MAIN = MODE == kModeMain;
@@ -144,7 +149,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
   constexpr int QPT = 16 / CPQ;  // queries per 16-column tile
   constexpr int NS = 4 / CPQ;    // scores per lane per tile
   constexpr int NQ = QT * QPT;   // queries held by one launch
-  constexpr int U = 8;           // key blocks in flight per wave
+  constexpr int U = SHARED ? 16 : 8;  // key blocks in flight per wave
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int lane = threadIdx.x & 63;
@@ -278,10 +283,14 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
     const int64_t vt = i / KB;
     return base + ((v0 + vt) * p.stride * KB + (i - vt * KB)) * 64;
   };
+  auto fetch = [](const u4 *a) -> u4 {
+    if constexpr (SHARED) return *a;
+    else return __builtin_nontemporal_load(a);
+  };
   u4 ring[U];
   if (J > 0) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) ring[u] = __builtin_nontemporal_load(block(u));
+    for (int u = 0; u < U; ++u) ring[u] = fetch(block(u));
   }
   f4 acc[QT];
 #pragma unroll
@@ -440,7 +449,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       mfma_block(ring[u]);
-      ring[u] = __builtin_nontemporal_load(block(jj + u + U));
+      ring[u] = fetch(block(jj + u + U));
       if (++ckb == KB) tile_end(false);
     }
   }
@@ -464,18 +473,68 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
   }
 }
 
+// The workgroup's query group and key range, and its waves' list index.
+// With several groups per launch, each group's R = gridDim.x / ngroups
+// workgroups split the key tiles into R ranges, and the ngroups workgroups
+// of one range sit next to each other in dispatch order on one XCD
+// (workgroups are dispatched round-robin over the 8 XCDs): they stream the
+// same keys at about the same time, so that XCD's L2 serves the re-reads.
+__device__ __forceinline__ int scan_group_view(ScanParams &p) {
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nwv = blockDim.x >> 6;
+  const int ng = p.ngroups;
+  if (ng <= 1) return (int)blockIdx.x * nwv + wv;
+  const int R = (int)gridDim.x / ng;
+  int gi, r;
+  if ((R & 7) == 0) {
+    const int x = (int)blockIdx.x & 7, j = (int)blockIdx.x >> 3;
+    gi = j % ng;
+    r = (j / ng) * 8 + x;
+  } else {
+    gi = (int)blockIdx.x % ng;
+    r = (int)blockIdx.x / ng;
+  }
+  // (readfirstlane: the values are wave-uniform, and LDS addresses derived
+  // from the group size must stay in scalar registers)
+  const int b0 = __builtin_amdgcn_readfirstlane((int)((int64_t)p.B * gi / ng));
+  const int b1 = __builtin_amdgcn_readfirstlane((int)((int64_t)p.B * (gi + 1) / ng));
+  p.queries += (size_t)b0 * p.d;
+  p.lists += (size_t)b0 * p.G * p.C;
+  p.lcnt += (size_t)b0 * p.G;
+  p.lkth += (size_t)b0 * p.G;
+  p.lfirst += (size_t)b0 * p.G;
+  if (p.tau) p.tau += b0;
+  if (p.next_tok) p.next_tok += b0;
+  p.B = b1 - b0;
+  return __builtin_amdgcn_readfirstlane(r) * nwv + wv;
+}
+
 // Two kernel names so that profiles separate the main pass from the
 // sampled passes that only set thresholds.
 template <int DT, int QT, int CPQ>
 __global__ void __launch_bounds__(kScanThreads) dresd_scan_main(ScanParams p) {
-  scan_body<DT, QT, CPQ, kModeMain>(p, blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
-                                    nullptr, nullptr);
+  const int gw = scan_group_view(p);
+  scan_body<DT, QT, CPQ, kModeMain>(p, gw, nullptr, nullptr);
 }
 
 template <int DT, int QT, int CPQ>
 __global__ void __launch_bounds__(kScanThreads) dresd_scan_sample(ScanParams p) {
-  scan_body<DT, QT, CPQ, kModeSample>(p, blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
-                                      nullptr, nullptr);
+  const int gw = scan_group_view(p);
+  scan_body<DT, QT, CPQ, kModeSample>(p, gw, nullptr, nullptr);
+}
+
+// The same two passes for launches of several query groups of one query
+// tile each (the groups' workgroups share the key ranges).
+template <int DT, int CPQ>
+__global__ void __launch_bounds__(kScanThreads) dresd_scan_main_shared(ScanParams p) {
+  const int gw = scan_group_view(p);
+  scan_body<DT, 1, CPQ, kModeMain, true>(p, gw, nullptr, nullptr);
+}
+
+template <int DT, int CPQ>
+__global__ void __launch_bounds__(kScanThreads) dresd_scan_sample_shared(ScanParams p) {
+  const int gw = scan_group_view(p);
+  scan_body<DT, 1, CPQ, kModeSample, true>(p, gw, nullptr, nullptr);
 }
 
 // Segments of one query from its probe list (S <= 1024 distinct ids in
@@ -562,10 +621,14 @@ __global__ void __launch_bounds__(kScanThreads) dresd_scan_parts(ScanParams p) {
         (ScanKernel)dresd_scan_sample<DT, 16, CPQ>                                            \
   }
 
-#define DRESD_VARIANT(V, DT, CPQ)                                    \
-  ScanKernel scan_kernel_variant##V(int qi, bool main_pass) {        \
-    static const ScanKernel table[2][5] = {DRESD_SCAN_ROW(DT, CPQ)}; \
-    return table[main_pass ? 0 : 1][qi];                             \
+#define DRESD_VARIANT(V, DT, CPQ)                                                      \
+  ScanKernel scan_kernel_variant##V(int qi, bool main_pass, bool shared) {             \
+    static const ScanKernel table[2][5] = {DRESD_SCAN_ROW(DT, CPQ)};                   \
+    if (shared)                                                                        \
+      return qi != 0 ? nullptr                                                         \
+             : main_pass ? (ScanKernel)dresd_scan_main_shared<DT, CPQ>                 \
+                         : (ScanKernel)dresd_scan_sample_shared<DT, CPQ>;              \
+    return table[main_pass ? 0 : 1][qi];                                               \
   }
 
 // variants: 0 = f32 keys, 1 = f16 keys x1, 2 = f16 keys x4, 3 = bf16 keys x4,
@@ -587,11 +650,11 @@ DRESD_VARIANT(4, kBF16, 2)
 #endif
 
 #if !defined(DRESD_TU) || DRESD_TU == 0
-ScanKernel scan_kernel_variant0(int, bool);
-ScanKernel scan_kernel_variant1(int, bool);
-ScanKernel scan_kernel_variant2(int, bool);
-ScanKernel scan_kernel_variant3(int, bool);
-ScanKernel scan_kernel_variant4(int, bool);
+ScanKernel scan_kernel_variant0(int, bool, bool);
+ScanKernel scan_kernel_variant1(int, bool, bool);
+ScanKernel scan_kernel_variant2(int, bool, bool);
+ScanKernel scan_kernel_variant3(int, bool, bool);
+ScanKernel scan_kernel_variant4(int, bool, bool);
 
 int qt_index(int qt) {
   switch (qt) {
@@ -604,14 +667,14 @@ int qt_index(int qt) {
   }
 }
 
-ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass) {
+ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass, bool shared) {
   int qi = qt_index(qt);
   if (qi < 0) return nullptr;
-  if (dtype == kF32 && cpq == 1) return scan_kernel_variant0(qi, main_pass);
-  if (dtype == kF16 && cpq == 1) return scan_kernel_variant1(qi, main_pass);
-  if (dtype == kF16 && cpq == 4) return scan_kernel_variant2(qi, main_pass);
-  if (dtype == kBF16 && cpq == 4) return scan_kernel_variant3(qi, main_pass);
-  if (dtype == kBF16 && cpq == 2) return scan_kernel_variant4(qi, main_pass);
+  if (dtype == kF32 && cpq == 1) return scan_kernel_variant0(qi, main_pass, shared);
+  if (dtype == kF16 && cpq == 1) return scan_kernel_variant1(qi, main_pass, shared);
+  if (dtype == kF16 && cpq == 4) return scan_kernel_variant2(qi, main_pass, shared);
+  if (dtype == kBF16 && cpq == 4) return scan_kernel_variant3(qi, main_pass, shared);
+  if (dtype == kBF16 && cpq == 2) return scan_kernel_variant4(qi, main_pass, shared);
   return nullptr;
 }
 

@@ -63,11 +63,13 @@ int next_pow2(int x) {
 // Dimensions per 1 KiB block: 16 lanes' rows x 4 lane groups x (8 | 4) dims.
 int block_dims(int dtype) { return dtype == kF32 ? 16 : 32; }
 
+// Queries [b0, b0 + nb) of the batch, scanned by one launch as ng query
+// groups (ng > 1 only for the single-tile scan).
 struct Group {
-  int b0, nb;
+  int b0, nb, ng;
 };
 
-constexpr size_t kMaxGroup = 256;  // 16 query tiles x 16 columns
+constexpr size_t kMaxGroup = 256;  // queries per launch: 16 query tiles x 16 columns
 constexpr int kMaxScanWgPerCu = 4;
 // One workgroup (4 waves, one per SIMD) per CU where it measured faster:
 // each wave (or workgroup) streams one contiguous range, and fewer, longer
@@ -76,11 +78,16 @@ constexpr int kMaxScanWgPerCu = 4;
 // scan on 4M x 1024 keys at B = 64-256: +3%).  Scans whose per-block work is
 // larger need the extra waves to hide latency.
 constexpr int kMaxTileWgPerCu = 1;
+// Query groups of the single-tile scan served by one launch: one per XCD
+// for each key range, so the range is read from HBM about once and its
+// re-reads come from that XCD's L2.
+constexpr int kGroupsPerLaunch = 8;
 
 struct Plan {
   int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
   bool mq = false;                  // shared-key scan (queries in registers)
   int bmax = 0;                 // queries per group
+  int bl = 0;                   // queries per launch (several groups)
   std::vector<Group> groups;
   int C = 0;                    // per-wave list capacity
   int CL = 0;                   // per-query LDS stage
@@ -194,10 +201,20 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
     pl.lds = scan_lds(bmax * pl.terms, ix->KB, pl.qt * pl.qpt, pl.CL, pl.C);
   }
   const int bmax = pl.bmax;
-  int ngr = (int)ceil_div(B, bmax);
-  for (int i = 0; i < ngr; ++i) {
-    int b0 = (int)((int64_t)B * i / ngr), b1 = (int)((int64_t)B * (i + 1) / ngr);
-    pl.groups.push_back({b0, b1 - b0});
+  const int ngr = (int)ceil_div(B, bmax);
+  // The single-tile scan serves several groups per launch; launch sizes
+  // differ by at most one query and each splits into groups of <= bmax.
+  const int per = pl.mq ? 1 : std::max(1, std::min({ngr, kGroupsPerLaunch, (int)(kMaxGroup / bmax)}));
+  const int nl = (int)ceil_div(ngr, per);
+  pl.bl = 0;
+  for (int i = 0; i < nl; ++i) {
+    int b0 = (int)((int64_t)B * i / nl), b1 = (int)((int64_t)B * (i + 1) / nl);
+    pl.groups.push_back({b0, b1 - b0, (int)ceil_div(b1 - b0, bmax)});
+    pl.bl = std::max(pl.bl, b1 - b0);
+  }
+  if (per > 1 && pl.qt == 1) {
+    pl.kmain = scan_kernel(ix->dtype, pl.qt, pl.terms, true, true);
+    pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.terms, false, true);
   }
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
   if (pl.lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS");
@@ -244,7 +261,7 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   // Lists end with at most k keys each, so a query never has more than
   // G_max * k merge candidates.
   pl.spill_cap = std::max<int64_t>(0, (int64_t)pl.G_max * k - kMergeCap);
-  size_t nb = (size_t)bmax;
+  size_t nb = (size_t)pl.bl;
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
   pl.off_tau = 0;
   pl.off_lcnt = up(2 * kMaxGroup * 8);
@@ -255,6 +272,17 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   pl.off_qop = pl.off_spill + up(nb * (size_t)std::max<int64_t>(1, pl.spill_cap) * 8);
   pl.bytes = pl.off_qop + (pl.mq ? up((size_t)pl.qt * ix->KB * kBlockBytes) : 0);
   return DRESD_OK;
+}
+
+// Workgroups per query group of one scan pass over nvisit tiles (the
+// launch has gr.ng times as many).  Several groups: each gets a multiple of
+// 8 (one key range per XCD slot) and together they fit the resident grid,
+// so the readers of a range run at the same time.
+int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit) {
+  const int wpg = kScanThreads / kWaveSize;
+  int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(nvisit, pl.mq ? 1 : wpg));
+  if (gr.ng > 1) wgs = std::min<int64_t>(wgs, std::max<int64_t>(8, pl.wg_max / gr.ng / 8 * 8));
+  return wgs;
 }
 
 dresd_status ensure_workspace(dresd_index *ix, size_t bytes) {
@@ -414,10 +442,13 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
     for (int qt : {1, 2, 4, 8, 16})
       for (int cpq : {1, 2, 4})
         for (int mp = 0; mp < 2; ++mp) {
-          ScanKernel kf = scan_kernel(v, qt, cpq, mp != 0);
-          if (kf)
-            (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                      (int)ix->lds_max);
+          for (bool shared : {false, true}) {
+            ScanKernel kf = scan_kernel(v, qt, cpq, mp != 0, shared);
+            if (kf)
+              (void)hipFuncSetAttribute((const void *)kf,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)ix->lds_max);
+          }
         }
   for (int v = 0; v < 3; ++v)
     if (ScanKernel kf = scan_parts_kernel(v))
@@ -496,7 +527,7 @@ dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int
   const int wpg = kScanThreads / kWaveSize;
   if (sample_passes) *sample_passes = (int32_t)pl.strides.size();
   if (scan_waves)
-    *scan_waves = (int32_t)std::min<int64_t>(pl.wg_max, ceil_div(ix->T, pl.mq ? 1 : wpg)) * wpg;
+    *scan_waves = (int32_t)(pass_wgs(pl, pl.groups[0], ix->T) * pl.groups[0].ng * wpg);
   if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
   if (scan_kind) *scan_kind = pl.mq ? 1 : 0;
   return DRESD_OK;
@@ -580,6 +611,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     sp.CL = pl.CL;
     sp.ftok = next_tok ? ix->ftok : nullptr;
     sp.next_tok = next_tok ? next_tok + gr.b0 : nullptr;
+    sp.ngroups = gr.ng;
     sp.qop = nullptr;
     sp.slot_row = nullptr;
     sp.seg_off = sp.seg_tile = nullptr;
@@ -619,7 +651,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       sp.stride = stride;
       sp.nvisit = ceil_div(ix->T, stride);
       sp.tau = tau_in;
-      int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(sp.nvisit, pl.mq ? 1 : wpg));
+      const int64_t wgs = pass_wgs(pl, gr, sp.nvisit);
       sp.G = (int)(pl.mq ? wgs : wgs * wpg);
       void *sargs[] = {&sp};
       hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -628,15 +660,15 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
         e1 = take_event(ix);
         if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
       }
-      DRESD_HIP(launch((const void *)(main_pass ? pl.kmain : pl.ksample), dim3((unsigned)wgs),
-                       dim3(kScanThreads), sargs, pl.lds, e0, e1));
+      DRESD_HIP(launch((const void *)(main_pass ? pl.kmain : pl.ksample),
+                       dim3((unsigned)(wgs * gr.ng)), dim3(kScanThreads), sargs, pl.lds, e0, e1));
       if (main_pass && ix->prof) {
         ix->ev_scan.push_back(e0);
         ix->ev_scan.push_back(e1);
       }
       mp.G = sp.G;
       mp.final_mode = main_pass ? 1 : 0;
-      mp.tau_out = tau + (size_t)(level & 1) * pl.bmax;
+      mp.tau_out = tau + (size_t)(level & 1) * pl.bl;
       mp.idx = idx + (size_t)gr.b0 * k;
       mp.score = score + (size_t)gr.b0 * k;
       mp.tokens = tokens ? tokens + (size_t)gr.b0 * k * ix->L : nullptr;

@@ -97,7 +97,7 @@ def test_filtered_golden_on_gpu(gpu_lib):
 FILTERED = [
     # (workload, reduced N, batches)
     ("flat16k_d256_f32", 16384, (8,)),
-    ("hidden1m_d4096_bf16", 6000 + 5, (1, 4)),
+    ("hidden1m_d4096_bf16", 6000 + 5, (1, 4, 20)),
     ("pca4m_d1024_f16", 40000 + 3, (1, 16)),
     ("batch10m_d256_f16", 120000 + 9, (64, 256)),
     ("zipf33m_d128_f16", 200000 + 11, (1, 128)),

@@ -122,6 +122,12 @@ EDGE = [
     ("f32", 5000, 64, 100, 20),      # fp32, seven query tiles
     ("f16", 3000, 2048, 40, 10),     # f16 blocks per tile outside the shared-key scan
     ("bf16", 2000, 2048, 64, 8),     # bf16 (three-part queries), sixteen query tiles
+    # d = 4096 bf16: 8 queries per single-tile group, several groups per
+    # launch (workgroups of one key range placed on one XCD when the ranges
+    # are a multiple of 8, else in plain order)
+    ("bf16", 20000, 4096, 64, 10),   # 8 groups, one launch, 256 ranges
+    ("bf16", 3001, 4096, 70, 12),    # 9 groups: two launches of 5, 47 ranges
+    ("f16", 9000, 4096, 19, 40),     # f16 at one column: 3 groups of 6-7
     # the largest d (16384): one query operand nearly fills the LDS, so
     # batches split into groups of one or two queries
     ("bf16", 300, 16384, 1, 5),
@@ -173,6 +179,29 @@ def test_shared_key_scan_shapes(gpu_lib, dt, N, d, B, k):
     q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
     cont = torch.randint(0, 32000, (N, 3), generator=gen, dtype=torch.int32)
     run_case(gpu_lib, x, cont, q, k, dt)
+
+
+def test_grouped_launch_matches_split_batches(gpu_lib):
+    """A batch whose single-tile groups share one launch returns, bit for
+    bit, what the same queries return as separate batches of one group each
+    (the answer is unique: every key names its row)."""
+    say("grouped vs split")
+    gen = torch.Generator().manual_seed(4096)
+    N, d, B, k = 20011, 4096, 40, 16
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(torch.bfloat16)
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 2), generator=gen, dtype=torch.int32)
+    from paper_2502_15572_amd import Index
+    ix = Index(x.to(DEV), cont.to(DEV))
+    qd = q.to(DEV)
+    whole = ix.search(qd, k)
+    parts = [ix.search(qd[b:b + 8].contiguous(), k) for b in range(0, B, 8)]
+    torch.cuda.synchronize()
+    for i, w in enumerate(whole):
+        assert torch.equal(w, torch.cat([p[i] for p in parts]))
+    ix.close()
 
 
 def test_shared_key_scan_all_scores_equal(gpu_lib):
