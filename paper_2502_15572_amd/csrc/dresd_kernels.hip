@@ -302,9 +302,13 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
   // Filtered search (Section 3.5): the first tokens of a group of four
   // tiles (64 rows, lane l: row l % 16 of tile 4 i + l / 16) are copied into
   // one of two per-wave LDS slots by an LDS-DMA copy issued a whole group
-  // ahead of use.  Every block load issued since is younger, so waiting for
-  // at most U pending loads covers the copy (all of them in the last,
-  // partial group of blocks, which issues no loads).
+  // ahead of use: the copy of group i + 2 at the end of tile 4 i + 3, read
+  // from the end of tile 4 i + 8 on.  By then the loads of 5 tiles and one
+  // more copy are younger, so waiting for at most U pending operations
+  // covers it when 5 KB + 1 >= U.  The first group's copy has only the
+  // second copy and the first tile's KB loads behind it (KB + 1 >= U).  Where
+  // that does not hold, and in the last, partial group of blocks (which
+  // issues no loads), the wait is for all of them.
   const bool filt = !PARTS && p.ftok != nullptr;
   const int64_t ntw = v1 - v0;  // tiles of this wave
   int64_t tdone = 0;            // tiles finished (wave-uniform)
@@ -381,7 +385,7 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
       // (even a threshold of -inf).
       const int tg = (int)(tdone & 3);
       if (tg == 0) {
-        if (tail) wait_vmcnt<0>();
+        if (tail || (tdone == 0 ? KB + 1 < U : 5 * KB + 1 < U)) wait_vmcnt<0>();
         else wait_vmcnt<U>();
       }
       const int f = ftbuf[(int)((tdone >> 2) & 1) * 64 + tg * 16 + m];

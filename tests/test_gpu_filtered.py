@@ -115,6 +115,35 @@ def test_filtered_parity_reduced(gpu_lib, name, N, batches):
         say("  exact-order rate %.3f" % rep["exact_order_rate"])
 
 
+# Few key blocks per tile (1-4): fewer block loads than the load ring's depth
+# follow a wave's copy of the tiles' first tokens before they are read.  With
+# about one tile per wave every tile is its wave's first, and in the larger
+# case each wave's tiles span several groups of four.
+FILTERED_SMALL_TILES = [
+    # (dtype, N, d, B, k)
+    ("f16", 2000, 128, 3, 10),     # 4 blocks per tile, one tile per wave
+    ("f16", 1500, 32, 2, 5),       # 1 block per tile
+    ("f32", 1800, 20, 4, 6),       # fp32, 2 blocks per tile
+    ("f16", 150000, 32, 1, 20),    # 1 block per tile, ~9 tiles per wave
+]
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", FILTERED_SMALL_TILES,
+                         ids=["%s-N%d-d%d-B%d-k%d" % c for c in FILTERED_SMALL_TILES])
+def test_filtered_few_blocks_per_tile(gpu_lib, dt, N, d, B, k):
+    say("filtered small tiles", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N + d * 13 + B * 7 + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    src = torch.randint(0, N, (B,), generator=gen)
+    q = x[src].to(torch.float64) + 0.05 * torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 4, (N, 3), generator=gen, dtype=torch.int32)  # ~1/4 of rows match
+    nt = cont[src, 0].numpy().astype(np.int32)
+    rep = run_filtered(x, cont, q, nt, k, dt)
+    say("  exact-order rate %.3f" % rep["exact_order_rate"])
+
+
 def test_filtered_all_rows_match_equals_unfiltered(gpu_lib):
     """A token every row starts with filters nothing: same result as the
     unfiltered search, bit for bit (shared-key scan and sampled passes)."""
