@@ -51,6 +51,10 @@ def built():
 
 
 CASES = [(name, B) for name, w in WORKLOADS.items() for B in w.batches]
+# The 1M x 4096 datastore at B = 64: eight 8-query groups in one scan launch
+# (their workgroups share each key range through one XCD's L2).
+CASES.insert(CASES.index(("hidden1m_d4096_bf16", max(WORKLOADS["hidden1m_d4096_bf16"].batches))) + 1,
+             ("hidden1m_d4096_bf16", 64))
 
 
 @pytest.mark.parametrize("name,B", CASES, ids=["%s-B%d" % c for c in CASES])
