@@ -33,7 +33,10 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-SCAN_UNIT = {"single_tile": "dresd_kernels.hip", "shared_key": "dresd_scan_mq.hip"}
+SCAN_UNIT = {"single_tile": "dresd_kernels.hip", "shared_key": "dresd_scan_mq.hip",
+             "single_tile_grouped": "dresd_kernels.hip"}
+SCAN_KERNEL_NAME = {"single_tile": "dresd_scan_main", "shared_key": "dresd_scanmq_main",
+                    "single_tile_grouped": "dresd_scan_main_shared"}
 
 
 def kernel_hash(unit: str) -> str:
@@ -486,7 +489,7 @@ def main():
     achieved = scan_bytes / (scan_ms * 1e-3) / 1e9
     flops = 2.0 * w.N * w.d * B
     plan = ix.plan(B, k)
-    kname = "dresd_scanmq_main" if plan["scan_kernel"] == "shared_key" else "dresd_scan_main"
+    kname = SCAN_KERNEL_NAME[plan["scan_kernel"]]
     # The scan's floor is the larger of its HBM time and its matrix-core time.
     mfma_peak = MFMA_PEAK_TFLOPS[w.dtype] * 1e12
     mfma_bound = flops / mfma_peak > scan_bytes / (HBM_PEAK_GBPS * 1e9)

@@ -232,7 +232,9 @@ dresd_status dresd_pack_drafts(const int32_t *tokens, int32_t B, int32_t k, int3
  * takes several), the bytes of workspace it needs, and
  * which scan kernel runs it: 0 = single-tile scan (batches within one
  * 16-column query tile group, queries staged in LDS), 1 = shared-key scan
- * (queries held in registers, keys staged through LDS).
+ * (queries held in registers, keys staged through LDS), 2 = single-tile scan
+ * serving several query groups per launch (batches whose query operands
+ * exceed one workgroup's LDS; the groups share each key range through L2).
  * Errors: EINVAL for the same argument errors as dresd_search.
  */
 dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,

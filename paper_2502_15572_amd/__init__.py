@@ -36,6 +36,10 @@ def _stream_handle(stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+# dresd_search_plan's scan kinds
+SCAN_KINDS = {0: "single_tile", 1: "shared_key", 2: "single_tile_grouped"}
+
+
 class Index:
     """An exact inner-product index over ``keys[N, d]`` with values ``cont[N, L]``.
 
@@ -104,7 +108,7 @@ class Index:
                                                ctypes.byref(w), ctypes.byref(ws),
                                                ctypes.byref(kind)))
         return {"sample_passes": sp.value, "scan_waves": w.value, "workspace_bytes": ws.value,
-                "scan_kernel": "shared_key" if kind.value else "single_tile"}
+                "scan_kernel": SCAN_KINDS[kind.value]}
 
     def profile(self, on: bool = True):
         _lib.check(self._lib.dresd_profile_enable(self._h, 1 if on else 0))

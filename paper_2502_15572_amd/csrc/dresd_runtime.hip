@@ -529,7 +529,7 @@ dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int
   if (scan_waves)
     *scan_waves = (int32_t)(pass_wgs(pl, pl.groups[0], ix->T) * pl.groups[0].ng * wpg);
   if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
-  if (scan_kind) *scan_kind = pl.mq ? 1 : 0;
+  if (scan_kind) *scan_kind = pl.mq ? 1 : (pl.groups[0].ng > 1 ? 2 : 0);
   return DRESD_OK;
 }
 

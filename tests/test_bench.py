@@ -54,6 +54,8 @@ def test_traffic_is_read_only_for_the_current_source(tmp_path, monkeypatch):
     path.write_text("kernel_source_sha256_16: %s\nhbm_bytes_per_launch: 1.25e+09\n" % h)
     assert bench.read_traffic("w", 3, "single_tile") == 1.25e9
     assert bench.read_traffic("w", 3, "shared_key") is None  # another kernel's source
+    # grouped launches run kernels of the same source file
+    assert bench.read_traffic("w", 3, "single_tile_grouped") == 1.25e9
     with open(csrc / "dresd_kernels.hip", "a") as f:
         f.write("\n// edit\n")
     assert bench.read_traffic("w", 3, "single_tile") is None  # source changed since
