@@ -59,3 +59,13 @@ def test_traffic_is_read_only_for_the_current_source(tmp_path, monkeypatch):
     with open(csrc / "dresd_kernels.hip", "a") as f:
         f.write("\n// edit\n")
     assert bench.read_traffic("w", 3, "single_tile") is None  # source changed since
+
+
+def test_every_scan_kind_names_a_kernel_of_its_source():
+    """Each kind the plan query reports maps to the source file whose hash
+    gates its traffic summary and to a kernel defined in that file."""
+    from paper_2502_15572_amd import SCAN_KINDS
+    assert set(SCAN_KINDS.values()) == set(bench.SCAN_UNIT) == set(bench.SCAN_KERNEL_NAME)
+    for kind in SCAN_KINDS.values():
+        src = open(os.path.join(bench.CSRC, bench.SCAN_UNIT[kind])).read()
+        assert " %s(ScanParams p)" % bench.SCAN_KERNEL_NAME[kind] in src, kind
