@@ -41,6 +41,15 @@ extern "C" {
  * the workspaces it uses (that first call may allocate and synchronise).
  * After such a warm-up call these calls can be captured in a HIP graph:
  * they issue no allocation, no synchronisation and no memset while running.
+ * A call that would have to grow a workspace while its stream is being
+ * captured fails with DRESD_EUNSUPPORTED instead.  A workspace that a later,
+ * larger call outgrows is never freed before its owner is (the index for
+ * search workspaces, the process for the per-device transform and k-means
+ * buffers), so a graph captured earlier stays valid after such a call.
+ *
+ * Allocation-failure test hook: with DRESD_FAIL_ALLOC_AT=n in the
+ * environment, the n-th device allocation the library makes (counted from
+ * when the variable last took a new value) fails as out of memory.
  */
 typedef struct dresd_index dresd_index; /* opaque, library-owned */
 typedef struct dresd_ivf dresd_ivf;     /* opaque: partitioned index */
@@ -114,10 +123,12 @@ dresd_status dresd_index_create(const void *embeddings,
  * Determinism: identical inputs give bitwise identical outputs.
  * Ownership: outputs are caller-owned and must stay alive until `stream`
  * completes.  The index owns a workspace that grows on first use with a new
- * batch shape (that growth allocates and synchronises); concurrent searches
- * on one index are not supported.
+ * batch shape (that growth allocates and synchronises; outgrown workspaces
+ * are kept until the index is destroyed); concurrent searches on one index
+ * are not supported.
  * Errors: EINVAL (null index/queries/idx/score, k out of range, B < 0),
- * ENOMEM (workspace growth failed), EDEVICE.
+ * ENOMEM (workspace growth failed; no output written), EUNSUPPORTED (the
+ * workspace would have to grow during stream capture), EDEVICE.
  */
 dresd_status dresd_search(dresd_index *ix, const float *queries, int32_t B,
                           int32_t k, int64_t *idx, float *score,
@@ -194,10 +205,12 @@ dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms,
  * fixed order, so results are deterministic.  Ownership: all buffers are
  * caller-owned and must stay alive until `stream` completes; the partial sums
  * use a per-device library buffer that is allocated (synchronously) on the
- * first call that needs a larger one and kept until the process ends, so
- * calls that overlap on one device must be serialised by the caller.
+ * first call that needs a larger one and kept, like every buffer it
+ * outgrows, until the process ends, so calls that overlap on one device must
+ * be serialised by the caller.
  * Errors: EINVAL (null pointer with M > 0, sizes or eps out of range),
- * ENOMEM, EDEVICE.
+ * ENOMEM, EUNSUPPORTED (the buffer would have to grow during stream
+ * capture), EDEVICE.
  */
 dresd_status dresd_transform(const float *x, int64_t M, int32_t D, const float *mean,
                              const float *var, float eps_z, const float *W, int32_t l,
@@ -314,8 +327,9 @@ dresd_status dresd_ivf_search_probes(dresd_ivf *ivf, const float *queries, const
  *   device [n] int32, each in [0, P) (not checked: the caller's contract);
  *   centroids device [P, d] fp32 in/out; counts device [P] int32 out (rows per
  *   centroid, NULL allowed).  Uses a per-device workspace of P*d*8 + P*4
- *   bytes, allocated (synchronously) on first use and kept; calls that
- *   overlap on one device race on it.
+ *   bytes, allocated (synchronously) on first use and kept, like every
+ *   buffer it outgrows, until the process ends; calls that overlap on one
+ *   device race on it.
  * Both are asynchronous on `stream`.  Errors: EINVAL (ranges, nulls), ENOMEM,
  * EDEVICE.
  */

@@ -49,7 +49,8 @@ struct ScanParams {
   int S, wgq;
   // ... or, when probes64 is set, each workgroup builds its query's segments
   // in LDS at byte offset seg_lds from the exact probe search's output
-  // ([B][S] distinct ids in [0, P)) and the partitions' first tiles.
+  // ([B][S] ids; outside [0, P) and repeats skipped) and the partitions'
+  // first tiles.
   const int64_t *probes64;
   const int32_t *part_tile;  // [P + 1]
   int seg_lds, P;
@@ -120,6 +121,7 @@ struct MergeParams {
   float *score;
   int32_t *tokens;           // may be null
   const int32_t *cont;       // [N, L]
+  int64_t N;                 // rows of cont: a winner outside [0, N) is written as (-1, -inf, 0)
   int L;
   int final_mode;
 };

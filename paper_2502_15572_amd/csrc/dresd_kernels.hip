@@ -541,22 +541,38 @@ __global__ void __launch_bounds__(kScanThreads) dresd_scan_sample_shared(ScanPar
   scan_body<DT, 1, CPQ, kModeSample, true>(p, gw, nullptr, nullptr);
 }
 
-// Segments of one query from its probe list (S <= 1024 distinct ids in
-// [0, P), in probe order): off[j + 1] = tiles of probes 0..j, tile[j] = first
-// tile of probe j.  All threads of the workgroup take part.
+// Segments of one query from its probe list (S <= 1024 ids, in probe
+// order): off[j + 1] = tiles of probes 0..j, tile[j] = first tile of probe j.
+// Ids outside [0, P) and repeats of an earlier probe get an empty segment, so
+// that no partition is scanned twice (its keys would enter the lists twice).
+// All threads of the workgroup take part.
 __device__ void parts_segments(const int64_t *probes, const int32_t *part_tile, int S, int P,
                                int32_t *off, int32_t *tile) {
   constexpr int E = 4;  // entries per thread: S <= E * kScanThreads
   __shared__ int32_t wsum[kScanThreads / kWaveSize];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  int32_t start[E], len[E], sum = 0;
+  int32_t id[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int j = t * E + e;
-    const int64_t id = j < S ? probes[j] : -1;
-    const bool ok = id >= 0 && id < P;
-    start[e] = ok ? part_tile[id] : 0;
-    len[e] = ok ? part_tile[id + 1] - start[e] : 0;
+    const int64_t v = j < S ? probes[j] : -1;
+    id[e] = (v >= 0 && v < P) ? (int32_t)v : -1;
+    if (j < S) tile[j] = id[e];  // the ids, until the segments replace them
+  }
+  __syncthreads();
+  const int last = min(S, t * E + E - 1);  // earlier entries of this thread's last one
+  for (int i = 0; i < last; ++i) {
+    const int32_t o = tile[i];
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (i < t * E + e && o == id[e]) id[e] = -1;
+  }
+  int32_t start[E], len[E], sum = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const bool ok = id[e] >= 0;
+    start[e] = ok ? part_tile[id[e]] : 0;
+    len[e] = ok ? part_tile[id[e] + 1] - start[e] : 0;
     sum += len[e];
   }
   int32_t x = sum;  // inclusive scan over the wave

@@ -171,7 +171,10 @@ __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk)
 // Output of one query from its sorted winners win[0..kk): the k-th best key
 // (sampled pass) or indices, scores and gathered continuations (final pass).
 // Each thread issues all of its continuation loads before its first store,
-// so the gather costs one memory latency rather than one per token.
+// so the gather costs one memory latency rather than one per token.  A
+// winner that names no row of the value table (only an upstream fault could
+// produce one) is written as index -1, score -inf and zero tokens instead of
+// being dereferenced.
 __device__ inline void write_result(const MergeParams &p, int b, const uint64_t *win,
                                     uint32_t kk, int tid, int nth) {
   if (!p.final_mode) {
@@ -180,11 +183,11 @@ __device__ inline void write_result(const MergeParams &p, int b, const uint64_t 
   }
   for (int r = tid; r < p.k; r += nth) {
     const size_t o = (size_t)b * p.k + r;
-    if (r < (int)kk) {
-      const uint64_t key = win[r];
-      p.idx[o] = (int64_t)(uint32_t)(~(uint32_t)key);
-      p.score[o] = order_value((uint32_t)(key >> 32));
-    } else {  // cannot happen when N >= k; filled defensively
+    const uint32_t row = r < (int)kk ? ~(uint32_t)win[r] : 0xFFFFFFFFu;
+    if ((int64_t)row < p.N) {
+      p.idx[o] = (int64_t)row;
+      p.score[o] = order_value((uint32_t)(win[r] >> 32));
+    } else {  // past the candidates (cannot happen when N >= k), or no row
       p.idx[o] = -1;
       p.score[o] = -__builtin_inff();
     }
@@ -202,7 +205,7 @@ __device__ inline void write_result(const MergeParams &p, int b, const uint64_t 
         v[u] = 0;
         if (i < n && r < (int)kk) {
           const uint32_t row = ~(uint32_t)win[r];
-          v[u] = p.cont[(size_t)row * L + (i - r * L)];
+          if ((int64_t)row < p.N) v[u] = p.cont[(size_t)row * L + (i - r * L)];
         }
       }
 #pragma unroll
@@ -250,7 +253,7 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
     cnt[j] = 0;
     first[j] = 0;
     if (w < G) {
-      cnt[j] = lcnt[w] & ~kSortedFlag;
+      cnt[j] = min(lcnt[w] & ~kSortedFlag, (uint32_t)p.C);
       first[j] = lfirst[w];
       const uint64_t v = lkth[w];
       mb = v > mb ? v : mb;
@@ -325,6 +328,9 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
       }
     }
   }
+  // Winner slots start empty (key 0 names no row), so that a slot no key
+  // reaches is written as a missing result rather than as stale LDS.
+  for (int i = tid; i < p.k; i += nth) sh.win[i] = 0ull;
   __threadfence_block();
   __syncthreads();
   const uint32_t M = sh.ncand;
@@ -350,6 +356,8 @@ __global__ void __launch_bounds__(kMergeThreads) dresd_merge(MergeParams p) {
   }
   __syncthreads();
   if (kk <= (uint32_t)kRankSortMax) {  // the winners, ordered into the free cache
+    for (uint32_t i = tid; i < kk; i += nth) sh.cache[i] = 0ull;
+    __syncthreads();
     rank_sort_desc(sh.win, kk, sh.cache, kk, tid, nth);
     __syncthreads();
     write_result(p, b, sh.cache, kk, tid, nth);

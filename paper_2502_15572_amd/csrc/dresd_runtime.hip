@@ -3,6 +3,7 @@
 // (sampled threshold passes, main scan, merge + gather).
 #include <algorithm>
 #include <mutex>
+#include <new>
 #include <string>
 #include <utility>
 #include <vector>
@@ -26,9 +27,11 @@ struct dresd_index {
   int32_t *ftok = nullptr;  // first token of each row's value [T * 16] (filtered search)
   int cus = 0;
   size_t lds_max = 0;
-  // workspace
+  // workspace; buffers it outgrew stay allocated until destroy (a captured
+  // graph may still use them)
   unsigned char *ws = nullptr;
   size_t ws_bytes = 0;
+  std::vector<void *> retired;
   // measurement
   bool prof = false;
   std::vector<hipEvent_t> ev_free;
@@ -53,6 +56,45 @@ dresd_status fail(dresd_status s, const std::string &msg) {
   } while (0)
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Every device allocation of the library goes through here.  Test hook: with
+// DRESD_FAIL_ALLOC_AT=n in the environment, the n-th allocation counted since
+// the variable last changed fails as out of memory without allocating, so
+// that each allocation-failure path can be driven on purpose.
+hipError_t dev_alloc(void **ptr, size_t bytes) {
+  static std::mutex mu;
+  static std::string armed;
+  static long seen = 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    const char *s = getenv("DRESD_FAIL_ALLOC_AT");
+    if (!s || !*s) {
+      armed.clear();
+    } else {
+      if (armed != s) {
+        armed = s;
+        seen = 0;
+      }
+      const long n = strtol(s, nullptr, 10);
+      if (n > 0 && ++seen == n) {
+        *ptr = nullptr;
+        return hipErrorOutOfMemory;
+      }
+    }
+  }
+  return hipMalloc(ptr, bytes);
+}
+
+// A buffer may only grow outside stream capture: growing allocates and
+// synchronises, which a capture cannot record.
+bool capturing(hipStream_t st) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cs) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return cs != hipStreamCaptureStatusNone;
+}
 
 int next_pow2(int x) {
   int n = 1;
@@ -285,16 +327,14 @@ int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit) {
   return wgs;
 }
 
-dresd_status ensure_workspace(dresd_index *ix, size_t bytes) {
+dresd_status ensure_workspace(dresd_index *ix, size_t bytes, hipStream_t st) {
   if (ix->ws_bytes >= bytes) return DRESD_OK;
-  if (ix->ws) {
-    DRESD_HIP(hipDeviceSynchronize());
-    (void)hipFree(ix->ws);
-    ix->ws = nullptr;
-    ix->ws_bytes = 0;
-  }
+  if (capturing(st))
+    return fail(DRESD_EUNSUPPORTED,
+                "the search needs a larger workspace while its stream is being captured; run one "
+                "uncaptured call of this shape first");
   void *p = nullptr;
-  if (hipMalloc(&p, bytes) != hipSuccess) {
+  if (dev_alloc(&p, bytes) != hipSuccess) {
     (void)hipGetLastError();
     return fail(DRESD_ENOMEM, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
   }
@@ -304,8 +344,42 @@ dresd_status ensure_workspace(dresd_index *ix, size_t bytes) {
     (void)hipFree(p);
     return fail(DRESD_EDEVICE, "workspace clear failed");
   }
+  // The outgrown buffer is kept until the index is destroyed: a graph
+  // captured from an earlier search may still replay on it.
+  if (ix->ws) ix->retired.push_back(ix->ws);
   ix->ws = static_cast<unsigned char *>(p);
   ix->ws_bytes = bytes;
+  return DRESD_OK;
+}
+
+// Per-device buffers kept until the process ends (the transform's partial
+// sums, the k-means sums).  One grows (allocating synchronously) when a call
+// needs more; the buffer it outgrows is kept as well, because a graph
+// captured from an earlier call may still replay on it.
+struct DeviceBuffers {
+  std::mutex mu;
+  std::vector<std::pair<void *, size_t>> cur;  // per device
+  std::vector<void *> retired;
+};
+
+dresd_status device_buffer(DeviceBuffers &db, int dev, size_t need, hipStream_t st,
+                           const char *what, void **out) {
+  std::lock_guard<std::mutex> lock(db.mu);
+  if (db.cur.size() <= (size_t)dev) db.cur.resize((size_t)dev + 1, {nullptr, 0});
+  if (db.cur[dev].second < need) {
+    if (capturing(st))
+      return fail(DRESD_EUNSUPPORTED, std::string(what) +
+                                          " must grow while the stream is being captured; run one "
+                                          "uncaptured call of this shape first");
+    void *b = nullptr;
+    if (dev_alloc(&b, need) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(DRESD_ENOMEM, std::string(what) + " allocation failed");
+    }
+    if (db.cur[dev].first) db.retired.push_back(db.cur[dev].first);
+    db.cur[dev] = {b, need};
+  }
+  *out = db.cur[dev].first;
   return DRESD_OK;
 }
 
@@ -411,18 +485,18 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
   ix->T = slot_row ? T : ceil_div(N, kTileRows);
   const size_t data_bytes = (size_t)ix->T * ix->KB * kBlockBytes;
   const size_t cont_bytes = (size_t)N * L * sizeof(int32_t);
-  if (hipMalloc(&ix->data, data_bytes) != hipSuccess) {
+  if (dev_alloc(&ix->data, data_bytes) != hipSuccess) {
     (void)hipGetLastError();
     ix->data = nullptr;
     return cleanup(fail(DRESD_ENOMEM, "key storage allocation failed"));
   }
-  if (hipMalloc((void **)&ix->cont, cont_bytes) != hipSuccess) {
+  if (dev_alloc((void **)&ix->cont, cont_bytes) != hipSuccess) {
     (void)hipGetLastError();
     ix->cont = nullptr;
     return cleanup(fail(DRESD_ENOMEM, "continuation storage allocation failed"));
   }
   const size_t ftok_bytes = (size_t)ix->T * kTileRows * sizeof(int32_t);
-  if (!slot_row && hipMalloc((void **)&ix->ftok, ftok_bytes) != hipSuccess) {
+  if (!slot_row && dev_alloc((void **)&ix->ftok, ftok_bytes) != hipSuccess) {
     (void)hipGetLastError();
     ix->ftok = nullptr;
     return cleanup(fail(DRESD_ENOMEM, "first-token column allocation failed"));
@@ -505,6 +579,7 @@ void dresd_index_destroy(dresd_index *ix) {
   if (ix->cont) (void)hipFree(ix->cont);
   if (ix->ftok) (void)hipFree(ix->ftok);
   if (ix->ws) (void)hipFree(ix->ws);
+  for (void *r : ix->retired) (void)hipFree(r);
   for (auto e : ix->ev_free) (void)hipEventDestroy(e);
   for (auto e : profile_events(ix)) (void)hipEventDestroy(e);
   (void)hipSetDevice(cur);
@@ -575,7 +650,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
   Plan pl;
   s = make_plan(ix, B, k, pl, next_tok != nullptr);
   if (s != DRESD_OK) return s;
-  s = ensure_workspace(ix, pl.bytes);
+  s = ensure_workspace(ix, pl.bytes, st);
   if (s != DRESD_OK) return s;
   uint64_t *tau = reinterpret_cast<uint64_t *>(ix->ws + pl.off_tau);
   uint32_t *lcnt = reinterpret_cast<uint32_t *>(ix->ws + pl.off_lcnt);
@@ -645,6 +720,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     mp.k = k;
     mp.cont = ix->cont;
     mp.L = ix->L;
+    mp.N = ix->N;
     const uint64_t *tau_in = nullptr;
     int level = 0;
     auto run_pass = [&](int64_t stride, bool main_pass) -> dresd_status {
@@ -718,27 +794,15 @@ dresd_status dresd_transform(const float *x, int64_t M, int32_t D, const float *
   p.dslice = (int)ceil_div(D, p.splits);
   p.part = nullptr;
   if (p.splits > 1) {
-    // Partial sums of the D slices: a per-device buffer kept for the life of
-    // the process, grown (synchronously) when a larger one is needed.
-    static std::mutex mu;
-    static std::vector<std::pair<void *, size_t>> bufs;
+    // Partial sums of the D slices (a per-device buffer kept for the life of
+    // the process).
+    static DeviceBuffers bufs;
     const size_t need = (size_t)p.splits * (size_t)M * (size_t)l * sizeof(float);
-    std::lock_guard<std::mutex> lock(mu);
-    if (bufs.size() <= (size_t)dev) bufs.resize((size_t)dev + 1, {nullptr, 0});
-    if (bufs[dev].second < need) {
-      if (bufs[dev].first) {
-        DRESD_HIP(hipDeviceSynchronize());
-        (void)hipFree(bufs[dev].first);
-        bufs[dev] = {nullptr, 0};
-      }
-      void *b = nullptr;
-      if (hipMalloc(&b, need) != hipSuccess) {
-        (void)hipGetLastError();
-        return fail(DRESD_ENOMEM, "transform workspace allocation failed");
-      }
-      bufs[dev] = {b, need};
-    }
-    p.part = static_cast<float *>(bufs[dev].first);
+    void *b = nullptr;
+    dresd_status s = device_buffer(bufs, dev, need, static_cast<hipStream_t>(stream),
+                                   "transform workspace", &b);
+    if (s != DRESD_OK) return s;
+    p.part = static_cast<float *>(b);
   }
   p.x = x;
   p.mean = mean;
@@ -824,6 +888,7 @@ struct dresd_ivf {
   int32_t P = 0;
   int64_t probe_bytes = 0;       // probe results of the last search: ids + scores
   unsigned char *probe = nullptr;
+  std::vector<void *> retired;   // outgrown probe buffers, freed at destroy
 };
 
 namespace {
@@ -836,6 +901,7 @@ void ivf_free(dresd_ivf *v) {
   if (v->ftok_slot) (void)hipFree(v->ftok_slot);
   if (v->part_tile) (void)hipFree(v->part_tile);
   if (v->probe) (void)hipFree(v->probe);
+  for (void *r : v->retired) (void)hipFree(r);
   delete v;
 }
 
@@ -878,7 +944,7 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   const size_t off_lists = off_lfirst + up(nb * G * 8);
   const size_t off_spill = off_lists + up(nb * G * (size_t)C * 8);
   const size_t bytes = off_spill + up(nb * (size_t)std::max<int64_t>(1, spill_cap) * 8);
-  dresd_status s = ensure_workspace(ix, bytes);
+  dresd_status s = ensure_workspace(ix, bytes, st);
   if (s != DRESD_OK) return s;
   unsigned char *ws = ix->ws;
 
@@ -954,6 +1020,7 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   mp.tokens = tokens;
   mp.cont = ix->cont;
   mp.L = ix->L;
+  mp.N = ix->N;
   mp.final_mode = 1;
   void *margs[] = {&mp};
   DRESD_HIP(launch(merge_kernel_ptr(), dim3((unsigned)B), dim3(kMergeThreads), margs, 0, nullptr,
@@ -970,7 +1037,7 @@ dresd_status validate_ivf_search(const dresd_ivf *v, int32_t B, int32_t k) {
 
 extern "C" {
 
-dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuations, int64_t N,
+static dresd_status ivf_create_impl(const void *embeddings, const int32_t *continuations, int64_t N,
                               int32_t d, int32_t L, int32_t dtype, const float *centroids,
                               int32_t P, const int32_t *assign, dresd_stream stream,
                               dresd_ivf **out) {
@@ -1013,9 +1080,9 @@ dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuatio
     ivf_free(v);
     return s;
   };
-  if (hipMalloc((void **)&v->slot_row, slot.size() * 4) != hipSuccess ||
-      hipMalloc((void **)&v->ftok_slot, slot.size() * 4) != hipSuccess ||
-      hipMalloc((void **)&v->part_tile, pt.size() * 4) != hipSuccess) {
+  if (dev_alloc((void **)&v->slot_row, slot.size() * 4) != hipSuccess ||
+      dev_alloc((void **)&v->ftok_slot, slot.size() * 4) != hipSuccess ||
+      dev_alloc((void **)&v->part_tile, pt.size() * 4) != hipSuccess) {
     (void)hipGetLastError();
     return bail(fail(DRESD_ENOMEM, "slot table allocation failed"));
   }
@@ -1034,7 +1101,7 @@ dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuatio
   std::vector<int32_t> ids((size_t)P);
   for (int32_t p = 0; p < P; ++p) ids[p] = p;
   int32_t *ids_dev = nullptr;
-  if (hipMalloc((void **)&ids_dev, (size_t)P * 4) != hipSuccess) {
+  if (dev_alloc((void **)&ids_dev, (size_t)P * 4) != hipSuccess) {
     (void)hipGetLastError();
     return bail(fail(DRESD_ENOMEM, "allocation failed"));
   }
@@ -1047,6 +1114,19 @@ dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuatio
   if (s != DRESD_OK) return bail(s);
   *out = v;
   return DRESD_OK;
+}
+
+dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuations, int64_t N,
+                              int32_t d, int32_t L, int32_t dtype, const float *centroids,
+                              int32_t P, const int32_t *assign, dresd_stream stream,
+                              dresd_ivf **out) {
+  // the slot table is built on the host: its vectors may fail to allocate
+  try {
+    return ivf_create_impl(embeddings, continuations, N, d, L, dtype, centroids, P, assign, stream,
+                           out);
+  } catch (const std::bad_alloc &) {
+    return fail(DRESD_ENOMEM, "host allocation for the slot table failed");
+  }
 }
 
 void dresd_ivf_destroy(dresd_ivf *v) {
@@ -1086,16 +1166,22 @@ dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t need = (int64_t)B * nprobe * 12;
   if (v->probe_bytes < need) {
-    if (v->probe) {
-      DRESD_HIP(hipDeviceSynchronize());
-      (void)hipFree(v->probe);
-      v->probe = nullptr;
-      v->probe_bytes = 0;
-    }
-    if (hipMalloc((void **)&v->probe, (size_t)need) != hipSuccess) {
+    if (capturing(st))
+      return fail(DRESD_EUNSUPPORTED,
+                  "the probe buffer must grow while the stream is being captured; run one "
+                  "uncaptured call of this shape first");
+    void *p = nullptr;
+    if (dev_alloc(&p, (size_t)need) != hipSuccess) {
       (void)hipGetLastError();
       return fail(DRESD_ENOMEM, "probe buffer allocation failed");
     }
+    if (hipMemset(p, 0, (size_t)need) != hipSuccess) {
+      (void)hipFree(p);
+      return fail(DRESD_EDEVICE, "probe buffer clear failed");
+    }
+    // kept until destroy: a captured graph may still use the outgrown buffer
+    if (v->probe) v->retired.push_back(v->probe);
+    v->probe = static_cast<unsigned char *>(p);
     v->probe_bytes = need;
   }
   int64_t *pid = reinterpret_cast<int64_t *>(v->probe);
@@ -1191,26 +1277,14 @@ dresd_status dresd_kmeans_update(const void *x, int64_t n, int32_t d, int32_t dt
   DRESD_HIP(hipGetDevice(&dev));
   int cus = 0;
   DRESD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-  // Fixed-point sums and counts: a per-device buffer kept for the life of
-  // the process, grown (synchronously) when a larger one is needed.
-  static std::mutex mu;
-  static std::vector<std::pair<void *, size_t>> bufs;
+  // Fixed-point sums and counts (a per-device buffer kept for the life of
+  // the process).
+  static DeviceBuffers bufs;
   const size_t need = (size_t)P * d * 8 + (size_t)P * 4;
-  std::lock_guard<std::mutex> lock(mu);
-  if (bufs.size() <= (size_t)dev) bufs.resize((size_t)dev + 1, {nullptr, 0});
-  if (bufs[dev].second < need) {
-    if (bufs[dev].first) {
-      DRESD_HIP(hipDeviceSynchronize());
-      (void)hipFree(bufs[dev].first);
-      bufs[dev] = {nullptr, 0};
-    }
-    void *b = nullptr;
-    if (hipMalloc(&b, need) != hipSuccess) {
-      (void)hipGetLastError();
-      return fail(DRESD_ENOMEM, "k-means workspace allocation failed");
-    }
-    bufs[dev] = {b, need};
-  }
+  void *wsp = nullptr;
+  dresd_status s = device_buffer(bufs, dev, need, static_cast<hipStream_t>(stream),
+                                 "k-means workspace", &wsp);
+  if (s != DRESD_OK) return s;
   KmeansParams p = {};
   p.x = x;
   p.n = n;
@@ -1220,9 +1294,8 @@ dresd_status dresd_kmeans_update(const void *x, int64_t n, int32_t d, int32_t dt
   p.assign_in = assign;
   p.centroids_out = centroids;
   p.counts = counts;
-  p.sums = static_cast<long long *>(bufs[dev].first);
-  p.cnt = reinterpret_cast<int32_t *>(static_cast<unsigned char *>(bufs[dev].first) +
-                                      (size_t)P * d * 8);
+  p.sums = static_cast<long long *>(wsp);
+  p.cnt = reinterpret_cast<int32_t *>(static_cast<unsigned char *>(wsp) + (size_t)P * d * 8);
   DRESD_HIP(launch_kmeans_update(p, cus, static_cast<hipStream_t>(stream)));
   return DRESD_OK;
 }

@@ -16,6 +16,14 @@ are bit-exact for the returned indices.
   R7  tokens[r, :] == cont[g_idx[r], :] bit for bit
 Also reported (not gating): exact-order agreement and max |g - exact|.
 
+Operand model (``check_operand_model``), per returned element: the device
+score lies within fp32 accumulation error of the exact inner product of the
+row with the query *as the matrix cores take it* (the operand precision the
+library documents for the batch size: the query itself, two bf16 parts, or
+the query rounded once to f16), and within the documented rounding bound of
+the exact inner product with the fp32 query.  This is much tighter than the
+2e-3 tolerance and fails for a truncating or double-rounding conversion.
+
 Searches over a subset of the rows -- next-token-filtered (Section 3.5) or
 partitioned (the probed partitions) -- add: every returned row is in the
 subset, and ranks past the subset's rows -- exactly where the oracle's are --
@@ -158,3 +166,76 @@ def check_batch(g_idx, g_score, g_tok, o_idx, o_score, o_next, exact_of_b, N, co
         "max_abs_vs_exact": max([r["max_abs_vs_exact"] for r in reps], default=0.0),
         "max_abs_vs_oracle": max([r["max_abs_vs_oracle"] for r in reps], default=0.0),
     }
+
+
+def _bf16_rne(x: np.ndarray) -> np.ndarray:
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.bfloat16).to(
+        torch.float32).numpy()
+
+
+def operand_model(q, key_dtype: str, B: int):
+    """The query as the matrix cores take it in a batch of B queries over keys
+    of this storage type, as the library documents it: the query itself for
+    fp32 keys and for 16-bit keys with B <= 4 (three 16-bit parts that sum to
+    it exactly); for larger bf16 batches the high part (the query rounded to
+    nearest-even bf16) plus the remainder rounded the same way; for larger
+    f16 batches the query rounded once to nearest-even f16.  Returns
+    (fp32 array, which it is, relative bound of its difference from q)."""
+    q = np.asarray(q, np.float32)
+    if key_dtype == "f32" or B <= 4:
+        return q.copy(), "exact", 0.0
+    if key_dtype == "f16":
+        return q.astype(np.float16).astype(np.float32), "f16-rounded", 2.0 ** -11
+    hi = _bf16_rne(q)
+    lo = _bf16_rne(q - hi)  # q - hi is exact in fp32
+    return (hi.astype(np.float64) + lo).astype(np.float32), "bf16-two-part", 2.0 ** -17
+
+
+def check_operand_model(g_idx, g_score, q, B, key_dtype, decode_rows, score_with):
+    """Check one query's returned elements against the operand model.
+
+    ``decode_rows(rows) -> float64 [n, d]`` decodes key rows exactly;
+    ``score_with(q_fp32, rows) -> fp32`` is the oracle's score of the rows for
+    an arbitrary fp32 query.  For every returned row x (index >= 0):
+      |g - model|  <= gam * sum_j |qm_j x_j|, qm the modelled query, gam =
+                      (d + 4) 2^-23 (16-bit keys: products exact, at most d + 4
+                      roundings of partial sums, each within 2^-23 of them),
+                      (2 d + 4) 2^-23 for fp32 keys (products rounded too);
+                      with f16 rounding, plus 2^-14 sum |x_j| over the
+                      components below f16's normal range (in case such tiny
+                      components do not keep their subnormal value);
+      |g - exact|  <= rel * sum_j |q_j x_j| + 2^-25 sum_j |x_j| (f16 only)
+                      + the first bound, rel the model's documented relative
+                      error (2^-11 f16-rounded, 2^-17 bf16 two-part, 0 exact).
+    Returns (max |g - model|, max |g - exact|, mode)."""
+    g_idx = np.asarray(g_idx, np.int64)
+    g_score = np.asarray(g_score, np.float32)
+    keep = g_idx >= 0
+    rows = g_idx[keep]
+    if rows.size == 0:
+        return 0.0, 0.0, "empty"
+    q = np.asarray(q, np.float32).reshape(-1)
+    d = q.size
+    qm, mode, rel = operand_model(q[None, :], key_dtype, B)
+    qm = qm[0]
+    x = np.abs(decode_rows(rows))
+    Sm = x @ np.abs(qm.astype(np.float64))
+    Sq = x @ np.abs(q.astype(np.float64))
+    A = x.sum(axis=1)
+    gam = (2 * d + 4 if key_dtype == "f32" else d + 4) * 2.0 ** -23
+    tiny = (np.abs(q) < 2.0 ** -14) if mode == "f16-rounded" else np.zeros(d, bool)
+    bound_m = gam * Sm + 2.0 ** -14 * (x[:, tiny].sum(axis=1) if tiny.any() else 0.0)
+    bound_e = rel * Sq + (2.0 ** -25 * A if mode == "f16-rounded" else 0.0) + bound_m
+    g = g_score[keep].astype(np.float64)
+    dm = np.abs(g - score_with(qm, rows).astype(np.float64))
+    de = np.abs(g - score_with(q, rows).astype(np.float64))
+    if np.any(dm > bound_m):
+        r = int(np.argmax(dm - bound_m))
+        raise ParityError("operand model (%s): row %d |g - model| %.3e > bound %.3e"
+                          % (mode, int(rows[r]), dm[r], bound_m[r]))
+    if np.any(de > bound_e):
+        r = int(np.argmax(de - bound_e))
+        raise ParityError("operand model (%s): row %d |g - exact| %.3e > bound %.3e"
+                          % (mode, int(rows[r]), de[r], bound_e[r]))
+    return float(dm.max()), float(de.max()), mode

@@ -180,3 +180,62 @@ def test_partitioned_row_outside_probes_fails():
     gt[0, -1] = cont[bad]
     with pytest.raises(ParityError):
         check_batch(gi, gs, gt, oi, os_, on, ex, N, cont, 1e-5, admitted_b=adm)
+
+
+# Operand model: a device that rounds the query as documented passes; one
+# whose conversion truncates, or rounds twice (through bf16 first), fails.
+def _model_case(dtype_name, B):
+    w = WORKLOADS[dtype_name].scaled(4000)
+    g = generate(w, "cpu")
+    keys, dt = to_numpy_bits(g["keys"])
+    q = g["queries"][:B].numpy()
+    x = oracle.decode_keys(keys, dt)
+    return keys, dt, q, x
+
+
+def _scores(x, qeff, rows):
+    # what a device computing exactly with operand qeff would return
+    return (x[rows] @ qeff.astype(np.float64)).astype(np.float32)
+
+
+def _f16_trunc(q):
+    # round toward zero to f16 (a truncating conversion)
+    r = q.astype(np.float16)
+    over = np.abs(r.astype(np.float32)) > np.abs(q)
+    step = np.nextafter(r, np.float16(0))
+    return np.where(over, step, r).astype(np.float32)
+
+
+@pytest.mark.parametrize("wl,B", [("batch10m_d256_f16", 64), ("zipf33m_d128_f16", 128),
+                                  ("hidden1m_d4096_bf16", 8), ("pca4m_d1024_f16", 4)])
+def test_operand_model_accepts_documented_rounding(wl, B):
+    from parity import check_operand_model, operand_model
+    keys, dt, q, x = _model_case(wl, min(B, 8))
+    for b in range(q.shape[0]):
+        rows = np.arange(0, 4000, 97)
+        qm, _, _ = operand_model(q[b][None, :], dt, B)
+        g = _scores(x, qm[0], rows)
+        check_operand_model(rows, g, q[b], B, dt, lambda r: x[r],
+                            lambda qq, r: oracle.score_rows(keys, dt, qq, r))
+
+
+@pytest.mark.parametrize("bad", ["truncate", "twice"])
+def test_operand_model_rejects_wrong_f16_rounding(bad):
+    from parity import check_operand_model
+    keys, dt, q, x = _model_case("zipf33m_d128_f16", 8)
+    rows = np.arange(0, 4000, 7)
+    failed = 0
+    for b in range(q.shape[0]):
+        if bad == "truncate":
+            qe = _f16_trunc(q[b])
+        else:  # through bf16 first, then f16
+            import torch
+            qb = torch.from_numpy(q[b]).to(torch.bfloat16).to(torch.float32).numpy()
+            qe = qb.astype(np.float16).astype(np.float32)
+        g = _scores(x, qe, rows)
+        try:
+            check_operand_model(rows, g, q[b], 128, dt, lambda r: x[r],
+                                lambda qq, r: oracle.score_rows(keys, dt, qq, r))
+        except ParityError:
+            failed += 1
+    assert failed == q.shape[0]

@@ -1,0 +1,272 @@
+"""Failure paths through the C ABI: allocation failures return DRESD_ENOMEM,
+write nothing and leak nothing; a workspace never grows inside a stream
+capture; a workspace outgrown after a capture stays valid for that graph.
+
+Allocation failures are driven by the library's DRESD_FAIL_ALLOC_AT hook
+(the n-th device allocation fails as out of memory), one test per
+allocation of index creation, search and partitioned-index creation, plus a
+real failure: a datastore larger than any device.
+"""
+import ctypes
+import os
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+OK, EINVAL, ENOMEM, EDEVICE, EUNSUPPORTED = 0, 1, 2, 3, 4
+P = ctypes.c_void_p
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+class fail_alloc_at:
+    """Make the n-th device allocation of the library fail."""
+
+    def __init__(self, n):
+        self.n = n
+
+    def __enter__(self):
+        os.environ["DRESD_FAIL_ALLOC_AT"] = str(self.n)
+        return self
+
+    def __exit__(self, *exc):
+        os.environ.pop("DRESD_FAIL_ALLOC_AT", None)
+        return False
+
+
+def free_bytes():
+    torch.cuda.synchronize()
+    return torch.cuda.mem_get_info()[0]
+
+
+def datastore(N=1 << 17, d=256, L=10, dtype=torch.float16, seed=0):
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    x = torch.randn(N, d, device=DEV, generator=gen)
+    x = (x / x.norm(dim=1, keepdim=True)).to(dtype)
+    cont = torch.randint(0, 32000, (N, L), device=DEV, generator=gen, dtype=torch.int32)
+    q = torch.randn(64, d, device=DEV, generator=gen)
+    q = q / q.norm(dim=1, keepdim=True)
+    return x, cont, q
+
+
+def create(lib, x, cont, code=1):
+    h = P()
+    st = lib.dresd_index_create(P(x.data_ptr()), P(cont.data_ptr()), x.shape[0], x.shape[1],
+                                cont.shape[1], code, None, ctypes.byref(h))
+    return st, h
+
+
+def outputs(B, k, L):
+    return (torch.full((B, k), -7, dtype=torch.int64, device=DEV),
+            torch.full((B, k), 7.0, dtype=torch.float32, device=DEV),
+            torch.full((B, k, L), -7, dtype=torch.int32, device=DEV))
+
+
+def search(lib, h, q, out):
+    idx, score, tok = out
+    B, k = idx.shape
+    st = lib.dresd_search(h, P(q.data_ptr()), B, k, P(idx.data_ptr()), P(score.data_ptr()),
+                          P(tok.data_ptr()), None)
+    torch.cuda.synchronize()
+    return st, out
+
+
+@pytest.fixture(scope="module", autouse=True)
+def warm(gpu_lib):
+    """One full cycle first, so that the library's kernels are loaded before
+    any free-memory comparison."""
+    x, cont, q = datastore(N=4096)
+    st, h = create(gpu_lib, x, cont)
+    assert st == OK
+    st, _ = search(gpu_lib, h, q[:8], outputs(8, 16, cont.shape[1]))
+    assert st == OK
+    gpu_lib.dresd_index_destroy(h)
+    st, h = ivf_create(gpu_lib, x, cont)
+    assert st == OK
+    gpu_lib.dresd_ivf_destroy(h)
+    torch.cuda.synchronize()
+
+
+def untouched(out):
+    idx, score, tok = out
+    return bool((idx == -7).all() and (score == 7.0).all() and (tok == -7).all())
+
+
+def test_datastore_larger_than_the_device(gpu_lib):
+    """N at the limit with 16,384 fp32 dims: ~281 TB of keys."""
+    x, cont, _ = datastore(N=64, d=64)
+    before = free_bytes()
+    h = P()
+    st = gpu_lib.dresd_index_create(P(x.data_ptr()), P(cont.data_ptr()), 4294967040, 16384, 10,
+                                    0, None, ctypes.byref(h))
+    assert st == ENOMEM, gpu_lib.dresd_last_error()
+    assert h.value is None
+    assert free_bytes() == before
+
+
+@pytest.mark.parametrize("n,what", [(1, "keys"), (2, "continuations"), (3, "first tokens")])
+def test_index_create_allocation_failure(gpu_lib, n, what):
+    x, cont, _ = datastore()
+    before = free_bytes()
+    with fail_alloc_at(n):
+        st, h = create(gpu_lib, x, cont)
+    say("create, allocation %d (%s) fails: status %d, %s" % (n, what, st,
+                                                             gpu_lib.dresd_last_error().decode()))
+    assert st == ENOMEM and h.value is None
+    assert free_bytes() == before
+    with fail_alloc_at(4):  # index creation makes three allocations
+        st, h = create(gpu_lib, x, cont)
+    assert st == OK
+    gpu_lib.dresd_index_destroy(h)
+    assert free_bytes() == before
+
+
+def test_search_workspace_allocation_failure(gpu_lib):
+    x, cont, q = datastore()
+    st, h = create(gpu_lib, x, cont)
+    assert st == OK
+    out = outputs(8, 16, cont.shape[1])
+    after_create = free_bytes()
+    with fail_alloc_at(1):
+        st, out = search(gpu_lib, h, q[:8], out)
+    assert st == ENOMEM, gpu_lib.dresd_last_error()
+    assert untouched(out)
+    assert free_bytes() == after_create
+    st, out = search(gpu_lib, h, q[:8], out)
+    assert st == OK and (out[0] >= 0).all()
+    gpu_lib.dresd_index_destroy(h)
+
+
+def _ivf_inputs(x):
+    N = x.shape[0]
+    Pn = 64
+    cents = x[:Pn].float()
+    assign = (torch.arange(N, device=DEV, dtype=torch.int32) % Pn).contiguous()
+    return cents.contiguous(), assign, Pn
+
+
+def ivf_create(lib, x, cont, parts=None):
+    cents, assign, Pn = parts or _ivf_inputs(x)
+    h = P()
+    st = lib.dresd_ivf_create(P(x.data_ptr()), P(cont.data_ptr()), x.shape[0], x.shape[1],
+                              cont.shape[1], 1, P(cents.data_ptr()), Pn, P(assign.data_ptr()),
+                              None, ctypes.byref(h))
+    return st, h
+
+
+# partitioned-index creation: slot table (3), keys and continuations (2), the
+# partition ids (1), the centroid index (3)
+IVF_ALLOCS = 9
+
+
+@pytest.mark.parametrize("n", list(range(1, IVF_ALLOCS + 1)))
+def test_ivf_create_allocation_failure(gpu_lib, n):
+    x, cont, _ = datastore(N=1 << 16)
+    parts = _ivf_inputs(x)
+    before = free_bytes()
+    with fail_alloc_at(n):
+        st, h = ivf_create(gpu_lib, x, cont, parts)
+    say("ivf create, allocation %d fails: status %d, %s" % (n, st,
+                                                            gpu_lib.dresd_last_error().decode()))
+    assert st == ENOMEM and h.value is None
+    assert free_bytes() == before
+
+
+def test_ivf_create_allocation_count(gpu_lib):
+    x, cont, _ = datastore(N=1 << 16)
+    parts = _ivf_inputs(x)
+    before = free_bytes()
+    with fail_alloc_at(IVF_ALLOCS + 1):
+        st, h = ivf_create(gpu_lib, x, cont, parts)
+    assert st == OK
+    gpu_lib.dresd_ivf_destroy(h)
+    assert free_bytes() == before
+
+
+@pytest.mark.parametrize("n,what", [(1, "probe buffer"), (2, "centroid-search workspace"),
+                                    (3, "partition-scan workspace")])
+def test_ivf_search_allocation_failure(gpu_lib, n, what):
+    x, cont, q = datastore(N=1 << 16)
+    st, h = ivf_create(gpu_lib, x, cont)
+    assert st == OK
+    B, k, nprobe, L = 4, 10, 8, cont.shape[1]
+    idx, score, tok = outputs(B, k, L)
+    args = (h, P(q.data_ptr()), B, k, nprobe, P(idx.data_ptr()), P(score.data_ptr()),
+            P(tok.data_ptr()), None)
+    with fail_alloc_at(n):
+        st = gpu_lib.dresd_ivf_search(*args)
+    torch.cuda.synchronize()
+    say("ivf search, allocation %d (%s) fails: status %d" % (n, what, st))
+    assert st == ENOMEM
+    assert untouched((idx, score, tok))
+    st = gpu_lib.dresd_ivf_search(*args)
+    torch.cuda.synchronize()
+    assert st == OK and (idx >= 0).all()
+    gpu_lib.dresd_ivf_destroy(h)
+
+
+def test_no_workspace_growth_inside_capture(gpu_lib):
+    """A search shape never run before needs a larger workspace: inside a
+    stream capture the call refuses (EUNSUPPORTED) and records nothing."""
+    x, cont, q = datastore()
+    st, h = create(gpu_lib, x, cont)
+    assert st == OK
+    s = torch.cuda.Stream()
+    B, k, L = 32, 16, cont.shape[1]
+    idx = torch.empty((B, k), dtype=torch.int64, device=DEV)
+    score = torch.empty((B, k), dtype=torch.float32, device=DEV)
+    qq = q[:B].contiguous()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        st = gpu_lib.dresd_search(h, P(qq.data_ptr()), B, k, P(idx.data_ptr()),
+                                  P(score.data_ptr()), None, P(s.cuda_stream))
+    torch.cuda.synchronize()
+    assert st == EUNSUPPORTED, gpu_lib.dresd_last_error()
+    assert b"captured" in gpu_lib.dresd_last_error()
+    gpu_lib.dresd_index_destroy(h)
+
+
+def test_graph_survives_later_workspace_growth(gpu_lib):
+    """A graph captured at B = 1 still replays correctly after a larger
+    eager search has grown (replaced) the index's workspace: the outgrown
+    workspace is kept until the index is destroyed."""
+    from paper_2502_15572_amd import Index
+    x, cont, q = datastore()
+    ix = Index(x, cont)
+    s = torch.cuda.Stream()
+    k, L = 10, cont.shape[1]
+    q1 = q[:1].contiguous()
+    out = (torch.empty((1, k), dtype=torch.int64, device=DEV),
+           torch.empty((1, k), dtype=torch.float32, device=DEV),
+           torch.empty((1, k, L), dtype=torch.int32, device=DEV))
+    with torch.cuda.stream(s):
+        ix.search(q1, k, out=out, stream=s)  # warm-up sizes the workspace for B = 1
+    torch.cuda.synchronize()
+    want = [t.clone() for t in out]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        ix.search(q1, k, out=out, stream=s)
+    torch.cuda.synchronize()
+    ws1 = ix.plan(1, k)["workspace_bytes"]
+    ws64 = ix.plan(64, 32)["workspace_bytes"]
+    assert ws64 > ws1
+    before = free_bytes()
+    big = ix.search(q[:64].contiguous(), 32)  # grows the workspace
+    torch.cuda.synchronize()
+    # the new workspace was allocated and the outgrown one not returned
+    assert before - free_bytes() >= ws64 - (2 << 20)
+    for t in out:
+        t.fill_(0)
+    for _ in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(out, want):
+            assert torch.equal(a, b)
+    assert (big[0] >= 0).all()
+    ix.close()

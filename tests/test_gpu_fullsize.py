@@ -1,13 +1,14 @@
 """Parity at the workloads' full sizes, in the launch configuration bench.py
 times (same index build, same plans).
 
-The oracle computes the full top-k for a sample of the batch's queries over
-the whole datastore (host copy of the same keys); for every query of the
-batch the returned rows are re-scored one by one by the oracle and checked
-for order, range, bit-exact tokens and score agreement.
+Every query of every batch is compared with the oracle's own exact top-k
+over the whole datastore (host copy of the same keys; one batched oracle call
+per case, each key row read once for all queries): rules R1-R7, and every
+returned score against the operand model (the query as the matrix cores take
+it for that batch size) within fp32 accumulation error, and against the
+exact score within the documented rounding bound.  Printed per case: the
+exact-order rate, max |g - exact| and max |g - model|.
 """
-import os
-import sys
 import time
 
 import numpy as np
@@ -16,11 +17,10 @@ import torch
 
 import oracle
 from datagen import WORKLOADS, generate, to_numpy_bits
-from parity import TOL, check_batch, check_query
+from parity import TOL, check_batch, check_operand_model
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-SAMPLED = 2  # queries per batch checked against the oracle's full top-k
 
 
 def say(*a):
@@ -67,20 +67,17 @@ def test_fullsize(built, name, B):
     gi, gs, gt = idx.cpu().numpy(), score.cpu().numpy(), tok.cpu().numpy()
     qn = q.cpu().numpy()
     tol = TOL[dt]
-    # every query: order, range, distinctness, tokens, scores vs exact
-    for b in range(B):
-        ex = oracle.score_rows(kb, dt, qn[b], gi[b])
-        assert np.all(np.diff(gs[b].astype(np.float64)) <= 0)
-        assert gi[b].min() >= 0 and gi[b].max() < w.N and np.unique(gi[b]).size == w.k
-        assert np.array_equal(gt[b], cont[gi[b]])
-        assert np.max(np.abs(gs[b].astype(np.float64) - ex)) <= tol
-    # sampled queries: full comparison with the oracle's own top-k
-    pick = sorted({0, B - 1})[:SAMPLED]
     t = time.time()
-    o_idx, o_score, _, o_next = oracle.topk(kb, dt, qn[pick], w.k, cont)
-    say("  oracle %d queries in %.1fs" % (len(pick), time.time() - t))
-    rep = check_batch(gi[pick], gs[pick], gt[pick], o_idx, o_score, o_next,
-                      lambda bb, rows: oracle.score_rows(kb, dt, qn[pick[bb]], rows), w.N, cont,
-                      tol)
-    say("  exact-order %.2f max|g-exact| %.2e" % (rep["exact_order_rate"],
-                                                   rep["max_abs_vs_exact"]))
+    say("  oracle over all %d queries ..." % B)
+    o_idx, o_score, _, o_next = oracle.topk(kb, dt, qn, w.k, cont)
+    say("  oracle %d queries in %.1fs" % (B, time.time() - t))
+    rep = check_batch(gi, gs, gt, o_idx, o_score, o_next,
+                      lambda bb, rows: oracle.score_rows(kb, dt, qn[bb], rows), w.N, cont, tol)
+    dm_max, mode = 0.0, ""
+    for b in range(B):
+        dm, _de, mode = check_operand_model(
+            gi[b], gs[b], qn[b], B, dt, lambda r: oracle.decode_keys(kb[r], dt),
+            lambda qq, r: oracle.score_rows(kb, dt, qq, r))
+        dm_max = max(dm_max, dm)
+    say("  %s B=%d: exact-order %.3f max|g-exact| %.2e max|g-model| %.2e (%s)"
+        % (name, B, rep["exact_order_rate"], rep["max_abs_vs_exact"], dm_max, mode))

@@ -16,7 +16,7 @@ import torch
 
 import oracle
 from datagen import WORKLOADS, generate, to_numpy_bits
-from parity import TOL, check_batch
+from parity import TOL, check_batch, check_operand_model
 
 pytestmark = pytest.mark.gpu
 
@@ -47,6 +47,14 @@ def run_case(gpu_lib, keys, cont, queries, k, dtype, tol=None, strict_report=Fal
     rep = check_batch(g_idx, g_score, g_tok, o_idx, o_score, o_next,
                       lambda b, rows: oracle.score_rows(kb, dt, qn[b], rows), kb.shape[0], cn,
                       TOL[dt] if tol is None else tol)
+    # every returned score against the documented operand precision
+    B = qn.shape[0]
+    for b in range(B):
+        dm, de, mode = check_operand_model(
+            g_idx[b], g_score[b], qn[b], B, dt, lambda r: oracle.decode_keys(kb[r], dt),
+            lambda qq, r: oracle.score_rows(kb, dt, qq, r))
+        rep["max_abs_vs_model"] = max(rep.get("max_abs_vs_model", 0.0), dm)
+        rep["operand"] = mode
     ix.close()
     return rep, (g_idx, g_score, g_tok)
 
@@ -88,8 +96,9 @@ def test_workload_parity_reduced(gpu_lib, name, N, _):
     for B in w.batches:
         say("parity", name, "N=%d B=%d k=%d" % (N, B, w.k))
         rep, _r = run_case(gpu_lib, g["keys"], g["cont"], g["queries"][:B], w.k, w.dtype)
-        say("  exact-order rate %.3f, max |g-exact| %.2e" % (rep["exact_order_rate"],
-                                                           rep["max_abs_vs_exact"]))
+        say("  exact-order rate %.3f, max |g-exact| %.2e, max |g-model| %.2e (%s)"
+            % (rep["exact_order_rate"], rep["max_abs_vs_exact"], rep["max_abs_vs_model"],
+               rep["operand"]))
         # split-query paths are within summation error of the oracle
         if w.dtype in ("f32", "bf16") or B <= 4:
             assert rep["max_abs_vs_exact"] <= 1e-5, rep

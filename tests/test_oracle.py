@@ -103,6 +103,32 @@ def pin_decode_bf16_all_patterns():
     assert np.array_equal(got, t[ok])
 
 
+def pin_decode_keys_all_patterns():
+    """The fp64 decoder that feeds the k-means, partitioned and pipeline
+    oracles, over every 16-bit pattern: f16 against numpy's binary16 (as bits
+    and as float16 values), bf16 against torch's bfloat16, and both against
+    the C decoder's scores of the same rows for a unit query."""
+    bits = np.arange(65536, dtype=np.uint16)
+    f16 = bits.view(np.float16).astype(np.float64)
+    bf16 = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    for dt, want in (("f16", f16), ("bf16", bf16)):
+        got = oracle.decode_keys(bits.reshape(-1, 1), dt).reshape(-1)
+        assert got.dtype == np.float64
+        assert np.array_equal(np.isnan(got), np.isnan(want)), dt
+        ok = ~np.isnan(want)
+        assert np.array_equal(got[ok], want[ok]), dt
+        assert np.array_equal(np.signbit(got[ok]), np.signbit(want[ok])), dt  # -0.0 kept
+        fin = np.isfinite(want)
+        c = oracle.score_rows(bits[fin].reshape(-1, 1), dt, np.ones(1, np.float32),
+                              np.arange(int(fin.sum())))
+        assert np.array_equal(c.astype(np.float64), got[fin]), dt
+    vals = bits.view(np.float16)
+    assert np.array_equal(oracle.decode_keys(vals.reshape(-1, 1), "f16").reshape(-1)[~np.isnan(f16)],
+                          f16[~np.isnan(f16)])
+    x = np.random.default_rng(5).standard_normal((7, 3)).astype(np.float32)
+    assert np.array_equal(oracle.decode_keys(x, "f32"), x.astype(np.float64))
+
+
 def _c1_like(N=4096):
     w = WORKLOADS["flat16k_d256_f32"].scaled(N)
     return w, generate(w, "cpu")
@@ -265,7 +291,7 @@ def test_filter_pin(pin):
 
 
 PINS = [pin_golden_closed_forms, pin_exact_bruteforce, pin_decode_f16_all_patterns,
-        pin_decode_bf16_all_patterns, pin_invariants_and_self_match, pin_self_match_16bit,
+        pin_decode_bf16_all_patterns, pin_decode_keys_all_patterns, pin_invariants_and_self_match, pin_self_match_16bit,
         pin_duplicates_and_mrr, pin_structural_continuations, pin_full_sort_permutation]
 
 
