@@ -7,7 +7,14 @@ cycling through the workload's query pool.  Inputs are resident in HBM before
 the timed region starts.  Prints one JSON line.
 
 Default workload: 1,048,576 keys x 4096 dims bf16 (a 7B model's hidden width),
-continuations [N,10], B = 1 query per step, k = 10.
+continuations [N,10], B = 1 query per step, k = 10.  The default run also
+measures, in the same JSON line under "secondary", the 33.5M x 128 f16
+datastore at B = 1 and B = 128 (k = 100) and the 10M x 256 f16 datastore at
+B = 256 (k = 32), each with its own roofline block; the achievable read
+bandwidth of the device (a probe with the scans' access pattern) is measured
+on the same run and each bandwidth is also given as a fraction of it.  The
+CPU-baseline leg times the oracle and checks query 0 of every measured
+workload against it (outside the timed regions).
 """
 from __future__ import annotations
 
@@ -99,27 +106,62 @@ def copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
 
 
-def cpu_baseline(keys_dev, queries, k, budget_s=12.0):
-    """The oracle (untuned) on this host's cores over a bounded query sample."""
+def cpu_baseline_leg(keys_dev, cont_dev, queries, k, device_result, budget_s=12.0, time_it=True):
+    """The oracle (untuned) on this host's cores.  Checks the device's result
+    for queries[0] against the oracle's exact top-k (rules R1-R7 of the
+    parity tests; outside every timed region) and, with ``time_it``, times
+    single-query oracle searches over a bounded sample.  Returns
+    (cpu_baseline dict or None, parity dict)."""
     import numpy as np
     import oracle
     from datagen import to_numpy_bits
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import TOL, ParityError, check_query
     threads = len(os.sched_getaffinity(0))
     t0 = time.time()
     kb, dt = to_numpy_bits(keys_dev)
+    cont = cont_dev.cpu().numpy()
     log("cpu_baseline: host copy of keys %.1fs" % (time.time() - t0))
     q = queries.cpu().numpy().astype(np.float32)
-    oracle.topk(kb, dt, q[:1], k, threads=threads)  # page the keys in, untimed
-    done, t = 0, time.time()
-    while time.time() - t < budget_s:
-        b = done % q.shape[0]
-        oracle.topk(kb, dt, q[b:b + 1], k, threads=threads)  # B = 1, as the metric
-        done += 1
-    el = time.time() - t
+    o_idx, o_score, _, o_next = oracle.topk(kb, dt, q[:1], k, cont, threads=threads)
+    g_idx, g_score, g_tok = (t[0].cpu().numpy() for t in device_result)
+    parity = {"queries_checked": 1, "against": "oracle exact top-k (fp64 sums rounded once)"}
+    try:
+        rep = check_query(g_idx, g_score, g_tok, o_idx[0], o_score[0], o_next[0],
+                          lambda rows: oracle.score_rows(kb, dt, q[0], rows), kb.shape[0], cont,
+                          TOL[dt])
+        parity.update({"verdict": "pass", "tol": TOL[dt], "exact_order": rep["exact_order"],
+                       "max_abs_vs_exact": rep["max_abs_vs_exact"]})
+    except ParityError as e:
+        parity.update({"verdict": "FAIL", "tol": TOL[dt], "error": str(e)})
+    base = None
+    if time_it:
+        done, t = 0, time.time()
+        while time.time() - t < budget_s:
+            b = done % q.shape[0]
+            oracle.topk(kb, dt, q[b:b + 1], k, threads=threads)  # B = 1, as the metric
+            done += 1
+        el = time.time() - t
+        base = {"value": done / el, "unit": "queries/s", "cores": threads, "kind": "oracle",
+                "sample": "%d single-query searches over the full datastore (cycling the query "
+                          "pool) in %.1f s, after one untimed search (the parity check of "
+                          "query 0)" % (done, el)}
     del kb
-    return {"value": done / el, "unit": "queries/s", "cores": threads, "kind": "oracle",
-            "sample": "%d single-query searches over the full datastore (cycling the query "
-                      "pool) in %.1f s, after one untimed warm-up search" % (done, el)}
+    return base, parity
+
+
+def bandwidth_probe(buf):
+    """Achievable read bandwidth (GB/s): the library's probe over `buf` with
+    the scans' access pattern, best over a few grid sizes."""
+    import torch
+    from paper_2502_15572_amd import bw_probe
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    best, per = 0.0, {}
+    for wpc in (1, 2, 4, 8):
+        gbps = bw_probe(buf, reps=10, workgroups=wpc * cus)
+        per["%d_per_cu" % wpc] = gbps
+        best = max(best, gbps)
+    return best, per
 
 
 def time_transform(args):
@@ -379,7 +421,12 @@ def main():
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--k", type=int, default=0, help="default: the workload's k")
     ap.add_argument("--n", type=int, default=0, help="override N (reduced runs; not a bench line)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the CPU-baseline leg (oracle timing and parity verdicts)")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="default run only: skip the secondary workloads")
+    ap.add_argument("--bw-probe", action="store_true",
+                    help="only measure the achievable read bandwidth (8 GiB buffer)")
     ap.add_argument("--filtered", action="store_true",
                     help="next-token-filtered search: each query's next token is the first "
                          "token of its source row's continuation (the most frequent first "
@@ -412,6 +459,14 @@ def main():
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
         return
+    if args.bw_probe:
+        import torch
+        buf = torch.ones((8 << 30) // 4, dtype=torch.float32, device="cuda")
+        best, per = bandwidth_probe(buf)
+        print(json.dumps({"bw_probe": {"buffer_bytes": 8 << 30, "best_GBps": best,
+                                       "frac_of_spec": best / HBM_PEAK_GBPS, "per_grid": per}}),
+              flush=True)
+        return
     if args.pipeline:
         time_pipeline(args)
         return
@@ -426,25 +481,69 @@ def main():
         return
 
     import torch
-    from datagen import WORKLOADS, generate
-    from paper_2502_15572_amd import Index
+    from datagen import WORKLOADS
 
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
     w = WORKLOADS[args.workload]
     if args.n:
         w = w.scaled(args.n)
-    k = args.k or w.k
-    B = args.batch
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
+    secondary = (not args.no_secondary and not args.n and not args.filtered and B_default(args)
+                 and args.workload == DEFAULT_WORKLOAD)
+    want_cpu = not args.no_cpu_baseline and not args.n
+    res, peak = measure(w, args.batch, args.k or w.k, args, dev, probe=not args.n,
+                        cpu=want_cpu, time_cpu=want_cpu and args.batch == 1 and not args.filtered)
+    if secondary:
+        res["secondary"] = []
+        cache = {}
+        for name, B in SECONDARY:
+            ws = WORKLOADS[name]
+            r, _ = measure(ws, B, ws.k, args, dev, cpu=want_cpu, time_cpu=False,
+                           measured_peak=peak, cache=cache)
+            res["secondary"].append(r)
+        if cache.get("ix") is not None:
+            cache["ix"].close()
+        cache.clear()
+    print(json.dumps(res), flush=True)
 
-    t0 = time.time()
-    g = generate(w, dev)
-    torch.cuda.synchronize()
-    log("generated %s N=%d d=%d %s in %.1fs" % (w.name, w.N, w.d, w.dtype, time.time() - t0))
-    t0 = time.time()
-    ix = Index(g["keys"], g["cont"])
-    build_s = time.time() - t0
-    log("index built in %.2fs" % build_s)
+
+# Secondary results of the default run: the datastore nearest to the paper's
+# (33.5M keys, 128 dims, Zipf-sized clusters) at one query per step and at a
+# 128-query batch, and the 10M x 256 datastore at 256 queries (the matrix-core
+# regime).
+SECONDARY = [("zipf33m_d128_f16", 1), ("zipf33m_d128_f16", 128), ("batch10m_d256_f16", 256)]
+
+
+def B_default(args):
+    return args.batch == 1 and not args.k
+
+
+def measure(w, B, k, args, dev, probe=False, cpu=False, time_cpu=False, measured_peak=None,
+            cache=None):
+    """Time `args.steps` searches of B queries on workload w (after
+    `args.warmup`), with the library's per-kernel events for the main scan
+    and the whole search.  Returns (result dict, measured read peak GB/s)."""
+    import torch
+    from datagen import generate
+    from paper_2502_15572_amd import Index
+
+    if cache is not None and cache.get("name") == w.name:
+        g, ix, build_s = cache["g"], cache["ix"], cache["build_s"]
+    else:
+        if cache is not None and cache.get("ix") is not None:
+            cache["ix"].close()
+            cache.clear()
+            torch.cuda.empty_cache()
+        t0 = time.time()
+        g = generate(w, dev)
+        torch.cuda.synchronize()
+        log("generated %s N=%d d=%d %s in %.1fs" % (w.name, w.N, w.d, w.dtype, time.time() - t0))
+        t0 = time.time()
+        ix = Index(g["keys"], g["cont"])
+        build_s = time.time() - t0
+        log("index built in %.2fs" % build_s)
+        if cache is not None:
+            cache.update(name=w.name, g=g, ix=ix, build_s=build_s)
     pool = g["queries"]
     nb = max(1, pool.shape[0] // B)
     batches = [pool[(i % nb) * B:(i % nb) * B + B].contiguous() for i in range(nb)]
@@ -466,7 +565,7 @@ def main():
     torch.cuda.synchronize()
 
     # Timed region: K back-to-back searches; the library times its main scan
-    # kernel with events tied to that kernel's dispatch.
+    # kernel and each whole search with events tied to kernels' dispatches.
     ix.profile(True)
     ix.profile_read()  # clear
     torch.cuda.synchronize()
@@ -479,6 +578,15 @@ def main():
     ix.profile(False)
     p50, p90 = search_latency(lambda i: ix.search(batches[i % nb], k, out=out,
                                                   next_tok=tok_batches[i % nb]), args.steps)
+    # the result that the CPU-baseline leg checks: the first batch
+    checked = tuple(t.clone() for t in ix.search(batches[0], k, next_tok=tok_batches[0]))
+    torch.cuda.synchronize()
+
+    peak = measured_peak
+    probe_detail = None
+    if probe:
+        peak, probe_detail = bandwidth_probe(g["keys"])
+        log("bandwidth probe: %.0f GB/s" % peak)
 
     s = w.elem_bytes
     scan_bytes = w.N * w.d * s + B * w.d * 4           # keys once + queries
@@ -486,6 +594,7 @@ def main():
         scan_bytes += w.N * 4 + B * 4                  # first-token column + next tokens
     search_bytes = scan_bytes + B * k * (8 + 4 + 4 * w.L)
     scan_ms = prof["scan_ms"] / max(1, prof["searches"])
+    search_ms = prof["search_ms"] / max(1, prof["searches"])
     achieved = scan_bytes / (scan_ms * 1e-3) / 1e9
     flops = 2.0 * w.N * w.d * B
     plan = ix.plan(B, k)
@@ -494,6 +603,7 @@ def main():
     mfma_peak = MFMA_PEAK_TFLOPS[w.dtype] * 1e12
     mfma_bound = flops / mfma_peak > scan_bytes / (HBM_PEAK_GBPS * 1e9)
     traffic = read_traffic(w.name, B, plan["scan_kernel"]) if not args.n else None
+    search_gbps = search_bytes / (search_ms * 1e-3) / 1e9
 
     res = {
         "metric": "retrieval queries/s + p50 latency at B=1; achieved HBM GB/s vs peak",
@@ -531,14 +641,30 @@ def main():
             "avg_launch_ms": scan_ms,
             "hbm_GBps": achieved,
             "hbm_frac": achieved / HBM_PEAK_GBPS,
+            "hbm_frac_of_measured_peak": (achieved / peak) if peak else None,
             "mfma_util": flops / (scan_ms * 1e-3) / mfma_peak,
+            # the whole search (sampled passes, main scan, merges, gather)
+            "search_ms": search_ms,
+            "search_hbm_GBps": search_gbps,
+            "search_hbm_frac": search_gbps / HBM_PEAK_GBPS,
         },
     }
-    if not args.no_cpu_baseline and not args.n and B == 1 and not args.filtered:
-        log("timing the oracle on the host ...")
-        res["cpu_baseline"] = cpu_baseline(g["keys"], pool, k)
-    ix.close()
-    print(json.dumps(res), flush=True)
+    if probe:
+        res["measured_read_peak"] = {"GBps": peak, "frac_of_spec": peak / HBM_PEAK_GBPS,
+                                     "kernel": "dresd_bw_read", "buffer_bytes":
+                                     g["keys"].numel() * g["keys"].element_size(),
+                                     "per_grid": probe_detail}
+    if cpu:
+        log("oracle on the host (%s B=%d) ..." % (w.name, B))
+        # query 0 of the checked batch is pool[0]; the timing cycles the pool
+        base, parity = cpu_baseline_leg(g["keys"], g["cont"], pool, k, checked,
+                                        time_it=time_cpu)
+        res["parity"] = parity
+        if base is not None:
+            res["cpu_baseline"] = base
+    if cache is None:
+        ix.close()
+    return res, peak
 
 
 if __name__ == "__main__":

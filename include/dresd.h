@@ -182,6 +182,25 @@ dresd_status dresd_profile_read(dresd_index *ix, double *scan_ms,
                                 double *search_ms, int64_t *searches);
 
 /*
+ * Measurement support: the achievable HBM read bandwidth of the device with
+ * the scans' access pattern (every wave streams one contiguous range in
+ * 1 KiB wave loads, 16 nontemporal loads in flight), the ceiling against
+ * which a scan's bandwidth is judged beside the spec sheet's figure.
+ *
+ *   buf         device, `bytes` readable bytes (contents do not matter;
+ *               only read).
+ *   bytes       a multiple of 1024, at least 1 MiB (use far more than the
+ *               last-level caches, e.g. several GiB).
+ *   reps        1 <= reps <= 1000 timed read passes, after one untimed pass.
+ *   workgroups  workgroups of 4 waves (0: four per compute unit).
+ *   ms          host; mean device milliseconds per pass (HIP events).
+ * Synchronises `stream`.  Allocates nothing on the device.
+ * Errors: EINVAL (null pointer, sizes out of range), EDEVICE.
+ */
+dresd_status dresd_bw_probe(const void *buf, int64_t bytes, int32_t reps, int32_t workgroups,
+                            double *ms, dresd_stream stream);
+
+/*
  * Query-side transform of Algorithm 1 steps 4-6, for decode-step queries (or,
  * once, for the datastore rows that become keys):
  *   z   = (x - mean) / sqrt(var + eps_z)        z-score normalisation, Eq. 1

@@ -15,7 +15,7 @@ from . import _lib
 from ._lib import DresdError, K_MAX  # noqa: F401
 
 __all__ = ["Index", "PartitionedIndex", "DresdError", "K_MAX", "transform", "pack_drafts",
-           "kmeans_assign", "kmeans_update", "train_partitions"]
+           "kmeans_assign", "kmeans_update", "train_partitions", "bw_probe"]
 
 _DTYPES = None
 
@@ -377,3 +377,18 @@ def train_partitions(x, P: int, iters: int = 10, seed: int = 0, stream=None):
         assign = kmeans_assign(x, centroids, stream=stream)
         kmeans_update(x, assign, centroids, stream)
     return centroids, kmeans_assign(x, centroids, stream=stream)
+
+
+def bw_probe(buf, reps: int = 10, workgroups: int = 0, stream=None) -> float:
+    """Achievable HBM read bandwidth with the scans' access pattern: reads
+    every byte of the GPU tensor ``buf`` (contents irrelevant; whole 1 KiB
+    blocks, at least 1 MiB) ``reps`` times after one untimed pass with
+    ``workgroups`` workgroups (0: four per compute unit).  Returns GB/s."""
+    if not buf.is_cuda:
+        raise ValueError("buf must be a GPU tensor")
+    nbytes = buf.numel() * buf.element_size() // 1024 * 1024
+    lib = _lib.load()
+    ms = ctypes.c_double()
+    _lib.check(lib.dresd_bw_probe(ctypes.c_void_p(buf.data_ptr()), nbytes, int(reps),
+                                  int(workgroups), ctypes.byref(ms), _stream_handle(stream)))
+    return nbytes / (ms.value * 1e-3) / 1e9

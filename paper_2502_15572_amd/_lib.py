@@ -23,7 +23,8 @@ EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_inde
            "dresd_pack_drafts", "dresd_ivf_create", "dresd_ivf_destroy", "dresd_ivf_info",
            "dresd_ivf_search", "dresd_ivf_search_filtered", "dresd_ivf_search_probes",
            "dresd_ivf_profile_enable",
-           "dresd_ivf_profile_read", "dresd_kmeans_assign", "dresd_kmeans_update"]
+           "dresd_ivf_profile_read", "dresd_kmeans_assign", "dresd_kmeans_update",
+           "dresd_bw_probe"]
 
 _lock = threading.Lock()
 _lib = None
@@ -86,6 +87,8 @@ def _declare(lib):
     lib.dresd_search_plan.argtypes = [P, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(I32),
                                       ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(I32)]
     lib.dresd_search_plan.restype = ctypes.c_int
+    lib.dresd_bw_probe.argtypes = [P, I64, I32, I32, ctypes.POINTER(ctypes.c_double), P]
+    lib.dresd_bw_probe.restype = ctypes.c_int
     return lib
 
 

@@ -35,7 +35,7 @@ UNITS = [("dresd_kernels.hip", ["-DDRESD_TU=%d" % t], "kernels%d" % t) for t in 
     ("dresd_scan_mq.hip", ["-DDRESD_MQ_TU=1"], "scanmq1"),
     ("dresd_merge.hip", [], "merge"), ("dresd_transform.hip", [], "transform"),
     ("dresd_drafts.hip", [], "drafts"), ("dresd_parts.hip", [], "parts"),
-    ("dresd_kmeans.hip", [], "kmeans"),
+    ("dresd_kmeans.hip", [], "kmeans"), ("dresd_bwprobe.hip", [], "bwprobe"),
     ("dresd_runtime.hip", [], "runtime")]
 
 

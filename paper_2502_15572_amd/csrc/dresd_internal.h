@@ -216,6 +216,9 @@ hipError_t launch_kmeans_assign(const KmeansParams &p, hipStream_t st);
 hipError_t launch_kmeans_update(const KmeansParams &p, int cus, hipStream_t st);
 
 void *merge_kernel_ptr();
+// Bandwidth probe (dresd_bwprobe.hip): one read pass over nblocks 1 KiB
+// blocks with `workgroups` workgroups of 4 waves.
+hipError_t launch_bw_read(const void *buf, int64_t nblocks, int workgroups, hipStream_t st);
 void *layout_kernel_ptr(int dtype);
 int qt_index(int qt);  // 1,2,4,8,16 -> 0..4, else -1
 

@@ -775,6 +775,42 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
 
 extern "C" {
 
+dresd_status dresd_bw_probe(const void *buf, int64_t bytes, int32_t reps, int32_t workgroups,
+                            double *ms, dresd_stream stream) {
+  if (!buf || !ms) return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (bytes < (1 << 20) || bytes % 1024 != 0)
+    return fail(DRESD_EINVAL, "bytes must be a multiple of 1024 and at least 1 MiB");
+  if (reps < 1 || reps > 1000) return fail(DRESD_EINVAL, "reps must be in [1, 1000]");
+  if (workgroups < 0 || workgroups > (1 << 20)) return fail(DRESD_EINVAL, "workgroups out of range");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int wg = workgroups;
+  if (wg == 0) {
+    int dev = 0, cus = 0;
+    DRESD_HIP(hipGetDevice(&dev));
+    DRESD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    wg = 4 * cus;
+  }
+  const int64_t nblocks = bytes / 1024;
+  hipEvent_t a = nullptr, b = nullptr;
+  DRESD_HIP(hipEventCreate(&a));
+  if (hipEventCreate(&b) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return fail(DRESD_EDEVICE, "hipEventCreate failed");
+  }
+  hipError_t e = launch_bw_read(buf, nblocks, wg, st);  // untimed pass
+  if (e == hipSuccess) e = hipEventRecord(a, st);
+  for (int r = 0; e == hipSuccess && r < reps; ++r) e = launch_bw_read(buf, nblocks, wg, st);
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float t = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&t, a, b);
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  if (e != hipSuccess) return fail(DRESD_EDEVICE, std::string("bandwidth probe: ") + hipGetErrorString(e));
+  *ms = (double)t / reps;
+  return DRESD_OK;
+}
+
 dresd_status dresd_transform(const float *x, int64_t M, int32_t D, const float *mean,
                              const float *var, float eps_z, const float *W, int32_t l, float eps_n,
                              float *y, dresd_stream stream) {

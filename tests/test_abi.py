@@ -109,3 +109,10 @@ def test_new_entry_points_reject_bad_arguments_before_device_work():
     assert lib.dresd_kmeans_assign(None, 10, 8, 0, None, 2, None, None, None) == E
     assert lib.dresd_kmeans_assign(None, 0, 8, 0, None, 2, None, None, None) == 0
     assert lib.dresd_kmeans_update(None, 10, 8, 0, None, 2, None, None, None) == E
+    # bandwidth probe
+    ms = ctypes.c_double()
+    assert lib.dresd_bw_probe(None, 1 << 20, 1, 0, ctypes.byref(ms), None) == E
+    assert lib.dresd_bw_probe(fake, 1 << 20, 1, 0, None, None) == E
+    for nbytes, reps, wg in [((1 << 20) + 1, 1, 0), (1 << 19, 1, 0), (1 << 20, 0, 0),
+                             (1 << 20, 1001, 0), (1 << 20, 1, -1)]:
+        assert lib.dresd_bw_probe(fake, nbytes, reps, wg, ctypes.byref(ms), None) == E

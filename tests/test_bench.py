@@ -69,3 +69,26 @@ def test_every_scan_kind_names_a_kernel_of_its_source():
     for kind in SCAN_KINDS.values():
         src = open(os.path.join(bench.CSRC, bench.SCAN_UNIT[kind])).read()
         assert " %s(ScanParams p)" % bench.SCAN_KERNEL_NAME[kind] in src, kind
+
+
+def test_cpu_baseline_leg_parity_verdict():
+    """The bench's parity verdict (query 0 against the oracle) passes the
+    oracle's own answer and fails a wrong row."""
+    import numpy as np
+    import torch
+    import oracle
+    from datagen import WORKLOADS, generate, to_numpy_bits
+    w = WORKLOADS["zipf33m_d128_f16"].scaled(5000)
+    g = generate(w, "cpu")
+    kb, dt = to_numpy_bits(g["keys"])
+    q = g["queries"][:3]
+    o = oracle.topk(kb, dt, q.numpy(), w.k, g["cont"].numpy())
+    good = (torch.from_numpy(o[0]), torch.from_numpy(o[1]), torch.from_numpy(o[2]))
+    base, par = bench.cpu_baseline_leg(g["keys"], g["cont"], q, w.k, good, time_it=False)
+    assert base is None and par["verdict"] == "pass" and par["exact_order"]
+    bad_idx = good[0].clone()
+    outside = next(i for i in range(w.N) if i not in set(bad_idx[0].tolist()))
+    bad_idx[0, 0] = outside
+    _, par = bench.cpu_baseline_leg(g["keys"], g["cont"], q, w.k, (bad_idx,) + good[1:],
+                                    time_it=False)
+    assert par["verdict"] == "FAIL"
