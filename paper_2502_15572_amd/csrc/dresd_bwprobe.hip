@@ -6,10 +6,11 @@
 
 namespace dresd {
 
-namespace {
-
-// Never written in practice: the loads need a use the compiler cannot drop.
+// Never written in practice: the loads need a use the compiler cannot drop
+// (a device variable with external linkage, which the host could read).
 __device__ uint32_t g_probe_sink;
+
+namespace {
 
 template <int U>
 __global__ void __launch_bounds__(256) dresd_bw_read(const u4 *__restrict__ p, int64_t nblocks) {

@@ -130,10 +130,11 @@ struct Plan {
   bool mq = false;                  // shared-key scan (queries in registers)
   int bmax = 0;                 // queries per group
   int bl = 0;                   // queries per launch (several groups)
-  std::vector<Group> groups;
+  int B = 0, nl = 0;            // batch, launches (launch i: group_of(pl, i))
   int C = 0;                    // per-wave list capacity
   int CL = 0;                   // per-query LDS stage
-  std::vector<int64_t> strides; // sampled passes, sparsest first
+  int64_t strides[3] = {0, 0, 0};  // sampled passes, sparsest first
+  int npass = 0;                   // sampled passes used
   ScanKernel kmain = nullptr, ksample = nullptr;
   size_t lds = 0;
   int wg_max = 0;               // resident workgroups of the scan kernels
@@ -146,6 +147,13 @@ struct Plan {
   size_t bytes = 0;
 };
 
+// Launch i of a plan: queries [B i / nl, B (i + 1) / nl), split into groups
+// of at most bmax queries.
+Group group_of(const Plan &pl, int i) {
+  const int b0 = (int)((int64_t)pl.B * i / pl.nl), b1 = (int)((int64_t)pl.B * (i + 1) / pl.nl);
+  return {b0, b1 - b0, (int)ceil_div(b1 - b0, pl.bmax)};
+}
+
 // Single-tile scan: query operand | zero chunk | candidate region per wave.
 size_t scan_lds(int ncols, int KB, int nq, int cl, int C) {
   return (size_t)ncols * KB * 64 + 16 + scan_ntok_bytes(nq) + (size_t)4 * scan_wave_bytes(nq, cl, C) +
@@ -157,16 +165,23 @@ size_t scan_lds(int ncols, int KB, int nq, int cl, int C) {
 // (after a spill has emptied the stage), so the stage holds at least a tile.
 int stage_cap(int nq) { return nq >= 16 ? kTileRows : 2 * kTileRows; }
 
-int occupancy(dresd_index *ix, ScanKernel k, size_t lds) {
+// Resident workgroups per CU of a scan kernel at an LDS size, cached per
+// index (not cached with `keep` false: the allocation-free search adds
+// nothing to the host-side cache).
+int occupancy(dresd_index *ix, ScanKernel k, size_t lds, bool keep = true) {
   for (size_t i = 0; i < ix->occ_key.size(); ++i)
     if (ix->occ_key[i].first == (const void *)k && ix->occ_key[i].second == lds) return ix->occ_val[i];
   int nb = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k, kScanThreads, lds) !=
-      hipSuccess)
+      hipSuccess) {
+    (void)hipGetLastError();
     nb = 1;
+  }
   nb = std::max(nb, 1);
-  ix->occ_key.emplace_back((const void *)k, lds);
-  ix->occ_val.push_back(nb);
+  if (keep) {
+    ix->occ_key.emplace_back((const void *)k, lds);
+    ix->occ_val.push_back(nb);
+  }
   return nb;
 }
 
@@ -178,7 +193,8 @@ dresd_status validate_search(const dresd_index *ix, int32_t B, int32_t k) {
   return DRESD_OK;
 }
 
-dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = false) {
+dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = false,
+                       bool keep_cache = true) {
   pl = Plan();
   pl.filt = filt;
   // The query enters the matrix cores as three 16-bit parts that sum to it
@@ -247,20 +263,17 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   // The single-tile scan serves several groups per launch; launch sizes
   // differ by at most one query and each splits into groups of <= bmax.
   const int per = pl.mq ? 1 : std::max(1, std::min({ngr, kGroupsPerLaunch, (int)(kMaxGroup / bmax)}));
-  const int nl = (int)ceil_div(ngr, per);
-  pl.bl = 0;
-  for (int i = 0; i < nl; ++i) {
-    int b0 = (int)((int64_t)B * i / nl), b1 = (int)((int64_t)B * (i + 1) / nl);
-    pl.groups.push_back({b0, b1 - b0, (int)ceil_div(b1 - b0, bmax)});
-    pl.bl = std::max(pl.bl, b1 - b0);
-  }
+  pl.B = B;
+  pl.nl = (int)ceil_div(ngr, per);
+  pl.bl = (int)ceil_div(B, pl.nl);  // launch sizes differ by at most one query
   if (per > 1 && pl.qt == 1) {
     pl.kmain = scan_kernel(ix->dtype, pl.qt, pl.terms, true, true);
     pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.terms, false, true);
   }
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
   if (pl.lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS");
-  int occ = std::min(occupancy(ix, pl.kmain, pl.lds), occupancy(ix, pl.ksample, pl.lds));
+  int occ = std::min(occupancy(ix, pl.kmain, pl.lds, keep_cache),
+                     occupancy(ix, pl.ksample, pl.lds, keep_cache));
   // At most four workgroups per CU (few enough lists for the merge to keep
   // their best keys in LDS); one where fewer, longer HBM streams measured
   // faster: the single-tile scan with one query tile, and the shared-key
@@ -297,7 +310,7 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
                  : std::vector<int64_t>{256};
     for (int64_t P : ladder) {
       int64_t nv = ceil_div(ix->T, P);
-      if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides.push_back(P);
+      if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides[pl.npass++] = P;
     }
   }
   // Lists end with at most k keys each, so a query never has more than
@@ -431,7 +444,8 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
 // `outer` (optional) carries the timing events of an enclosing search.
 dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *next_tok, int32_t B,
                          int32_t k, int64_t *idx, float *score, int32_t *tokens,
-                         dresd_stream stream, Launcher *outer = nullptr);
+                         dresd_stream stream, Launcher *outer = nullptr,
+                         unsigned char *fixed_ws = nullptr, size_t fixed_bytes = 0);
 
 }  // namespace
 
@@ -600,11 +614,11 @@ dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int
   s = make_plan(ix, B, k, pl);
   if (s != DRESD_OK) return s;
   const int wpg = kScanThreads / kWaveSize;
-  if (sample_passes) *sample_passes = (int32_t)pl.strides.size();
-  if (scan_waves)
-    *scan_waves = (int32_t)(pass_wgs(pl, pl.groups[0], ix->T) * pl.groups[0].ng * wpg);
+  const Group g0 = group_of(pl, 0);
+  if (sample_passes) *sample_passes = (int32_t)pl.npass;
+  if (scan_waves) *scan_waves = (int32_t)(pass_wgs(pl, g0, ix->T) * g0.ng * wpg);
   if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
-  if (scan_kind) *scan_kind = pl.mq ? 1 : (pl.groups[0].ng > 1 ? 2 : 0);
+  if (scan_kind) *scan_kind = pl.mq ? 1 : (g0.ng > 1 ? 2 : 0);
   return DRESD_OK;
 }
 
@@ -641,26 +655,42 @@ std::vector<hipEvent_t> profile_events(const dresd_index *ix) {
 
 dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *next_tok, int32_t B,
                          int32_t k, int64_t *idx, float *score, int32_t *tokens,
-                         dresd_stream stream, Launcher *outer) {
+                         dresd_stream stream, Launcher *outer, unsigned char *fixed_ws,
+                         size_t fixed_bytes) {
   dresd_status s = DRESD_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Launcher own;
   own.st = st;
   Launcher &launch = outer ? *outer : own;
+  // With a fixed workspace of fixed_bytes (the allocation-free search)
+  // nothing is allocated on the device or the host, and no profiling events
+  // are taken.
+  const bool fixed = fixed_ws != nullptr;
   Plan pl;
-  s = make_plan(ix, B, k, pl, next_tok != nullptr);
+  s = make_plan(ix, B, k, pl, next_tok != nullptr, !fixed);
   if (s != DRESD_OK) return s;
-  s = ensure_workspace(ix, pl.bytes, st);
-  if (s != DRESD_OK) return s;
-  uint64_t *tau = reinterpret_cast<uint64_t *>(ix->ws + pl.off_tau);
-  uint32_t *lcnt = reinterpret_cast<uint32_t *>(ix->ws + pl.off_lcnt);
-  uint64_t *lkth = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lkth);
-  uint64_t *lfirst = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lfirst);
-  uint64_t *lists = reinterpret_cast<uint64_t *>(ix->ws + pl.off_lists);
-  uint64_t *spill = reinterpret_cast<uint64_t *>(ix->ws + pl.off_spill);
+  unsigned char *ws = fixed_ws;
+  if (fixed) {
+    if (pl.bytes > fixed_bytes)
+      return fail(DRESD_EINVAL, "this search needs " + std::to_string(pl.bytes) +
+                                    " bytes of workspace, more than the " +
+                                    std::to_string(fixed_bytes) +
+                                    " bytes of the fixed scratch (use dresd_search)");
+  } else {
+    s = ensure_workspace(ix, pl.bytes, st);
+    if (s != DRESD_OK) return s;
+    ws = ix->ws;
+  }
+  const bool prof = ix->prof && !fixed;
+  uint64_t *tau = reinterpret_cast<uint64_t *>(ws + pl.off_tau);
+  uint32_t *lcnt = reinterpret_cast<uint32_t *>(ws + pl.off_lcnt);
+  uint64_t *lkth = reinterpret_cast<uint64_t *>(ws + pl.off_lkth);
+  uint64_t *lfirst = reinterpret_cast<uint64_t *>(ws + pl.off_lfirst);
+  uint64_t *lists = reinterpret_cast<uint64_t *>(ws + pl.off_lists);
+  uint64_t *spill = reinterpret_cast<uint64_t *>(ws + pl.off_spill);
 
   hipEvent_t e_all0 = nullptr, e_all1 = nullptr;
-  if (ix->prof && !outer) {
+  if (prof && !outer) {
     e_all0 = take_event(ix);
     e_all1 = take_event(ix);
     if (!e_all0 || !e_all1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
@@ -668,7 +698,8 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     own.last = e_all1;
   }
   const int wpg = kScanThreads / kWaveSize;
-  for (const Group &gr : pl.groups) {
+  for (int li = 0; li < pl.nl; ++li) {
+    const Group gr = group_of(pl, li);
     ScanParams sp;
     sp.data = ix->data;
     sp.queries = queries + (size_t)gr.b0 * ix->d;
@@ -697,7 +728,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     if (pl.mq) {
       QopParams qp;
       qp.queries = sp.queries;
-      qp.out = ix->ws + pl.off_qop;
+      qp.out = ws + pl.off_qop;
       qp.B = gr.nb;
       qp.d = ix->d;
       qp.KB = ix->KB;
@@ -731,14 +762,14 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       sp.G = (int)(pl.mq ? wgs : wgs * wpg);
       void *sargs[] = {&sp};
       hipEvent_t e0 = nullptr, e1 = nullptr;
-      if (main_pass && ix->prof) {
+      if (main_pass && prof) {
         e0 = take_event(ix);
         e1 = take_event(ix);
         if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
       }
       DRESD_HIP(launch((const void *)(main_pass ? pl.kmain : pl.ksample),
                        dim3((unsigned)(wgs * gr.ng)), dim3(kScanThreads), sargs, pl.lds, e0, e1));
-      if (main_pass && ix->prof) {
+      if (main_pass && prof) {
         ix->ev_scan.push_back(e0);
         ix->ev_scan.push_back(e1);
       }
@@ -750,13 +781,13 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       mp.tokens = tokens ? tokens + (size_t)gr.b0 * k * ix->L : nullptr;
       void *margs[] = {&mp};
       DRESD_HIP(launch(merge_kernel_ptr(), dim3((unsigned)gr.nb), dim3(kMergeThreads), margs, 0,
-                       nullptr, nullptr, main_pass && &gr == &pl.groups.back()));
+                       nullptr, nullptr, main_pass && li == pl.nl - 1));
       tau_in = mp.tau_out;
       ++level;
       return DRESD_OK;
     };
-    for (int64_t P : pl.strides) {
-      s = run_pass(P, false);
+    for (int pi = 0; pi < pl.npass; ++pi) {
+      s = run_pass(pl.strides[pi], false);
       if (s != DRESD_OK) return s;
     }
     s = run_pass(1, true);
