@@ -154,6 +154,32 @@ dresd_status dresd_search_filtered(dresd_index *ix, const float *queries,
                                    int64_t *idx, float *score, int32_t *tokens,
                                    dresd_stream stream);
 
+/*
+ * Allocation-free search, for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  The same search as dresd_search (same kernels, bitwise the same
+ * outputs), with its workspace in a fixed library scratch of
+ * DRESD_SCRATCH_BYTES that every device the library runs on holds until the
+ * process ends, instead of the index's growable workspace.  It allocates no
+ * device or host memory and never synchronises; the caller still passes the
+ * queries and the outputs.
+ *
+ *   Arguments, order, determinism and errors as for dresd_search, and
+ *   EINVAL when the search needs more workspace than DRESD_SCRATCH_BYTES
+ *   (dresd_search_plan's workspace_bytes tells beforehand; e.g. one query up
+ *   to k = 1024, or 64 queries at k = 32, fit).  Profiling (dresd_profile_*)
+ *   does not time these calls.
+ * Every call on one device shares that device's scratch, which keeps the
+ * last call's contents (each search writes every scratch byte it reads
+ * before reading it, so nothing needs clearing): calls that overlap on one
+ * device -- on different streams, or with different indexes -- race, and
+ * must be serialised by the caller (e.g. issued on one stream).
+ */
+#define DRESD_SCRATCH_BYTES (64LL << 20)
+dresd_status dresd_search_noalloc(dresd_index *ix, const float *queries, int32_t B,
+                                  int32_t k, int64_t *idx, float *score,
+                                  int32_t *tokens, dresd_stream stream);
+
 /* Describe an index.  Any output pointer (host) may be NULL.
  * Errors: EINVAL when ix is NULL. */
 dresd_status dresd_index_info(const dresd_index *ix, int64_t *N, int32_t *d,

@@ -24,7 +24,7 @@ EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_inde
            "dresd_ivf_search", "dresd_ivf_search_filtered", "dresd_ivf_search_probes",
            "dresd_ivf_profile_enable",
            "dresd_ivf_profile_read", "dresd_kmeans_assign", "dresd_kmeans_update",
-           "dresd_bw_probe"]
+           "dresd_bw_probe", "dresd_search_noalloc"]
 
 _lock = threading.Lock()
 _lib = None
@@ -89,6 +89,8 @@ def _declare(lib):
     lib.dresd_search_plan.restype = ctypes.c_int
     lib.dresd_bw_probe.argtypes = [P, I64, I32, I32, ctypes.POINTER(ctypes.c_double), P]
     lib.dresd_bw_probe.restype = ctypes.c_int
+    lib.dresd_search_noalloc.argtypes = [P, P, I32, I32, P, P, P, P]
+    lib.dresd_search_noalloc.restype = ctypes.c_int
     return lib
 
 

@@ -16,6 +16,13 @@
 
 using namespace dresd;
 
+// Fixed device scratch of the allocation-free search (dresd_search_noalloc):
+// one copy per device, held until the process ends.  In host code `scratch`
+// names a host-side stand-in, never the device array: host code uses only
+// the per-device address that hipGetSymbolAddress returns (scratch_address).
+static constexpr size_t kScratchBytes = (size_t)DRESD_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 struct dresd_index {
   int device = 0;
   int64_t N = 0;
@@ -94,6 +101,33 @@ bool capturing(hipStream_t st) {
     return false;
   }
   return cs != hipStreamCaptureStatusNone;
+}
+
+// Device address of `scratch` on each device, resolved once per device with
+// that device current (at index creation, or at the first allocation-free
+// search on the device).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char *g_scratch_addr[kMaxDevices] = {};
+
+dresd_status scratch_address(int dev, unsigned char **out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(DRESD_EUNSUPPORTED, "device ordinal too large");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != dev)
+      return fail(DRESD_EDEVICE, "the index's device must be current");
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(DRESD_EDEVICE, std::string("hipGetSymbolAddress(scratch): ") +
+                                     hipGetErrorString(e));
+    }
+    g_scratch_addr[dev] = static_cast<unsigned char *>(p);
+  }
+  *out = g_scratch_addr[dev];
+  return DRESD_OK;
 }
 
 int next_pow2(int x) {
@@ -490,6 +524,11 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
     return cleanup(fail(DRESD_EDEVICE, "hipGetDeviceProperties failed"));
   ix->cus = prop.multiProcessorCount;
   ix->lds_max = prop.sharedMemPerBlock;
+  {  // set-up of the allocation-free search on this device
+    unsigned char *sc = nullptr;
+    const dresd_status ss = scratch_address(ix->device, &sc);
+    if (ss != DRESD_OK) return cleanup(ss);
+  }
   ix->N = N;
   ix->d = d;
   ix->L = L;
@@ -640,6 +679,20 @@ dresd_status dresd_search_filtered(dresd_index *ix, const float *queries, const 
     return fail(DRESD_EINVAL, "NULL pointer argument");
   if (B == 0) return DRESD_OK;
   return search_impl(ix, queries, next_tok, B, k, idx, score, tokens, stream);
+}
+
+dresd_status dresd_search_noalloc(dresd_index *ix, const float *queries, int32_t B, int32_t k,
+                                  int64_t *idx, float *score, int32_t *tokens,
+                                  dresd_stream stream) {
+  dresd_status s = validate_search(ix, B, k);
+  if (s != DRESD_OK) return s;
+  if (B > 0 && (!queries || !idx || !score)) return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (B == 0) return DRESD_OK;
+  unsigned char *sc = nullptr;
+  s = scratch_address(ix->device, &sc);
+  if (s != DRESD_OK) return s;
+  return search_impl(ix, queries, nullptr, B, k, idx, score, tokens, stream, nullptr, sc,
+                     kScratchBytes);
 }
 
 }  // extern "C"
