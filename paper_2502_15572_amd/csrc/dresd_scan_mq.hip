@@ -128,6 +128,11 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   constexpr int BPT = KBT >= SB ? SB : KBT;      // blocks of a tile per stage
   constexpr int CB = kMqCandBuf;
   constexpr int WAIT = 2 * (S - 2);  // copies of later stages still in flight
+  // Interleave each tile's threshold test with the next tile's matrix
+  // instructions when a key tile carries few of them (measured: 33.5M keys x
+  // 128 dims at 128 queries, 8 per tile, main pass 1.43 -> 1.37 ms; at
+  // 10M x 256 and 256 queries, 32 per tile, it was slower).
+  constexpr bool kDefer = BPT * QTW <= 16;
   static_assert(KBT >= 4 && S >= 3 && NP <= 32, "shape");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
@@ -271,59 +276,53 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     const int64_t row64 = tile * kTileRows + m;
     const bool row_ok = row64 < p.N;
     const uint32_t row = (uint32_t)row64;
-    // Count first, so that at most one flush makes room for the whole tile.
-    auto count = [&]() {
-      int n = 0;
+    // One pass over the slots of the query tiles with hits: a slot's hits
+    // are appended while they fit; the first slot that does not fit stops
+    // the pass, and the rest (rare: thresholds still low) goes one slot at
+    // a time with a flush whenever the next one does not fit.
+    const uint64_t okm = __ballot(row_ok);
+    int jstop = NP;
 #pragma unroll
-      for (int j = 0; j < NP; ++j)
-        if (hit_t & (1u << (j / NS))) n += __popcll(__ballot(row_ok && sc[j] >= thr[j]));
-      return n;
-    };
-    int n = count();
-    if (cnt + n > CB) {
-      flush();
-      n = count();
-    }
-    if (cnt + n <= CB) {
-#pragma unroll
-      for (int j = 0; j < NP; ++j) {
-        if (!(hit_t & (1u << (j / NS)))) continue;
-        const bool h = row_ok && sc[j] >= thr[j];
-        const uint64_t mk = __ballot(h);
-        if (mk == 0) continue;
-        if (h) {
-          const int at = cnt + rank_in(mk);
-          ck[at] = make_key(sc[j], row);
-          cq[at] = (uint8_t)((j / NS) * QPT + g * NS + (j % NS));
-        }
-        cnt += __popcll(mk);
+    for (int j = 0; j < NP; ++j) {
+      if (jstop < NP || !(hit_t & (1u << (j / NS)))) continue;
+      const uint64_t mk = __ballot(sc[j] >= thr[j]) & okm;
+      if (mk == 0) continue;
+      if (cnt + __popcll(mk) > CB) {
+        jstop = j;
+        continue;
       }
-    } else {
-      // More candidates than the buffer holds (thresholds still low): one
-      // slot at a time with a flush whenever the next one does not fit.
+      if ((mk >> lane) & 1ull) {
+        const int at = cnt + rank_in(mk);
+        ck[at] = make_key(sc[j], row);
+        cq[at] = (uint8_t)((j / NS) * QPT + g * NS + (j % NS));
+      }
+      cnt += __popcll(mk);
+    }
+    if (jstop < NP) {
       // Slot j's score is rotated into cur[0] (no indexed register access).
       float cur[NP];
 #pragma unroll
       for (int j = 0; j < NP; ++j) cur[j] = sc[j];
 #pragma unroll 1
       for (int j = 0; j < NP; ++j) {
-        const int qi = (j / NS) * QPT + g * NS + (j % NS);
-        if (cnt + __popcll(__ballot(row_ok && cur[0] >= st_thr[qi])) > CB) flush();
-        const bool h = row_ok && cur[0] >= st_thr[qi];
-        const uint64_t mk = __ballot(h);
-        if (h) {
-          const int at = cnt + rank_in(mk);
-          ck[at] = make_key(cur[0], row);
-          cq[at] = (uint8_t)qi;
+        if (j >= jstop && (hit_t & (1u << (j / NS)))) {
+          const int qi = (j / NS) * QPT + g * NS + (j % NS);
+          if (cnt + __popcll(__ballot(row_ok && cur[0] >= st_thr[qi])) > CB) flush();
+          const bool h = row_ok && cur[0] >= st_thr[qi];
+          const uint64_t mk = __ballot(h);
+          if (h) {
+            const int at = cnt + rank_in(mk);
+            ck[at] = make_key(cur[0], row);
+            cq[at] = (uint8_t)qi;
+          }
+          cnt += __popcll(mk);
         }
-        cnt += __popcll(mk);
 #pragma unroll
         for (int i = 0; i + 1 < NP; ++i) cur[i] = cur[i + 1];
       }
     }
   };
 
-  int tslot = 0;  // ring slot of the stage that holds the current tile's last blocks
   // Filtered search with few score slots: their next tokens stay in VGPRs.
   int ntr[NP <= 8 ? NP : 1];
   if (filt && NP <= 8) {
@@ -331,48 +330,49 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
 #pragma unroll
     for (int j = 0; j < (NP <= 8 ? NP : 1); ++j) ntr[j] = nt_slot[g * NP + j];
   }
-  auto tile_end = [&](int64_t vt) {
-    float sc[NP];
+  // Scores of a finished key tile from its accumulators (the query parts
+  // recombined), NaN where the filter drops the row (`f`: the row's first
+  // token); NaN fails every threshold test and fmaxf ignores it.
+  auto scores_of = [&](const f4 (&a)[QTW], int f, float (&sc)[NP]) {
 #pragma unroll
     for (int t = 0; t < QTW; ++t)
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        float v = acc[t][s * CPQ];
+        float v = a[t][s * CPQ];
         if (CPQ == 4) {
           const float s1 = (DT == kF16) ? (1.0f / 2048.0f) : 1.0f;
           const float s2 = (DT == kF16) ? (1.0f / 4194304.0f) : 1.0f;
-          v = (v + acc[t][s * CPQ + 1] * s1) + acc[t][s * CPQ + 2] * s2;
+          v = (v + a[t][s * CPQ + 1] * s1) + a[t][s * CPQ + 2] * s2;
         } else if (CPQ == 2) {
-          v = v + acc[t][s * CPQ + 1];
+          v = v + a[t][s * CPQ + 1];
         }
         sc[t * NS + s] = v;
       }
     if (filt) {
-      // Rows whose value does not start with the slot's next token drop out:
-      // NaN fails every threshold test and is ignored by fmaxf.
-      const int f = fring[tslot * 64 + (TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * 16 + m];
 #pragma unroll
       for (int j = 0; j < NP; ++j)
         if (f != (NP <= 8 ? ntr[j] : nt_slot[g * NP + j])) sc[j] = __builtin_nanf("");
     }
-    // v >= thr exactly when v - thr >= 0 (round-to-nearest keeps the sign).
-    float mt[QTW];
+  };
+  // Lanes whose row passes some threshold (v >= thr exactly when
+  // v - thr >= 0: round-to-nearest keeps the sign).
+  auto any_hit = [&](const float (&sc)[NP]) {
+    float mx = sc[0] - thr[0];
+#pragma unroll
+    for (int j = 1; j < NP; ++j) mx = fmaxf(mx, sc[j] - thr[j]);
+    return __ballot(mx >= 0.0f);
+  };
+  // The slow path of a tile with hits: which query tiles hit, then buffer.
+  auto take = [&](int64_t vt, const float (&sc)[NP]) {
+    uint32_t hit_t = 0;
 #pragma unroll
     for (int t = 0; t < QTW; ++t) {
-      mt[t] = sc[t * NS] - thr[t * NS];
+      float mt = sc[t * NS] - thr[t * NS];
 #pragma unroll
-      for (int s = 1; s < NS; ++s) mt[t] = fmaxf(mt[t], sc[t * NS + s] - thr[t * NS + s]);
+      for (int s = 1; s < NS; ++s) mt = fmaxf(mt, sc[t * NS + s] - thr[t * NS + s]);
+      if (__ballot(mt >= 0.0f)) hit_t |= 1u << t;
     }
-    float mx = mt[0];
-#pragma unroll
-    for (int t = 1; t < QTW; ++t) mx = fmaxf(mx, mt[t]);
-    if (__ballot(mx >= 0.0f)) {
-      uint32_t hit_t = 0;
-#pragma unroll
-      for (int t = 0; t < QTW; ++t)
-        if (__ballot(mt[t] >= 0.0f)) hit_t |= 1u << t;
-      candidates((v0 + vt) * p.stride, sc, hit_t);
-    }
+    candidates((v0 + vt) * p.stride, sc, hit_t);
   };
 
   if (ntile > 0) {
@@ -383,13 +383,23 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     // LDS offsets: the low half of a generic LDS address.
     const uint32_t ring = (uint32_t)(uintptr_t)smem;
     const uint32_t fring_lds = (uint32_t)(uintptr_t)fring;
+    // Source of this wave's 2 blocks of stage `st` (blocks j = st*SB + 2wv,
+    // +1 of the visited sequence; past the end, the last two blocks again).
+    const int64_t jl = NB - 2;
+    const unsigned char *last_src =
+        dbase + (jl / KBT) * tstep + (jl - (jl / KBT) * KBT) * kBlockBytes;
+    const int64_t stage_step = (SPT == 1) ? (int64_t)TPS * tstep : 0;
+    const int64_t woff = (SPT == 1) ? (int64_t)((wv * 2) / KBT) * tstep +
+                                          (int64_t)((wv * 2) % KBT) * kBlockBytes
+                                    : 0;
+    auto src_of = [&](int64_t st) -> const unsigned char * {
+      if (st * SB + wv * 2 > jl) return last_src;
+      if constexpr (SPT == 1) return dbase + st * stage_step + woff;
+      return dbase + (st / SPT) * tstep + ((st % SPT) * SB + wv * 2) * kBlockBytes;
+    };
     // Copy this wave's 2 blocks of stage `st` into ring slot `slot`.
     auto issue = [&](int64_t st, int slot) {
-      int64_t j = st * SB + wv * 2;
-      j = j < NB - 2 ? j : NB - 2;  // past the end: the last two blocks again
-      const int64_t vt = j / KBT;
-      const unsigned char *src = dbase + vt * tstep + (j - vt * KBT) * kBlockBytes;
-      copy2_to_lds(src, voff0, voff1,
+      copy2_to_lds(src_of(st), voff0, voff1,
                    ring + (uint32_t)(slot * SB + wv * 2) * (uint32_t)kBlockBytes);
       if (filt) {
         // first tokens of the stage's tiles: lane l takes row l % 16 of the
@@ -405,60 +415,155 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     int64_t next_st = S - 1;  // next stage to copy
     int next_slot = S - 1;    // its ring slot
     int cur_slot = 0;         // ring slot of the stage being consumed
-    const int64_t ntile_pad = (ntile + TPS - 1) / TPS * TPS;
-    for (int64_t vt = 0; vt < ntile_pad; ++vt) {
-#pragma unroll
-      for (int c = 0; c < SPT; ++c) {
-        if (TPS == 1 || (vt & (TPS - 1)) == 0) {
-          // Stage start: this wave's copies of it have landed; after the
-          // barrier so have every wave's, and the slot consumed last is free
-          // for the copy S - 1 stages ahead.
-          if (filt) wait_vmcnt<WAIT + (S - 2)>();  // one more copy per stage
-          else wait_vmcnt<WAIT>();
-          __syncthreads();
-          issue(next_st, next_slot);
-          ++next_st;
-          next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
-        }
-        const u4 *blk =
-            reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes +
-                                         (size_t)((TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * KBT) *
-                                             kBlockBytes) +
-            lane;
-        // Two blocks at a time, the next two read from LDS while the
-        // matrix cores work on these (the read latency is exposed once per
-        // stage instead of once per pair).
-        u4 kv0 = blk[0], kv1 = blk[64];
-#pragma unroll
-        for (int i = 0; i < BPT; i += 2) {
-          u4 nx0 = kv0, nx1 = kv1;
-          if (i + 2 < BPT) {
-            nx0 = blk[(i + 2) * 64];
-            nx1 = blk[(i + 3) * 64];
-          }
-          const int kb = c * SB + i;
-#pragma unroll
-          for (int t = 0; t < QTW; ++t)
-            acc[t] = MfmaMQ<DT>::run(qreg[t][kb], kv0, kb == 0 ? f4{0.f, 0.f, 0.f, 0.f} : acc[t]);
-#pragma unroll
-          for (int t = 0; t < QTW; ++t) acc[t] = MfmaMQ<DT>::run(qreg[t][kb + 1], kv1, acc[t]);
-          kv0 = nx0;
-          kv1 = nx1;
-        }
-        // Keep that order through instruction scheduling: the first two
-        // reads, then per pair of blocks the next two reads and the pair's
-        // matrix instructions.
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-        for (int i = 0; i < BPT; i += 2) {
-          if (i + 2 < BPT) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 2 * QTW, 0);
-        }
-        tslot = cur_slot;
-        if (TPS == 1 || (vt & (TPS - 1)) == TPS - 1)  // stage end
-          cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
+    // Stage bookkeeping at the start of a key tile's c-th stage: this wave's
+    // copies of it have landed; after the barrier so have every wave's, and
+    // the slot consumed last is free for the copy S - 1 stages ahead.
+    auto stage_start = [&](int64_t vt) {
+      if (TPS == 1 || (vt & (TPS - 1)) == 0) {
+        if (filt) wait_vmcnt<WAIT + (S - 2)>();  // one more copy per stage
+        else wait_vmcnt<WAIT>();
+        __syncthreads();
+        issue(next_st, next_slot);
+        ++next_st;
+        next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
       }
-      if (vt < ntile) tile_end(vt);
+    };
+    // First token of this lane's row of tile vt (filtered search), read
+    // from the tile's ring slot before a later stage may overwrite it; and
+    // the ring slot advance at a stage end.
+    auto stage_end = [&](int64_t vt, int &ftok_row) {
+      if (filt) ftok_row = fring[cur_slot * 64 + (TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * 16 + m];
+      if (TPS == 1 || (vt & (TPS - 1)) == TPS - 1) cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
+    };
+    auto stage_blocks = [&](int64_t vt) {
+      return reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes +
+                                          (size_t)((TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * KBT) *
+                                              kBlockBytes) +
+             lane;
+    };
+    const int64_t ntile_pad = (ntile + TPS - 1) / TPS * TPS;
+    if constexpr (!kDefer) {
+      // Many matrix instructions per key tile: the tile's threshold test
+      // follows its own matrix instructions.
+      f4 acc[QTW];
+#pragma unroll 1
+      for (int64_t vt = 0; vt < ntile_pad; ++vt) {
+        int fr = 0;
+#pragma unroll
+        for (int c = 0; c < SPT; ++c) {
+          stage_start(vt);
+          const u4 *blk = stage_blocks(vt);
+          // Two blocks at a time, the next two read from LDS while the
+          // matrix cores work on these.
+          u4 kv0 = blk[0], kv1 = blk[64];
+#pragma unroll
+          for (int i = 0; i < BPT; i += 2) {
+            u4 nx0 = kv0, nx1 = kv1;
+            if (i + 2 < BPT) {
+              nx0 = blk[(i + 2) * 64];
+              nx1 = blk[(i + 3) * 64];
+            }
+            const int kb = c * SB + i;
+#pragma unroll
+            for (int t = 0; t < QTW; ++t)
+              acc[t] = MfmaMQ<DT>::run(qreg[t][kb], kv0, kb == 0 ? f4{0.f, 0.f, 0.f, 0.f} : acc[t]);
+#pragma unroll
+            for (int t = 0; t < QTW; ++t) acc[t] = MfmaMQ<DT>::run(qreg[t][kb + 1], kv1, acc[t]);
+            kv0 = nx0;
+            kv1 = nx1;
+          }
+          // Keep that order through instruction scheduling: the first two
+          // reads, then per pair of blocks the next two reads and the pair's
+          // matrix instructions.
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+          for (int i = 0; i < BPT; i += 2) {
+            if (i + 2 < BPT) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * QTW, 0);
+          }
+          stage_end(vt, fr);
+        }
+        if (vt < ntile) {
+          float sc[NP];
+          scores_of(acc, fr, sc);
+          if (any_hit(sc)) take(vt, sc);
+        }
+      }
+    } else {
+      // Few matrix instructions per key tile (the threshold test is a large
+      // share of a tile's work): each tile's test runs interleaved with the
+      // next tile's matrix instructions, from a second set of accumulators.
+      f4 accA[QTW], accB[QTW];
+      int fA = 0, fB = 0;  // filtered search: this lane's first token of the tile in accA / accB
+      // One key tile: its matrix instructions into `acc`, the test of the
+      // previous tile (complete in `prev`) split over its pairs of blocks,
+      // then that tile's slow path if it has hits.
+      auto step = [&](int64_t vt, f4 (&acc)[QTW], const f4 (&prev)[QTW], int &fcur, int fprev) {
+        const int64_t pv = vt - 1;
+        float psc[NP];
+        uint64_t hits = 0;
+#pragma unroll
+        for (int c = 0; c < SPT; ++c) {
+          stage_start(vt);
+          if (c == 0) scores_of(prev, fprev, psc);
+          const u4 *blk = stage_blocks(vt);
+          constexpr int NPAIR = BPT / 2;
+          constexpr int CH = (NP + NPAIR - 1) / NPAIR;  // test slots per pair of blocks
+          float pmx[NPAIR];
+          u4 kv0 = blk[0], kv1 = blk[64];
+#pragma unroll
+          for (int i = 0; i < BPT; i += 2) {
+            u4 nx0 = kv0, nx1 = kv1;
+            if (i + 2 < BPT) {
+              nx0 = blk[(i + 2) * 64];
+              nx1 = blk[(i + 3) * 64];
+            }
+            const int kb = c * SB + i;
+#pragma unroll
+            for (int t = 0; t < QTW; ++t)
+              acc[t] = MfmaMQ<DT>::run(qreg[t][kb], kv0, kb == 0 ? f4{0.f, 0.f, 0.f, 0.f} : acc[t]);
+            if (c == 0) {
+              const int j0 = (i / 2) * CH;
+              float mm = -__builtin_inff();
+#pragma unroll
+              for (int j = j0; j < j0 + CH; ++j)
+                if (j < NP) mm = fmaxf(mm, psc[j] - thr[j]);
+              pmx[i / 2] = mm;
+            }
+#pragma unroll
+            for (int t = 0; t < QTW; ++t) acc[t] = MfmaMQ<DT>::run(qreg[t][kb + 1], kv1, acc[t]);
+            kv0 = nx0;
+            kv1 = nx1;
+            // per pair: the next two reads, half the matrix instructions,
+            // the pair's share of the test, the other half
+            if (i + 2 < BPT) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, QTW, 0);
+            if (c == 0) __builtin_amdgcn_sched_group_barrier(0x002, 2 * CH, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, QTW, 0);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          if (c == 0) {
+            float mx = pmx[0];
+#pragma unroll
+            for (int q = 1; q < NPAIR; ++q) mx = fmaxf(mx, pmx[q]);
+            hits = __ballot(mx >= 0.0f) & (0ull - (uint64_t)(pv >= 0 && pv < ntile));
+          }
+          stage_end(vt, fcur);
+        }
+        if (hits) take(pv, psc);
+      };
+      const int64_t nsteps = (ntile_pad + 1) / 2 * 2;  // even: the last tile is in accB
+#pragma unroll 1
+      for (int64_t vt = 0; vt < nsteps; vt += 2) {
+        step(vt, accA, accB, fA, fB);
+        step(vt + 1, accB, accA, fB, fA);
+      }
+      const int64_t lt = nsteps - 1;  // the last tile's test
+      if (lt < ntile) {
+        float sc[NP];
+        scores_of(accB, fB, sc);
+        if (any_hit(sc)) take(lt, sc);
+      }
     }
     wait_vmcnt<0>();  // no LDS copy may land after the workgroup ends
   }
