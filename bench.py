@@ -417,8 +417,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--workload", default=None,
+                    help="default: %s (and the secondary workloads)" % DEFAULT_WORKLOAD)
+    ap.add_argument("--batch", type=int, default=None, help="default: 1")
     ap.add_argument("--k", type=int, default=0, help="default: the workload's k")
     ap.add_argument("--n", type=int, default=0, help="override N (reduced runs; not a bench line)")
     ap.add_argument("--no-cpu-baseline", action="store_true",
@@ -451,6 +452,10 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
+    # the secondary workloads belong to the default run only
+    default_run = args.workload is None and args.batch is None
+    args.workload = args.workload or DEFAULT_WORKLOAD
+    args.batch = args.batch or 1
 
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -485,11 +490,11 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    secondary = (default_run and not args.k and not args.n and not args.filtered
+                 and not args.no_secondary)
     w = WORKLOADS[args.workload]
     if args.n:
         w = w.scaled(args.n)
-    secondary = (not args.no_secondary and not args.n and not args.filtered and B_default(args)
-                 and args.workload == DEFAULT_WORKLOAD)
     want_cpu = not args.no_cpu_baseline and not args.n
     res, peak = measure(w, args.batch, args.k or w.k, args, dev, probe=not args.n,
                         cpu=want_cpu, time_cpu=want_cpu and args.batch == 1 and not args.filtered)
@@ -512,10 +517,6 @@ def main():
 # 128-query batch, and the 10M x 256 datastore at 256 queries (the matrix-core
 # regime).
 SECONDARY = [("zipf33m_d128_f16", 1), ("zipf33m_d128_f16", 128), ("batch10m_d256_f16", 256)]
-
-
-def B_default(args):
-    return args.batch == 1 and not args.k
 
 
 def measure(w, B, k, args, dev, probe=False, cpu=False, time_cpu=False, measured_peak=None,
