@@ -375,8 +375,17 @@ dresd_status dresd_ivf_search_probes(dresd_ivf *ivf, const float *queries, const
  *   bytes, allocated (synchronously) on first use and kept, like every
  *   buffer it outgrows, until the process ends; calls that overlap on one
  *   device race on it.
- * Both are asynchronous on `stream`.  Errors: EINVAL (ranges, nulls), ENOMEM,
- * EDEVICE.
+ * dresd_kmeans_init: the starting centroids of the iteration: P distinct
+ *   rows spread evenly through the row order, centroid j = row pick(j)
+ *   scaled to unit length (a zero row gives a zero centroid), with
+ *   pick(j) = (o + floor(j n / P)) mod n and o = s mod n, where s is the
+ *   first output of SplitMix64 (Steele, Lea and Flood, 2014) started from
+ *   state `seed`.  x as above with 1 <= n; 1 <= P <= min(n,
+ *   DRESD_PARTS_MAX); centroids device [P, d] fp32 out (the norm is taken in
+ *   fp64 over the decoded elements, each element rounded to fp32 once).
+ *   Allocates nothing.
+ * All three are asynchronous on `stream`.  Errors: EINVAL (ranges, nulls),
+ * ENOMEM, EDEVICE.
  */
 dresd_status dresd_kmeans_assign(const void *x, int64_t n, int32_t d, int32_t dtype,
                                  const float *centroids, int32_t P, int32_t *assign,
@@ -384,6 +393,8 @@ dresd_status dresd_kmeans_assign(const void *x, int64_t n, int32_t d, int32_t dt
 dresd_status dresd_kmeans_update(const void *x, int64_t n, int32_t d, int32_t dtype,
                                  const int32_t *assign, int32_t P, float *centroids,
                                  int32_t *counts, dresd_stream stream);
+dresd_status dresd_kmeans_init(const void *x, int64_t n, int32_t d, int32_t dtype, int32_t P,
+                               uint64_t seed, float *centroids, dresd_stream stream);
 
 dresd_status dresd_ivf_profile_enable(dresd_ivf *ivf, int32_t on);
 dresd_status dresd_ivf_profile_read(dresd_ivf *ivf, double *scan_ms, double *search_ms,

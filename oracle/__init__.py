@@ -233,6 +233,42 @@ def kmeans_update(x: np.ndarray, assign, centroids: np.ndarray) -> np.ndarray:
     return c
 
 
+def splitmix64(state: int, count: int) -> list:
+    """The first ``count`` outputs of SplitMix64 (Steele, Lea and Flood,
+    "Fast splittable pseudorandom number generators", OOPSLA 2014) from
+    ``state``: add the golden-ratio increment, then two xor-shift-multiply
+    rounds and a final xor-shift.  The seeded source of k-means seeding."""
+    m = (1 << 64) - 1
+    out = []
+    for _ in range(count):
+        state = (state + 0x9E3779B97F4A7C15) & m
+        z = state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & m
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & m
+        out.append(z ^ (z >> 31))
+    return out
+
+
+def kmeans_init(x: np.ndarray, P: int, seed: int):
+    """Starting centroids of spherical k-means: P distinct rows spread
+    evenly through the row order from a seeded offset o (the first SplitMix64
+    output from ``seed``, mod n), row (o + floor(j n / P)) mod n for
+    centroid j, each scaled to unit length (a zero row stays zero).
+    Returns (picked rows [P] int64, centroids [P, d] float64)."""
+    x = np.asarray(x, np.float64)
+    n = x.shape[0]
+    if not 1 <= P <= n:
+        raise ValueError("need 1 <= P <= n")
+    o = splitmix64(seed, 1)[0] % n
+    pick = np.array([(o + (j * n) // P) % n for j in range(P)], np.int64)
+    rows = x[pick]
+    nrm = np.sqrt(np.sum(rows * rows, axis=1))
+    c = np.zeros_like(rows)
+    ok = nrm > 0
+    c[ok] = rows[ok] / nrm[ok, None]
+    return pick, c
+
+
 def kmeans_objective(x: np.ndarray, centroids: np.ndarray) -> float:
     """Sum over rows of the best inner product with a centroid: the quantity
     spherical k-means never decreases."""

@@ -15,7 +15,7 @@ from . import _lib
 from ._lib import DresdError, K_MAX  # noqa: F401
 
 __all__ = ["Index", "PartitionedIndex", "DresdError", "K_MAX", "transform", "pack_drafts",
-           "kmeans_assign", "kmeans_update", "train_partitions", "bw_probe"]
+           "kmeans_assign", "kmeans_update", "kmeans_init", "train_partitions", "bw_probe"]
 
 _DTYPES = None
 
@@ -358,21 +358,30 @@ def kmeans_update(x, assign, centroids, stream=None):
     return counts
 
 
-def train_partitions(x, P: int, iters: int = 10, seed: int = 0, stream=None):
-    """Spherical k-means on the GPU: P centroids started from P distinct rows
-    of ``x`` chosen by a seeded permutation, then ``iters`` assign + update
-    steps.  Returns (centroids float32 [P, d], assign int32 [n])."""
+def kmeans_init(x, P: int, seed: int = 0, stream=None):
+    """Starting centroids of spherical k-means (float32 [P, d]): P distinct
+    rows of ``x`` at even spacing through the row order from an offset drawn
+    from ``seed`` (SplitMix64), each scaled to unit length."""
     import torch
     x = _rows(x)
     n, d = int(x.shape[0]), int(x.shape[1])
     if not (1 <= P <= n):
         raise ValueError("need 1 <= P <= n")
-    pick = torch.randperm(n, generator=torch.Generator().manual_seed(seed))[:P].to(x.device)
-    centroids = torch.zeros((P, d), dtype=torch.float32, device=x.device)
-    # each picked row alone in its partition: the update makes it a unit centroid
-    kmeans_update(x[pick], torch.arange(P, dtype=torch.int32, device=x.device), centroids,
-                  stream)
-    assign = None
+    if not (0 <= seed < 1 << 64):
+        raise ValueError("seed must be in [0, 2^64)")
+    centroids = torch.empty((P, d), dtype=torch.float32, device=x.device)
+    _lib.check(_lib.load().dresd_kmeans_init(
+        ctypes.c_void_p(x.data_ptr()), n, d, _dtype_code(x), P, seed,
+        ctypes.c_void_p(centroids.data_ptr()), _stream_handle(stream)))
+    return centroids
+
+
+def train_partitions(x, P: int, iters: int = 10, seed: int = 0, stream=None):
+    """Spherical k-means on the GPU: P centroids started by kmeans_init, then
+    ``iters`` assign + update steps.  Returns (centroids float32 [P, d],
+    assign int32 [n])."""
+    x = _rows(x)
+    centroids = kmeans_init(x, P, seed, stream)
     for _ in range(iters):
         assign = kmeans_assign(x, centroids, stream=stream)
         kmeans_update(x, assign, centroids, stream)

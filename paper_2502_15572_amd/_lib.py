@@ -24,7 +24,7 @@ EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_inde
            "dresd_ivf_search", "dresd_ivf_search_filtered", "dresd_ivf_search_probes",
            "dresd_ivf_profile_enable",
            "dresd_ivf_profile_read", "dresd_kmeans_assign", "dresd_kmeans_update",
-           "dresd_bw_probe", "dresd_search_noalloc"]
+           "dresd_kmeans_init", "dresd_bw_probe", "dresd_search_noalloc"]
 
 _lock = threading.Lock()
 _lib = None
@@ -72,6 +72,8 @@ def _declare(lib):
     lib.dresd_kmeans_assign.restype = ctypes.c_int
     lib.dresd_kmeans_update.argtypes = [P, I64, I32, I32, P, I32, P, P, P]
     lib.dresd_kmeans_update.restype = ctypes.c_int
+    lib.dresd_kmeans_init.argtypes = [P, I64, I32, I32, I32, ctypes.c_uint64, P, P]
+    lib.dresd_kmeans_init.restype = ctypes.c_int
     lib.dresd_index_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I32),
                                      ctypes.POINTER(I32), ctypes.POINTER(I32)]
     lib.dresd_index_info.restype = ctypes.c_int

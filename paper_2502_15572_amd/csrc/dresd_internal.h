@@ -211,9 +211,11 @@ struct KmeansParams {
   int32_t *counts;           // [P] out, may be null (update)
   long long *sums;           // [P, d] fixed-point workspace (update)
   int32_t *cnt;              // [P] workspace (update)
+  int64_t offset;            // first picked row, in [0, n) (init)
 };
 hipError_t launch_kmeans_assign(const KmeansParams &p, hipStream_t st);
 hipError_t launch_kmeans_update(const KmeansParams &p, int cus, hipStream_t st);
+hipError_t launch_kmeans_init(const KmeansParams &p, hipStream_t st);
 
 void *merge_kernel_ptr();
 // Bandwidth probe (dresd_bwprobe.hip): one read pass over nblocks 1 KiB

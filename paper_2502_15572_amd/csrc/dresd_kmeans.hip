@@ -14,6 +14,9 @@
 //            rows (unchanged when it has none).  Rows are added into 64-bit
 //            fixed point (2^-30 units) with integer atomics, so the sums, and
 //            the centroids, do not depend on the order of the additions.
+//   init   : the starting centroids, P distinct rows taken at even spacing
+//            through the row order from a seeded offset, each scaled to unit
+//            length.
 #include "dresd_device.h"
 
 namespace dresd {
@@ -258,6 +261,28 @@ __global__ void __launch_bounds__(256) dresd_kmeans_finish(KmeansParams p) {
   for (int j = lane; j < p.d; j += kWaveSize) out[j] = (float)((double)s[j] * inv);
 }
 
+// One wave per centroid: centroid j = row pick(j) / ||row pick(j)||, with
+// pick(j) = (offset + floor(j n / P)) mod n; a zero row gives a zero centroid.
+template <int DT>
+__global__ void __launch_bounds__(256) dresd_kmeans_init(KmeansParams p) {
+  const int lane = threadIdx.x & 63;
+  const int part = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (part >= p.P) return;
+  const uint64_t n = (uint64_t)p.n;
+  const uint64_t row = ((uint64_t)p.offset + (uint64_t)part * n / (uint64_t)p.P) % n;
+  const int64_t base = (int64_t)row * p.d;
+  double ss = 0.0;
+  for (int j = lane; j < p.d; j += kWaveSize) {
+    const double v = (double)load_elem<DT>(p.x, base + j);
+    ss += v * v;
+  }
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, kWaveSize);
+  const double inv = ss > 0.0 ? 1.0 / sqrt(ss) : 0.0;
+  float *out = p.centroids_out + (int64_t)part * p.d;
+  for (int j = lane; j < p.d; j += kWaveSize)
+    out[j] = (float)((double)load_elem<DT>(p.x, base + j) * inv);
+}
+
 template <typename F>
 hipError_t launch1(F *k, dim3 grid, dim3 block, KmeansParams &p, hipStream_t st) {
   void *args[] = {&p};
@@ -292,6 +317,14 @@ hipError_t launch_kmeans_update(const KmeansParams &pin, int cus, hipStream_t st
     if (e != hipSuccess) return e;
   }
   return launch1(dresd_kmeans_finish, dim3((unsigned)((p.P + 3) / 4)), dim3(256), p, st);
+}
+
+hipError_t launch_kmeans_init(const KmeansParams &pin, hipStream_t st) {
+  KmeansParams p = pin;
+  const dim3 grid((unsigned)((p.P + 3) / 4));
+  if (p.dtype == kF32) return launch1(dresd_kmeans_init<kF32>, grid, dim3(256), p, st);
+  if (p.dtype == kF16) return launch1(dresd_kmeans_init<kF16>, grid, dim3(256), p, st);
+  return launch1(dresd_kmeans_init<kBF16>, grid, dim3(256), p, st);
 }
 
 }  // namespace dresd

@@ -1420,6 +1420,34 @@ dresd_status dresd_kmeans_update(const void *x, int64_t n, int32_t d, int32_t dt
   return DRESD_OK;
 }
 
+// First output of SplitMix64 (Steele, Lea and Flood, "Fast splittable
+// pseudorandom number generators", 2014) started from state `seed`.
+static uint64_t splitmix64_first(uint64_t seed) {
+  uint64_t z = seed + 0x9e3779b97f4a7c15ULL;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+  return z ^ (z >> 31);
+}
+
+dresd_status dresd_kmeans_init(const void *x, int64_t n, int32_t d, int32_t dtype, int32_t P,
+                               uint64_t seed, float *centroids, dresd_stream stream) {
+  if (n < 1 || n > DRESD_N_MAX) return fail(DRESD_EINVAL, "n out of range");
+  if (d < 1 || d > 16384) return fail(DRESD_EINVAL, "d out of range");
+  if (dtype < DRESD_F32 || dtype > DRESD_BF16) return fail(DRESD_EINVAL, "unknown dtype");
+  if (P < 1 || P > DRESD_PARTS_MAX || P > n) return fail(DRESD_EINVAL, "need 1 <= P <= n");
+  if (!x || !centroids) return fail(DRESD_EINVAL, "NULL pointer argument");
+  KmeansParams p = {};
+  p.x = x;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.P = P;
+  p.centroids_out = centroids;
+  p.offset = (int64_t)(splitmix64_first(seed) % (uint64_t)n);
+  DRESD_HIP(launch_kmeans_init(p, static_cast<hipStream_t>(stream)));
+  return DRESD_OK;
+}
+
 dresd_status dresd_ivf_profile_enable(dresd_ivf *v, int32_t on) {
   if (!v) return fail(DRESD_EINVAL, "partitioned index is NULL");
   return dresd_profile_enable(v->ix, on);

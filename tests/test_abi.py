@@ -109,6 +109,11 @@ def test_new_entry_points_reject_bad_arguments_before_device_work():
     assert lib.dresd_kmeans_assign(None, 10, 8, 0, None, 2, None, None, None) == E
     assert lib.dresd_kmeans_assign(None, 0, 8, 0, None, 2, None, None, None) == 0
     assert lib.dresd_kmeans_update(None, 10, 8, 0, None, 2, None, None, None) == E
+    for n, d, dt, P in [(0, 8, 0, 1), (10, 0, 0, 2), (10, 20000, 0, 2), (10, 8, 3, 2),
+                        (10, 8, 0, 0), (10, 8, 0, 11)]:
+        assert lib.dresd_kmeans_init(fake, n, d, dt, P, 7, fake, None) == E
+    assert lib.dresd_kmeans_init(None, 10, 8, 0, 2, 7, fake, None) == E
+    assert lib.dresd_kmeans_init(fake, 10, 8, 0, 2, 7, None, None) == E
     # bandwidth probe
     ms = ctypes.c_double()
     assert lib.dresd_bw_probe(None, 1 << 20, 1, 0, ctypes.byref(ms), None) == E

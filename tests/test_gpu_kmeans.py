@@ -5,7 +5,9 @@ least tol the GPU picks the same centroid; elsewhere its pick scores within
 tol of the best (exact scores from the oracle); its reported score is within
 tol of the best.  tol = (d + 2) 2^-24 bounds an fp32 sum of d exact products
 of unit vectors.  Exact ties (duplicate centroids) go to the lower id.
-Update: given the oracle's assignment, centroids within 1e-6 of the oracle's
+Seeding: centroids within 6e-8 of the oracle's picks made unit (one fp32
+rounding of each element), a zero row giving a zero centroid.  Update: given
+the oracle's assignment, centroids within 1e-6 of the oracle's
 (2^-30 fixed-point sums), counts exact, bitwise deterministic, empty and
 zero-sum partitions unchanged.  Training: the objective never decreases, and
 the trained partitions give a partitioned search whose every row comes from a
@@ -108,6 +110,31 @@ def test_kmeans_update(gpu_lib, dt, n, d, P):
     cg2 = torch.from_numpy(old).to(DEV)
     kmeans_update(keys.to(DEV), torch.from_numpy(a).to(DEV), cg2)
     assert torch.equal(cg, cg2)
+
+
+@pytest.mark.parametrize("dt,n,d,P,seed", [
+    ("f32", 37, 5, 1, 0), ("f16", 1000, 128, 64, 5), ("bf16", 999, 130, 999, 2 ** 64 - 1),
+    ("f16", 4097, 67, 300, 12345)])
+def test_kmeans_init_matches_oracle(gpu_lib, dt, n, d, P, seed):
+    from paper_2502_15572_amd import kmeans_init
+    say("kmeans init %s n=%d d=%d P=%d seed=%d" % (dt, n, d, P, seed))
+    rng = np.random.default_rng(n + d)
+    keys = as_keys(unit(rng, n, d), dt)
+    pick, _ = oracle.kmeans_init(np.ones((n, 1)), P, seed)
+    if P > 3:
+        keys[int(pick[3])] = 0  # a zero row gives a zero centroid
+    kb, kdt = to_numpy_bits(keys)
+    x = oracle.decode_keys(kb, kdt)
+    pick, want = oracle.kmeans_init(x, P, seed)
+    xd = keys.to(DEV)
+    got = kmeans_init(xd, P, seed)
+    torch.cuda.synchronize()
+    got = got.cpu().numpy().astype(np.float64)
+    # one fp32 rounding of each element of a unit vector: within 2^-25 (+ slack)
+    assert np.max(np.abs(got - want)) <= 6e-8
+    zero = ~np.any(x[pick] != 0, axis=1)
+    assert zero.sum() == (1 if P > 3 else 0)
+    assert np.array_equal(got[zero], np.zeros_like(got[zero]))
 
 
 def test_train_partitions_and_search(gpu_lib):

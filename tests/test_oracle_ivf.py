@@ -170,6 +170,38 @@ def test_kmeans_separated_clusters_and_monotone_objective():
         prev = obj
 
 
+def test_splitmix64_published_outputs():
+    # outputs of the generator's published reference implementation: from
+    # state 0, and from state 1234567 (the sequence its authors' test prints)
+    assert oracle.splitmix64(0, 3) == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4,
+                                       0x06C45D188009454F]
+    assert oracle.splitmix64(1234567, 5) == [6457827717110365317, 3203168211198807973,
+                                             9817491932198370423, 4593380528125082431,
+                                             16408922859458223821]
+
+
+def test_kmeans_init_picks_and_units():
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((23, 5))
+    x[4] = 0.0
+    o = oracle.splitmix64(9, 1)[0] % 23
+    for P in (1, 2, 5, 7, 22, 23):
+        pick, c = oracle.kmeans_init(x, P, 9)
+        # brute force of the definition: offset, then floor(j n / P) steps
+        assert pick.tolist() == [(o + math.floor(j * 23 / P)) % 23 for j in range(P)]
+        assert len(set(pick.tolist())) == P and pick[0] == o
+        for j, r in enumerate(pick):
+            nrm = math.sqrt(sum(float(v) ** 2 for v in x[r]))
+            want = x[r] / nrm if nrm > 0 else np.zeros(5)
+            assert np.allclose(c[j], want, atol=1e-15)
+    # P = n takes every row once; seeds move the offset
+    pick, _ = oracle.kmeans_init(x, 23, 9)
+    assert sorted(pick.tolist()) == list(range(23))
+    assert len({int(oracle.kmeans_init(x, 3, s)[0][0]) for s in range(10)}) > 1
+    with pytest.raises(ValueError):
+        oracle.kmeans_init(x, 24, 0)
+
+
 def test_partitioned_filtered_reductions_and_brute_force():
     """With the next-token filter: every partition probed is the filtered
     exact search; a tiny brute force of filter-and-probe; one token that no
