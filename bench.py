@@ -41,9 +41,9 @@ def log(*a):
 
 
 SCAN_UNIT = {"single_tile": "dresd_kernels.hip", "shared_key": "dresd_scan_mq.hip",
-             "single_tile_grouped": "dresd_kernels.hip"}
+             "single_tile_grouped": "dresd_kernels.hip", "tiled": "dresd_scan_mq.hip"}
 SCAN_KERNEL_NAME = {"single_tile": "dresd_scan_main", "shared_key": "dresd_scanmq_main",
-                    "single_tile_grouped": "dresd_scan_main_shared"}
+                    "single_tile_grouped": "dresd_scan_main_shared", "tiled": "dresd_scantc_main"}
 
 
 def kernel_hash(unit: str) -> str:

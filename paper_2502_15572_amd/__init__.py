@@ -37,7 +37,7 @@ def _stream_handle(stream=None):
 
 
 # dresd_search_plan's scan kinds
-SCAN_KINDS = {0: "single_tile", 1: "shared_key", 2: "single_tile_grouped"}
+SCAN_KINDS = {0: "single_tile", 1: "shared_key", 2: "single_tile_grouped", 3: "tiled"}
 
 
 class Index:

@@ -179,6 +179,20 @@ inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, bo
 }
 // Query-operand kernel of the shared-key scan for a key type (launch with
 // 256 threads, one thread per 16-byte chunk).
+// Tiled contraction (both operands through LDS): qtw query tiles per
+// launch (4, or 8 for bf16), tpw key tiles per wave (4 or 1), ring stages
+// (5 or 3 at tpw 4; 8 or 4 at tpw 1); null for other shapes.
+ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int stages, bool main_pass);
+ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int stages, bool main_pass);
+inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int stages, bool main_pass) {
+  if (dtype == kF16) return scan_tc_kernel_f16(qtw, tpw, stages, main_pass);
+  if (dtype == kBF16) return scan_tc_kernel_bf16(qtw, tpw, stages, main_pass);
+  return nullptr;
+}
+__host__ __device__ inline size_t scan_tc_lds_bytes(int qtw, int tpw, int stages, int nq, int C) {
+  return (size_t)stages * (4 * tpw + qtw) * kBlockBytes +
+         (size_t)(kScanThreads / kWaveSize) * scan_mq_wave_bytes(nq, C);
+}
 void *qop_kernel_f16();
 void *qop_kernel_bf16();
 inline void *qop_kernel(int dtype) {

@@ -162,6 +162,8 @@ constexpr int kGroupsPerLaunch = 8;
 struct Plan {
   int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
   bool mq = false;                  // shared-key scan (queries in registers)
+  bool tc = false;                  // tiled contraction (queries and keys through LDS)
+  int tpw_main = 4, tpw_sample = 1;  // tiled contraction: key tiles per wave per pass kind
   int bmax = 0;                 // queries per group
   int bl = 0;                   // queries per launch (several groups)
   int B = 0, nl = 0;            // batch, launches (launch i: group_of(pl, i))
@@ -170,7 +172,7 @@ struct Plan {
   int64_t strides[3] = {0, 0, 0};  // sampled passes, sparsest first
   int npass = 0;                   // sampled passes used
   ScanKernel kmain = nullptr, ksample = nullptr;
-  size_t lds = 0;
+  size_t lds = 0, lds_s = 0;    // LDS bytes of the main and the sampled scans
   int wg_max = 0;               // resident workgroups of the scan kernels
   int G_max = 0;
   int64_t spill_cap = 0;        // merge candidates per query beyond its LDS cache
@@ -244,7 +246,30 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   const int qt_all = (int)ceil_div((int64_t)B * pl.terms, 16);  // query tiles of the batch
   const bool mq_type = (ix->dtype == kF16 && pl.terms == 1) || ix->dtype == kBF16;
   const bool mq_kb = ix->KB == 4 || ix->KB == 8 || ix->KB == 16 || ix->KB == 32;
-  if (mq_type && mq_kb && (qt_all >= 2 || pl.terms < 4)) {
+  // Keys wider than the shared-key scan can hold the queries for, at batches
+  // of two or more query tiles: the tiled contraction streams both operands
+  // through LDS (4 query tiles per launch, or 8 for bf16: 64 queries).
+  if (mq_type && ix->KB > 32 && qt_all >= 2 && pl.terms < 4 && !filt) {
+    const int qtw = (ix->dtype == kBF16 && qt_all > 4) ? 8 : 4;
+    const int nq = qtw * pl.qpt;
+    int sm = 0, ss = 0;
+    for (int st : {5, 3})
+      if (!sm && scan_tc_lds_bytes(qtw, pl.tpw_main, st, nq, pl.C) <= ix->lds_max) sm = st;
+    for (int st : {8, 4})
+      if (!ss && scan_tc_lds_bytes(qtw, pl.tpw_sample, st, nq, pl.C) <= ix->lds_max) ss = st;
+    if (sm && ss) {
+      pl.tc = true;
+      pl.qt = qtw;
+      pl.bmax = std::min(B, nq);
+      pl.CL = 0;
+      pl.kmain = scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, sm, true);
+      pl.ksample = scan_tc_kernel(ix->dtype, qtw, pl.tpw_sample, ss, false);
+      pl.lds = scan_tc_lds_bytes(qtw, pl.tpw_main, sm, nq, pl.C);
+      pl.lds_s = scan_tc_lds_bytes(qtw, pl.tpw_sample, ss, nq, pl.C);
+    }
+  }
+  if (pl.tc) {
+  } else if (mq_type && mq_kb && (qt_all >= 2 || pl.terms < 4)) {
     // Several query tiles, or one of one- or two-column queries (four or
     // two scores per lane per key tile): queries stationary in registers,
     // keys shared
@@ -296,7 +321,9 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   const int ngr = (int)ceil_div(B, bmax);
   // The single-tile scan serves several groups per launch; launch sizes
   // differ by at most one query and each splits into groups of <= bmax.
-  const int per = pl.mq ? 1 : std::max(1, std::min({ngr, kGroupsPerLaunch, (int)(kMaxGroup / bmax)}));
+  const int per = (pl.mq || pl.tc)
+                      ? 1
+                      : std::max(1, std::min({ngr, kGroupsPerLaunch, (int)(kMaxGroup / bmax)}));
   pl.B = B;
   pl.nl = (int)ceil_div(ngr, per);
   pl.bl = (int)ceil_div(B, pl.nl);  // launch sizes differ by at most one query
@@ -305,18 +332,19 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
     pl.ksample = scan_kernel(ix->dtype, pl.qt, pl.terms, false, true);
   }
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
+  if (!pl.tc) pl.lds_s = pl.lds;
   if (pl.lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS");
   int occ = std::min(occupancy(ix, pl.kmain, pl.lds, keep_cache),
-                     occupancy(ix, pl.ksample, pl.lds, keep_cache));
+                     occupancy(ix, pl.ksample, pl.lds_s, keep_cache));
   // At most four workgroups per CU (few enough lists for the merge to keep
   // their best keys in LDS); one where fewer, longer HBM streams measured
   // faster: the single-tile scan with one query tile, and the shared-key
   // scan over 32-block (1 KiB-row) key tiles.
-  const bool one_per_cu = pl.mq ? ix->KB >= 32 : pl.qt == 1;
+  const bool one_per_cu = pl.tc || (pl.mq ? ix->KB >= 32 : pl.qt == 1);
   pl.wg_max = ix->cus * std::min(occ, one_per_cu ? kMaxTileWgPerCu : kMaxScanWgPerCu);
   // lists per query: one per wave, or one per workgroup for the shared-key
   // scan; at most kMergeLists
-  const int lists_per_wg = pl.mq ? 1 : kScanThreads / kWaveSize;
+  const int lists_per_wg = pl.mq ? 1 : kScanThreads / kWaveSize;  // tiled contraction: per wave
   pl.wg_max = std::min(pl.wg_max, kMergeLists / lists_per_wg);
   pl.G_max = pl.wg_max * lists_per_wg;
   // Small batches (B <= 8): every wave keeps its own running top-k and sorts
@@ -338,8 +366,12 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   pl.sort_lists = B <= 8;
   if (!pl.sort_lists || (k >= 16 && (int64_t)B * k >= 64)) {
     const bool dense = (int64_t)B * k >= 8192;
+    // The tiled contraction's passes take about as long at stride 64 as
+    // at 256 (a K loop over every column per panel, whatever the panel
+    // count): one pass at 64.
     const std::vector<int64_t> ladder =
-        dense    ? std::vector<int64_t>{4096, 256, 16}
+        pl.tc    ? std::vector<int64_t>{64}
+        : dense  ? std::vector<int64_t>{4096, 256, 16}
         : pl.mq  ? std::vector<int64_t>{4096, 64}
                  : std::vector<int64_t>{256};
     for (int64_t P : ladder) {
@@ -359,7 +391,7 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   pl.off_lists = pl.off_lfirst + up(nb * pl.G_max * 8);
   pl.off_spill = pl.off_lists + up(nb * pl.G_max * pl.C * 8);
   pl.off_qop = pl.off_spill + up(nb * (size_t)std::max<int64_t>(1, pl.spill_cap) * 8);
-  pl.bytes = pl.off_qop + (pl.mq ? up((size_t)pl.qt * ix->KB * kBlockBytes) : 0);
+  pl.bytes = pl.off_qop + ((pl.mq || pl.tc) ? up((size_t)pl.qt * ix->KB * kBlockBytes) : 0);
   return DRESD_OK;
 }
 
@@ -367,9 +399,11 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
 // launch has gr.ng times as many).  Several groups: each gets a multiple of
 // 8 (one key range per XCD slot) and together they fit the resident grid,
 // so the readers of a range run at the same time.
-int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit) {
+int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit, bool main_pass = true) {
   const int wpg = kScanThreads / kWaveSize;
-  int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(nvisit, pl.mq ? 1 : wpg));
+  // tiled contraction: whole panels of 4 tpw tiles
+  const int per_wg = pl.tc ? wpg * (main_pass ? pl.tpw_main : pl.tpw_sample) : pl.mq ? 1 : wpg;
+  int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(nvisit, per_wg));
   if (gr.ng > 1) wgs = std::min<int64_t>(wgs, std::max<int64_t>(8, pl.wg_max / gr.ng / 8 * 8));
   return wgs;
 }
@@ -578,6 +612,15 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
           }
         }
   for (int v = 0; v < 3; ++v)
+    for (int qtw : {4, 8})
+      for (int tpw : {1, 4})
+        for (int st : {3, 4, 5, 8})
+          for (bool mp : {false, true})
+            if (ScanKernel kf = scan_tc_kernel(v, qtw, tpw, st, mp))
+              (void)hipFuncSetAttribute((const void *)kf,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)ix->lds_max);
+  for (int v = 0; v < 3; ++v)
     if (ScanKernel kf = scan_parts_kernel(v))
       (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)ix->lds_max);
@@ -657,7 +700,7 @@ dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int
   if (sample_passes) *sample_passes = (int32_t)pl.npass;
   if (scan_waves) *scan_waves = (int32_t)(pass_wgs(pl, g0, ix->T) * g0.ng * wpg);
   if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
-  if (scan_kind) *scan_kind = pl.mq ? 1 : (g0.ng > 1 ? 2 : 0);
+  if (scan_kind) *scan_kind = pl.tc ? 3 : pl.mq ? 1 : (g0.ng > 1 ? 2 : 0);
   return DRESD_OK;
 }
 
@@ -778,7 +821,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     sp.probes64 = nullptr;
     sp.part_tile = nullptr;
     sp.seg_lds = sp.P = 0;
-    if (pl.mq) {
+    if (pl.mq || pl.tc) {
       QopParams qp;
       qp.queries = sp.queries;
       qp.out = ws + pl.off_qop;
@@ -811,7 +854,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       sp.stride = stride;
       sp.nvisit = ceil_div(ix->T, stride);
       sp.tau = tau_in;
-      const int64_t wgs = pass_wgs(pl, gr, sp.nvisit);
+      const int64_t wgs = pass_wgs(pl, gr, sp.nvisit, main_pass);
       sp.G = (int)(pl.mq ? wgs : wgs * wpg);
       void *sargs[] = {&sp};
       hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -821,7 +864,8 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
         if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
       }
       DRESD_HIP(launch((const void *)(main_pass ? pl.kmain : pl.ksample),
-                       dim3((unsigned)(wgs * gr.ng)), dim3(kScanThreads), sargs, pl.lds, e0, e1));
+                       dim3((unsigned)(wgs * gr.ng)), dim3(kScanThreads), sargs,
+                       main_pass ? pl.lds : pl.lds_s, e0, e1));
       if (main_pass && prof) {
         ix->ev_scan.push_back(e0);
         ix->ev_scan.push_back(e1);

@@ -112,99 +112,96 @@ __device__ __forceinline__ void copy2_to_lds(const void *src, uint32_t voff0, ui
 
 }  // namespace
 
-// QTW query tiles per wave, KBT 32-dim blocks per key tile (must equal the
-// index's blocks per tile), CPQ operand columns per query, S LDS stages;
-// FILT: next-token-filtered search (a separate instantiation, so the
-// unfiltered stream loop carries none of its code).
-template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
-__device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
-  constexpr int QPT = 16 / CPQ;   // queries per tile
-  constexpr int NS = 4 / CPQ;     // scores per lane per query tile
-  constexpr int NQW = QTW * QPT;  // queries per wave
-  constexpr int NP = QTW * NS;    // scores per lane per key tile
-  constexpr int SB = kMqStageBlocks;
-  constexpr int TPS = KBT >= SB ? 1 : SB / KBT;  // key tiles per stage
-  constexpr int SPT = KBT >= SB ? KBT / SB : 1;  // stages per key tile
-  constexpr int BPT = KBT >= SB ? SB : KBT;      // blocks of a tile per stage
-  constexpr int CB = kMqCandBuf;
-  constexpr int WAIT = 2 * (S - 2);  // copies of later stages still in flight
-  // Interleave each tile's threshold test with the next tile's matrix
-  // instructions when a key tile carries few of them (measured: 33.5M keys x
-  // 128 dims at 128 queries, 8 per tile, main pass 1.43 -> 1.37 ms; at
-  // 10M x 256 and 256 queries, 32 per tile, it was slower).
-  constexpr bool kDefer = BPT * QTW <= 16;
-  static_assert(KBT >= 4 && S >= 3 && NP <= 32, "shape");
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+// Candidate state of one wave of the shared-key scans.  The wave owns NQW
+// queries starting at q0.  For each it keeps, in LDS, an exact threshold
+// (keys above it may enter), that threshold as a float for the per-tile
+// test, the length of its list in HBM (one list per (query, list slot)) and
+// the best key listed; and a buffer of (key, query) pairs that passed the
+// test, moved into the lists only when it fills up.  QTW query tiles of CPQ
+// operand columns per query; FILT: next-token-filtered search.
+template <int DT, int QTW, int CPQ, bool FILT>
+struct WaveCands {
+  static constexpr int QPT = 16 / CPQ;   // queries per tile
+  static constexpr int NS = 4 / CPQ;     // scores per lane per query tile
+  static constexpr int NQW = QTW * QPT;  // queries per wave
+  static constexpr int NP = QTW * NS;    // scores per lane per key tile
+  static constexpr int CB = kMqCandBuf;
+  static_assert(NP <= 32, "score slots");
 
-  const int lane = threadIdx.x & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 4, m = lane & 15;
-  const int B = p.B, C = p.C, k = p.k, G = p.G;
-  const int wg = blockIdx.x;
+  const ScanParams &p;
+  const int lane, g, m, q0, lslot;
+  uint64_t *ck;       // buffered keys [CB]
+  uint64_t *scr;      // sort scratch [C]
+  uint64_t *st_key;   // keep keys > st_key [NQW]
+  uint8_t *cq;        // query of ck[e] [CB]
+  uint32_t *st_cnt;   // HBM list length [NQW]
+  float *st_thr;      // float threshold [NQW]
+  uint64_t *st_max;   // best listed key [NQW]
+  int32_t *nt_slot;   // filtered search: next token per score slot [4 lane groups][NP]
+  float thr[NP];      // this lane's thresholds, slot j = t * NS + s
+  int ntr[NP <= 8 ? NP : 1];  // filtered search with few slots: nt_slot in VGPRs
+  int cnt = 0;        // buffered candidates (wave-uniform)
 
-  // LDS: ring of S stages, then one candidate region per wave.
-  const size_t wreg = scan_mq_wave_bytes(NQW, C);
-  unsigned char *w0 = smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg;
-  uint64_t *ck = reinterpret_cast<uint64_t *>(w0);  // buffered keys [CB]
-  uint64_t *scr = ck + CB;                          // sort scratch [C]
-  uint64_t *st_key = scr + C;                       // keep keys > st_key [NQW]
-  uint8_t *cq = reinterpret_cast<uint8_t *>(st_key + NQW);    // query of ck[e] [CB]
-  uint32_t *st_cnt = reinterpret_cast<uint32_t *>(cq + CB);   // HBM list length [NQW]
-  float *st_thr = reinterpret_cast<float *>(st_cnt + NQW);    // float threshold [NQW]
-  uint64_t *st_max = reinterpret_cast<uint64_t *>(st_thr + NQW);  // best listed key [NQW]
-  // Filtered search (Section 3.5): next token of each score slot, and a
-  // ring of first-token copies, one per stage (its tiles' 16 rows each).
-  constexpr bool filt = FILT;
-  int32_t *nt_slot = reinterpret_cast<int32_t *>(
-      smem + (size_t)S * SB * kBlockBytes + (size_t)(kScanThreads / kWaveSize) * wreg +
-      (size_t)wv * scan_mq_filter_bytes(S, NP));  // [4 lane groups][NP]
-  int32_t *fring = nt_slot + 4 * NP;              // [S][64]
-
-  // Queries of this wave: tiles [wv*QTW, wv*QTW + QTW) of the batch.
-  const int q0 = wv * NQW;
-  const u4 *qop = static_cast<const u4 *>(p.qop) + lane;
-  u4 qreg[QTW][KBT];
-#pragma unroll
-  for (int t = 0; t < QTW; ++t)
-#pragma unroll
-    for (int kb = 0; kb < KBT; ++kb) qreg[t][kb] = qop[((wv * QTW + t) * KBT + kb) * 64];
-  // Wait for these loads here: left to the compiler, the wait lands at their
-  // first use inside the stream loop, where (not knowing the LDS copies are
-  // younger) it would drain the whole copy ring on every stage.
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-  for (int i = lane; i < NQW; i += kWaveSize) {
-    uint64_t tk = 0;
-    float tf = -__builtin_inff();
-    if (q0 + i >= B) {
-      tk = ~0ull;
-      tf = __builtin_inff();
-    } else if (p.tau && p.tau[q0 + i] != 0) {
-      tk = p.tau[q0 + i] - 1;  // keep keys >= tau
-      tf = order_value((uint32_t)(tk >> 32));
-    }
-    st_key[i] = tk;
-    st_cnt[i] = 0;
-    st_thr[i] = tf;
-    st_max[i] = 0;
+  // `region`: the wave's scan_mq_wave_bytes(NQW, C) bytes of LDS.
+  __device__ __forceinline__ WaveCands(const ScanParams &p_, unsigned char *region, int32_t *nt,
+                                       int q0_, int lslot_)
+      : p(p_), lane(threadIdx.x & 63), g((threadIdx.x & 63) >> 4), m(threadIdx.x & 15), q0(q0_),
+        lslot(lslot_), nt_slot(nt) {
+    ck = reinterpret_cast<uint64_t *>(region);
+    scr = ck + CB;
+    st_key = scr + p.C;
+    cq = reinterpret_cast<uint8_t *>(st_key + NQW);
+    st_cnt = reinterpret_cast<uint32_t *>(cq + CB);
+    st_thr = reinterpret_cast<float *>(st_cnt + NQW);
+    st_max = reinterpret_cast<uint64_t *>(st_thr + NQW);
   }
-  if (filt)
-    for (int i = lane; i < 4 * NP; i += kWaveSize) {
-      const int gg = i / NP, j = i % NP;
-      const int q = q0 + (j / NS) * QPT + gg * NS + (j % NS);
-      nt_slot[i] = q < B ? p.next_tok[q] : 0;
+
+  // Thresholds from the sampled passes (none: every key enters; queries
+  // past the batch: none ever does).
+  __device__ __forceinline__ void init() {
+    const int B = p.B;
+    for (int i = lane; i < NQW; i += kWaveSize) {
+      uint64_t tk = 0;
+      float tf = -__builtin_inff();
+      if (q0 + i >= B) {
+        tk = ~0ull;
+        tf = __builtin_inff();
+      } else if (p.tau && p.tau[q0 + i] != 0) {
+        tk = p.tau[q0 + i] - 1;  // keep keys >= tau
+        tf = order_value((uint32_t)(tk >> 32));
+      }
+      st_key[i] = tk;
+      st_cnt[i] = 0;
+      st_thr[i] = tf;
+      st_max[i] = 0;
     }
-  wave_sync_lds();
+    if (FILT)
+      for (int i = lane; i < 4 * NP; i += kWaveSize) {
+        const int gg = i / NP, j = i % NP;
+        const int q = q0 + (j / NS) * QPT + gg * NS + (j % NS);
+        nt_slot[i] = q < B ? p.next_tok[q] : 0;
+      }
+    wave_sync_lds();
+    load_thr();
+    if (FILT && NP <= 8) {
+#pragma unroll
+      for (int j = 0; j < (NP <= 8 ? NP : 1); ++j) ntr[j] = nt_slot[g * NP + j];
+    }
+  }
+
   // Score slot j = t * NS + s of a lane belongs to query t * QPT + g * NS + s.
-  float thr[NP];
-  auto load_thr = [&]() {
+  __device__ __forceinline__ void load_thr() {
 #pragma unroll
     for (int j = 0; j < NP; ++j) thr[j] = st_thr[(j / NS) * QPT + g * NS + (j % NS)];
-  };
-  load_thr();
-  auto list_of = [&](int i) { return p.lists + ((size_t)(q0 + i) * G + wg) * C; };
+  }
+
+  __device__ __forceinline__ uint64_t *list_of(int i) const {
+    return p.lists + ((size_t)(q0 + i) * p.G + lslot) * p.C;
+  }
 
   // Cut query i's full HBM list to its k best keys and raise its threshold.
-  auto cut = [&](int i) {
+  __device__ void cut(int i) {
+    const int C = p.C, k = p.k;
     uint64_t *list = list_of(i);
     __threadfence_block();  // this wave's list stores are visible to its loads
     for (int e = lane; e < C; e += kWaveSize) scr[e] = list[e];
@@ -221,12 +218,12 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
       }
     }
     wave_sync_lds();
-  };
+  }
 
   // Move the buffered candidates into the HBM lists (keys that still beat
   // their query's exact threshold), cutting lists that fill up.
-  int cnt = 0;  // buffered candidates (wave-uniform)
-  auto flush = [&]() {
+  __device__ __forceinline__ void flush() {
+    const int C = p.C;
     wave_sync_lds();
     for (int e0 = 0; e0 < cnt; e0 += kWaveSize) {
       const int e = e0 + lane;
@@ -256,23 +253,17 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     cnt = 0;
     wave_sync_lds();
     load_thr();
-  };
-
-  // This workgroup's key tiles: visited tiles [v0, v1), KBT blocks each.
-  const int64_t v0 = wave_uniform(p.nvisit * wg / G);
-  const int64_t v1 = wave_uniform(p.nvisit * (wg + 1) / G);
-  const int64_t ntile = v1 - v0;
-  f4 acc[QTW];
+  }
 
   // Lanes below this one holding a set bit of mask `mk`.
-  auto rank_in = [&](uint64_t mk) {
+  __device__ __forceinline__ int rank_in(uint64_t mk) const {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32),
                                           __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u));
-  };
+  }
 
   // Buffer the candidates of key tile `tile` (rows tile*16 .. +15); rare.
   // Bit t of hit_t: some score of query tile t reached its threshold.
-  auto candidates = [&](int64_t tile, const float (&sc)[NP], uint32_t hit_t) {
+  __device__ __forceinline__ void candidates(int64_t tile, const float (&sc)[NP], uint32_t hit_t) {
     const int64_t row64 = tile * kTileRows + m;
     const bool row_ok = row64 < p.N;
     const uint32_t row = (uint32_t)row64;
@@ -321,19 +312,12 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
         for (int i = 0; i + 1 < NP; ++i) cur[i] = cur[i + 1];
       }
     }
-  };
-
-  // Filtered search with few score slots: their next tokens stay in VGPRs.
-  int ntr[NP <= 8 ? NP : 1];
-  if (filt && NP <= 8) {
-    wave_sync_lds();
-#pragma unroll
-    for (int j = 0; j < (NP <= 8 ? NP : 1); ++j) ntr[j] = nt_slot[g * NP + j];
   }
+
   // Scores of a finished key tile from its accumulators (the query parts
   // recombined), NaN where the filter drops the row (`f`: the row's first
   // token); NaN fails every threshold test and fmaxf ignores it.
-  auto scores_of = [&](const f4 (&a)[QTW], int f, float (&sc)[NP]) {
+  __device__ __forceinline__ void scores_of(const f4 (&a)[QTW], int f, float (&sc)[NP]) const {
 #pragma unroll
     for (int t = 0; t < QTW; ++t)
 #pragma unroll
@@ -348,22 +332,25 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
         }
         sc[t * NS + s] = v;
       }
-    if (filt) {
+    if (FILT) {
 #pragma unroll
       for (int j = 0; j < NP; ++j)
         if (f != (NP <= 8 ? ntr[j] : nt_slot[g * NP + j])) sc[j] = __builtin_nanf("");
     }
-  };
+  }
+
   // Lanes whose row passes some threshold (v >= thr exactly when
   // v - thr >= 0: round-to-nearest keeps the sign).
-  auto any_hit = [&](const float (&sc)[NP]) {
+  __device__ __forceinline__ uint64_t any_hit(const float (&sc)[NP]) const {
     float mx = sc[0] - thr[0];
 #pragma unroll
     for (int j = 1; j < NP; ++j) mx = fmaxf(mx, sc[j] - thr[j]);
     return __ballot(mx >= 0.0f);
-  };
-  // The slow path of a tile with hits: which query tiles hit, then buffer.
-  auto take = [&](int64_t vt, const float (&sc)[NP]) {
+  }
+
+  // The slow path of key tile `tile` with hits: which query tiles hit,
+  // then buffer.
+  __device__ __forceinline__ void take(int64_t tile, const float (&sc)[NP]) {
     uint32_t hit_t = 0;
 #pragma unroll
     for (int t = 0; t < QTW; ++t) {
@@ -372,8 +359,122 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
       for (int s = 1; s < NS; ++s) mt = fmaxf(mt, sc[t * NS + s] - thr[t * NS + s]);
       if (__ballot(mt >= 0.0f)) hit_t |= 1u << t;
     }
-    candidates((v0 + vt) * p.stride, sc, hit_t);
-  };
+    candidates(tile, sc, hit_t);
+  }
+
+  // Publish this wave's lists (one per query per list slot) and per list
+  // its length (kSortedFlag when sorted), best key (0 when empty) and k-th
+  // key (0 unless it holds k sorted keys).  Lane i takes query i; lists
+  // longer than k (every non-empty list when sort_lists) are sorted and cut
+  // to k first.
+  __device__ __forceinline__ void publish() {
+    static_assert(NQW <= kWaveSize, "one lane per query");
+    const int B = p.B, k = p.k, G = p.G;
+    if (cnt > 0) flush();
+    const int i = lane;
+    const bool valid = i < NQW && q0 + i < B;
+    const int n = valid ? (int)st_cnt[i] : 0;
+    const bool sort_me = valid && (n > k || (p.sort_lists && n > 0));
+    if (valid && !sort_me) {
+      const size_t o = (size_t)(q0 + i) * G + lslot;
+      p.lcnt[o] = (uint32_t)n | ((n == 1) ? kSortedFlag : 0u);
+      p.lfirst[o] = (n == 0) ? 0ull : st_max[i];
+      p.lkth[o] = 0ull;
+    }
+    uint64_t todo = __ballot(sort_me);
+    while (todo) {
+      const int qi = __ffsll((long long)todo) - 1;
+      todo &= todo - 1;
+      uint64_t *list = list_of(qi);
+      const int nq = __builtin_amdgcn_readlane(n, qi);
+      __threadfence_block();
+      const int keep = nq < k ? nq : k;
+      RankEnds ends;
+      if (nq <= kWaveRankMax) {
+        for (int e = lane; e < nq; e += kWaveSize) scr[e] = list[e];
+        wave_sync_lds();
+        ends = wave_rank_top(scr, nq, list, keep, lane);
+      } else {
+        int np2 = 2;
+        while (np2 < nq) np2 <<= 1;
+        for (int e = lane; e < np2; e += kWaveSize) scr[e] = (e < nq) ? list[e] : 0ull;
+        wave_sync_lds();
+        wave_bitonic_desc(scr, np2, lane);
+        for (int e = lane; e < keep; e += kWaveSize) list[e] = scr[e];
+        ends.first = scr[0];
+        ends.last = scr[keep - 1];
+      }
+      if (lane == 0) {
+        const size_t o = (size_t)(q0 + qi) * G + lslot;
+        p.lcnt[o] = (uint32_t)keep | kSortedFlag;
+        p.lfirst[o] = ends.first;
+        p.lkth[o] = (keep == k) ? ends.last : 0ull;
+      }
+      wave_sync_lds();
+    }
+  }
+};
+
+// QTW query tiles per wave, KBT 32-dim blocks per key tile (must equal the
+// index's blocks per tile), CPQ operand columns per query, S LDS stages;
+// FILT: next-token-filtered search (a separate instantiation, so the
+// unfiltered stream loop carries none of its code).
+template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
+__device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
+  using WC = WaveCands<DT, QTW, CPQ, FILT>;
+  constexpr int NQW = WC::NQW;  // queries per wave
+  constexpr int NP = WC::NP;    // scores per lane per key tile
+  constexpr int SB = kMqStageBlocks;
+  constexpr int TPS = KBT >= SB ? 1 : SB / KBT;  // key tiles per stage
+  constexpr int SPT = KBT >= SB ? KBT / SB : 1;  // stages per key tile
+  constexpr int BPT = KBT >= SB ? SB : KBT;      // blocks of a tile per stage
+  constexpr int WAIT = 2 * (S - 2);  // copies of later stages still in flight
+  // Interleave each tile's threshold test with the next tile's matrix
+  // instructions when a key tile carries few of them (measured: 33.5M keys x
+  // 128 dims at 128 queries, 8 per tile, main pass 1.43 -> 1.37 ms; at
+  // 10M x 256 and 256 queries, 32 per tile, it was slower).
+  constexpr bool kDefer = BPT * QTW <= 16;
+  static_assert(KBT >= 4 && S >= 3, "shape");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int m = lane & 15;
+  const int G = p.G;
+  const int wg = blockIdx.x;
+
+  // LDS: ring of S stages, then one candidate region per wave, then (filtered
+  // search) per wave the next token of each score slot and a ring of
+  // first-token copies, one per stage (its tiles' 16 rows each).
+  const size_t wreg = scan_mq_wave_bytes(NQW, p.C);
+  constexpr bool filt = FILT;
+  int32_t *nt_slot = reinterpret_cast<int32_t *>(
+      smem + (size_t)S * SB * kBlockBytes + (size_t)(kScanThreads / kWaveSize) * wreg +
+      (size_t)wv * scan_mq_filter_bytes(S, NP));  // [4 lane groups][NP]
+  int32_t *fring = nt_slot + 4 * NP;              // [S][64]
+
+  // Queries of this wave: tiles [wv*QTW, wv*QTW + QTW) of the batch.
+  const int q0 = wv * NQW;
+  const u4 *qop = static_cast<const u4 *>(p.qop) + lane;
+  u4 qreg[QTW][KBT];
+#pragma unroll
+  for (int t = 0; t < QTW; ++t)
+#pragma unroll
+    for (int kb = 0; kb < KBT; ++kb) qreg[t][kb] = qop[((wv * QTW + t) * KBT + kb) * 64];
+  // Wait for these loads here: left to the compiler, the wait lands at their
+  // first use inside the stream loop, where (not knowing the LDS copies are
+  // younger) it would drain the whole copy ring on every stage.
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nt_slot, q0, wg);
+  wc.init();
+
+  // This workgroup's key tiles: visited tiles [v0, v1), KBT blocks each.
+  const int64_t v0 = wave_uniform(p.nvisit * wg / G);
+  const int64_t v1 = wave_uniform(p.nvisit * (wg + 1) / G);
+  const int64_t ntile = v1 - v0;
+
+  // The slow path of visited tile vt with hits.
+  auto take = [&](int64_t vt, const float (&sc)[NP]) { wc.take((v0 + vt) * p.stride, sc); };
 
   if (ntile > 0) {
     const int64_t NB = ntile * KBT;
@@ -485,8 +586,8 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
         }
         if (vt < ntile) {
           float sc[NP];
-          scores_of(acc, fr, sc);
-          if (any_hit(sc)) take(vt, sc);
+          wc.scores_of(acc, fr, sc);
+          if (wc.any_hit(sc)) take(vt, sc);
         }
       }
     } else {
@@ -505,7 +606,7 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
 #pragma unroll
         for (int c = 0; c < SPT; ++c) {
           stage_start(vt);
-          if (c == 0) scores_of(prev, fprev, psc);
+          if (c == 0) wc.scores_of(prev, fprev, psc);
           const u4 *blk = stage_blocks(vt);
           constexpr int NPAIR = BPT / 2;
           constexpr int CH = (NP + NPAIR - 1) / NPAIR;  // test slots per pair of blocks
@@ -527,7 +628,7 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
               float mm = -__builtin_inff();
 #pragma unroll
               for (int j = j0; j < j0 + CH; ++j)
-                if (j < NP) mm = fmaxf(mm, psc[j] - thr[j]);
+                if (j < NP) mm = fmaxf(mm, psc[j] - wc.thr[j]);
               pmx[i / 2] = mm;
             }
 #pragma unroll
@@ -561,62 +662,14 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
       const int64_t lt = nsteps - 1;  // the last tile's test
       if (lt < ntile) {
         float sc[NP];
-        scores_of(accB, fB, sc);
-        if (any_hit(sc)) take(lt, sc);
+        wc.scores_of(accB, fB, sc);
+        if (wc.any_hit(sc)) take(lt, sc);
       }
     }
     wait_vmcnt<0>();  // no LDS copy may land after the workgroup ends
   }
 
-  // Publish this wave's lists (one per query per workgroup) and per list its
-  // length (kSortedFlag when sorted), best key (0 when empty) and k-th key (0
-  // unless it holds k sorted keys).  Lane i takes query i; lists longer than
-  // k (every non-empty list when sort_lists) are sorted and cut to k first.
-  if (cnt > 0) flush();
-  static_assert(NQW <= kWaveSize, "one lane per query");
-  {
-    const int i = lane;
-    const bool valid = i < NQW && q0 + i < B;
-    const int n = valid ? (int)st_cnt[i] : 0;
-    const bool sort_me = valid && (n > k || (p.sort_lists && n > 0));
-    if (valid && !sort_me) {
-      const size_t o = (size_t)(q0 + i) * G + wg;
-      p.lcnt[o] = (uint32_t)n | ((n == 1) ? kSortedFlag : 0u);
-      p.lfirst[o] = (n == 0) ? 0ull : st_max[i];
-      p.lkth[o] = 0ull;
-    }
-    uint64_t todo = __ballot(sort_me);
-    while (todo) {
-      const int qi = __ffsll((long long)todo) - 1;
-      todo &= todo - 1;
-      uint64_t *list = list_of(qi);
-      const int nq = __builtin_amdgcn_readlane(n, qi);
-      __threadfence_block();
-      const int keep = nq < k ? nq : k;
-      RankEnds ends;
-      if (nq <= kWaveRankMax) {
-        for (int e = lane; e < nq; e += kWaveSize) scr[e] = list[e];
-        wave_sync_lds();
-        ends = wave_rank_top(scr, nq, list, keep, lane);
-      } else {
-        int np2 = 2;
-        while (np2 < nq) np2 <<= 1;
-        for (int e = lane; e < np2; e += kWaveSize) scr[e] = (e < nq) ? list[e] : 0ull;
-        wave_sync_lds();
-        wave_bitonic_desc(scr, np2, lane);
-        for (int e = lane; e < keep; e += kWaveSize) list[e] = scr[e];
-        ends.first = scr[0];
-        ends.last = scr[keep - 1];
-      }
-      if (lane == 0) {
-        const size_t o = (size_t)(q0 + qi) * G + wg;
-        p.lcnt[o] = (uint32_t)keep | kSortedFlag;
-        p.lfirst[o] = ends.first;
-        p.lkth[o] = (keep == k) ? ends.last : 0ull;
-      }
-      wave_sync_lds();
-    }
-  }
+  wc.publish();
 }
 
 template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
@@ -627,6 +680,163 @@ __global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_main(ScanParams 
 template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
 __global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_sample(ScanParams p) {
   scan_mq_body<DT, QTW, KBT, CPQ, S, FILT>(p);
+}
+
+// Copy one 1 KiB block at `src` into LDS at `lds` (lane l's 16 bytes to
+// lds + 16 l); `nt` marks data read once (keys), which should not stay in
+// the caches.  Inline assembly for the reason given at copy2_to_lds.
+template <bool NT>
+__device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff, uint32_t lds) {
+  if constexpr (NT) {
+    asm volatile(
+        "s_mov_b32 m0, %2\n\t"
+        "global_load_lds_dwordx4 %0, %1 nt"
+        :
+        : "v"(voff), "s"(src), "s"(lds)
+        : "memory");
+  } else {
+    asm volatile(
+        "s_mov_b32 m0, %2\n\t"
+        "global_load_lds_dwordx4 %0, %1"
+        :
+        : "v"(voff), "s"(src), "s"(lds)
+        : "memory");
+  }
+}
+
+// Tiled contraction for keys wider than the shared-key scan can hold the
+// queries for (more than 32 blocks per key tile) at batches of QTW = 4 or 8
+// query tiles: both operands stream through LDS.  A workgroup walks its key
+// tiles in panels of 4 TPW tiles.  For each 32-dim column of the keys one
+// ring stage holds the panel's key blocks of that column and the batch's
+// query blocks of that column (a plain GEMM K loop); wave w multiplies its
+// TPW tiles by every query tile and, after the last column, tests the
+// finished tiles against the thresholds.  Each key block reaches the CU
+// once for the whole batch; the query operand (QTW KiB per column, shared
+// by every workgroup) is re-read from L2 once per panel.  Every wave issues
+// TPW + QTW / 4 copies per stage (past the end, the last stage again), so
+// the wait before each stage is a constant.  Lists: one per (query, wave).
+template <int DT, int QTW, int CPQ, int TPW, int S>
+__device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
+  using WC = WaveCands<DT, QTW, CPQ, false>;
+  constexpr int NP = WC::NP;
+  constexpr int PT = 4 * TPW;         // key tiles per panel
+  constexpr int SB = PT + QTW;        // 1 KiB blocks per stage
+  constexpr int CPW = TPW + QTW / 4;  // copies per wave per stage
+  constexpr int WAIT = CPW * (S - 2);  // copies of later stages still in flight
+  static_assert(QTW % 4 == 0 && S >= 3, "shape");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wg = blockIdx.x;
+  const int nwg = p.G / (kScanThreads / kWaveSize);
+  const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C);
+  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nullptr, 0,
+        wg * (kScanThreads / kWaveSize) + wv);
+  wc.init();
+
+  // This workgroup's key tiles: visited tiles [v0, v1).
+  const int64_t v0 = wave_uniform(p.nvisit * wg / nwg);
+  const int64_t v1 = wave_uniform(p.nvisit * (wg + 1) / nwg);
+  const int64_t ntile = v1 - v0;
+  if (ntile > 0) {
+    const int KB = p.KB;
+    const int64_t npanel = (ntile + PT - 1) / PT;
+    const int64_t tstep = p.stride * KB * kBlockBytes;  // bytes between visited tiles
+    const unsigned char *dbase = static_cast<const unsigned char *>(p.data) + v0 * tstep;
+    const unsigned char *qbase = static_cast<const unsigned char *>(p.qop);
+    const uint32_t voff = (uint32_t)lane * 16u;
+    const uint32_t ring = (uint32_t)(uintptr_t)smem;
+    // Stage (panel pn, column c) into ring slot `slot`: this wave's TPW key
+    // tiles (clamped to the last tile) and query tiles wv, wv + 4, ...
+    auto issue = [&](int64_t pn, int c, int slot) {
+      const uint32_t sbase = ring + (uint32_t)(slot * SB) * (uint32_t)kBlockBytes;
+#pragma unroll
+      for (int i = 0; i < TPW; ++i) {
+        int64_t t = pn * PT + wv * TPW + i;
+        t = t < ntile ? t : ntile - 1;
+        const int64_t src = wave_uniform((int64_t)(uintptr_t)(dbase + t * tstep) +
+                                         (int64_t)c * kBlockBytes);
+        copy_block_to_lds<true>((const void *)(uintptr_t)src, voff,
+                                sbase + (uint32_t)(wv * TPW + i) * (uint32_t)kBlockBytes);
+      }
+#pragma unroll
+      for (int j = 0; j < QTW / 4; ++j) {
+        const int qt = wv + 4 * j;
+        const int64_t src =
+            wave_uniform((int64_t)(uintptr_t)qbase + ((int64_t)qt * KB + c) * kBlockBytes);
+        copy_block_to_lds<false>((const void *)(uintptr_t)src, voff,
+                                 sbase + (uint32_t)(PT + qt) * (uint32_t)kBlockBytes);
+      }
+    };
+    // Stages in order: (panel, column) with the column fastest; past the
+    // last stage the copies repeat it.
+    int64_t npn = 0;
+    int nc = 0;
+    auto issue_next = [&](int slot) {
+      issue(npn, nc, slot);
+      if (npn < npanel - 1 || nc < KB - 1) {
+        if (++nc == KB) {
+          nc = 0;
+          ++npn;
+        }
+      }
+    };
+#pragma unroll
+    for (int st = 0; st < S - 1; ++st) issue_next(st);
+    int next_slot = S - 1;  // ring slot of the next stage to copy
+    int cur_slot = 0;       // ring slot of the stage being consumed
+    f4 acc[TPW][QTW];
+#pragma unroll 1
+    for (int64_t pn = 0; pn < npanel; ++pn) {
+#pragma unroll
+      for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int t = 0; t < QTW; ++t) acc[i][t] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+      for (int c = 0; c < KB; ++c) {
+        // this wave's copies of the stage have landed; after the barrier so
+        // have every wave's, and the slot consumed last is free again
+        wait_vmcnt<WAIT>();
+        __syncthreads();
+        issue_next(next_slot);
+        next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
+        const u4 *sl = reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes) + lane;
+        u4 kv[TPW], qv[QTW];
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) kv[i] = sl[(wv * TPW + i) * 64];
+#pragma unroll
+        for (int t = 0; t < QTW; ++t) qv[t] = sl[(PT + t) * 64];
+#pragma unroll
+        for (int t = 0; t < QTW; ++t)
+#pragma unroll
+          for (int i = 0; i < TPW; ++i) acc[i][t] = MfmaMQ<DT>::run(qv[t], kv[i], acc[i][t]);
+        cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
+      }
+#pragma unroll
+      for (int i = 0; i < TPW; ++i) {
+        const int64_t vt = pn * PT + wv * TPW + i;
+        if (vt < ntile) {
+          float sc[NP];
+          wc.scores_of(acc[i], 0, sc);
+          if (wc.any_hit(sc)) wc.take((v0 + vt) * p.stride, sc);
+        }
+      }
+    }
+    wait_vmcnt<0>();  // no LDS copy may land after the workgroup ends
+  }
+  wc.publish();
+}
+
+template <int DT, int QTW, int CPQ, int TPW, int S>
+__global__ void __launch_bounds__(kScanThreads, 2) dresd_scantc_main(ScanParams p) {
+  scan_tc_body<DT, QTW, CPQ, TPW, S>(p);
+}
+
+template <int DT, int QTW, int CPQ, int TPW, int S>
+__global__ void __launch_bounds__(kScanThreads, 2) dresd_scantc_sample(ScanParams p) {
+  scan_tc_body<DT, QTW, CPQ, TPW, S>(p);
 }
 
 // One thread per 16-byte chunk (t, kb, lane) of the query operands.
@@ -659,6 +869,30 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
   DRESD_MQ_CASE(DT, CPQ, 2, 4, 4) DRESD_MQ_CASE(DT, CPQ, 2, 8, 4)                 \
   DRESD_MQ_CASE(DT, CPQ, 2, 16, 6) DRESD_MQ_CASE(DT, CPQ, 4, 4, 4)                \
   DRESD_MQ_CASE(DT, CPQ, 4, 8, 6)
+
+// Tiled contraction: (QTW, TPW, S) per pass kind; a shallower ring (S = 3)
+// where large lists leave less LDS.
+#define DRESD_TC_CASE(DT, CPQ, QTW, TPW, S)                                              \
+  if (qtw == QTW && tpw == TPW && stages == S)                                           \
+    return main_pass ? (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, S>               \
+                     : (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, S>;
+#define DRESD_TC_ALL(DT, CPQ, QTW)                                                      \
+  DRESD_TC_CASE(DT, CPQ, QTW, 4, 5) DRESD_TC_CASE(DT, CPQ, QTW, 4, 3)                   \
+  DRESD_TC_CASE(DT, CPQ, QTW, 1, 8) DRESD_TC_CASE(DT, CPQ, QTW, 1, 4)
+
+#if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
+ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int stages, bool main_pass) {
+  DRESD_TC_ALL(kF16, 1, 4)
+  return nullptr;
+}
+#endif
+#if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
+ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int stages, bool main_pass) {
+  DRESD_TC_ALL(kBF16, 2, 4)
+  DRESD_TC_ALL(kBF16, 2, 8)
+  return nullptr;
+}
+#endif
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
 ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, bool filtered, int *stages) {

@@ -30,13 +30,15 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_case(gpu_lib, keys, cont, queries, k, dtype, tol=None, strict_report=False):
+def run_case(gpu_lib, keys, cont, queries, k, dtype, tol=None, strict_report=False, kind=None):
     """Search on the GPU and check against the oracle.  keys/cont/queries are
-    torch tensors (any device)."""
+    torch tensors (any device); `kind`: the scan kernel the plan must pick."""
     from paper_2502_15572_amd import Index
     kd = keys.to(DEV)
     ix = Index(kd, cont.to(DEV))
     q = queries.to(DEV, torch.float32)
+    if kind is not None:
+        assert ix.plan(q.shape[0], k)["scan_kernel"] == kind
     idx, score, tok = ix.search(q, k)
     torch.cuda.synchronize()
     g_idx, g_score, g_tok = idx.cpu().numpy(), score.cpu().numpy(), tok.cpu().numpy()
@@ -188,6 +190,38 @@ def test_shared_key_scan_shapes(gpu_lib, dt, N, d, B, k):
     q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
     cont = torch.randint(0, 32000, (N, 3), generator=gen, dtype=torch.int32)
     run_case(gpu_lib, x, cont, q, k, dt)
+
+
+# Keys of more than 1,024 dims at batches of two or more query tiles take the
+# tiled contraction (key and query blocks both streamed through LDS): the
+# smallest padded batch, ragged dims and column counts just past the
+# shared-key scan's, f16 and bf16 operand layouts, fewer key tiles than one
+# panel, k == N, large k (the shallower LDS rings), and batches split over
+# several launches.
+TC_EDGE = [
+    # (dtype, N, d, B, k)
+    ("bf16", 5003, 4096, 9, 10),      # two query tiles padded to four
+    ("bf16", 4099, 1050, 33, 20),     # 33 columns, the last ragged; eight query tiles
+    ("f16", 7001, 1600, 64, 5),       # f16, four query tiles of 16 queries
+    ("bf16", 2000, 4096, 64, 1000),   # large k: three- and four-stage rings
+    ("bf16", 100, 4096, 40, 100),     # 7 key tiles (less than a panel), k == N
+    ("f16", 33000, 2048, 130, 16),    # three launches of 43-44 queries
+    ("bf16", 16411, 4096, 17, 64),
+]
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", TC_EDGE, ids=["%s-N%d-d%d-B%d-k%d" % e for e in TC_EDGE])
+def test_tiled_contraction_shapes(gpu_lib, dt, N, d, B, k):
+    say("tiled", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N * 3 + d * 13 + B + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 3), generator=gen, dtype=torch.int32)
+    rep, _r = run_case(gpu_lib, x, cont, q, k, dt, kind="tiled")
+    say("  max |g-exact| %.2e, max |g-model| %.2e (%s)"
+        % (rep["max_abs_vs_exact"], rep["max_abs_vs_model"], rep["operand"]))
 
 
 def test_grouped_launch_matches_split_batches(gpu_lib):
