@@ -368,15 +368,21 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
     const bool dense = (int64_t)B * k >= 8192;
     // The tiled contraction's passes take about as long at stride 64 as
     // at 256 (a K loop over every column per panel, whatever the panel
-    // count): one pass at 64.
+    // count): one pass, at the sparsest of 64, 16 and 4 that lists enough
+    // tiles.
     const std::vector<int64_t> ladder =
-        pl.tc    ? std::vector<int64_t>{64}
+        pl.tc    ? std::vector<int64_t>{64, 16, 4}
         : dense  ? std::vector<int64_t>{4096, 256, 16}
         : pl.mq  ? std::vector<int64_t>{4096, 64}
                  : std::vector<int64_t>{256};
     for (int64_t P : ladder) {
       int64_t nv = ceil_div(ix->T, P);
-      if (nv * kTileRows >= 4 * (int64_t)k && ix->T >= 4 * P) pl.strides[pl.npass++] = P;
+      // the tiled contraction's sampled pass lists one key per tile and query
+      const int64_t rows = pl.tc ? nv : nv * kTileRows;
+      if (rows >= 4 * (int64_t)k && ix->T >= 4 * P) {
+        pl.strides[pl.npass++] = P;
+        if (pl.tc) break;
+      }
     }
   }
   // Lists end with at most k keys each, so a query never has more than

@@ -362,6 +362,37 @@ struct WaveCands {
     candidates(tile, sc, hit_t);
   }
 
+  // A sampled pass's cheaper candidates: of key tile `tile`, only each
+  // query's best key (the 16 rows of a lane group belong to one query per
+  // slot).  The k-th best of these per-tile maxima is still the key of a
+  // row, so it bounds the query's k-th best from below like the k-th best
+  // of every sampled row, while a tile adds one candidate per query instead
+  // of up to 16.
+  __device__ __forceinline__ void take_tile_max(int64_t tile, const float (&sc)[NP]) {
+    const int64_t row64 = tile * kTileRows + m;
+    const bool row_ok = row64 < p.N;
+    const uint32_t row = (uint32_t)row64;
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      uint64_t key = row_ok ? make_key(sc[j], row) : 0ull;
+#pragma unroll
+      for (int off = 1; off < kTileRows; off <<= 1) {
+        const uint64_t o = __shfl_xor(key, off, kWaveSize);
+        key = o > key ? o : key;
+      }
+      const bool h = m == 0 && key != 0ull && order_value((uint32_t)(key >> 32)) >= thr[j];
+      const uint64_t mk = __ballot(h);
+      if (mk == 0) continue;
+      if (cnt + __popcll(mk) > CB) flush();
+      if (h) {
+        const int at = cnt + rank_in(mk);
+        ck[at] = key;
+        cq[at] = (uint8_t)((j / NS) * QPT + g * NS + (j % NS));
+      }
+      cnt += __popcll(mk);
+    }
+  }
+
   // Publish this wave's lists (one per query per list slot) and per list
   // its length (kSortedFlag when sorted), best key (0 when empty) and k-th
   // key (0 unless it holds k sorted keys).  Lane i takes query i; lists
@@ -382,16 +413,43 @@ struct WaveCands {
       p.lkth[o] = 0ull;
     }
     uint64_t todo = __ballot(sort_me);
-    while (todo) {
-      const int qi = __ffsll((long long)todo) - 1;
+    // The lists are ordered one after another; a list of at most
+    // kWaveRankMax keys is loaded (up to PF keys per lane) while the one
+    // before it is being ordered, so the loads' latency is paid about once
+    // rather than once per query.
+    constexpr int PF = kWaveRankMax / kWaveSize;
+    uint64_t nxt[PF];
+    int qn = -1, nn = 0;
+    auto prefetch = [&]() {
+      if (!todo) {
+        qn = -1;
+        return;
+      }
+      qn = __ffsll((long long)todo) - 1;
       todo &= todo - 1;
+      nn = __builtin_amdgcn_readlane(n, qn);
+      const uint64_t *list = list_of(qn);
+#pragma unroll
+      for (int j = 0; j < PF; ++j) {
+        const int e = lane + j * kWaveSize;
+        nxt[j] = (nn <= kWaveRankMax && e < nn) ? list[e] : 0ull;
+      }
+    };
+    __threadfence_block();  // this wave's list stores are visible to its loads
+    prefetch();
+    while (qn >= 0) {
+      const int qi = qn, nq = nn;
+      uint64_t cur[PF];
+#pragma unroll
+      for (int j = 0; j < PF; ++j) cur[j] = nxt[j];
+      prefetch();
       uint64_t *list = list_of(qi);
-      const int nq = __builtin_amdgcn_readlane(n, qi);
-      __threadfence_block();
       const int keep = nq < k ? nq : k;
       RankEnds ends;
       if (nq <= kWaveRankMax) {
-        for (int e = lane; e < nq; e += kWaveSize) scr[e] = list[e];
+#pragma unroll
+        for (int j = 0; j < PF; ++j)
+          if (lane + j * kWaveSize < nq) scr[lane + j * kWaveSize] = cur[j];
         wave_sync_lds();
         ends = wave_rank_top(scr, nq, list, keep, lane);
       } else {
@@ -716,7 +774,8 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 // by every workgroup) is re-read from L2 once per panel.  Every wave issues
 // TPW + QTW / 4 copies per stage (past the end, the last stage again), so
 // the wait before each stage is a constant.  Lists: one per (query, wave).
-template <int DT, int QTW, int CPQ, int TPW, int S>
+// A sampled pass (TMAX) lists only each tile's best key per query.
+template <int DT, int QTW, int CPQ, int TPW, int S, bool TMAX>
 __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   using WC = WaveCands<DT, QTW, CPQ, false>;
   constexpr int NP = WC::NP;
@@ -820,7 +879,8 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         if (vt < ntile) {
           float sc[NP];
           wc.scores_of(acc[i], 0, sc);
-          if (wc.any_hit(sc)) wc.take((v0 + vt) * p.stride, sc);
+          if (TMAX) wc.take_tile_max((v0 + vt) * p.stride, sc);
+          else if (wc.any_hit(sc)) wc.take((v0 + vt) * p.stride, sc);
         }
       }
     }
@@ -831,12 +891,13 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
 
 template <int DT, int QTW, int CPQ, int TPW, int S>
 __global__ void __launch_bounds__(kScanThreads, 2) dresd_scantc_main(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, S>(p);
+  scan_tc_body<DT, QTW, CPQ, TPW, S, false>(p);
 }
 
+// Sampled pass: per-tile maxima as candidates.
 template <int DT, int QTW, int CPQ, int TPW, int S>
 __global__ void __launch_bounds__(kScanThreads, 2) dresd_scantc_sample(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, S>(p);
+  scan_tc_body<DT, QTW, CPQ, TPW, S, true>(p);
 }
 
 // One thread per 16-byte chunk (t, kb, lane) of the query operands.

@@ -207,6 +207,11 @@ TC_EDGE = [
     ("bf16", 100, 4096, 40, 100),     # 7 key tiles (less than a panel), k == N
     ("f16", 33000, 2048, 130, 16),    # three launches of 43-44 queries
     ("bf16", 16411, 4096, 17, 64),
+    # sampled threshold passes (per-tile maxima) at strides 64, 16 and 4
+    ("bf16", 40000, 1100, 20, 2),     # stride 64, 35 columns (ragged)
+    ("f16", 30000, 2048, 64, 4),      # stride 64
+    ("bf16", 20000, 4096, 64, 10),    # stride 16
+    ("bf16", 6000, 2048, 50, 16),     # stride 4
 ]
 
 
