@@ -97,9 +97,11 @@ __host__ __device__ inline size_t scan_mq_filter_bytes(int stages, int np) {
 // key [nqw] u64.
 constexpr int kMqCandBuf = 256;
 constexpr int kMqStageBlocks = 8;  // 1 KiB key blocks per LDS stage
-__host__ __device__ inline size_t scan_mq_wave_bytes(int nqw, int C) {
-  return ((size_t)kMqCandBuf * 9 + (size_t)C * 8 + (size_t)nqw * 24 + 15) / 16 * 16;
+__host__ __device__ inline size_t scan_mq_wave_bytes(int nqw, int C, int cb = kMqCandBuf) {
+  return ((size_t)cb * 9 + (size_t)C * 8 + (size_t)nqw * 24 + 15) / 16 * 16;
 }
+// The tiled contraction tests a tile once per K loop: a smaller buffer.
+constexpr int kTcCandBuf = 128;
 __host__ __device__ inline size_t scan_mq_lds_bytes(int stages, int nqw, int C) {
   return (size_t)stages * kMqStageBlocks * kBlockBytes +
          (size_t)(kScanThreads / kWaveSize) * scan_mq_wave_bytes(nqw, C);
@@ -180,8 +182,9 @@ inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, bo
 // Query-operand kernel of the shared-key scan for a key type (launch with
 // 256 threads, one thread per 16-byte chunk).
 // Tiled contraction (both operands through LDS): qtw query tiles per
-// launch (4, or 8 for bf16), tpw key tiles per wave (4 or 1), ring stages
-// (5 or 3 at tpw 4; 8 or 4 at tpw 1); null for other shapes.
+// launch (4, or 8 for bf16), tpw key tiles per wave, ring stages: main
+// passes (4, 5) and (4, 3), sampled passes (1, 8) and (1, 4); null for other
+// shapes.
 ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int stages, bool main_pass);
 ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int stages, bool main_pass);
 inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int stages, bool main_pass) {
@@ -191,7 +194,7 @@ inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int stages, bool m
 }
 __host__ __device__ inline size_t scan_tc_lds_bytes(int qtw, int tpw, int stages, int nq, int C) {
   return (size_t)stages * (4 * tpw + qtw) * kBlockBytes +
-         (size_t)(kScanThreads / kWaveSize) * scan_mq_wave_bytes(nq, C);
+         (size_t)(kScanThreads / kWaveSize) * scan_mq_wave_bytes(nq, C, kTcCandBuf);
 }
 void *qop_kernel_f16();
 void *qop_kernel_bf16();

@@ -119,13 +119,13 @@ __device__ __forceinline__ void copy2_to_lds(const void *src, uint32_t voff0, ui
 // the best key listed; and a buffer of (key, query) pairs that passed the
 // test, moved into the lists only when it fills up.  QTW query tiles of CPQ
 // operand columns per query; FILT: next-token-filtered search.
-template <int DT, int QTW, int CPQ, bool FILT>
+template <int DT, int QTW, int CPQ, bool FILT, int CBUF = kMqCandBuf>
 struct WaveCands {
   static constexpr int QPT = 16 / CPQ;   // queries per tile
   static constexpr int NS = 4 / CPQ;     // scores per lane per query tile
   static constexpr int NQW = QTW * QPT;  // queries per wave
   static constexpr int NP = QTW * NS;    // scores per lane per key tile
-  static constexpr int CB = kMqCandBuf;
+  static constexpr int CB = CBUF;
   static_assert(NP <= 32, "score slots");
 
   const ScanParams &p;
@@ -142,7 +142,7 @@ struct WaveCands {
   int ntr[NP <= 8 ? NP : 1];  // filtered search with few slots: nt_slot in VGPRs
   int cnt = 0;        // buffered candidates (wave-uniform)
 
-  // `region`: the wave's scan_mq_wave_bytes(NQW, C) bytes of LDS.
+  // `region`: the wave's scan_mq_wave_bytes(NQW, C, CB) bytes of LDS.
   __device__ __forceinline__ WaveCands(const ScanParams &p_, unsigned char *region, int32_t *nt,
                                        int q0_, int lslot_)
       : p(p_), lane(threadIdx.x & 63), g((threadIdx.x & 63) >> 4), m(threadIdx.x & 15), q0(q0_),
@@ -766,23 +766,28 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 // queries for (more than 32 blocks per key tile) at batches of QTW = 4 or 8
 // query tiles: both operands stream through LDS.  A workgroup walks its key
 // tiles in panels of 4 TPW tiles.  For each 32-dim column of the keys one
-// ring stage holds the panel's key blocks of that column and the batch's
-// query blocks of that column (a plain GEMM K loop); wave w multiplies its
-// TPW tiles by every query tile and, after the last column, tests the
-// finished tiles against the thresholds.  Each key block reaches the CU
-// once for the whole batch; the query operand (QTW KiB per column, shared
-// by every workgroup) is re-read from L2 once per panel.  Every wave issues
-// TPW + QTW / 4 copies per stage (past the end, the last stage again), so
-// the wait before each stage is a constant.  Lists: one per (query, wave).
-// A sampled pass (TMAX) lists only each tile's best key per query.
+// ring stage holds the panel's key blocks and the batch's query blocks of
+// that column (a plain GEMM K loop); wave w multiplies its TPW tiles by
+// every query tile, column after column into one accumulator per (tile,
+// query tile) -- the same order in every pass, so a key scores the same in
+// the sampled and the main passes -- and after the last column tests the
+// finished tiles against the thresholds.  Each key block reaches the CU once
+// for the whole batch; the query operand (QTW KiB per column, shared by
+// every workgroup) is re-read from L2 once per panel.  Every wave issues
+// TPW + QTW / 4 copies per stage (past the end, the last stage again),
+// spread over the query tiles' matrix instructions so that the copies'
+// address work overlaps the matrix cores, and the wait before each stage is
+// a constant.  Lists: one per (query, wave).  A sampled pass (TMAX) lists only
+// each tile's best key per query.
 template <int DT, int QTW, int CPQ, int TPW, int S, bool TMAX>
 __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
-  using WC = WaveCands<DT, QTW, CPQ, false>;
+  using WC = WaveCands<DT, QTW, CPQ, false, kTcCandBuf>;
   constexpr int NP = WC::NP;
-  constexpr int PT = 4 * TPW;         // key tiles per panel
-  constexpr int SB = PT + QTW;        // 1 KiB blocks per stage
-  constexpr int CPW = TPW + QTW / 4;  // copies per wave per stage
+  constexpr int PT = 4 * TPW;          // key tiles per panel
+  constexpr int SB = PT + QTW;         // 1 KiB blocks per stage
+  constexpr int CPW = TPW + QTW / 4;   // copies per wave per stage
   constexpr int WAIT = CPW * (S - 2);  // copies of later stages still in flight
+  constexpr int CPT = (CPW + QTW - 1) / QTW;  // copies after each query tile's instructions
   static_assert(QTW % 4 == 0 && S >= 3, "shape");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
@@ -790,7 +795,7 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wg = blockIdx.x;
   const int nwg = p.G / (kScanThreads / kWaveSize);
-  const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C);
+  const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C, kTcCandBuf);
   WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nullptr, 0,
         wg * (kScanThreads / kWaveSize) + wv);
   wc.init();
@@ -807,22 +812,20 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
     const unsigned char *qbase = static_cast<const unsigned char *>(p.qop);
     const uint32_t voff = (uint32_t)lane * 16u;
     const uint32_t ring = (uint32_t)(uintptr_t)smem;
-    // Stage (panel pn, column c) into ring slot `slot`: this wave's TPW key
-    // tiles (clamped to the last tile) and query tiles wv, wv + 4, ...
-    auto issue = [&](int64_t pn, int c, int slot) {
+    // Copy j of stage (panel pn, column c) into ring slot `slot`: j < TPW is
+    // this wave's key tile j (clamped to the last tile), the others its
+    // query tiles wv, wv + 4, ...
+    auto copy = [&](int j, int64_t pn, int c, int slot) {
       const uint32_t sbase = ring + (uint32_t)(slot * SB) * (uint32_t)kBlockBytes;
-#pragma unroll
-      for (int i = 0; i < TPW; ++i) {
-        int64_t t = pn * PT + wv * TPW + i;
+      if (j < TPW) {
+        int64_t t = pn * PT + wv * TPW + j;
         t = t < ntile ? t : ntile - 1;
         const int64_t src = wave_uniform((int64_t)(uintptr_t)(dbase + t * tstep) +
                                          (int64_t)c * kBlockBytes);
         copy_block_to_lds<true>((const void *)(uintptr_t)src, voff,
-                                sbase + (uint32_t)(wv * TPW + i) * (uint32_t)kBlockBytes);
-      }
-#pragma unroll
-      for (int j = 0; j < QTW / 4; ++j) {
-        const int qt = wv + 4 * j;
+                                sbase + (uint32_t)(wv * TPW + j) * (uint32_t)kBlockBytes);
+      } else {
+        const int qt = wv + 4 * (j - TPW);
         const int64_t src =
             wave_uniform((int64_t)(uintptr_t)qbase + ((int64_t)qt * KB + c) * kBlockBytes);
         copy_block_to_lds<false>((const void *)(uintptr_t)src, voff,
@@ -833,8 +836,7 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
     // last stage the copies repeat it.
     int64_t npn = 0;
     int nc = 0;
-    auto issue_next = [&](int slot) {
-      issue(npn, nc, slot);
+    auto advance = [&]() {
       if (npn < npanel - 1 || nc < KB - 1) {
         if (++nc == KB) {
           nc = 0;
@@ -843,7 +845,11 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
       }
     };
 #pragma unroll
-    for (int st = 0; st < S - 1; ++st) issue_next(st);
+    for (int st = 0; st < S - 1; ++st) {
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) copy(j, npn, nc, st);
+      advance();
+    }
     int next_slot = S - 1;  // ring slot of the next stage to copy
     int cur_slot = 0;       // ring slot of the stage being consumed
     f4 acc[TPW][QTW];
@@ -859,18 +865,27 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         // have every wave's, and the slot consumed last is free again
         wait_vmcnt<WAIT>();
         __syncthreads();
-        issue_next(next_slot);
-        next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
         const u4 *sl = reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes) + lane;
         u4 kv[TPW], qv[QTW];
 #pragma unroll
         for (int i = 0; i < TPW; ++i) kv[i] = sl[(wv * TPW + i) * 64];
 #pragma unroll
         for (int t = 0; t < QTW; ++t) qv[t] = sl[(PT + t) * 64];
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int t = 0; t < QTW; ++t)
+        for (int t = 0; t < QTW; ++t) {
 #pragma unroll
           for (int i = 0; i < TPW; ++i) acc[i][t] = MfmaMQ<DT>::run(qv[t], kv[i], acc[i][t]);
+          if (t * CPT < CPW) {
+            // the stage S - 1 ahead, CPT copies per query tile
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int j = t * CPT; j < (t + 1) * CPT && j < CPW; ++j) copy(j, npn, nc, next_slot);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+        advance();
+        next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
         cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
       }
 #pragma unroll
@@ -931,15 +946,15 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
   DRESD_MQ_CASE(DT, CPQ, 2, 16, 6) DRESD_MQ_CASE(DT, CPQ, 4, 4, 4)                \
   DRESD_MQ_CASE(DT, CPQ, 4, 8, 6)
 
-// Tiled contraction: (QTW, TPW, S) per pass kind; a shallower ring (S = 3)
-// where large lists leave less LDS.
-#define DRESD_TC_CASE(DT, CPQ, QTW, TPW, S)                                              \
-  if (qtw == QTW && tpw == TPW && stages == S)                                           \
-    return main_pass ? (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, S>               \
-                     : (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, S>;
-#define DRESD_TC_ALL(DT, CPQ, QTW)                                                      \
-  DRESD_TC_CASE(DT, CPQ, QTW, 4, 5) DRESD_TC_CASE(DT, CPQ, QTW, 4, 3)                   \
-  DRESD_TC_CASE(DT, CPQ, QTW, 1, 8) DRESD_TC_CASE(DT, CPQ, QTW, 1, 4)
+// Tiled contraction: the main pass with TPW = 4 (5 stages, or 3 where large
+// lists leave less LDS), the sampled pass with TPW = 1 (8 or 4 stages).
+#define DRESD_TC_MAIN(DT, CPQ, QTW, TPW, S) \
+  if (main_pass && qtw == QTW && tpw == TPW && stages == S) return dresd_scantc_main<DT, QTW, CPQ, TPW, S>;
+#define DRESD_TC_SAMPLE(DT, CPQ, QTW, TPW, S) \
+  if (!main_pass && qtw == QTW && tpw == TPW && stages == S) return dresd_scantc_sample<DT, QTW, CPQ, TPW, S>;
+#define DRESD_TC_ALL(DT, CPQ, QTW)                                                   \
+  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 5) DRESD_TC_MAIN(DT, CPQ, QTW, 4, 3)                \
+  DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 8) DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4)
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
 ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int stages, bool main_pass) {
