@@ -212,6 +212,7 @@ TC_EDGE = [
     ("f16", 30000, 2048, 64, 4),      # stride 64
     ("bf16", 20000, 4096, 64, 10),    # stride 16
     ("bf16", 6000, 2048, 50, 16),     # stride 4
+    ("bf16", 256003, 1100, 20, 1000),  # stride 4 at large k: the shallow rings of both passes
 ]
 
 
