@@ -154,7 +154,6 @@ __device__ __forceinline__ void scan_body(const ScanParams &p, const int gw,
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int nwv = blockDim.x >> 6;
   const int G = p.G, C = p.C, KB = p.KB, B = p.B;
   const int ncols = B * CPQ;
   const int g = lane >> 4, m = lane & 15;

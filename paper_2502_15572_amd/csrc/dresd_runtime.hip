@@ -164,6 +164,7 @@ struct Plan {
   bool mq = false;                  // shared-key scan (queries in registers)
   bool tc = false;                  // tiled contraction (queries and keys through LDS)
   int tpw_main = 4, tpw_sample = 1;  // tiled contraction: key tiles per wave per pass kind
+  int nw_main = 4, nw_sample = 4;    // tiled contraction: waves per workgroup per pass kind
   int bmax = 0;                 // queries per group
   int bl = 0;                   // queries per launch (several groups)
   int B = 0, nl = 0;            // batch, launches (launch i: group_of(pl, i))
@@ -182,6 +183,12 @@ struct Plan {
   size_t off_qop = 0;               // shared-key scan: query operands of a group
   size_t bytes = 0;
 };
+
+// Threads per workgroup of a plan's main or sampled scan.
+int threads_of(const Plan &pl, bool main_pass) {
+  if (!pl.tc) return kScanThreads;
+  return (main_pass ? pl.nw_main : pl.nw_sample) * kWaveSize;
+}
 
 // Launch i of a plan: queries [B i / nl, B (i + 1) / nl), split into groups
 // of at most bmax queries.
@@ -204,11 +211,12 @@ int stage_cap(int nq) { return nq >= 16 ? kTileRows : 2 * kTileRows; }
 // Resident workgroups per CU of a scan kernel at an LDS size, cached per
 // index (not cached with `keep` false: the allocation-free search adds
 // nothing to the host-side cache).
-int occupancy(dresd_index *ix, ScanKernel k, size_t lds, bool keep = true) {
+int occupancy(dresd_index *ix, ScanKernel k, size_t lds, bool keep = true,
+              int threads = kScanThreads) {
   for (size_t i = 0; i < ix->occ_key.size(); ++i)
     if (ix->occ_key[i].first == (const void *)k && ix->occ_key[i].second == lds) return ix->occ_val[i];
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k, kScanThreads, lds) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k, threads, lds) !=
       hipSuccess) {
     (void)hipGetLastError();
     nb = 1;
@@ -252,20 +260,29 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   if (mq_type && ix->KB > 32 && qt_all >= 2 && pl.terms < 4 && !filt) {
     const int qtw = (ix->dtype == kBF16 && qt_all > 4) ? 8 : 4;
     const int nq = qtw * pl.qpt;
-    int sm = 0, ss = 0;
-    for (int st : {5, 3})
-      if (!sm && scan_tc_lds_bytes(qtw, pl.tpw_main, st, nq, pl.C) <= ix->lds_max) sm = st;
+    // main pass: 8 waves over panels of 32 key tiles (one query read per 32
+    // tiles) where that kernel exists and fits, else 4 waves over 16 tiles
+    int sm = 0, ss = 0, nwm = 0;
+    for (auto nw_st : {std::make_pair(8, 3), std::make_pair(4, 5), std::make_pair(4, 3)})
+      if (!sm && scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nw_st.first, nw_st.second, true) &&
+          scan_tc_lds_bytes(qtw, pl.tpw_main, nw_st.first, nw_st.second, nq, pl.C) <=
+              ix->lds_max) {
+        nwm = nw_st.first;
+        sm = nw_st.second;
+      }
     for (int st : {8, 4})
-      if (!ss && scan_tc_lds_bytes(qtw, pl.tpw_sample, st, nq, pl.C) <= ix->lds_max) ss = st;
+      if (!ss && scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, st, nq, pl.C) <= ix->lds_max)
+        ss = st;
     if (sm && ss) {
       pl.tc = true;
+      pl.nw_main = nwm;
       pl.qt = qtw;
       pl.bmax = std::min(B, nq);
       pl.CL = 0;
-      pl.kmain = scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, sm, true);
-      pl.ksample = scan_tc_kernel(ix->dtype, qtw, pl.tpw_sample, ss, false);
-      pl.lds = scan_tc_lds_bytes(qtw, pl.tpw_main, sm, nq, pl.C);
-      pl.lds_s = scan_tc_lds_bytes(qtw, pl.tpw_sample, ss, nq, pl.C);
+      pl.kmain = scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nwm, sm, true);
+      pl.ksample = scan_tc_kernel(ix->dtype, qtw, pl.tpw_sample, pl.nw_sample, ss, false);
+      pl.lds = scan_tc_lds_bytes(qtw, pl.tpw_main, nwm, sm, nq, pl.C);
+      pl.lds_s = scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, ss, nq, pl.C);
     }
   }
   if (pl.tc) {
@@ -334,8 +351,8 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   if (!pl.kmain || !pl.ksample) return fail(DRESD_EUNSUPPORTED, "no scan kernel for this shape");
   if (!pl.tc) pl.lds_s = pl.lds;
   if (pl.lds > ix->lds_max) return fail(DRESD_EUNSUPPORTED, "scan state does not fit in LDS");
-  int occ = std::min(occupancy(ix, pl.kmain, pl.lds, keep_cache),
-                     occupancy(ix, pl.ksample, pl.lds_s, keep_cache));
+  int occ = std::min(occupancy(ix, pl.kmain, pl.lds, keep_cache, threads_of(pl, true)),
+                     occupancy(ix, pl.ksample, pl.lds_s, keep_cache, threads_of(pl, false)));
   // At most four workgroups per CU (few enough lists for the merge to keep
   // their best keys in LDS); one where fewer, longer HBM streams measured
   // faster: the single-tile scan with one query tile, and the shared-key
@@ -344,7 +361,10 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   pl.wg_max = ix->cus * std::min(occ, one_per_cu ? kMaxTileWgPerCu : kMaxScanWgPerCu);
   // lists per query: one per wave, or one per workgroup for the shared-key
   // scan; at most kMergeLists
-  const int lists_per_wg = pl.mq ? 1 : kScanThreads / kWaveSize;  // tiled contraction: per wave
+  // lists per workgroup: one per wave (the tiled contraction: of its larger
+  // workgroup), or one for the shared-key scan
+  const int lists_per_wg = pl.mq ? 1 : pl.tc ? std::max(pl.nw_main, pl.nw_sample)
+                                             : kScanThreads / kWaveSize;
   pl.wg_max = std::min(pl.wg_max, kMergeLists / lists_per_wg);
   pl.G_max = pl.wg_max * lists_per_wg;
   // Small batches (B <= 8): every wave keeps its own running top-k and sorts
@@ -408,7 +428,8 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
 int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit, bool main_pass = true) {
   const int wpg = kScanThreads / kWaveSize;
   // tiled contraction: whole panels of 4 tpw tiles
-  const int per_wg = pl.tc ? wpg * (main_pass ? pl.tpw_main : pl.tpw_sample) : pl.mq ? 1 : wpg;
+  const int per_wg = pl.tc ? (main_pass ? pl.nw_main * pl.tpw_main : pl.nw_sample * pl.tpw_sample)
+                   : pl.mq ? 1 : wpg;
   int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(nvisit, per_wg));
   if (gr.ng > 1) wgs = std::min<int64_t>(wgs, std::max<int64_t>(8, pl.wg_max / gr.ng / 8 * 8));
   return wgs;
@@ -620,12 +641,13 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
   for (int v = 0; v < 3; ++v)
     for (int qtw : {4, 8})
       for (int tpw : {1, 4})
-        for (int st : {3, 4, 5, 8})
-          for (bool mp : {false, true})
-            if (ScanKernel kf = scan_tc_kernel(v, qtw, tpw, st, mp))
-              (void)hipFuncSetAttribute((const void *)kf,
-                                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                                        (int)ix->lds_max);
+        for (int nw : {4, 8})
+          for (int st : {3, 4, 5, 8})
+            for (bool mp : {false, true})
+              if (ScanKernel kf = scan_tc_kernel(v, qtw, tpw, nw, st, mp))
+                (void)hipFuncSetAttribute((const void *)kf,
+                                          hipFuncAttributeMaxDynamicSharedMemorySize,
+                                          (int)ix->lds_max);
   for (int v = 0; v < 3; ++v)
     if (ScanKernel kf = scan_parts_kernel(v))
       (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -701,10 +723,10 @@ dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int
   Plan pl;
   s = make_plan(ix, B, k, pl);
   if (s != DRESD_OK) return s;
-  const int wpg = kScanThreads / kWaveSize;
   const Group g0 = group_of(pl, 0);
   if (sample_passes) *sample_passes = (int32_t)pl.npass;
-  if (scan_waves) *scan_waves = (int32_t)(pass_wgs(pl, g0, ix->T) * g0.ng * wpg);
+  if (scan_waves)
+    *scan_waves = (int32_t)(pass_wgs(pl, g0, ix->T) * g0.ng * (threads_of(pl, true) / kWaveSize));
   if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
   if (scan_kind) *scan_kind = pl.tc ? 3 : pl.mq ? 1 : (g0.ng > 1 ? 2 : 0);
   return DRESD_OK;
@@ -799,7 +821,6 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     own.first = e_all0;
     own.last = e_all1;
   }
-  const int wpg = kScanThreads / kWaveSize;
   for (int li = 0; li < pl.nl; ++li) {
     const Group gr = group_of(pl, li);
     ScanParams sp;
@@ -861,7 +882,8 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       sp.nvisit = ceil_div(ix->T, stride);
       sp.tau = tau_in;
       const int64_t wgs = pass_wgs(pl, gr, sp.nvisit, main_pass);
-      sp.G = (int)(pl.mq ? wgs : wgs * wpg);
+      const int threads = threads_of(pl, main_pass);
+      sp.G = (int)(pl.mq ? wgs : wgs * (threads / kWaveSize));
       void *sargs[] = {&sp};
       hipEvent_t e0 = nullptr, e1 = nullptr;
       if (main_pass && prof) {
@@ -870,7 +892,7 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
         if (!e0 || !e1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
       }
       DRESD_HIP(launch((const void *)(main_pass ? pl.kmain : pl.ksample),
-                       dim3((unsigned)(wgs * gr.ng)), dim3(kScanThreads), sargs,
+                       dim3((unsigned)(wgs * gr.ng)), dim3((unsigned)threads), sargs,
                        main_pass ? pl.lds : pl.lds_s, e0, e1));
       if (main_pass && prof) {
         ix->ev_scan.push_back(e0);

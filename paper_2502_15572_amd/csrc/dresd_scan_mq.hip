@@ -764,8 +764,8 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 
 // Tiled contraction for keys wider than the shared-key scan can hold the
 // queries for (more than 32 blocks per key tile) at batches of QTW = 4 or 8
-// query tiles: both operands stream through LDS.  A workgroup walks its key
-// tiles in panels of 4 TPW tiles.  For each 32-dim column of the keys one
+// query tiles: both operands stream through LDS.  A workgroup of NW waves
+// walks its key tiles in panels of NW TPW tiles.  For each 32-dim column of the keys one
 // ring stage holds the panel's key blocks and the batch's query blocks of
 // that column (a plain GEMM K loop); wave w multiplies its TPW tiles by
 // every query tile, column after column into one accumulator per (tile,
@@ -773,31 +773,33 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 // the sampled and the main passes -- and after the last column tests the
 // finished tiles against the thresholds.  Each key block reaches the CU once
 // for the whole batch; the query operand (QTW KiB per column, shared by
-// every workgroup) is re-read from L2 once per panel.  Every wave issues
-// TPW + QTW / 4 copies per stage (past the end, the last stage again),
-// spread over the query tiles' matrix instructions so that the copies'
-// address work overlaps the matrix cores, and the wait before each stage is
-// a constant.  Lists: one per (query, wave).  A sampled pass (TMAX) lists only
+// every workgroup) is re-read from L2 once per panel.  Wave w issues its
+// TPW key copies and the copies of query tiles w, w + NW, ... per stage
+// (past the end, the last stage again), spread over the query tiles' matrix
+// instructions so that the copies' address work overlaps the matrix cores;
+// its wait before each stage is a constant of its copy count.  Lists: one per (query, wave).  A sampled pass (TMAX) lists only
 // each tile's best key per query.
-template <int DT, int QTW, int CPQ, int TPW, int S, bool TMAX>
+template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool TMAX>
 __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   using WC = WaveCands<DT, QTW, CPQ, false, kTcCandBuf>;
   constexpr int NP = WC::NP;
-  constexpr int PT = 4 * TPW;          // key tiles per panel
-  constexpr int SB = PT + QTW;         // 1 KiB blocks per stage
-  constexpr int CPW = TPW + QTW / 4;   // copies per wave per stage
-  constexpr int WAIT = CPW * (S - 2);  // copies of later stages still in flight
-  constexpr int CPT = (CPW + QTW - 1) / QTW;  // copies after each query tile's instructions
-  static_assert(QTW % 4 == 0 && S >= 3, "shape");
+  constexpr int PT = NW * TPW;  // key tiles per panel
+  constexpr int SB = PT + QTW;  // 1 KiB blocks per stage
+  // copies per wave per stage: TPW key blocks and one or two query blocks
+  // (or none, when there are fewer query tiles than waves)
+  constexpr int CPW_HI = TPW + (QTW + NW - 1) / NW;
+  constexpr int CPW_LO = TPW + QTW / NW;
+  constexpr int CPT = (CPW_HI + QTW - 1) / QTW;  // copies after each query tile's instructions
+  static_assert(S >= 3 && (QTW % NW == 0 || NW % QTW == 0), "shape");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wg = blockIdx.x;
-  const int nwg = p.G / (kScanThreads / kWaveSize);
+  const int nwg = p.G / NW;
+  const int cpw = TPW + (QTW - wv + NW - 1) / NW;  // this wave's copies per stage
   const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C, kTcCandBuf);
-  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nullptr, 0,
-        wg * (kScanThreads / kWaveSize) + wv);
+  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nullptr, 0, wg * NW + wv);
   wc.init();
 
   // This workgroup's key tiles: visited tiles [v0, v1).
@@ -814,7 +816,7 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
     const uint32_t ring = (uint32_t)(uintptr_t)smem;
     // Copy j of stage (panel pn, column c) into ring slot `slot`: j < TPW is
     // this wave's key tile j (clamped to the last tile), the others its
-    // query tiles wv, wv + 4, ...
+    // query tiles wv, wv + NW, ...
     auto copy = [&](int j, int64_t pn, int c, int slot) {
       const uint32_t sbase = ring + (uint32_t)(slot * SB) * (uint32_t)kBlockBytes;
       if (j < TPW) {
@@ -825,7 +827,7 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         copy_block_to_lds<true>((const void *)(uintptr_t)src, voff,
                                 sbase + (uint32_t)(wv * TPW + j) * (uint32_t)kBlockBytes);
       } else {
-        const int qt = wv + 4 * (j - TPW);
+        const int qt = wv + NW * (j - TPW);
         const int64_t src =
             wave_uniform((int64_t)(uintptr_t)qbase + ((int64_t)qt * KB + c) * kBlockBytes);
         copy_block_to_lds<false>((const void *)(uintptr_t)src, voff,
@@ -847,7 +849,8 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) {
 #pragma unroll
-      for (int j = 0; j < CPW; ++j) copy(j, npn, nc, st);
+      for (int j = 0; j < CPW_HI; ++j)
+        if (j < cpw) copy(j, npn, nc, st);
       advance();
     }
     int next_slot = S - 1;  // ring slot of the next stage to copy
@@ -861,9 +864,11 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         for (int t = 0; t < QTW; ++t) acc[i][t] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 1
       for (int c = 0; c < KB; ++c) {
-        // this wave's copies of the stage have landed; after the barrier so
-        // have every wave's, and the slot consumed last is free again
-        wait_vmcnt<WAIT>();
+        // this wave's copies of the stage have landed (those of the S - 2
+        // later stages may still be in flight); after the barrier so have
+        // every wave's, and the slot consumed last is free again
+        if (CPW_HI == CPW_LO || cpw == CPW_HI) wait_vmcnt<CPW_HI * (S - 2)>();
+        else wait_vmcnt<CPW_LO * (S - 2)>();
         __syncthreads();
         const u4 *sl = reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes) + lane;
         u4 kv[TPW], qv[QTW];
@@ -876,11 +881,12 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         for (int t = 0; t < QTW; ++t) {
 #pragma unroll
           for (int i = 0; i < TPW; ++i) acc[i][t] = MfmaMQ<DT>::run(qv[t], kv[i], acc[i][t]);
-          if (t * CPT < CPW) {
+          if (t * CPT < CPW_HI) {
             // the stage S - 1 ahead, CPT copies per query tile
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int j = t * CPT; j < (t + 1) * CPT && j < CPW; ++j) copy(j, npn, nc, next_slot);
+            for (int j = t * CPT; j < (t + 1) * CPT && j < CPW_HI; ++j)
+              if (j < cpw) copy(j, npn, nc, next_slot);
             __builtin_amdgcn_sched_barrier(0);
           }
         }
@@ -904,15 +910,15 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   wc.publish();
 }
 
-template <int DT, int QTW, int CPQ, int TPW, int S>
-__global__ void __launch_bounds__(kScanThreads, 2) dresd_scantc_main(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, S, false>(p);
+template <int DT, int QTW, int CPQ, int TPW, int NW, int S>
+__global__ void __launch_bounds__(NW * kWaveSize, 8 / NW) dresd_scantc_main(ScanParams p) {
+  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, false>(p);
 }
 
 // Sampled pass: per-tile maxima as candidates.
-template <int DT, int QTW, int CPQ, int TPW, int S>
-__global__ void __launch_bounds__(kScanThreads, 2) dresd_scantc_sample(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, S, true>(p);
+template <int DT, int QTW, int CPQ, int TPW, int NW, int S>
+__global__ void __launch_bounds__(NW * kWaveSize, 8 / NW) dresd_scantc_sample(ScanParams p) {
+  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, true>(p);
 }
 
 // One thread per 16-byte chunk (t, kb, lane) of the query operands.
@@ -946,24 +952,29 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
   DRESD_MQ_CASE(DT, CPQ, 2, 16, 6) DRESD_MQ_CASE(DT, CPQ, 4, 4, 4)                \
   DRESD_MQ_CASE(DT, CPQ, 4, 8, 6)
 
-// Tiled contraction: the main pass with TPW = 4 (5 stages, or 3 where large
-// lists leave less LDS), the sampled pass with TPW = 1 (8 or 4 stages).
-#define DRESD_TC_MAIN(DT, CPQ, QTW, TPW, S) \
-  if (main_pass && qtw == QTW && tpw == TPW && stages == S) return dresd_scantc_main<DT, QTW, CPQ, TPW, S>;
-#define DRESD_TC_SAMPLE(DT, CPQ, QTW, TPW, S) \
-  if (!main_pass && qtw == QTW && tpw == TPW && stages == S) return dresd_scantc_sample<DT, QTW, CPQ, TPW, S>;
-#define DRESD_TC_ALL(DT, CPQ, QTW)                                                   \
-  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 5) DRESD_TC_MAIN(DT, CPQ, QTW, 4, 3)                \
-  DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 8) DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4)
+// Tiled contraction: main passes with 4 key tiles per wave, 8 waves (3
+// stages: one query read per 32 key tiles) or 4 waves (5 stages, or 3 where
+// large lists leave less LDS); sampled passes with 1 key tile per wave and
+// 4 waves (8 or 4 stages).
+#define DRESD_TC_MAIN(DT, CPQ, QTW, TPW, NW, S)                           \
+  if (main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S) \
+    return dresd_scantc_main<DT, QTW, CPQ, TPW, NW, S>;
+#define DRESD_TC_SAMPLE(DT, CPQ, QTW, TPW, NW, S)                          \
+  if (!main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S) \
+    return dresd_scantc_sample<DT, QTW, CPQ, TPW, NW, S>;
+#define DRESD_TC_ALL(DT, CPQ, QTW)                                                            \
+  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 8, 3)                                                        \
+  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 5) DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 3)                   \
+  DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 8) DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 4)
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
-ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int stages, bool main_pass) {
+ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nw, int stages, bool main_pass) {
   DRESD_TC_ALL(kF16, 1, 4)
   return nullptr;
 }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
-ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int stages, bool main_pass) {
+ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nw, int stages, bool main_pass) {
   DRESD_TC_ALL(kBF16, 2, 4)
   DRESD_TC_ALL(kBF16, 2, 8)
   return nullptr;
