@@ -294,8 +294,8 @@ dresd_status dresd_pack_drafts(const int32_t *tokens, int32_t B, int32_t k, int3
  * serving several query groups per launch (batches whose query operands
  * exceed one workgroup's LDS; the groups share each key range through L2),
  * 3 = tiled contraction (keys of more than 1,024 dims at batches of two or
- * more query tiles, unfiltered: key and query blocks both streamed through
- * LDS, column by column, for panels of 16 key tiles).
+ * more query tiles: key and query blocks both streamed through LDS, column
+ * by column, for panels of 32 key tiles).
  * Errors: EINVAL for the same argument errors as dresd_search.
  */
 dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,

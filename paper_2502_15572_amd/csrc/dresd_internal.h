@@ -184,19 +184,24 @@ inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, bo
 // Tiled contraction (both operands through LDS): qtw query tiles per
 // launch (4, or 8 for bf16), tpw key tiles per wave, nw waves per
 // workgroup, ring stages: main passes (4, 8, 3), (4, 4, 5) and (4, 4, 3);
-// sampled passes (1, 4, 8) and (1, 4, 4); null for other shapes.
-ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nw, int stages, bool main_pass);
-ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nw, int stages, bool main_pass);
-inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int nw, int stages,
-                                 bool main_pass) {
-  if (dtype == kF16) return scan_tc_kernel_f16(qtw, tpw, nw, stages, main_pass);
-  if (dtype == kBF16) return scan_tc_kernel_bf16(qtw, tpw, nw, stages, main_pass);
+// sampled passes (1, 4, 8) and (1, 4, 4); each also next-token filtered;
+// null for other shapes.
+ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nw, int stages, bool main_pass, bool filtered);
+ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nw, int stages, bool main_pass,
+                               bool filtered);
+inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int nw, int stages, bool main_pass,
+                                 bool filtered) {
+  if (dtype == kF16) return scan_tc_kernel_f16(qtw, tpw, nw, stages, main_pass, filtered);
+  if (dtype == kBF16) return scan_tc_kernel_bf16(qtw, tpw, nw, stages, main_pass, filtered);
   return nullptr;
 }
+// LDS of the tiled contraction: ring | per wave a candidate region |
+// (filtered search) per wave the next tokens of its score slots.
 __host__ __device__ inline size_t scan_tc_lds_bytes(int qtw, int tpw, int nw, int stages, int nq,
-                                                    int C) {
+                                                    int C, int np, bool filtered) {
   return (size_t)stages * (nw * tpw + qtw) * kBlockBytes +
-         (size_t)nw * scan_mq_wave_bytes(nq, C, kTcCandBuf);
+         (size_t)nw * scan_mq_wave_bytes(nq, C, kTcCandBuf) +
+         (filtered ? (size_t)nw * 16 * np : 0);
 }
 void *qop_kernel_f16();
 void *qop_kernel_bf16();

@@ -257,21 +257,24 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   // Keys wider than the shared-key scan can hold the queries for, at batches
   // of two or more query tiles: the tiled contraction streams both operands
   // through LDS (4 query tiles per launch, or 8 for bf16: 64 queries).
-  if (mq_type && ix->KB > 32 && qt_all >= 2 && pl.terms < 4 && !filt) {
+  if (mq_type && ix->KB > 32 && qt_all >= 2 && pl.terms < 4) {
     const int qtw = (ix->dtype == kBF16 && qt_all > 4) ? 8 : 4;
     const int nq = qtw * pl.qpt;
+    const int np = qtw * (4 / pl.terms);  // score slots per lane
     // main pass: 8 waves over panels of 32 key tiles (one query read per 32
     // tiles) where that kernel exists and fits, else 4 waves over 16 tiles
     int sm = 0, ss = 0, nwm = 0;
     for (auto nw_st : {std::make_pair(8, 3), std::make_pair(4, 5), std::make_pair(4, 3)})
-      if (!sm && scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nw_st.first, nw_st.second, true) &&
-          scan_tc_lds_bytes(qtw, pl.tpw_main, nw_st.first, nw_st.second, nq, pl.C) <=
+      if (!sm &&
+          scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nw_st.first, nw_st.second, true, filt) &&
+          scan_tc_lds_bytes(qtw, pl.tpw_main, nw_st.first, nw_st.second, nq, pl.C, np, filt) <=
               ix->lds_max) {
         nwm = nw_st.first;
         sm = nw_st.second;
       }
     for (int st : {8, 4})
-      if (!ss && scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, st, nq, pl.C) <= ix->lds_max)
+      if (!ss &&
+          scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, st, nq, pl.C, np, filt) <= ix->lds_max)
         ss = st;
     if (sm && ss) {
       pl.tc = true;
@@ -279,10 +282,10 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
       pl.qt = qtw;
       pl.bmax = std::min(B, nq);
       pl.CL = 0;
-      pl.kmain = scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nwm, sm, true);
-      pl.ksample = scan_tc_kernel(ix->dtype, qtw, pl.tpw_sample, pl.nw_sample, ss, false);
-      pl.lds = scan_tc_lds_bytes(qtw, pl.tpw_main, nwm, sm, nq, pl.C);
-      pl.lds_s = scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, ss, nq, pl.C);
+      pl.kmain = scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nwm, sm, true, filt);
+      pl.ksample = scan_tc_kernel(ix->dtype, qtw, pl.tpw_sample, pl.nw_sample, ss, false, filt);
+      pl.lds = scan_tc_lds_bytes(qtw, pl.tpw_main, nwm, sm, nq, pl.C, np, filt);
+      pl.lds_s = scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, ss, nq, pl.C, np, filt);
     }
   }
   if (pl.tc) {
@@ -643,8 +646,8 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
       for (int tpw : {1, 4})
         for (int nw : {4, 8})
           for (int st : {3, 4, 5, 8})
-            for (bool mp : {false, true})
-              if (ScanKernel kf = scan_tc_kernel(v, qtw, tpw, nw, st, mp))
+            for (int mp = 0; mp < 4; ++mp)
+              if (ScanKernel kf = scan_tc_kernel(v, qtw, tpw, nw, st, (mp & 1) != 0, mp >= 2))
                 (void)hipFuncSetAttribute((const void *)kf,
                                           hipFuncAttributeMaxDynamicSharedMemorySize,
                                           (int)ix->lds_max);

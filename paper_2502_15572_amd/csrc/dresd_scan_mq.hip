@@ -374,7 +374,8 @@ struct WaveCands {
     const uint32_t row = (uint32_t)row64;
 #pragma unroll
     for (int j = 0; j < NP; ++j) {
-      uint64_t key = row_ok ? make_key(sc[j], row) : 0ull;
+      // rows outside the datastore, and rows the filter drops (NaN), list nothing
+      uint64_t key = (row_ok && sc[j] == sc[j]) ? make_key(sc[j], row) : 0ull;
 #pragma unroll
       for (int off = 1; off < kTileRows; off <<= 1) {
         const uint64_t o = __shfl_xor(key, off, kWaveSize);
@@ -765,23 +766,25 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 // Tiled contraction for keys wider than the shared-key scan can hold the
 // queries for (more than 32 blocks per key tile) at batches of QTW = 4 or 8
 // query tiles: both operands stream through LDS.  A workgroup of NW waves
-// walks its key tiles in panels of NW TPW tiles.  For each 32-dim column of the keys one
-// ring stage holds the panel's key blocks and the batch's query blocks of
-// that column (a plain GEMM K loop); wave w multiplies its TPW tiles by
-// every query tile, column after column into one accumulator per (tile,
-// query tile) -- the same order in every pass, so a key scores the same in
-// the sampled and the main passes -- and after the last column tests the
-// finished tiles against the thresholds.  Each key block reaches the CU once
-// for the whole batch; the query operand (QTW KiB per column, shared by
-// every workgroup) is re-read from L2 once per panel.  Wave w issues its
-// TPW key copies and the copies of query tiles w, w + NW, ... per stage
-// (past the end, the last stage again), spread over the query tiles' matrix
+// walks its key tiles in panels of NW TPW tiles.  For each 32-dim column of
+// the keys one ring stage holds the panel's key blocks and the batch's query
+// blocks of that column (a plain GEMM K loop); wave w multiplies its TPW
+// tiles by every query tile, column after column into one accumulator per
+// (tile, query tile) -- the same order in every pass, so a key scores the
+// same in the sampled and the main passes -- and after the last column tests
+// the finished tiles against the thresholds.  Each key block reaches the CU
+// once for the whole batch; the query operand (QTW KiB per column, shared by
+// every workgroup) is re-read from L2 once per panel.  Wave w issues its TPW
+// key copies and the copies of query tiles w, w + NW, ... per stage (past
+// the end, the last stage again), spread over the query tiles' matrix
 // instructions so that the copies' address work overlaps the matrix cores;
-// its wait before each stage is a constant of its copy count.  Lists: one per (query, wave).  A sampled pass (TMAX) lists only
-// each tile's best key per query.
-template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool TMAX>
+// its wait before each stage is a constant of its copy count.  Lists: one per
+// (query, wave).  A sampled pass (TMAX) lists only each tile's best key per
+// query.  FILT: the next-token filter; a panel's test reads its rows' first
+// tokens, a load that waits once per panel for the ring copies in flight.
+template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool TMAX, bool FILT>
 __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
-  using WC = WaveCands<DT, QTW, CPQ, false, kTcCandBuf>;
+  using WC = WaveCands<DT, QTW, CPQ, FILT, kTcCandBuf>;
   constexpr int NP = WC::NP;
   constexpr int PT = NW * TPW;  // key tiles per panel
   constexpr int SB = PT + QTW;  // 1 KiB blocks per stage
@@ -799,7 +802,13 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   const int nwg = p.G / NW;
   const int cpw = TPW + (QTW - wv + NW - 1) / NW;  // this wave's copies per stage
   const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C, kTcCandBuf);
-  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nullptr, 0, wg * NW + wv);
+  // LDS: ring | one candidate region per wave | (filtered search) per wave
+  // the next token of each score slot [4 lane groups][NP]
+  int32_t *nt_slot = FILT ? reinterpret_cast<int32_t *>(smem + (size_t)S * SB * kBlockBytes +
+                                                        (size_t)NW * wreg) +
+                                wv * 4 * NP
+                          : nullptr;
+  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nt_slot, 0, wg * NW + wv);
   wc.init();
 
   // This workgroup's key tiles: visited tiles [v0, v1).
@@ -894,12 +903,19 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
         cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
       }
+      int ft[TPW];  // filtered search: this lane's row's first token per tile
+#pragma unroll
+      for (int i = 0; i < TPW; ++i) {
+        int64_t vt = pn * PT + wv * TPW + i;
+        vt = vt < ntile ? vt : ntile - 1;
+        ft[i] = FILT ? p.ftok[(v0 + vt) * p.stride * kTileRows + (lane & 15)] : 0;
+      }
 #pragma unroll
       for (int i = 0; i < TPW; ++i) {
         const int64_t vt = pn * PT + wv * TPW + i;
         if (vt < ntile) {
           float sc[NP];
-          wc.scores_of(acc[i], 0, sc);
+          wc.scores_of(acc[i], ft[i], sc);
           if (TMAX) wc.take_tile_max((v0 + vt) * p.stride, sc);
           else if (wc.any_hit(sc)) wc.take((v0 + vt) * p.stride, sc);
         }
@@ -910,15 +926,15 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   wc.publish();
 }
 
-template <int DT, int QTW, int CPQ, int TPW, int NW, int S>
+template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool FILT>
 __global__ void __launch_bounds__(NW * kWaveSize, 8 / NW) dresd_scantc_main(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, false>(p);
+  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, false, FILT>(p);
 }
 
 // Sampled pass: per-tile maxima as candidates.
-template <int DT, int QTW, int CPQ, int TPW, int NW, int S>
+template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool FILT>
 __global__ void __launch_bounds__(NW * kWaveSize, 8 / NW) dresd_scantc_sample(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, true>(p);
+  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, true, FILT>(p);
 }
 
 // One thread per 16-byte chunk (t, kb, lane) of the query operands.
@@ -956,25 +972,29 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
 // stages: one query read per 32 key tiles) or 4 waves (5 stages, or 3 where
 // large lists leave less LDS); sampled passes with 1 key tile per wave and
 // 4 waves (8 or 4 stages).
-#define DRESD_TC_MAIN(DT, CPQ, QTW, TPW, NW, S)                           \
-  if (main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S) \
-    return dresd_scantc_main<DT, QTW, CPQ, TPW, NW, S>;
-#define DRESD_TC_SAMPLE(DT, CPQ, QTW, TPW, NW, S)                          \
-  if (!main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S) \
-    return dresd_scantc_sample<DT, QTW, CPQ, TPW, NW, S>;
+#define DRESD_TC_MAIN(DT, CPQ, QTW, TPW, NW, S)                                          \
+  if (main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S)                \
+    return filtered ? (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, NW, S, true>    \
+                    : (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, NW, S, false>;
+#define DRESD_TC_SAMPLE(DT, CPQ, QTW, TPW, NW, S)                                         \
+  if (!main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S)                \
+    return filtered ? (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, NW, S, true>  \
+                    : (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, NW, S, false>;
 #define DRESD_TC_ALL(DT, CPQ, QTW)                                                            \
   DRESD_TC_MAIN(DT, CPQ, QTW, 4, 8, 3)                                                        \
   DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 5) DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 3)                   \
   DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 8) DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 4)
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
-ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nw, int stages, bool main_pass) {
+ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nw, int stages, bool main_pass,
+                              bool filtered) {
   DRESD_TC_ALL(kF16, 1, 4)
   return nullptr;
 }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
-ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nw, int stages, bool main_pass) {
+ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nw, int stages, bool main_pass,
+                               bool filtered) {
   DRESD_TC_ALL(kBF16, 2, 4)
   DRESD_TC_ALL(kBF16, 2, 8)
   return nullptr;

@@ -160,3 +160,56 @@ def test_filtered_all_rows_match_equals_unfiltered(gpu_lib):
     for x, y in zip(a, b):
         assert torch.equal(x, y)
     ix.close()
+
+
+# Keys of more than 1,024 dims at batches of two or more query tiles take the
+# tiled contraction; its filtered form tests each panel's rows against the
+# slots' next tokens, and its sampled pass (per-tile maxima) skips the rows
+# the filter drops.
+FILTERED_TILED = [
+    # (dtype, N, d, B, k)
+    ("bf16", 20000, 4096, 64, 10),   # 8 query tiles, sampled pass at stride 16
+    ("f16", 30000, 2048, 40, 16),    # f16, 4 query tiles (8 waves, per-wave copy counts)
+    ("bf16", 3001, 1100, 33, 12),    # ragged columns, no sampled pass
+]
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", FILTERED_TILED,
+                         ids=["%s-N%d-d%d-B%d-k%d" % c for c in FILTERED_TILED])
+def test_filtered_tiled_contraction(gpu_lib, dt, N, d, B, k):
+    from paper_2502_15572_amd import Index
+    say("filtered tiled", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N + d * 17 + B * 3 + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    src = torch.randint(0, N, (B,), generator=gen)
+    q = x[src].to(torch.float64) + 0.05 * torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 4, (N, 3), generator=gen, dtype=torch.int32)  # ~1/4 of rows match
+    nt = cont[src, 0].numpy().astype(np.int32)
+    nt[3::4] = NO_ROW_TOKEN
+    ix = Index(x.to(DEV), cont.to(DEV))
+    assert ix.plan(B, k)["scan_kernel"] == "tiled"
+    ix.close()
+    rep = run_filtered(x, cont, q, nt, k, dt)
+    say("  exact-order rate %.3f" % rep["exact_order_rate"])
+
+
+def test_filtered_tiled_all_rows_match_equals_unfiltered(gpu_lib):
+    """The tiled contraction's filtered form with a token every row starts
+    with returns the unfiltered result bit for bit."""
+    from paper_2502_15572_amd import Index
+    say("filtered tiled all-match")
+    gen = torch.Generator().manual_seed(77)
+    N, d, B, k = 20000, 4096, 64, 10
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(torch.bfloat16)
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32).to(DEV)
+    cont = torch.full((N, 2), 5, dtype=torch.int32)
+    ix = Index(x.to(DEV), cont.to(DEV))
+    a = ix.search(q, k)
+    b = ix.search(q, k, next_tok=torch.full((B,), 5, dtype=torch.int32, device=DEV))
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
+    ix.close()
