@@ -196,12 +196,13 @@ inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int nw, int stages
   return nullptr;
 }
 // LDS of the tiled contraction: ring | per wave a candidate region |
-// (filtered search) per wave the next tokens of its score slots.
+// (filtered search) per wave the next tokens of its score slots and the
+// first tokens of its panel tiles' rows.
 __host__ __device__ inline size_t scan_tc_lds_bytes(int qtw, int tpw, int nw, int stages, int nq,
                                                     int C, int np, bool filtered) {
   return (size_t)stages * (nw * tpw + qtw) * kBlockBytes +
          (size_t)nw * scan_mq_wave_bytes(nq, C, kTcCandBuf) +
-         (filtered ? (size_t)nw * 16 * np : 0);
+         (filtered ? (size_t)nw * (16 * np + 4 * kWaveSize) : 0);
 }
 void *qop_kernel_f16();
 void *qop_kernel_bf16();

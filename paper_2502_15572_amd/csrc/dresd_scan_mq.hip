@@ -780,8 +780,10 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 // instructions so that the copies' address work overlaps the matrix cores;
 // its wait before each stage is a constant of its copy count.  Lists: one per
 // (query, wave).  A sampled pass (TMAX) lists only each tile's best key per
-// query.  FILT: the next-token filter; a panel's test reads its rows' first
-// tokens, a load that waits once per panel for the ring copies in flight.
+// query.  FILT: the next-token filter; each wave copies its panel tiles'
+// first tokens into LDS with one more LDS-DMA copy at the panel's first
+// stage (a load the compiler tracked would make it drain the ring at every
+// stage), covered by the next stage's constant wait.
 template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool TMAX, bool FILT>
 __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   using WC = WaveCands<DT, QTW, CPQ, FILT, kTcCandBuf>;
@@ -803,11 +805,16 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   const int cpw = TPW + (QTW - wv + NW - 1) / NW;  // this wave's copies per stage
   const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C, kTcCandBuf);
   // LDS: ring | one candidate region per wave | (filtered search) per wave
-  // the next token of each score slot [4 lane groups][NP]
+  // the next token of each score slot [4 lane groups][NP] | per wave the
+  // first tokens of its panel tiles' rows [64] (TPW * 16 used)
   int32_t *nt_slot = FILT ? reinterpret_cast<int32_t *>(smem + (size_t)S * SB * kBlockBytes +
                                                         (size_t)NW * wreg) +
                                 wv * 4 * NP
                           : nullptr;
+  int32_t *ftb = FILT ? reinterpret_cast<int32_t *>(smem + (size_t)S * SB * kBlockBytes +
+                                                    (size_t)NW * wreg) +
+                            NW * 4 * NP + wv * kWaveSize
+                      : nullptr;
   WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nt_slot, 0, wg * NW + wv);
   wc.init();
 
@@ -879,6 +886,17 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         if (CPW_HI == CPW_LO || cpw == CPW_HI) wait_vmcnt<CPW_HI * (S - 2)>();
         else wait_vmcnt<CPW_LO * (S - 2)>();
         __syncthreads();
+        if (FILT && c == 0) {
+          // first tokens of this wave's tiles of the panel (lane l: tile
+          // l / 16, row l % 16; clamped to the last tile; lanes past TPW
+          // tiles copy unused values), read after the panel's last column.
+          // Issued before this stage's copies, it is complete once the next
+          // stage's wait leaves at most CPW copies in flight.
+          int64_t t = pn * PT + wv * TPW + (lane >> 4);
+          t = t < ntile ? t : ntile - 1;
+          copy1_to_lds(p.ftok + (v0 + t) * p.stride * kTileRows + (lane & 15),
+                       (uint32_t)(uintptr_t)ftb);
+        }
         const u4 *sl = reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes) + lane;
         u4 kv[TPW], qv[QTW];
 #pragma unroll
@@ -905,11 +923,7 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
       }
       int ft[TPW];  // filtered search: this lane's row's first token per tile
 #pragma unroll
-      for (int i = 0; i < TPW; ++i) {
-        int64_t vt = pn * PT + wv * TPW + i;
-        vt = vt < ntile ? vt : ntile - 1;
-        ft[i] = FILT ? p.ftok[(v0 + vt) * p.stride * kTileRows + (lane & 15)] : 0;
-      }
+      for (int i = 0; i < TPW; ++i) ft[i] = FILT ? ftb[i * kTileRows + (lane & 15)] : 0;
 #pragma unroll
       for (int i = 0; i < TPW; ++i) {
         const int64_t vt = pn * PT + wv * TPW + i;
