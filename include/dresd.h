@@ -63,7 +63,7 @@ typedef enum {
   DRESD_EINVAL = 1,      /* an argument is out of its documented range     */
   DRESD_ENOMEM = 2,      /* a device allocation failed (nothing leaked)    */
   DRESD_EDEVICE = 3,     /* a HIP call failed; message in dresd_last_error */
-  DRESD_EUNSUPPORTED = 4 /* valid request this build cannot serve          */
+  DRESD_EUNSUPPORTED = 4 /* valid request the library cannot serve        */
 } dresd_status;
 
 /* Largest k a search may ask for. */

@@ -1,8 +1,10 @@
-// gfx950 scan for batches spanning several 16-column query tiles (the same
+// gfx950 scans for batches spanning several 16-column query tiles (the same
 // computation as the scan in dresd_kernels.hip: DReSD Section 3.5, Eq. 3
-// with unit-norm keys as exact top-k, Section 3.6).
+// with unit-norm keys as exact top-k, Section 3.6): the shared-key scan
+// below, and the tiled contraction (scan_tc_body) for keys too wide for it.
 //
-// The queries stay in registers and the keys are shared through LDS:
+// Shared-key scan: the queries stay in registers and the keys are shared
+// through LDS:
 //   * the workgroup's 4 waves split the query tiles; each wave holds its
 //     tiles' A operands for every 32-dim block of the keys in VGPRs;
 //   * the workgroup streams its key tiles through a ring of S LDS stages of
