@@ -516,7 +516,7 @@ def main():
 # (33.5M keys, 128 dims, Zipf-sized clusters) at one query per step and at a
 # 128-query batch, and the 10M x 256 datastore at 256 queries (the matrix-core
 # regime).
-SECONDARY = [("hidden1m_d4096_bf16", 64), ("zipf33m_d128_f16", 1), ("zipf33m_d128_f16", 128),
+SECONDARY = [("zipf33m_d128_f16", 1), ("zipf33m_d128_f16", 128), ("hidden1m_d4096_bf16", 64),
              ("batch10m_d256_f16", 256)]
 
 
