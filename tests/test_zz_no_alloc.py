@@ -82,3 +82,46 @@ def test_noalloc_matches_search(gpu_lib):
     assert st == EINVAL and b"scratch" in gpu_lib.dresd_last_error()
     assert (big[0] == -7).all() and (big[1] == 7.0).all() and (big[2] == -7).all()
     ix.close()
+
+
+def test_noalloc_tiled_contraction(gpu_lib):
+    """The same contract on the tiled contraction (keys of 2,048 dims, 9-16
+    queries, each with a sampled pass): bit-identical to dresd_search on two
+    calls in a row, the second smaller, with no device allocation."""
+    from paper_2502_15572_amd import Index
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    N, d, L = 20011, 2048, 4
+    x = torch.randn(N, d, device=DEV, generator=gen)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    cont = torch.randint(0, 32000, (N, L), device=DEV, generator=gen, dtype=torch.int32)
+    q = torch.randn(16, d, device=DEV, generator=gen)
+    q = (q / q.norm(dim=1, keepdim=True)).contiguous()
+    ix = Index(x, cont)
+    cases = [(16, 12), (9, 5)]
+    outs = {c: _outs(c[0], c[1], L) for c in cases}
+    refs = {}
+    for B, k in cases:
+        plan = ix.plan(B, k)
+        assert plan["scan_kernel"] == "tiled" and plan["sample_passes"] == 1
+        assert plan["workspace_bytes"] <= SCRATCH_BYTES
+        refs[(B, k)] = [t.clone() for t in ix.search(q[:B].contiguous(), k)]
+    torch.cuda.synchronize()
+    qs = {c: q[:c[0]].contiguous() for c in cases}
+    st = _noalloc(gpu_lib, ix, qs[cases[0]], outs[cases[0]])
+    assert st == OK, gpu_lib.dresd_last_error()
+    torch.cuda.synchronize()
+    free0 = torch.cuda.mem_get_info()[0]
+    os.environ["DRESD_FAIL_ALLOC_AT"] = "1"
+    try:
+        for B, k in cases:
+            say("noalloc tiled B=%d k=%d" % (B, k))
+            st = _noalloc(gpu_lib, ix, qs[(B, k)], outs[(B, k)])
+            assert st == OK, gpu_lib.dresd_last_error()
+        torch.cuda.synchronize()
+    finally:
+        os.environ.pop("DRESD_FAIL_ALLOC_AT", None)
+    assert torch.cuda.mem_get_info()[0] == free0
+    for c in cases:
+        for a, b in zip(outs[c], refs[c]):
+            assert torch.equal(a, b), c
+    ix.close()
