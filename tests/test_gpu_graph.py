@@ -74,3 +74,50 @@ def test_captured_step_replays_match_eager(gpu_lib, partitioned):
             assert torch.equal(a, b), i
     assert (out[0] >= -1).all() and int(dout[1].max()) >= 1
     ix.close()
+
+
+@pytest.mark.parametrize("kind,N,d,B,k", [
+    ("shared_key", 60000, 128, 64, 16),   # queries in registers, keys through the LDS ring
+    ("tiled", 20011, 2048, 24, 12),       # both operands through the LDS ring, sampled pass
+], ids=["shared_key", "tiled"])
+def test_captured_search_replays_match_eager(gpu_lib, kind, N, d, B, k):
+    """The batched scans in a captured graph (after one warm-up search of the
+    same shape): each replay, with other work and synchronisations between
+    replays, returns what the eager search returns for its input, bit for bit."""
+    from paper_2502_15572_amd import Index
+    dev = torch.device(DEV)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    keys = torch.randn(N, d, device=dev, generator=gen)
+    keys = (keys / keys.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    cont = torch.randint(0, 32000, (N, 3), device=dev, generator=gen, dtype=torch.int32)
+    qs = torch.randn(4, B, d, device=dev, generator=gen)
+    qs = qs / qs.norm(dim=2, keepdim=True)
+    ix = Index(keys, cont)
+    assert ix.plan(B, k)["scan_kernel"] == kind
+    q_in = torch.empty(B, d, device=dev)
+    out = (torch.empty((B, k), dtype=torch.int64, device=dev),
+           torch.empty((B, k), dtype=torch.float32, device=dev),
+           torch.empty((B, k, 3), dtype=torch.int32, device=dev))
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        q_in.copy_(qs[0])
+        ix.search(q_in, k, out=out, stream=s)  # warm-up: the workspace reaches its size
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        ix.search(q_in, k, out=out, stream=s)
+    torch.cuda.synchronize()
+    for i in range(6):
+        q_in.copy_(qs[i % 4])
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        replayed = [t.clone() for t in out]
+        torch.randn(4096, device=dev).sum().item()  # other work between replays
+        with torch.cuda.stream(s):
+            ix.search(q_in, k, out=out, stream=s)
+        torch.cuda.synchronize()
+        for a, b in zip(replayed, out):
+            assert torch.equal(a, b), i
+    assert (out[0] >= 0).all()
+    ix.close()
