@@ -230,6 +230,39 @@ def test_tiled_contraction_shapes(gpu_lib, dt, N, d, B, k):
         % (rep["max_abs_vs_exact"], rep["max_abs_vs_model"], rep["operand"]))
 
 
+def _random_tiled_cases(n, seed):
+    """Seeded random shapes for the tiled contraction: dims past 1,024 (ragged
+    column counts included), 9-140 queries (one to three launches), k from 1
+    to 257, and as many rows as keep the oracle to a few seconds."""
+    import random
+    rng = random.Random(seed)
+    out = []
+    while len(out) < n:
+        dt = rng.choice(["bf16", "f16"])
+        d = rng.choice([1056, 1200, 1536, 2048, 2500, 3072, 4096])
+        B = rng.randint(9 if dt == "bf16" else 17, 140)
+        k = rng.choice([1, 3, 10, 33, 100, 257])
+        N = rng.randint(max(k, 300), 30000)
+        if N * d * B <= 2.5e9:
+            out.append((dt, N, d, B, k))
+    return out
+
+
+TC_RANDOM = _random_tiled_cases(8, 2025)
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", TC_RANDOM, ids=["%s-N%d-d%d-B%d-k%d" % e for e in TC_RANDOM])
+def test_tiled_contraction_random_shapes(gpu_lib, dt, N, d, B, k):
+    say("tiled random", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N + d + B * 31 + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 2), generator=gen, dtype=torch.int32)
+    run_case(gpu_lib, x, cont, q, k, dt, kind="tiled")
+
+
 def test_grouped_launch_matches_split_batches(gpu_lib):
     """A batch whose single-tile groups share one launch returns, bit for
     bit, what the same queries return as separate batches of one group each
