@@ -315,6 +315,7 @@ def time_partitioned(args):
         w = w.scaled(args.n)
     k = args.k or w.k
     B, P = args.batch, args.ivf
+    w = w.with_pool(B)  # every batch holds B distinct queries
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     t0 = time.time()
@@ -342,6 +343,7 @@ def time_partitioned(args):
         % (P, ns, train_s, build_s, info["tiles"]))
     nb = max(1, pool.shape[0] // B)
     batches = [pool[i * B:(i + 1) * B].contiguous() for i in range(nb)]
+    assert all(b.shape[0] == B for b in batches), "query pool smaller than the batch"
     nts = [None] * nb
     if args.filtered:  # as in the exact bench: the source row's first token
         c0 = cont[:, 0]
@@ -529,7 +531,8 @@ def measure(w, B, k, args, dev, probe=False, cpu=False, time_cpu=False, measured
     from datagen import generate
     from paper_2502_15572_amd import Index
 
-    if cache is not None and cache.get("name") == w.name:
+    w = w.with_pool(B)  # every batch holds B distinct queries
+    if cache is not None and cache.get("name") == (w.name, w.pool):
         g, ix, build_s = cache["g"], cache["ix"], cache["build_s"]
     else:
         if cache is not None and cache.get("ix") is not None:
@@ -545,10 +548,11 @@ def measure(w, B, k, args, dev, probe=False, cpu=False, time_cpu=False, measured
         build_s = time.time() - t0
         log("index built in %.2fs" % build_s)
         if cache is not None:
-            cache.update(name=w.name, g=g, ix=ix, build_s=build_s)
+            cache.update(name=(w.name, w.pool), g=g, ix=ix, build_s=build_s)
     pool = g["queries"]
     nb = max(1, pool.shape[0] // B)
     batches = [pool[(i % nb) * B:(i % nb) * B + B].contiguous() for i in range(nb)]
+    assert all(b.shape[0] == B for b in batches), "query pool smaller than the batch"
     tok_batches = [None] * nb
     if args.filtered:
         c0 = g["cont"][:, 0]

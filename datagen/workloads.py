@@ -59,6 +59,11 @@ class Workload:
         """Same recipe at a different datastore size (for fast parity runs)."""
         return dataclasses.replace(self, N=int(N))
 
+    def with_pool(self, n: int) -> "Workload":
+        """Same recipe with a query pool of at least n queries (a batch larger
+        than the pool takes a larger one; smaller batches keep the pool)."""
+        return self if n <= self.pool else dataclasses.replace(self, pool=int(n))
+
     @property
     def elem_bytes(self) -> int:
         return 4 if self.dtype == "f32" else 2

@@ -66,3 +66,15 @@ def test_mixed_queries_interleave():
     kinds = g["query_kind"].tolist()
     assert kinds[0::2] == [0] * (w.pool // 2) and kinds[1::2] == [1] * (w.pool // 2)
     assert all(s >= 0 for s in g["query_src"][0::2].tolist())
+
+
+def test_pool_grows_to_the_batch():
+    # a batch larger than the workload's query pool takes a pool of that many
+    # distinct queries (the bench never repeats or drops queries in a batch)
+    w = WORKLOADS["pca4m_d1024_f16"].scaled(2000)
+    assert w.with_pool(w.pool) is w and w.with_pool(1) is w
+    big = w.with_pool(256)
+    assert big.pool == 256 and big.N == w.N and big.d == w.d
+    q = generate(big, "cpu")["queries"]
+    assert tuple(q.shape) == (256, w.d)
+    assert torch.unique(q, dim=0).shape[0] == 256
