@@ -628,7 +628,7 @@ def measure(w, B, k, args, dev, probe=False, cpu=False, time_cpu=False, measured
                    "filtered": bool(args.filtered),
                    "L": w.L, "query_pool": int(pool.shape[0]),
                    "sample_passes": plan["sample_passes"], "scan_waves": plan["scan_waves"],
-                   "scan_kernel": plan["scan_kernel"]},
+                   "scan_kernel": plan["scan_kernel"], "scan_launches": plan["launches"]},
         "p50_latency_us": p50 * 1e3,
         "p90_latency_us": p90 * 1e3,
         "search_hbm_GBps_at_p50": search_bytes / (p50 * 1e-3) / 1e9,
@@ -642,9 +642,13 @@ def measure(w, B, k, args, dev, probe=False, cpu=False, time_cpu=False, measured
             "frac": (flops / (scan_ms * 1e-3) / mfma_peak) if mfma_bound
                     else achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
+            # a batch that takes several launches (each a pass over the keys
+            # for its part of the batch) counts the keys once: bytes, flops
+            # and time are those of the whole batch's main scan
             "algorithmic_bytes_per_launch": scan_bytes,
             "algorithmic_flops_per_launch": flops,
             "avg_launch_ms": scan_ms,
+            "launches": plan["launches"],
             "hbm_GBps": achieved,
             "hbm_frac": achieved / HBM_PEAK_GBPS,
             "hbm_frac_of_measured_peak": (achieved / peak) if peak else None,

@@ -287,20 +287,23 @@ dresd_status dresd_pack_drafts(const int32_t *tokens, int32_t B, int32_t k, int3
  * Describe how the next search of this shape would run (host outputs, NULL
  * allowed): the number of passes over sampled keys before the main pass, the
  * number of waves of the main scan (of the first launch when the batch
- * takes several), the bytes of workspace it needs, and
+ * takes several), the bytes of workspace it needs,
  * which scan kernel runs it: 0 = single-tile scan (batches within one
  * 16-column query tile group, queries staged in LDS), 1 = shared-key scan
  * (queries held in registers, keys staged through LDS), 2 = single-tile scan
  * serving several query groups per launch (batches whose query operands
  * exceed one workgroup's LDS; the groups share each key range through L2),
  * 3 = tiled contraction (keys of more than 1,024 dims at batches of two or
- * more query tiles: key and query blocks both streamed through LDS, column
- * by column, for panels of 32 key tiles).
+ * more query tiles, and 1,024-dim keys at batches past four query tiles: key
+ * and query blocks both streamed through LDS, column by column, for panels
+ * of 16 or 32 key tiles), and the number of launches of the main scan (each
+ * one pass over the keys for a part of the batch).
  * Errors: EINVAL for the same argument errors as dresd_search.
  */
 dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,
                                int32_t *sample_passes, int32_t *scan_waves,
-                               int64_t *workspace_bytes, int32_t *scan_kind);
+                               int64_t *workspace_bytes, int32_t *scan_kind,
+                               int32_t *launches);
 
 /*
  * Partitioned (approximate) search.  The paper retrieves with an approximate

@@ -103,12 +103,13 @@ class Index:
         return idx, score, tok
 
     def plan(self, B: int, k: int):
-        sp, w, ws, kind = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int32()
+        sp, w, ws = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+        kind, nl = ctypes.c_int32(), ctypes.c_int32()
         _lib.check(self._lib.dresd_search_plan(self._h, int(B), int(k), ctypes.byref(sp),
                                                ctypes.byref(w), ctypes.byref(ws),
-                                               ctypes.byref(kind)))
+                                               ctypes.byref(kind), ctypes.byref(nl)))
         return {"sample_passes": sp.value, "scan_waves": w.value, "workspace_bytes": ws.value,
-                "scan_kernel": SCAN_KINDS[kind.value]}
+                "scan_kernel": SCAN_KINDS[kind.value], "launches": nl.value}
 
     def profile(self, on: bool = True):
         _lib.check(self._lib.dresd_profile_enable(self._h, 1 if on else 0))

@@ -87,7 +87,8 @@ def _declare(lib):
                                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]
     lib.dresd_profile_read.restype = ctypes.c_int
     lib.dresd_search_plan.argtypes = [P, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(I32),
-                                      ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(I32)]
+                                      ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(I32),
+                                      ctypes.POINTER(I32)]
     lib.dresd_search_plan.restype = ctypes.c_int
     lib.dresd_bw_probe.argtypes = [P, I64, I32, I32, ctypes.POINTER(ctypes.c_double), P]
     lib.dresd_bw_probe.restype = ctypes.c_int

@@ -179,31 +179,37 @@ inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, bo
   if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass, filtered, stages);
   return nullptr;
 }
-// Query-operand kernel of the shared-key scan for a key type (launch with
-// 256 threads, one thread per 16-byte chunk).
-// Tiled contraction (both operands through LDS): qtw query tiles per
-// launch (4, or 8 for bf16), tpw key tiles per wave, nw waves per
-// workgroup, ring stages: main passes (4, 8, 3), (4, 4, 5) and (4, 4, 3);
-// sampled passes (1, 4, 8) and (1, 4, 4); each also next-token filtered;
-// null for other shapes.
-ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nw, int stages, bool main_pass, bool filtered);
-ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nw, int stages, bool main_pass,
+// Tiled contraction (both operands through LDS): qtw query tiles per wave
+// (4, or 8 for bf16), tpw key tiles per wave, nk key groups x nq query groups
+// of waves per workgroup, ring stages.  One query group: main passes
+// (tpw, nk, stages) = (4, 8, 3), (4, 4, 5) and (4, 4, 3), sampled passes
+// (1, 4, 8) and (1, 4, 4).  Two query groups: main (4, 4, 3), sampled
+// (2, 4, 4).  Four (f16): main (8, 2, 3), sampled (4, 2, 4).  Each also next-
+// token filtered; null for other shapes.
+ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nk, int nq, int stages, bool main_pass,
+                              bool filtered);
+ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nk, int nq, int stages, bool main_pass,
                                bool filtered);
-inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int nw, int stages, bool main_pass,
-                                 bool filtered) {
-  if (dtype == kF16) return scan_tc_kernel_f16(qtw, tpw, nw, stages, main_pass, filtered);
-  if (dtype == kBF16) return scan_tc_kernel_bf16(qtw, tpw, nw, stages, main_pass, filtered);
+inline ScanKernel scan_tc_kernel(int dtype, int qtw, int tpw, int nk, int nq, int stages,
+                                 bool main_pass, bool filtered) {
+  if (dtype == kF16) return scan_tc_kernel_f16(qtw, tpw, nk, nq, stages, main_pass, filtered);
+  if (dtype == kBF16) return scan_tc_kernel_bf16(qtw, tpw, nk, nq, stages, main_pass, filtered);
   return nullptr;
 }
 // LDS of the tiled contraction: ring | per wave a candidate region |
 // (filtered search) per wave the next tokens of its score slots and the
-// first tokens of its panel tiles' rows.
-__host__ __device__ inline size_t scan_tc_lds_bytes(int qtw, int tpw, int nw, int stages, int nq,
-                                                    int C, int np, bool filtered) {
-  return (size_t)stages * (nw * tpw + qtw) * kBlockBytes +
-         (size_t)nw * scan_mq_wave_bytes(nq, C, kTcCandBuf) +
-         (filtered ? (size_t)nw * (16 * np + 4 * kWaveSize) : 0);
+// first tokens of its panel tiles' rows.  nqw queries and np score slots
+// per lane per wave.
+__host__ __device__ inline size_t scan_tc_lds_bytes(int qtw, int tpw, int nk, int nq, int stages,
+                                                    int nqw, int C, int np, bool filtered) {
+  const int nw = nk * nq;
+  const int ftw = 16 * tpw > kWaveSize ? 16 * tpw : kWaveSize;
+  return (size_t)stages * (nk * tpw + nq * qtw) * kBlockBytes +
+         (size_t)nw * scan_mq_wave_bytes(nqw, C, kTcCandBuf) +
+         (filtered ? (size_t)nw * (16 * np + 4 * ftw) : 0);
 }
+// Query-operand kernel of the shared-key scan and the tiled contraction for
+// a key type (launch with 256 threads, one thread per 16-byte chunk).
 void *qop_kernel_f16();
 void *qop_kernel_bf16();
 inline void *qop_kernel(int dtype) {

@@ -163,8 +163,10 @@ struct Plan {
   int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
   bool mq = false;                  // shared-key scan (queries in registers)
   bool tc = false;                  // tiled contraction (queries and keys through LDS)
-  int tpw_main = 4, tpw_sample = 1;  // tiled contraction: key tiles per wave per pass kind
-  int nw_main = 4, nw_sample = 4;    // tiled contraction: waves per workgroup per pass kind
+  // tiled contraction: key tiles per wave and key groups of waves per pass
+  // kind, query groups of waves (waves per workgroup: nk * nq)
+  int tpw_main = 4, tpw_sample = 1;
+  int nk_main = 4, nk_sample = 4, nq = 1;
   int bmax = 0;                 // queries per group
   int bl = 0;                   // queries per launch (several groups)
   int B = 0, nl = 0;            // batch, launches (launch i: group_of(pl, i))
@@ -187,7 +189,7 @@ struct Plan {
 // Threads per workgroup of a plan's main or sampled scan.
 int threads_of(const Plan &pl, bool main_pass) {
   if (!pl.tc) return kScanThreads;
-  return (main_pass ? pl.nw_main : pl.nw_sample) * kWaveSize;
+  return (main_pass ? pl.nk_main : pl.nk_sample) * pl.nq * kWaveSize;
 }
 
 // Launch i of a plan: queries [B i / nl, B (i + 1) / nl), split into groups
@@ -254,38 +256,57 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   const int qt_all = (int)ceil_div((int64_t)B * pl.terms, 16);  // query tiles of the batch
   const bool mq_type = (ix->dtype == kF16 && pl.terms == 1) || ix->dtype == kBF16;
   const bool mq_kb = ix->KB == 4 || ix->KB == 8 || ix->KB == 16 || ix->KB == 32;
-  // Keys wider than the shared-key scan can hold the queries for, at batches
-  // of two or more query tiles: the tiled contraction streams both operands
-  // through LDS (4 query tiles per launch, or 8 for bf16: 64 queries).
-  if (mq_type && ix->KB > 32 && qt_all >= 2 && pl.terms < 4) {
-    const int qtw = (ix->dtype == kBF16 && qt_all > 4) ? 8 : 4;
-    const int nq = qtw * pl.qpt;
+  // Keys wider than the shared-key scan can hold the queries for (more than
+  // 32 blocks per key tile) at batches of two or more query tiles, and
+  // 32-block keys at batches past the four query tiles one shared-key launch
+  // holds: the tiled contraction streams both operands through LDS.  One
+  // query group of waves serves 4 query tiles (8 for bf16: 64 queries);
+  // larger batches take 2 or 4 query groups (up to 256 f16 or 128 bf16
+  // queries per launch), fewer where the lists leave too little LDS.
+  const bool tc_kb = ix->KB > 32 || (ix->KB == 32 && qt_all > 4);
+  if (mq_type && tc_kb && qt_all >= 2 && pl.terms < 4) {
+    const bool bf = ix->dtype == kBF16;
+    const int qtw = (bf && qt_all > 4) ? 8 : 4;
+    const int nqw = qtw * pl.qpt;         // queries per wave
     const int np = qtw * (4 / pl.terms);  // score slots per lane
-    // main pass: 8 waves over panels of 32 key tiles (one query read per 32
+    int nq = 1;
+    while (nq < (bf ? 2 : 4) && nq * qtw < qt_all) nq <<= 1;
+    struct TcShape {
+      int tpw, nk, st;
+    };
+    // main-pass shapes, then sampled-pass shapes, in order of preference; one
+    // query group: 8 waves over panels of 32 key tiles (one query read per 32
     // tiles) where that kernel exists and fits, else 4 waves over 16 tiles
-    int sm = 0, ss = 0, nwm = 0;
-    for (auto nw_st : {std::make_pair(8, 3), std::make_pair(4, 5), std::make_pair(4, 3)})
-      if (!sm &&
-          scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nw_st.first, nw_st.second, true, filt) &&
-          scan_tc_lds_bytes(qtw, pl.tpw_main, nw_st.first, nw_st.second, nq, pl.C, np, filt) <=
-              ix->lds_max) {
-        nwm = nw_st.first;
-        sm = nw_st.second;
-      }
-    for (int st : {8, 4})
-      if (!ss &&
-          scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, st, nq, pl.C, np, filt) <= ix->lds_max)
-        ss = st;
-    if (sm && ss) {
+    static const std::vector<TcShape> main1 = {{4, 8, 3}, {4, 4, 5}, {4, 4, 3}},
+                                      samp1 = {{1, 4, 8}, {1, 4, 4}}, main2 = {{4, 4, 3}},
+                                      samp2 = {{2, 4, 4}}, main4 = {{8, 2, 3}},
+                                      samp4 = {{4, 2, 4}};
+    for (; nq >= 1 && !pl.tc; nq >>= 1) {
+      const auto &ms = nq == 4 ? main4 : nq == 2 ? main2 : main1;
+      const auto &ss = nq == 4 ? samp4 : nq == 2 ? samp2 : samp1;
+      const TcShape *m = nullptr, *smp = nullptr;
+      for (const auto &c : ms)
+        if (!m && scan_tc_kernel(ix->dtype, qtw, c.tpw, c.nk, nq, c.st, true, filt) &&
+            scan_tc_lds_bytes(qtw, c.tpw, c.nk, nq, c.st, nqw, pl.C, np, filt) <= ix->lds_max)
+          m = &c;
+      for (const auto &c : ss)
+        if (!smp && scan_tc_kernel(ix->dtype, qtw, c.tpw, c.nk, nq, c.st, false, filt) &&
+            scan_tc_lds_bytes(qtw, c.tpw, c.nk, nq, c.st, nqw, pl.C, np, filt) <= ix->lds_max)
+          smp = &c;
+      if (!m || !smp) continue;
       pl.tc = true;
-      pl.nw_main = nwm;
-      pl.qt = qtw;
-      pl.bmax = std::min(B, nq);
+      pl.nq = nq;
+      pl.tpw_main = m->tpw;
+      pl.nk_main = m->nk;
+      pl.tpw_sample = smp->tpw;
+      pl.nk_sample = smp->nk;
+      pl.qt = nq * qtw;
+      pl.bmax = std::min(B, nq * nqw);
       pl.CL = 0;
-      pl.kmain = scan_tc_kernel(ix->dtype, qtw, pl.tpw_main, nwm, sm, true, filt);
-      pl.ksample = scan_tc_kernel(ix->dtype, qtw, pl.tpw_sample, pl.nw_sample, ss, false, filt);
-      pl.lds = scan_tc_lds_bytes(qtw, pl.tpw_main, nwm, sm, nq, pl.C, np, filt);
-      pl.lds_s = scan_tc_lds_bytes(qtw, pl.tpw_sample, pl.nw_sample, ss, nq, pl.C, np, filt);
+      pl.kmain = scan_tc_kernel(ix->dtype, qtw, m->tpw, m->nk, nq, m->st, true, filt);
+      pl.ksample = scan_tc_kernel(ix->dtype, qtw, smp->tpw, smp->nk, nq, smp->st, false, filt);
+      pl.lds = scan_tc_lds_bytes(qtw, m->tpw, m->nk, nq, m->st, nqw, pl.C, np, filt);
+      pl.lds_s = scan_tc_lds_bytes(qtw, smp->tpw, smp->nk, nq, smp->st, nqw, pl.C, np, filt);
     }
   }
   if (pl.tc) {
@@ -362,11 +383,10 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   // scan over 32-block (1 KiB-row) key tiles.
   const bool one_per_cu = pl.tc || (pl.mq ? ix->KB >= 32 : pl.qt == 1);
   pl.wg_max = ix->cus * std::min(occ, one_per_cu ? kMaxTileWgPerCu : kMaxScanWgPerCu);
-  // lists per query: one per wave, or one per workgroup for the shared-key
-  // scan; at most kMergeLists
-  // lists per workgroup: one per wave (the tiled contraction: of its larger
-  // workgroup), or one for the shared-key scan
-  const int lists_per_wg = pl.mq ? 1 : pl.tc ? std::max(pl.nw_main, pl.nw_sample)
+  // lists per query from each workgroup (at most kMergeLists in all): one per
+  // wave, one for the shared-key scan, and one per key group of waves for
+  // the tiled contraction (of the pass kind with more)
+  const int lists_per_wg = pl.mq ? 1 : pl.tc ? std::max(pl.nk_main, pl.nk_sample)
                                              : kScanThreads / kWaveSize;
   pl.wg_max = std::min(pl.wg_max, kMergeLists / lists_per_wg);
   pl.G_max = pl.wg_max * lists_per_wg;
@@ -431,7 +451,7 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
 int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit, bool main_pass = true) {
   const int wpg = kScanThreads / kWaveSize;
   // tiled contraction: whole panels of nw * tpw tiles
-  const int per_wg = pl.tc ? (main_pass ? pl.nw_main * pl.tpw_main : pl.nw_sample * pl.tpw_sample)
+  const int per_wg = pl.tc ? (main_pass ? pl.nk_main * pl.tpw_main : pl.nk_sample * pl.tpw_sample)
                    : pl.mq ? 1 : wpg;
   int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(nvisit, per_wg));
   if (gr.ng > 1) wgs = std::min<int64_t>(wgs, std::max<int64_t>(8, pl.wg_max / gr.ng / 8 * 8));
@@ -643,14 +663,16 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
         }
   for (int v = 0; v < 3; ++v)
     for (int qtw : {4, 8})
-      for (int tpw : {1, 4})
-        for (int nw : {4, 8})
-          for (int st : {3, 4, 5, 8})
-            for (int mp = 0; mp < 4; ++mp)
-              if (ScanKernel kf = scan_tc_kernel(v, qtw, tpw, nw, st, (mp & 1) != 0, mp >= 2))
-                (void)hipFuncSetAttribute((const void *)kf,
-                                          hipFuncAttributeMaxDynamicSharedMemorySize,
-                                          (int)ix->lds_max);
+      for (int tpw : {1, 2, 4, 8})
+        for (int nk : {2, 4, 8})
+          for (int nq : {1, 2, 4})
+            for (int st : {3, 4, 5, 8})
+              for (int mp = 0; mp < 4; ++mp)
+                if (ScanKernel kf =
+                        scan_tc_kernel(v, qtw, tpw, nk, nq, st, (mp & 1) != 0, mp >= 2))
+                  (void)hipFuncSetAttribute((const void *)kf,
+                                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                                            (int)ix->lds_max);
   for (int v = 0; v < 3; ++v)
     if (ScanKernel kf = scan_parts_kernel(v))
       (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -714,7 +736,8 @@ void dresd_index_destroy(dresd_index *ix) {
 }
 
 dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int32_t *sample_passes,
-                               int32_t *scan_waves, int64_t *workspace_bytes, int32_t *scan_kind) {
+                               int32_t *scan_waves, int64_t *workspace_bytes, int32_t *scan_kind,
+                               int32_t *launches) {
   dresd_status s = validate_search(cix, B, k);
   if (s != DRESD_OK) return s;
   dresd_index *ix = const_cast<dresd_index *>(cix);
@@ -722,6 +745,7 @@ dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int
   if (scan_waves) *scan_waves = 0;
   if (workspace_bytes) *workspace_bytes = 0;
   if (scan_kind) *scan_kind = 0;
+  if (launches) *launches = 0;
   if (B == 0) return DRESD_OK;
   Plan pl;
   s = make_plan(ix, B, k, pl);
@@ -732,6 +756,7 @@ dresd_status dresd_search_plan(const dresd_index *cix, int32_t B, int32_t k, int
     *scan_waves = (int32_t)(pass_wgs(pl, g0, ix->T) * g0.ng * (threads_of(pl, true) / kWaveSize));
   if (workspace_bytes) *workspace_bytes = (int64_t)pl.bytes;
   if (scan_kind) *scan_kind = pl.tc ? 3 : pl.mq ? 1 : (g0.ng > 1 ? 2 : 0);
+  if (launches) *launches = (int32_t)pl.nl;
   return DRESD_OK;
 }
 
@@ -886,7 +911,9 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       sp.tau = tau_in;
       const int64_t wgs = pass_wgs(pl, gr, sp.nvisit, main_pass);
       const int threads = threads_of(pl, main_pass);
-      sp.G = (int)(pl.mq ? wgs : wgs * (threads / kWaveSize));
+      sp.G = (int)(pl.mq ? wgs
+                         : pl.tc ? wgs * (main_pass ? pl.nk_main : pl.nk_sample)
+                                 : wgs * (threads / kWaveSize));
       void *sargs[] = {&sp};
       hipEvent_t e0 = nullptr, e1 = nullptr;
       if (main_pass && prof) {

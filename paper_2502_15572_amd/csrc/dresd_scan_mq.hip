@@ -369,8 +369,14 @@ struct WaveCands {
   // slot).  The k-th best of these per-tile maxima is still the key of a
   // row, so it bounds the query's k-th best from below like the k-th best
   // of every sampled row, while a tile adds one candidate per query instead
-  // of up to 16.
+  // of up to 16.  ROOM: room for the tile's maxima (at most one key per
+  // score slot and lane group) is made once, before the slot loop, rather
+  // than in it: for scans with several tiles per wave, whose epilogue would
+  // otherwise hold a flush per slot and tile.
+  template <bool ROOM>
   __device__ __forceinline__ void take_tile_max(int64_t tile, const float (&sc)[NP]) {
+    static_assert(!ROOM || 4 * NP <= CB, "buffer holds one tile's maxima");
+    if (ROOM && cnt + 4 * NP > CB) flush();
     const int64_t row64 = tile * kTileRows + m;
     const bool row_ok = row64 < p.N;
     const uint32_t row = (uint32_t)row64;
@@ -386,7 +392,7 @@ struct WaveCands {
       const bool h = m == 0 && key != 0ull && order_value((uint32_t)(key >> 32)) >= thr[j];
       const uint64_t mk = __ballot(h);
       if (mk == 0) continue;
-      if (cnt + __popcll(mk) > CB) flush();
+      if (!ROOM && cnt + __popcll(mk) > CB) flush();
       if (h) {
         const int at = cnt + rank_in(mk);
         ck[at] = key;
@@ -786,39 +792,51 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 // first tokens into LDS with one more LDS-DMA copy at the panel's first
 // stage (a load the compiler tracked would make it drain the ring at every
 // stage), covered by the next stage's constant wait.
-template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool TMAX, bool FILT>
+template <int DT, int QTW, int CPQ, int TPW, int NK, int NQ, int S, bool TMAX, bool FILT>
 __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   using WC = WaveCands<DT, QTW, CPQ, FILT, kTcCandBuf>;
   constexpr int NP = WC::NP;
-  constexpr int PT = NW * TPW;  // key tiles per panel
-  constexpr int SB = PT + QTW;  // 1 KiB blocks per stage
-  // copies per wave per stage: TPW key blocks and one or two query blocks
+  constexpr int NW = NK * NQ;   // waves: NK key groups x NQ query groups
+  constexpr int PT = NK * TPW;  // key tiles per panel
+  constexpr int QT = NQ * QTW;  // query tiles of the launch
+  constexpr int SB = PT + QT;   // 1 KiB blocks per stage
+  // copies per wave per stage: KPW key blocks and one or more query blocks
   // (or none, when there are fewer query tiles than waves)
-  constexpr int CPW_HI = TPW + (QTW + NW - 1) / NW;
-  constexpr int CPW_LO = TPW + QTW / NW;
+  constexpr int KPW = PT / NW;
+  constexpr int CPW_HI = KPW + (QT + NW - 1) / NW;
+  constexpr int CPW_LO = KPW + QT / NW;
   constexpr int CPT = (CPW_HI + QTW - 1) / QTW;  // copies after each query tile's instructions
-  static_assert(S >= 3 && (QTW % NW == 0 || NW % QTW == 0), "shape");
+  constexpr int FTW = TPW * kTileRows > kWaveSize ? TPW * kTileRows : kWaveSize;
+  static_assert(S >= 3 && PT % NW == 0 && (QT % NW == 0 || NW % QT == 0), "shape");
+  static_assert(TPW * kTileRows <= 2 * kWaveSize, "first tokens: at most two copies per panel");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // this wave's key group and query group
+  const int kg = NQ == 1 ? wv : wv % NK, qg = NQ == 1 ? 0 : wv / NK;
   const int wg = blockIdx.x;
-  const int nwg = p.G / NW;
-  const int cpw = TPW + (QTW - wv + NW - 1) / NW;  // this wave's copies per stage
+  const int nwg = p.G / NK;
+  const int cpw = KPW + (QT - wv + NW - 1) / NW;  // this wave's copies per stage
   const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C, kTcCandBuf);
   // LDS: ring | one candidate region per wave | (filtered search) per wave
   // the next token of each score slot [4 lane groups][NP] | per wave the
-  // first tokens of its panel tiles' rows [64] (TPW * 16 used)
+  // first tokens of its panel tiles' rows [FTW] (TPW * 16 used)
   int32_t *nt_slot = FILT ? reinterpret_cast<int32_t *>(smem + (size_t)S * SB * kBlockBytes +
                                                         (size_t)NW * wreg) +
                                 wv * 4 * NP
                           : nullptr;
   int32_t *ftb = FILT ? reinterpret_cast<int32_t *>(smem + (size_t)S * SB * kBlockBytes +
                                                     (size_t)NW * wreg) +
-                            NW * 4 * NP + wv * kWaveSize
+                            NW * 4 * NP + wv * FTW
                       : nullptr;
-  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nt_slot, 0, wg * NW + wv);
+  // queries [qg * NQW, (qg + 1) * NQW) of the launch; one list per query
+  // per key group of each workgroup
+  WC wc(p, smem + (size_t)S * SB * kBlockBytes + (size_t)wv * wreg, nt_slot, qg * WC::NQW,
+        wg * NK + kg);
   wc.init();
+  // a query group wholly past the batch only copies its share of the ring
+  const bool active = NQ == 1 || qg * WC::NQW < p.B;
 
   // This workgroup's key tiles: visited tiles [v0, v1).
   const int64_t v0 = wave_uniform(p.nvisit * wg / nwg);
@@ -832,20 +850,20 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
     const unsigned char *qbase = static_cast<const unsigned char *>(p.qop);
     const uint32_t voff = (uint32_t)lane * 16u;
     const uint32_t ring = (uint32_t)(uintptr_t)smem;
-    // Copy j of stage (panel pn, column c) into ring slot `slot`: j < TPW is
-    // this wave's key tile j (clamped to the last tile), the others its
-    // query tiles wv, wv + NW, ...
+    // Copy j of stage (panel pn, column c) into ring slot `slot`: j < KPW is
+    // panel tile wv * KPW + j (clamped to the last tile), the others query
+    // tiles wv, wv + NW, ...
     auto copy = [&](int j, int64_t pn, int c, int slot) {
       const uint32_t sbase = ring + (uint32_t)(slot * SB) * (uint32_t)kBlockBytes;
-      if (j < TPW) {
-        int64_t t = pn * PT + wv * TPW + j;
+      if (j < KPW) {
+        int64_t t = pn * PT + wv * KPW + j;
         t = t < ntile ? t : ntile - 1;
         const int64_t src = wave_uniform((int64_t)(uintptr_t)(dbase + t * tstep) +
                                          (int64_t)c * kBlockBytes);
         copy_block_to_lds<true>((const void *)(uintptr_t)src, voff,
-                                sbase + (uint32_t)(wv * TPW + j) * (uint32_t)kBlockBytes);
+                                sbase + (uint32_t)(wv * KPW + j) * (uint32_t)kBlockBytes);
       } else {
-        const int qt = wv + NW * (j - TPW);
+        const int qt = wv + NW * (j - KPW);
         const int64_t src =
             wave_uniform((int64_t)(uintptr_t)qbase + ((int64_t)qt * KB + c) * kBlockBytes);
         copy_block_to_lds<false>((const void *)(uintptr_t)src, voff,
@@ -888,52 +906,65 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         if (CPW_HI == CPW_LO || cpw == CPW_HI) wait_vmcnt<CPW_HI * (S - 2)>();
         else wait_vmcnt<CPW_LO * (S - 2)>();
         __syncthreads();
-        if (FILT && c == 0) {
-          // first tokens of this wave's tiles of the panel (lane l: tile
-          // l / 16, row l % 16; clamped to the last tile; lanes past TPW
-          // tiles copy unused values), read after the panel's last column.
-          // Issued before this stage's copies, it is complete once the next
-          // stage's wait leaves at most CPW copies in flight.
-          int64_t t = pn * PT + wv * TPW + (lane >> 4);
-          t = t < ntile ? t : ntile - 1;
-          copy1_to_lds(p.ftok + (v0 + t) * p.stride * kTileRows + (lane & 15),
-                       (uint32_t)(uintptr_t)ftb);
-        }
-        const u4 *sl = reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes) + lane;
-        u4 kv[TPW], qv[QTW];
+        if (FILT && c == 0 && active) {
+          // first tokens of this wave's tiles of the panel (lane l of copy
+          // h: tile 4 h + l / 16, row l % 16; clamped to the last tile;
+          // lanes past TPW tiles copy unused values), read after the
+          // panel's last column.  Issued before this stage's copies, they
+          // are complete once the next stage's wait leaves at most CPW
+          // copies in flight.
 #pragma unroll
-        for (int i = 0; i < TPW; ++i) kv[i] = sl[(wv * TPW + i) * 64];
-#pragma unroll
-        for (int t = 0; t < QTW; ++t) qv[t] = sl[(PT + t) * 64];
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int t = 0; t < QTW; ++t) {
-#pragma unroll
-          for (int i = 0; i < TPW; ++i) acc[i][t] = MfmaMQ<DT>::run(qv[t], kv[i], acc[i][t]);
-          if (t * CPT < CPW_HI) {
-            // the stage S - 1 ahead, CPT copies per query tile
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int j = t * CPT; j < (t + 1) * CPT && j < CPW_HI; ++j)
-              if (j < cpw) copy(j, npn, nc, next_slot);
-            __builtin_amdgcn_sched_barrier(0);
+          for (int h = 0; h < (TPW > 4 ? 2 : 1); ++h) {
+            int64_t t = pn * PT + kg * TPW + 4 * h + (lane >> 4);
+            t = t < ntile ? t : ntile - 1;
+            copy1_to_lds(p.ftok + (v0 + t) * p.stride * kTileRows + (lane & 15),
+                         (uint32_t)(uintptr_t)(ftb + h * kWaveSize));
           }
+        }
+        if (active) {
+          const u4 *sl =
+              reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes) + lane;
+          u4 kv[TPW], qv[QTW];
+#pragma unroll
+          for (int i = 0; i < TPW; ++i) kv[i] = sl[(kg * TPW + i) * 64];
+#pragma unroll
+          for (int t = 0; t < QTW; ++t) qv[t] = sl[(PT + qg * QTW + t) * 64];
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int t = 0; t < QTW; ++t) {
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) acc[i][t] = MfmaMQ<DT>::run(qv[t], kv[i], acc[i][t]);
+            if (t * CPT < CPW_HI) {
+              // the stage S - 1 ahead, CPT copies per query tile
+              __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+              for (int j = t * CPT; j < (t + 1) * CPT && j < CPW_HI; ++j)
+                if (j < cpw) copy(j, npn, nc, next_slot);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < CPW_HI; ++j)
+            if (j < cpw) copy(j, npn, nc, next_slot);
         }
         advance();
         next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
         cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
       }
-      int ft[TPW];  // filtered search: this lane's row's first token per tile
+      if (active) {
+        int ft[TPW];  // filtered search: this lane's row's first token per tile
 #pragma unroll
-      for (int i = 0; i < TPW; ++i) ft[i] = FILT ? ftb[i * kTileRows + (lane & 15)] : 0;
+        for (int i = 0; i < TPW; ++i) ft[i] = FILT ? ftb[i * kTileRows + (lane & 15)] : 0;
 #pragma unroll
-      for (int i = 0; i < TPW; ++i) {
-        const int64_t vt = pn * PT + wv * TPW + i;
-        if (vt < ntile) {
-          float sc[NP];
-          wc.scores_of(acc[i], ft[i], sc);
-          if (TMAX) wc.take_tile_max((v0 + vt) * p.stride, sc);
-          else if (wc.any_hit(sc)) wc.take((v0 + vt) * p.stride, sc);
+        for (int i = 0; i < TPW; ++i) {
+          const int64_t vt = pn * PT + kg * TPW + i;
+          if (vt < ntile) {
+            float sc[NP];
+            wc.scores_of(acc[i], ft[i], sc);
+            if (TMAX) wc.template take_tile_max<(TPW >= 4)>((v0 + vt) * p.stride, sc);
+            else if (wc.any_hit(sc)) wc.take((v0 + vt) * p.stride, sc);
+          }
         }
       }
     }
@@ -942,15 +973,17 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   wc.publish();
 }
 
-template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool FILT>
-__global__ void __launch_bounds__(NW * kWaveSize, 8 / NW) dresd_scantc_main(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, false, FILT>(p);
+template <int DT, int QTW, int CPQ, int TPW, int NK, int NQ, int S, bool FILT>
+__global__ void __launch_bounds__(NK * NQ * kWaveSize, 8 / (NK * NQ))
+    dresd_scantc_main(ScanParams p) {
+  scan_tc_body<DT, QTW, CPQ, TPW, NK, NQ, S, false, FILT>(p);
 }
 
 // Sampled pass: per-tile maxima as candidates.
-template <int DT, int QTW, int CPQ, int TPW, int NW, int S, bool FILT>
-__global__ void __launch_bounds__(NW * kWaveSize, 8 / NW) dresd_scantc_sample(ScanParams p) {
-  scan_tc_body<DT, QTW, CPQ, TPW, NW, S, true, FILT>(p);
+template <int DT, int QTW, int CPQ, int TPW, int NK, int NQ, int S, bool FILT>
+__global__ void __launch_bounds__(NK * NQ * kWaveSize, 8 / (NK * NQ))
+    dresd_scantc_sample(ScanParams p) {
+  scan_tc_body<DT, QTW, CPQ, TPW, NK, NQ, S, true, FILT>(p);
 }
 
 // One thread per 16-byte chunk (t, kb, lane) of the query operands.
@@ -984,35 +1017,40 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
   DRESD_MQ_CASE(DT, CPQ, 2, 16, 6) DRESD_MQ_CASE(DT, CPQ, 4, 4, 4)                \
   DRESD_MQ_CASE(DT, CPQ, 4, 8, 6)
 
-// Tiled contraction: main passes with 4 key tiles per wave, 8 waves (3
-// stages: one query read per 32 key tiles) or 4 waves (5 stages, or 3 where
-// large lists leave less LDS); sampled passes with 1 key tile per wave and
-// 4 waves (8 or 4 stages).
-#define DRESD_TC_MAIN(DT, CPQ, QTW, TPW, NW, S)                                          \
-  if (main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S)                \
-    return filtered ? (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, NW, S, true>    \
-                    : (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, NW, S, false>;
-#define DRESD_TC_SAMPLE(DT, CPQ, QTW, TPW, NW, S)                                         \
-  if (!main_pass && qtw == QTW && tpw == TPW && nw == NW && stages == S)                \
-    return filtered ? (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, NW, S, true>  \
-                    : (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, NW, S, false>;
-#define DRESD_TC_ALL(DT, CPQ, QTW)                                                            \
-  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 8, 3)                                                        \
-  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 5) DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 3)                   \
-  DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 8) DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 4)
+// Tiled contraction, one query group (NQ = 1): main passes with 4 key
+// tiles per wave, 8 waves (3 stages: one query read per 32 key tiles) or 4
+// waves (5 stages, or 3 where large lists leave less LDS); sampled passes
+// with 1 key tile per wave and 4 waves (8 or 4 stages).  Larger batches: 2
+// or 4 query groups of waves over 16-tile panels (8 waves), sampled passes
+// over 8-tile panels (4 stages).
+#define DRESD_TC_MAIN(DT, CPQ, QTW, TPW, NK, NQ, S)                                        \
+  if (main_pass && qtw == QTW && tpw == TPW && nk == NK && nq == NQ && stages == S)      \
+    return filtered ? (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, NK, NQ, S, true>  \
+                    : (ScanKernel)dresd_scantc_main<DT, QTW, CPQ, TPW, NK, NQ, S, false>;
+#define DRESD_TC_SAMPLE(DT, CPQ, QTW, TPW, NK, NQ, S)                                       \
+  if (!main_pass && qtw == QTW && tpw == TPW && nk == NK && nq == NQ && stages == S)      \
+    return filtered ? (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, NK, NQ, S, true>  \
+                    : (ScanKernel)dresd_scantc_sample<DT, QTW, CPQ, TPW, NK, NQ, S, false>;
+#define DRESD_TC_ONE(DT, CPQ, QTW)                                                      \
+  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 8, 1, 3)                                               \
+  DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 1, 5) DRESD_TC_MAIN(DT, CPQ, QTW, 4, 4, 1, 3)       \
+  DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 1, 8) DRESD_TC_SAMPLE(DT, CPQ, QTW, 1, 4, 1, 4)
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
-ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nw, int stages, bool main_pass,
+ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nk, int nq, int stages, bool main_pass,
                               bool filtered) {
-  DRESD_TC_ALL(kF16, 1, 4)
+  DRESD_TC_ONE(kF16, 1, 4)
+  DRESD_TC_MAIN(kF16, 1, 4, 4, 4, 2, 3) DRESD_TC_SAMPLE(kF16, 1, 4, 2, 4, 2, 4)
+  DRESD_TC_MAIN(kF16, 1, 4, 8, 2, 4, 3) DRESD_TC_SAMPLE(kF16, 1, 4, 4, 2, 4, 4)
   return nullptr;
 }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
-ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nw, int stages, bool main_pass,
+ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nk, int nq, int stages, bool main_pass,
                                bool filtered) {
-  DRESD_TC_ALL(kBF16, 2, 4)
-  DRESD_TC_ALL(kBF16, 2, 8)
+  DRESD_TC_ONE(kBF16, 2, 4)
+  DRESD_TC_ONE(kBF16, 2, 8)
+  DRESD_TC_MAIN(kBF16, 2, 8, 4, 4, 2, 3) DRESD_TC_SAMPLE(kBF16, 2, 8, 2, 4, 2, 4)
   return nullptr;
 }
 #endif

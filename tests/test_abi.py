@@ -36,7 +36,7 @@ def test_null_arguments_are_rejected_before_any_device_work():
     assert lib.dresd_index_info(None, None, None, None, None) == _lib.EINVAL
     assert lib.dresd_profile_enable(None, 1) == _lib.EINVAL
     assert lib.dresd_profile_read(None, None, None, None) == _lib.EINVAL
-    assert lib.dresd_search_plan(None, 1, 1, None, None, None, None) == _lib.EINVAL
+    assert lib.dresd_search_plan(None, 1, 1, None, None, None, None, None) == _lib.EINVAL
     lib.dresd_index_destroy(None)  # ignored
 
 

@@ -171,6 +171,8 @@ FILTERED_TILED = [
     ("bf16", 20000, 4096, 64, 10),   # 8 query tiles, sampled pass at stride 16
     ("f16", 30000, 2048, 40, 16),    # f16, 4 query tiles (8 waves, per-wave copy counts)
     ("bf16", 3001, 1100, 33, 12),    # ragged columns, no sampled pass
+    ("f16", 20011, 1024, 200, 12),   # four query groups (8 key tiles per wave)
+    ("bf16", 5003, 4096, 100, 10),   # two query groups
 ]
 
 

@@ -230,6 +230,38 @@ def test_tiled_contraction_shapes(gpu_lib, dt, N, d, B, k):
         % (rep["max_abs_vs_exact"], rep["max_abs_vs_model"], rep["operand"]))
 
 
+TC_GROUPS = [
+    # (dtype, N, d, B, k, launches): batches past one query group of waves
+    ("f16", 20011, 1024, 130, 16, 1),   # four query groups, the last past the batch
+    ("f16", 9001, 1024, 256, 32, 1),    # four query groups, all full
+    ("f16", 12007, 1024, 100, 10, 1),   # two query groups
+    ("f16", 6007, 2048, 256, 100, 1),   # four query groups at larger lists
+    ("f16", 100, 1024, 200, 50, 1),     # 7 key tiles, less than a 16-tile panel
+    ("bf16", 9001, 1024, 40, 16, 1),    # 1,024 dims, one group of 8 query tiles
+    ("bf16", 7001, 1024, 128, 8, 1),    # two query groups of 8 tiles
+    ("bf16", 5003, 4096, 100, 10, 1),   # two query groups
+    ("bf16", 3001, 4096, 256, 10, 2),   # two launches of 128 queries
+    ("f16", 4001, 1024, 256, 1000, 4),  # lists too large for query groups: one group per launch
+]
+
+
+@pytest.mark.parametrize("dt,N,d,B,k,nl", TC_GROUPS,
+                         ids=["%s-N%d-d%d-B%d-k%d" % e[:5] for e in TC_GROUPS])
+def test_tiled_contraction_query_groups(gpu_lib, dt, N, d, B, k, nl):
+    from paper_2502_15572_amd import Index
+    say("tiled groups", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N * 7 + d + B * 5 + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 2), generator=gen, dtype=torch.int32)
+    ix = Index(x.to(DEV), cont.to(DEV))
+    assert ix.plan(B, k)["launches"] == nl
+    ix.close()
+    run_case(gpu_lib, x, cont, q, k, dt, kind="tiled")
+
+
 def _random_tiled_cases(n, seed):
     """Seeded random shapes for the tiled contraction: dims past 1,024 (ragged
     column counts included), 9-140 queries (one to three launches), k from 1
