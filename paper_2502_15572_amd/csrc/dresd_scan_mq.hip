@@ -809,6 +809,7 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   constexpr int FTW = TPW * kTileRows > kWaveSize ? TPW * kTileRows : kWaveSize;
   static_assert(S >= 3 && PT % NW == 0 && (QT % NW == 0 || NW % QT == 0), "shape");
   static_assert(TPW * kTileRows <= 2 * kWaveSize, "first tokens: at most two copies per panel");
+  static_assert(KPW <= 4, "32-bit key copy offsets");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int lane = threadIdx.x & 63;
@@ -817,7 +818,8 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   const int kg = NQ == 1 ? wv : wv % NK, qg = NQ == 1 ? 0 : wv / NK;
   const int wg = blockIdx.x;
   const int nwg = p.G / NK;
-  const int cpw = KPW + (QT - wv + NW - 1) / NW;  // this wave's copies per stage
+  // this wave's copies per stage
+  const int cpw = QT % NW == 0 ? CPW_HI : KPW + (QT - wv + NW - 1) / NW;
   const size_t wreg = scan_mq_wave_bytes(WC::NQW, p.C, kTcCandBuf);
   // LDS: ring | one candidate region per wave | (filtered search) per wave
   // the next token of each score slot [4 lane groups][NP] | per wave the
@@ -841,44 +843,57 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   // This workgroup's key tiles: visited tiles [v0, v1).
   const int64_t v0 = wave_uniform(p.nvisit * wg / nwg);
   const int64_t v1 = wave_uniform(p.nvisit * (wg + 1) / nwg);
-  const int64_t ntile = v1 - v0;
+  const int ntile = (int)(v1 - v0);
   if (ntile > 0) {
     const int KB = p.KB;
-    const int64_t npanel = (ntile + PT - 1) / PT;
+    const int npanel = (ntile + PT - 1) / PT;
     const int64_t tstep = p.stride * KB * kBlockBytes;  // bytes between visited tiles
     const unsigned char *dbase = static_cast<const unsigned char *>(p.data) + v0 * tstep;
     const unsigned char *qbase = static_cast<const unsigned char *>(p.qop);
     const uint32_t voff = (uint32_t)lane * 16u;
     const uint32_t ring = (uint32_t)(uintptr_t)smem;
-    // Copy j of stage (panel pn, column c) into ring slot `slot`: j < KPW is
-    // panel tile wv * KPW + j (clamped to the last tile), the others query
-    // tiles wv, wv + NW, ...
-    auto copy = [&](int j, int64_t pn, int c, int slot) {
+    // The copy stream runs S - 1 stages ahead of the arithmetic: stage
+    // (panel npn, column nc).  Copy j < KPW of a stage is panel tile
+    // wv * KPW + j (clamped to the last tile), the others query tiles wv,
+    // wv + NW, ...  The key tiles' base address and clamp change once per
+    // panel; per stage only the column moves.  Offsets from the base fit 32
+    // bits: at most KPW - 1 <= 3 tile steps of at most 64 tiles (the
+    // sparsest sampled pass) of at most 512 blocks, plus a column.
+    int npn = 0, nc = 0;
+    const unsigned char *kbase = dbase;
+    int kjmax = 0;  // key copies past this one read the last tile
+    auto set_panel = [&]() {
+      const int t0 = npn * PT + wv * KPW;
+      const int t0c = t0 < ntile ? t0 : ntile - 1;
+      kjmax = ntile - 1 - t0c;
+      kbase = dbase + (int64_t)t0c * tstep;
+    };
+    set_panel();
+    const uint32_t tstep32 = (uint32_t)tstep;
+    auto copy = [&](int j, int slot) {
       const uint32_t sbase = ring + (uint32_t)(slot * SB) * (uint32_t)kBlockBytes;
       if (j < KPW) {
-        int64_t t = pn * PT + wv * KPW + j;
-        t = t < ntile ? t : ntile - 1;
-        const int64_t src = wave_uniform((int64_t)(uintptr_t)(dbase + t * tstep) +
-                                         (int64_t)c * kBlockBytes);
+        const uint32_t jj = (uint32_t)(j < kjmax ? j : kjmax);
+        const int64_t src = wave_uniform((int64_t)(uintptr_t)kbase +
+                                         (int64_t)(jj * tstep32 + (uint32_t)nc * kBlockBytes));
         copy_block_to_lds<true>((const void *)(uintptr_t)src, voff,
                                 sbase + (uint32_t)(wv * KPW + j) * (uint32_t)kBlockBytes);
       } else {
         const int qt = wv + NW * (j - KPW);
-        const int64_t src =
-            wave_uniform((int64_t)(uintptr_t)qbase + ((int64_t)qt * KB + c) * kBlockBytes);
+        const int64_t src = wave_uniform((int64_t)(uintptr_t)qbase +
+                                         (int64_t)((uint32_t)(qt * KB + nc) * kBlockBytes));
         copy_block_to_lds<false>((const void *)(uintptr_t)src, voff,
                                  sbase + (uint32_t)(PT + qt) * (uint32_t)kBlockBytes);
       }
     };
     // Stages in order: (panel, column) with the column fastest; past the
     // last stage the copies repeat it.
-    int64_t npn = 0;
-    int nc = 0;
     auto advance = [&]() {
       if (npn < npanel - 1 || nc < KB - 1) {
         if (++nc == KB) {
           nc = 0;
           ++npn;
+          set_panel();
         }
       }
     };
@@ -886,14 +901,14 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
     for (int st = 0; st < S - 1; ++st) {
 #pragma unroll
       for (int j = 0; j < CPW_HI; ++j)
-        if (j < cpw) copy(j, npn, nc, st);
+        if (j < cpw) copy(j, st);
       advance();
     }
     int next_slot = S - 1;  // ring slot of the next stage to copy
     int cur_slot = 0;       // ring slot of the stage being consumed
     f4 acc[TPW][QTW];
 #pragma unroll 1
-    for (int64_t pn = 0; pn < npanel; ++pn) {
+    for (int pn = 0; pn < npanel; ++pn) {
 #pragma unroll
       for (int i = 0; i < TPW; ++i)
 #pragma unroll
@@ -939,14 +954,14 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
               __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
               for (int j = t * CPT; j < (t + 1) * CPT && j < CPW_HI; ++j)
-                if (j < cpw) copy(j, npn, nc, next_slot);
+                if (j < cpw) copy(j, next_slot);
               __builtin_amdgcn_sched_barrier(0);
             }
           }
         } else {
 #pragma unroll
           for (int j = 0; j < CPW_HI; ++j)
-            if (j < cpw) copy(j, npn, nc, next_slot);
+            if (j < cpw) copy(j, next_slot);
         }
         advance();
         next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
@@ -958,7 +973,7 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         for (int i = 0; i < TPW; ++i) ft[i] = FILT ? ftb[i * kTileRows + (lane & 15)] : 0;
 #pragma unroll
         for (int i = 0; i < TPW; ++i) {
-          const int64_t vt = pn * PT + kg * TPW + i;
+          const int vt = pn * PT + kg * TPW + i;
           if (vt < ntile) {
             float sc[NP];
             wc.scores_of(acc[i], ft[i], sc);
