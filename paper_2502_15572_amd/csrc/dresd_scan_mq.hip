@@ -538,13 +538,13 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   // This workgroup's key tiles: visited tiles [v0, v1), KBT blocks each.
   const int64_t v0 = wave_uniform(p.nvisit * wg / G);
   const int64_t v1 = wave_uniform(p.nvisit * (wg + 1) / G);
-  const int64_t ntile = v1 - v0;
+  const int ntile = (int)(v1 - v0);
 
   // The slow path of visited tile vt with hits.
-  auto take = [&](int64_t vt, const float (&sc)[NP]) { wc.take((v0 + vt) * p.stride, sc); };
+  auto take = [&](int vt, const float (&sc)[NP]) { wc.take((v0 + vt) * p.stride, sc); };
 
   if (ntile > 0) {
-    const int64_t NB = ntile * KBT;
+    const int64_t NB = (int64_t)ntile * KBT;
     const int64_t tstep = p.stride * KBT * kBlockBytes;  // bytes between visited tiles
     const unsigned char *dbase = static_cast<const unsigned char *>(p.data) + v0 * tstep;
     const uint32_t voff0 = (uint32_t)lane * 16u, voff1 = voff0 + kBlockBytes;
@@ -580,42 +580,65 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     };
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) issue(st, st);
-    int64_t next_st = S - 1;  // next stage to copy
+    // The stream loop's copies: stage next_st, whose source address moves
+    // by a fixed step per stage (and per key tile when a tile spans several
+    // stages) instead of being recomputed; stages past last_ok repeat the
+    // last two blocks.
+    const int last_ok = jl >= wv * 2 ? (int)((jl - wv * 2) / SB) : -1;
+    int next_st = S - 1;  // next stage to copy
+    int next_c = (S - 1) % SPT;  // its stage within its key tile
+    const unsigned char *next_src = src_of(S - 1);
     int next_slot = S - 1;    // its ring slot
     int cur_slot = 0;         // ring slot of the stage being consumed
+    auto issue_next = [&]() {
+      if (filt || next_st > last_ok) {
+        issue(next_st, next_slot);
+      } else {
+        copy2_to_lds(next_src, voff0, voff1,
+                     ring + (uint32_t)(next_slot * SB + wv * 2) * (uint32_t)kBlockBytes);
+      }
+      ++next_st;
+      if constexpr (SPT == 1) {
+        next_src += stage_step;
+      } else if (++next_c == SPT) {
+        next_c = 0;
+        next_src += tstep - (int64_t)(SPT - 1) * SB * kBlockBytes;
+      } else {
+        next_src += SB * kBlockBytes;
+      }
+      next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
+    };
     // Stage bookkeeping at the start of a key tile's c-th stage: this wave's
     // copies of it have landed; after the barrier so have every wave's, and
     // the slot consumed last is free for the copy S - 1 stages ahead.
-    auto stage_start = [&](int64_t vt) {
+    auto stage_start = [&](int vt) {
       if (TPS == 1 || (vt & (TPS - 1)) == 0) {
         if (filt) wait_vmcnt<WAIT + (S - 2)>();  // one more copy per stage
         else wait_vmcnt<WAIT>();
         __syncthreads();
-        issue(next_st, next_slot);
-        ++next_st;
-        next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
+        issue_next();
       }
     };
     // First token of this lane's row of tile vt (filtered search), read
     // from the tile's ring slot before a later stage may overwrite it; and
     // the ring slot advance at a stage end.
-    auto stage_end = [&](int64_t vt, int &ftok_row) {
+    auto stage_end = [&](int vt, int &ftok_row) {
       if (filt) ftok_row = fring[cur_slot * 64 + (TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * 16 + m];
       if (TPS == 1 || (vt & (TPS - 1)) == TPS - 1) cur_slot = cur_slot == S - 1 ? 0 : cur_slot + 1;
     };
-    auto stage_blocks = [&](int64_t vt) {
+    auto stage_blocks = [&](int vt) {
       return reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes +
                                           (size_t)((TPS > 1 ? (int)(vt & (TPS - 1)) : 0) * KBT) *
                                               kBlockBytes) +
              lane;
     };
-    const int64_t ntile_pad = (ntile + TPS - 1) / TPS * TPS;
+    const int ntile_pad = (ntile + TPS - 1) / TPS * TPS;
     if constexpr (!kDefer) {
       // Many matrix instructions per key tile: the tile's threshold test
       // follows its own matrix instructions.
       f4 acc[QTW];
 #pragma unroll 1
-      for (int64_t vt = 0; vt < ntile_pad; ++vt) {
+      for (int vt = 0; vt < ntile_pad; ++vt) {
         int fr = 0;
 #pragma unroll
         for (int c = 0; c < SPT; ++c) {
@@ -666,8 +689,8 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
       // One key tile: its matrix instructions into `acc`, the test of the
       // previous tile (complete in `prev`) split over its pairs of blocks,
       // then that tile's slow path if it has hits.
-      auto step = [&](int64_t vt, f4 (&acc)[QTW], const f4 (&prev)[QTW], int &fcur, int fprev) {
-        const int64_t pv = vt - 1;
+      auto step = [&](int vt, f4 (&acc)[QTW], const f4 (&prev)[QTW], int &fcur, int fprev) {
+        const int pv = vt - 1;
         float psc[NP];
         uint64_t hits = 0;
 #pragma unroll
@@ -720,9 +743,9 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
         }
         if (hits) take(pv, psc);
       };
-      const int64_t nsteps = (ntile_pad + 1) / 2 * 2;  // even: the last tile is in accB
+      const int nsteps = (ntile_pad + 1) / 2 * 2;  // even: the last tile is in accB
 #pragma unroll 1
-      for (int64_t vt = 0; vt < nsteps; vt += 2) {
+      for (int vt = 0; vt < nsteps; vt += 2) {
         step(vt, accA, accB, fA, fB);
         step(vt + 1, accB, accA, fB, fA);
       }
