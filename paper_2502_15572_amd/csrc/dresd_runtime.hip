@@ -278,9 +278,9 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
     // query group: 8 waves over panels of 32 key tiles (one query read per 32
     // tiles) where that kernel exists and fits, else 4 waves over 16 tiles
     static const std::vector<TcShape> main1 = {{4, 8, 3}, {4, 4, 5}, {4, 4, 3}},
-                                      samp1 = {{1, 4, 8}, {1, 4, 4}}, main2 = {{4, 4, 3}},
-                                      samp2 = {{2, 4, 4}}, main4 = {{8, 2, 3}},
-                                      samp4 = {{4, 2, 4}};
+                                      samp1 = {{1, 4, 8}, {1, 4, 4}},
+                                      main2 = {{4, 4, 4}, {4, 4, 3}}, samp2 = {{2, 4, 4}},
+                                      main4 = {{8, 2, 4}, {8, 2, 3}}, samp4 = {{4, 2, 4}};
     for (; nq >= 1 && !pl.tc; nq >>= 1) {
       const auto &ms = nq == 4 ? main4 : nq == 2 ? main2 : main1;
       const auto &ss = nq == 4 ? samp4 : nq == 2 ? samp2 : samp1;

@@ -828,7 +828,6 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   constexpr int KPW = PT / NW;
   constexpr int CPW_HI = KPW + (QT + NW - 1) / NW;
   constexpr int CPW_LO = KPW + QT / NW;
-  constexpr int CPT = (CPW_HI + QTW - 1) / QTW;  // copies after each query tile's instructions
   constexpr int FTW = TPW * kTileRows > kWaveSize ? TPW * kTileRows : kWaveSize;
   static_assert(S >= 3 && PT % NW == 0 && (QT % NW == 0 || NW % QT == 0), "shape");
   static_assert(TPW * kTileRows <= 2 * kWaveSize, "first tokens: at most two copies per panel");
@@ -930,6 +929,47 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
     int next_slot = S - 1;  // ring slot of the next stage to copy
     int cur_slot = 0;       // ring slot of the stage being consumed
     f4 acc[TPW][QTW];
+    // Operand prefetch (query-group kernels with four or more stages): a
+    // stage's barrier also covers the next stage's copies, and each operand
+    // register is refilled with the next stage's block once this stage's
+    // last instruction reading it has issued, so that one stage's LDS reads
+    // overlap the matrix instructions of the stage before.  Without it all
+    // waves read their operands from LDS at once after the barrier, then
+    // run their instructions.
+    constexpr bool PF = NQ > 1 && S >= 4;
+    constexpr int NO = TPW > QTW ? TPW : QTW;    // outer blocks
+    constexpr int CPO = (CPW_HI + NO - 1) / NO;  // copies after each outer block's instructions
+    u4 kv[TPW], qv[QTW];
+    auto slot_ops = [&](int slot) {
+      return reinterpret_cast<const u4 *>(smem + (size_t)slot * SB * kBlockBytes) + lane;
+    };
+    // The operand blocks of the smaller side are read first and the
+    // instructions run over the larger side outermost, so that they can
+    // start once one block of the larger side has arrived.
+    auto read_inner = [&](const u4 *sl) {
+      if constexpr (TPW > QTW) {
+#pragma unroll
+        for (int t = 0; t < QTW; ++t) qv[t] = sl[(PT + qg * QTW + t) * 64];
+      } else {
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) kv[i] = sl[(kg * TPW + i) * 64];
+      }
+    };
+    auto read_outer = [&](const u4 *sl, int o) {
+      if constexpr (TPW > QTW) kv[o] = sl[(kg * TPW + o) * 64];
+      else qv[o] = sl[(PT + qg * QTW + o) * 64];
+    };
+    if constexpr (PF) {
+      // stage 0 has landed and is visible; its operands into registers
+      if (CPW_HI == CPW_LO || cpw == CPW_HI) wait_vmcnt<CPW_HI * (S - 2)>();
+      else wait_vmcnt<CPW_LO * (S - 2)>();
+      __syncthreads();
+      if (active) {
+        read_inner(slot_ops(0));
+#pragma unroll
+        for (int o = 0; o < NO; ++o) read_outer(slot_ops(0), o);
+      }
+    }
 #pragma unroll 1
     for (int pn = 0; pn < npanel; ++pn) {
 #pragma unroll
@@ -938,11 +978,13 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
         for (int t = 0; t < QTW; ++t) acc[i][t] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 1
       for (int c = 0; c < KB; ++c) {
-        // this wave's copies of the stage have landed (those of the S - 2
-        // later stages may still be in flight); after the barrier so have
-        // every wave's, and the slot consumed last is free again
-        if (CPW_HI == CPW_LO || cpw == CPW_HI) wait_vmcnt<CPW_HI * (S - 2)>();
-        else wait_vmcnt<CPW_LO * (S - 2)>();
+        // this wave's copies of the stage (and with prefetch of the next
+        // one) have landed, those of the later stages may still be in
+        // flight; after the barrier so have every wave's, and the slot
+        // consumed last is free again
+        constexpr int WST = PF ? S - 3 : S - 2;
+        if (CPW_HI == CPW_LO || cpw == CPW_HI) wait_vmcnt<CPW_HI * WST>();
+        else wait_vmcnt<CPW_LO * WST>();
         __syncthreads();
         if (FILT && c == 0 && active) {
           // first tokens of this wave's tiles of the panel (lane l of copy
@@ -960,27 +1002,35 @@ __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
           }
         }
         if (active) {
-          const u4 *sl =
-              reinterpret_cast<const u4 *>(smem + (size_t)cur_slot * SB * kBlockBytes) + lane;
-          u4 kv[TPW], qv[QTW];
+          // the next stage's operands (prefetch)
+          const u4 *sn = slot_ops(cur_slot == S - 1 ? 0 : cur_slot + 1);
+          if constexpr (!PF) {
+            const u4 *sl = slot_ops(cur_slot);
+            read_inner(sl);
 #pragma unroll
-          for (int i = 0; i < TPW; ++i) kv[i] = sl[(kg * TPW + i) * 64];
-#pragma unroll
-          for (int t = 0; t < QTW; ++t) qv[t] = sl[(PT + qg * QTW + t) * 64];
+            for (int o = 0; o < NO; ++o) read_outer(sl, o);
+          }
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int t = 0; t < QTW; ++t) {
+          for (int o = 0; o < NO; ++o) {
+            if constexpr (TPW > QTW) {
 #pragma unroll
-            for (int i = 0; i < TPW; ++i) acc[i][t] = MfmaMQ<DT>::run(qv[t], kv[i], acc[i][t]);
-            if (t * CPT < CPW_HI) {
-              // the stage S - 1 ahead, CPT copies per query tile
+              for (int t = 0; t < QTW; ++t) acc[o][t] = MfmaMQ<DT>::run(qv[t], kv[o], acc[o][t]);
+            } else {
+#pragma unroll
+              for (int i = 0; i < TPW; ++i) acc[i][o] = MfmaMQ<DT>::run(qv[o], kv[i], acc[i][o]);
+            }
+            if constexpr (PF) read_outer(sn, o);
+            if (o * CPO < CPW_HI) {
+              // the stage S - 1 ahead, CPO copies per outer block
               __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-              for (int j = t * CPT; j < (t + 1) * CPT && j < CPW_HI; ++j)
+              for (int j = o * CPO; j < (o + 1) * CPO && j < CPW_HI; ++j)
                 if (j < cpw) copy(j, next_slot);
               __builtin_amdgcn_sched_barrier(0);
             }
           }
+          if constexpr (PF) read_inner(sn);
         } else {
 #pragma unroll
           for (int j = 0; j < CPW_HI; ++j)
@@ -1078,8 +1128,10 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
 ScanKernel scan_tc_kernel_f16(int qtw, int tpw, int nk, int nq, int stages, bool main_pass,
                               bool filtered) {
   DRESD_TC_ONE(kF16, 1, 4)
-  DRESD_TC_MAIN(kF16, 1, 4, 4, 4, 2, 3) DRESD_TC_SAMPLE(kF16, 1, 4, 2, 4, 2, 4)
-  DRESD_TC_MAIN(kF16, 1, 4, 8, 2, 4, 3) DRESD_TC_SAMPLE(kF16, 1, 4, 4, 2, 4, 4)
+  DRESD_TC_MAIN(kF16, 1, 4, 4, 4, 2, 4) DRESD_TC_MAIN(kF16, 1, 4, 4, 4, 2, 3)
+  DRESD_TC_SAMPLE(kF16, 1, 4, 2, 4, 2, 4)
+  DRESD_TC_MAIN(kF16, 1, 4, 8, 2, 4, 4) DRESD_TC_MAIN(kF16, 1, 4, 8, 2, 4, 3)
+  DRESD_TC_SAMPLE(kF16, 1, 4, 4, 2, 4, 4)
   return nullptr;
 }
 #endif
@@ -1088,7 +1140,8 @@ ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nk, int nq, int stages, boo
                                bool filtered) {
   DRESD_TC_ONE(kBF16, 2, 4)
   DRESD_TC_ONE(kBF16, 2, 8)
-  DRESD_TC_MAIN(kBF16, 2, 8, 4, 4, 2, 3) DRESD_TC_SAMPLE(kBF16, 2, 8, 2, 4, 2, 4)
+  DRESD_TC_MAIN(kBF16, 2, 8, 4, 4, 2, 4) DRESD_TC_MAIN(kBF16, 2, 8, 4, 4, 2, 3)
+  DRESD_TC_SAMPLE(kBF16, 2, 8, 2, 4, 2, 4)
   return nullptr;
 }
 #endif
