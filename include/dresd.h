@@ -158,7 +158,9 @@ dresd_status dresd_search_filtered(dresd_index *ix, const float *queries,
  * Allocation-free search, for callers that cannot allocate device memory:
  * code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc.  The same search as dresd_search (same kernels, bitwise the same
- * outputs), with its workspace in a fixed library scratch of
+ * outputs; a batch of 1,024-dim keys whose tiled-contraction lists would
+ * not fit the scratch runs the shared-key scan instead), with its workspace
+ * in a fixed library scratch of
  * DRESD_SCRATCH_BYTES that every device the library runs on holds until the
  * process ends, instead of the index's growable workspace.  It allocates no
  * device or host memory and never synchronises; the caller still passes the
@@ -166,8 +168,9 @@ dresd_status dresd_search_filtered(dresd_index *ix, const float *queries,
  *
  *   Arguments, order, determinism and errors as for dresd_search, and
  *   EINVAL when the search needs more workspace than DRESD_SCRATCH_BYTES
- *   (dresd_search_plan's workspace_bytes tells beforehand; e.g. one query up
- *   to k = 1024, or 64 queries at k = 32, fit).  Profiling (dresd_profile_*)
+ *   even so (dresd_search_plan's workspace_bytes, the need of dresd_search,
+ *   is an upper bound; e.g. one query up to k = 1024, or 64 queries at
+ *   k = 32, fit).  Profiling (dresd_profile_*)
  *   does not time these calls.
  * Every call on one device shares that device's scratch, which keeps the
  * last call's contents (each search writes every scratch byte it reads

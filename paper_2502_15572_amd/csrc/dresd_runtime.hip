@@ -240,7 +240,7 @@ dresd_status validate_search(const dresd_index *ix, int32_t B, int32_t k) {
 }
 
 dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = false,
-                       bool keep_cache = true) {
+                       bool keep_cache = true, bool tc32 = true) {
   pl = Plan();
   pl.filt = filt;
   // The query enters the matrix cores as three 16-bit parts that sum to it
@@ -263,7 +263,7 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
   // query group of waves serves 4 query tiles (8 for bf16: 64 queries);
   // larger batches take 2 or 4 query groups (up to 256 f16 or 128 bf16
   // queries per launch), fewer where the lists leave too little LDS.
-  const bool tc_kb = ix->KB > 32 || (ix->KB == 32 && qt_all > 4);
+  const bool tc_kb = ix->KB > 32 || (tc32 && ix->KB == 32 && qt_all > 4);
   if (mq_type && tc_kb && qt_all >= 2 && pl.terms < 4) {
     const bool bf = ix->dtype == kBF16;
     const int qtw = (bf && qt_all > 4) ? 8 : 4;
@@ -821,6 +821,14 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
   Plan pl;
   s = make_plan(ix, B, k, pl, next_tok != nullptr, !fixed);
   if (s != DRESD_OK) return s;
+  // A fixed workspace too small for the tiled contraction's lists (one per
+  // query per key group of waves of each workgroup): 1,024-dim keys take the
+  // shared-key scan instead (one list per query per workgroup, a launch per
+  // 64 queries).
+  if (fixed && pl.bytes > fixed_bytes && pl.tc && ix->KB == 32) {
+    s = make_plan(ix, B, k, pl, next_tok != nullptr, false, false);
+    if (s != DRESD_OK) return s;
+  }
   unsigned char *ws = fixed_ws;
   if (fixed) {
     if (pl.bytes > fixed_bytes)

@@ -125,3 +125,48 @@ def test_noalloc_tiled_contraction(gpu_lib):
         for a, b in zip(outs[c], refs[c]):
             assert torch.equal(a, b), c
     ix.close()
+
+
+def test_noalloc_wide_batch_takes_shared_key_scan(gpu_lib):
+    """1,024-dim keys past 64 queries: dresd_search runs the tiled contraction
+    with query groups, whose lists exceed the fixed scratch; the allocation-
+    free search runs the shared-key scan instead (a launch per 64 queries)
+    and returns bitwise the same results, on two calls in a row, the second
+    smaller, with no device allocation."""
+    from paper_2502_15572_amd import Index
+    gen = torch.Generator(device="cuda").manual_seed(12)
+    N, d, L = 20011, 1024, 3
+    x = torch.randn(N, d, device=DEV, generator=gen)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float16)
+    cont = torch.randint(0, 32000, (N, L), device=DEV, generator=gen, dtype=torch.int32)
+    q = torch.randn(130, d, device=DEV, generator=gen)
+    q = (q / q.norm(dim=1, keepdim=True)).contiguous()
+    ix = Index(x, cont)
+    cases = [(130, 16), (100, 10)]
+    outs = {c: _outs(c[0], c[1], L) for c in cases}
+    refs = {}
+    for B, k in cases:
+        plan = ix.plan(B, k)
+        assert plan["scan_kernel"] == "tiled" and plan["launches"] == 1
+        assert plan["workspace_bytes"] > SCRATCH_BYTES
+        refs[(B, k)] = [t.clone() for t in ix.search(q[:B].contiguous(), k)]
+    torch.cuda.synchronize()
+    qs = {c: q[:c[0]].contiguous() for c in cases}
+    st = _noalloc(gpu_lib, ix, qs[cases[0]], outs[cases[0]])
+    assert st == OK, gpu_lib.dresd_last_error()
+    torch.cuda.synchronize()
+    free0 = torch.cuda.mem_get_info()[0]
+    os.environ["DRESD_FAIL_ALLOC_AT"] = "1"
+    try:
+        for B, k in cases:
+            say("noalloc wide B=%d k=%d" % (B, k))
+            st = _noalloc(gpu_lib, ix, qs[(B, k)], outs[(B, k)])
+            assert st == OK, gpu_lib.dresd_last_error()
+        torch.cuda.synchronize()
+    finally:
+        os.environ.pop("DRESD_FAIL_ALLOC_AT", None)
+    assert torch.cuda.mem_get_info()[0] == free0
+    for c in cases:
+        for a, b in zip(outs[c], refs[c]):
+            assert torch.equal(a, b), c
+    ix.close()
