@@ -276,7 +276,9 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
     };
     // main-pass shapes, then sampled-pass shapes, in order of preference; one
     // query group: 8 waves over panels of 32 key tiles (one query read per 32
-    // tiles) where that kernel exists and fits, else 4 waves over 16 tiles
+    // tiles) where that kernel exists and fits, else 4 waves over 16 tiles;
+    // two or four query groups: 8 waves over 16-tile panels, with a 4-stage
+    // ring (operand prefetch) where the lists leave room for it
     static const std::vector<TcShape> main1 = {{4, 8, 3}, {4, 4, 5}, {4, 4, 3}},
                                       samp1 = {{1, 4, 8}, {1, 4, 4}},
                                       main2 = {{4, 4, 4}, {4, 4, 3}}, samp2 = {{2, 4, 4}},

@@ -1,7 +1,8 @@
 // gfx950 scans for batches spanning several 16-column query tiles (the same
 // computation as the scan in dresd_kernels.hip: DReSD Section 3.5, Eq. 3
 // with unit-norm keys as exact top-k, Section 3.6): the shared-key scan
-// below, and the tiled contraction (scan_tc_body) for keys too wide for it.
+// below, and the tiled contraction (scan_tc_body) for keys too wide for it
+// and for batches larger than it holds at 1,024 dims.
 //
 // Shared-key scan: the queries stay in registers and the keys are shared
 // through LDS:
@@ -795,26 +796,28 @@ __device__ __forceinline__ void copy_block_to_lds(const void *src, uint32_t voff
 }
 
 // Tiled contraction for keys wider than the shared-key scan can hold the
-// queries for (more than 32 blocks per key tile) at batches of QTW = 4 or 8
-// query tiles: both operands stream through LDS.  A workgroup of NW waves
-// walks its key tiles in panels of NW TPW tiles.  For each 32-dim column of
-// the keys one ring stage holds the panel's key blocks and the batch's query
-// blocks of that column (a plain GEMM K loop); wave w multiplies its TPW
-// tiles by every query tile, column after column into one accumulator per
-// (tile, query tile) -- the same order in every pass, so a key scores the
-// same in the sampled and the main passes -- and after the last column tests
-// the finished tiles against the thresholds.  Each key block reaches the CU
-// once for the whole batch; the query operand (QTW KiB per column, shared by
-// every workgroup) is re-read from L2 once per panel.  Wave w issues its TPW
-// key copies and the copies of query tiles w, w + NW, ... per stage (past
-// the end, the last stage again), spread over the query tiles' matrix
+// queries for (more than 32 blocks per key tile), and for 32-block keys at
+// batches past one shared-key launch: both operands stream through LDS.  A
+// workgroup of NW = NK x NQ waves (NK key groups, NQ query groups of QTW = 4
+// or 8 query tiles each) walks its key tiles in panels of NK TPW tiles.  For
+// each 32-dim column of the keys one ring stage holds the panel's key blocks
+// and the batch's query blocks of that column (a plain GEMM K loop); a wave
+// multiplies its key group's TPW tiles by its query group's tiles, column
+// after column into one accumulator per (tile, query tile) -- the same order
+// in every pass and launch shape, so a key scores the same in the sampled and
+// the main passes -- and after the last column tests the finished tiles
+// against the thresholds.  Each key block reaches the CU once for the whole
+// batch; the query operand (NQ QTW KiB per column, shared by every
+// workgroup) is re-read from L2 once per panel.  Wave w issues the copies of
+// panel tiles w KPW ... w KPW + KPW - 1 and of query tiles w, w + NW, ... per
+// stage (past the end, the last stage again), spread over its matrix
 // instructions so that the copies' address work overlaps the matrix cores;
 // its wait before each stage is a constant of its copy count.  Lists: one per
-// (query, wave).  A sampled pass (TMAX) lists only each tile's best key per
-// query.  FILT: the next-token filter; each wave copies its panel tiles'
-// first tokens into LDS with one more LDS-DMA copy at the panel's first
-// stage (a load the compiler tracked would make it drain the ring at every
-// stage), covered by the next stage's constant wait.
+// (query, key group of a workgroup).  A sampled pass (TMAX) lists only each
+// tile's best key per query.  FILT: the next-token filter; each wave copies
+// its tiles' first tokens into LDS with one or two more LDS-DMA copies at the
+// panel's first stage (a load the compiler tracked would make it drain the
+// ring at every stage), covered by the later stages' constant waits.
 template <int DT, int QTW, int CPQ, int TPW, int NK, int NQ, int S, bool TMAX, bool FILT>
 __device__ __forceinline__ void scan_tc_body(const ScanParams &p) {
   using WC = WaveCands<DT, QTW, CPQ, FILT, kTcCandBuf>;
