@@ -173,6 +173,8 @@ FILTERED_TILED = [
     ("bf16", 3001, 1100, 33, 12),    # ragged columns, no sampled pass
     ("f16", 20011, 1024, 200, 12),   # four query groups (8 key tiles per wave)
     ("bf16", 5003, 4096, 100, 10),   # two query groups
+    ("f16", 7001, 2048, 256, 64),    # four query groups, three-stage ring (the filter's LDS)
+    ("bf16", 4001, 1024, 128, 32),   # 1,024-dim bf16 keys, two query groups
 ]
 
 

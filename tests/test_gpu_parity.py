@@ -262,6 +262,40 @@ def test_tiled_contraction_query_groups(gpu_lib, dt, N, d, B, k, nl):
     run_case(gpu_lib, x, cont, q, k, dt, kind="tiled")
 
 
+def _random_group_cases(n, seed):
+    """Seeded random shapes past one query group: dims from 1,024 (1,024-dim
+    keys take the contraction past 64 f16 / 32 bf16 queries), 33-256
+    queries, k from 1 to 128."""
+    import random
+    rng = random.Random(seed)
+    out = []
+    while len(out) < n:
+        dt = rng.choice(["bf16", "f16"])
+        d = rng.choice([1024, 1056, 2048, 3000, 4096])
+        B = rng.randint(33 if (dt == "bf16" and d == 1024) else 65, 256)
+        k = rng.choice([1, 7, 16, 50, 128])
+        N = rng.randint(max(k, 500), 20000)
+        if N * d * B <= 3e9:
+            out.append((dt, N, d, B, k))
+    return out
+
+
+TC_GROUPS_RANDOM = _random_group_cases(8, 77)
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", TC_GROUPS_RANDOM,
+                         ids=["%s-N%d-d%d-B%d-k%d" % e for e in TC_GROUPS_RANDOM])
+def test_tiled_contraction_random_groups(gpu_lib, dt, N, d, B, k):
+    say("tiled random groups", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N * 5 + d + B + k * 3)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    q = torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 2), generator=gen, dtype=torch.int32)
+    run_case(gpu_lib, x, cont, q, k, dt, kind="tiled")
+
+
 def _random_tiled_cases(n, seed):
     """Seeded random shapes for the tiled contraction: dims past 1,024 (ragged
     column counts included), 9-140 queries (one to three launches), k from 1
