@@ -31,20 +31,21 @@ def say(*a):
 def built():
     cache = {}
 
-    def get(name):
-        if name not in cache:
+    def get(name, B):
+        w = WORKLOADS[name].with_pool(B)  # a pool of at least B distinct queries
+        key = (name, w.pool)
+        if key not in cache:
             cache.clear()
             torch.cuda.empty_cache()
             from paper_2502_15572_amd import Index
-            w = WORKLOADS[name]
             t = time.time()
             g = generate(w, DEV)
             ix = Index(g["keys"], g["cont"])
             kb, dt = to_numpy_bits(g["keys"])
             cont = g["cont"].cpu().numpy()
             say("built %s in %.1fs" % (name, time.time() - t))
-            cache[name] = (w, g, ix, kb, dt, cont)
-        return cache[name]
+            cache[key] = (w, g, ix, kb, dt, cont)
+        return cache[key]
 
     yield get
     cache.clear()
@@ -55,13 +56,20 @@ CASES = [(name, B) for name, w in WORKLOADS.items() for B in w.batches]
 # (their workgroups share each key range through one XCD's L2).
 CASES.insert(CASES.index(("hidden1m_d4096_bf16", max(WORKLOADS["hidden1m_d4096_bf16"].batches))) + 1,
              ("hidden1m_d4096_bf16", 64))
+# Past one query group of the tiled contraction: 128 bf16 queries over the
+# 1M x 4096 datastore (two query groups) and 256 f16 queries over the
+# 4M x 1024 one (four), each one pass over the keys.
+CASES.insert(CASES.index(("hidden1m_d4096_bf16", 64)) + 1, ("hidden1m_d4096_bf16", 128))
+CASES.insert(CASES.index(("pca4m_d1024_f16", max(WORKLOADS["pca4m_d1024_f16"].batches))) + 1,
+             ("pca4m_d1024_f16", 256))
 
 
 @pytest.mark.parametrize("name,B", CASES, ids=["%s-B%d" % c for c in CASES])
 def test_fullsize(built, name, B):
-    w, g, ix, kb, dt, cont = built(name)
+    w, g, ix, kb, dt, cont = built(name, B)
     q = g["queries"][:B].contiguous()
-    say("search %s B=%d k=%d" % (name, B, w.k))
+    assert q.shape[0] == B
+    say("search %s B=%d k=%d plan %s" % (name, B, w.k, ix.plan(B, w.k)))
     idx, score, tok = ix.search(q, w.k)
     torch.cuda.synchronize()
     gi, gs, gt = idx.cpu().numpy(), score.cpu().numpy(), tok.cpu().numpy()
