@@ -452,7 +452,7 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
 // so the readers of a range run at the same time.
 int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit, bool main_pass = true) {
   const int wpg = kScanThreads / kWaveSize;
-  // tiled contraction: whole panels of nw * tpw tiles
+  // tiled contraction: whole panels of nk * tpw tiles
   const int per_wg = pl.tc ? (main_pass ? pl.nk_main * pl.tpw_main : pl.nk_sample * pl.tpw_sample)
                    : pl.mq ? 1 : wpg;
   int64_t wgs = std::min<int64_t>(pl.wg_max, ceil_div(nvisit, per_wg));
