@@ -44,8 +44,9 @@ extern "C" {
  * A call that would have to grow a workspace while its stream is being
  * captured fails with DRESD_EUNSUPPORTED instead.  A workspace that a later,
  * larger call outgrows is never freed before its owner is (the index for
- * search workspaces, the process for the per-device transform and k-means
- * buffers), so a graph captured earlier stays valid after such a call.
+ * search workspaces, the process for the transform and k-means buffers, one
+ * per device and stream), so a graph captured earlier stays valid after such
+ * a call.
  *
  * Allocation-failure test hook: with DRESD_FAIL_ALLOC_AT=n in the
  * environment, the n-th device allocation the library makes (counted from
@@ -252,10 +253,10 @@ dresd_status dresd_bw_probe(const void *buf, int64_t bytes, int32_t reps, int32_
  * few output tiles split D across workgroups and add the partial sums in a
  * fixed order, so results are deterministic.  Ownership: all buffers are
  * caller-owned and must stay alive until `stream` completes; the partial sums
- * use a per-device library buffer that is allocated (synchronously) on the
- * first call that needs a larger one and kept, like every buffer it
- * outgrows, until the process ends, so calls that overlap on one device must
- * be serialised by the caller.
+ * use a library buffer per (device, stream) that is allocated (synchronously)
+ * on the first call on that stream that needs a larger one and kept, like
+ * every buffer it outgrows, until the process ends: calls on different
+ * streams may overlap, calls on one stream are ordered by it.
  * Errors: EINVAL (null pointer with M > 0, sizes or eps out of range),
  * ENOMEM, EUNSUPPORTED (the buffer would have to grow during stream
  * capture), EDEVICE.
@@ -380,10 +381,10 @@ dresd_status dresd_ivf_search_probes(dresd_ivf *ivf, const float *queries, const
  *   order of the rows (deterministic).  x as above with n < 2^31; assign
  *   device [n] int32, each in [0, P) (not checked: the caller's contract);
  *   centroids device [P, d] fp32 in/out; counts device [P] int32 out (rows per
- *   centroid, NULL allowed).  Uses a per-device workspace of P*d*8 + P*4
- *   bytes, allocated (synchronously) on first use and kept, like every
- *   buffer it outgrows, until the process ends; calls that overlap on one
- *   device race on it.
+ *   centroid, NULL allowed).  Uses a workspace of P*d*8 + P*4 bytes per
+ *   (device, stream), allocated (synchronously) on first use on that stream
+ *   and kept, like every buffer it outgrows, until the process ends: calls
+ *   on different streams may overlap, calls on one stream are ordered by it.
  * dresd_kmeans_init: the starting centroids of the iteration: P distinct
  *   rows spread evenly through the row order, centroid j = row pick(j)
  *   scaled to unit length (a zero row gives a zero centroid), with

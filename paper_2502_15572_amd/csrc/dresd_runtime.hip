@@ -2,6 +2,7 @@
 // one-time key layout, workspace management and the per-search launch plan
 // (sampled threshold passes, main scan, merge + gather).
 #include <algorithm>
+#include <map>
 #include <mutex>
 #include <new>
 #include <string>
@@ -485,21 +486,23 @@ dresd_status ensure_workspace(dresd_index *ix, size_t bytes, hipStream_t st) {
   return DRESD_OK;
 }
 
-// Per-device buffers kept until the process ends (the transform's partial
-// sums, the k-means sums).  One grows (allocating synchronously) when a call
-// needs more; the buffer it outgrows is kept as well, because a graph
-// captured from an earlier call may still replay on it.
+// Library buffers kept until the process ends (the transform's partial
+// sums, the k-means sums), one per (device, stream): calls on different
+// streams never share one, and calls on one stream are ordered by it.  One
+// grows (allocating synchronously) when a call needs more; the buffer it
+// outgrows is kept as well, because a graph captured from an earlier call
+// may still replay on it.
 struct DeviceBuffers {
   std::mutex mu;
-  std::vector<std::pair<void *, size_t>> cur;  // per device
+  std::map<std::pair<int, hipStream_t>, std::pair<void *, size_t>> cur;
   std::vector<void *> retired;
 };
 
 dresd_status device_buffer(DeviceBuffers &db, int dev, size_t need, hipStream_t st,
                            const char *what, void **out) {
   std::lock_guard<std::mutex> lock(db.mu);
-  if (db.cur.size() <= (size_t)dev) db.cur.resize((size_t)dev + 1, {nullptr, 0});
-  if (db.cur[dev].second < need) {
+  auto &c = db.cur[{dev, st}];
+  if (c.second < need) {
     if (capturing(st))
       return fail(DRESD_EUNSUPPORTED, std::string(what) +
                                           " must grow while the stream is being captured; run one "
@@ -509,10 +512,10 @@ dresd_status device_buffer(DeviceBuffers &db, int dev, size_t need, hipStream_t 
       (void)hipGetLastError();
       return fail(DRESD_ENOMEM, std::string(what) + " allocation failed");
     }
-    if (db.cur[dev].first) db.retired.push_back(db.cur[dev].first);
-    db.cur[dev] = {b, need};
+    if (c.first) db.retired.push_back(c.first);
+    c = {b, need};
   }
-  *out = db.cur[dev].first;
+  *out = c.first;
   return DRESD_OK;
 }
 

@@ -177,3 +177,32 @@ def test_train_partitions_and_search(gpu_lib):
         checked += 1
     assert checked >= len(q) // 2
     ix.close()
+
+
+def test_kmeans_update_on_two_streams(gpu_lib):
+    """k-means updates issued back to back on two streams (each with its own
+    library buffer of sums): every result equals the one computed alone."""
+    from paper_2502_15572_amd import kmeans_update
+    rng = np.random.default_rng(31)
+    data = []
+    for n, d, P in ((20000, 128, 300), (15000, 128, 200)):
+        keys = as_keys(unit(rng, n, d), "f16").to(DEV)
+        a = torch.from_numpy(rng.integers(0, P, n).astype(np.int32)).to(DEV)
+        c0 = torch.from_numpy(unit(rng, P, d).astype(np.float32)).to(DEV)
+        ref = c0.clone()
+        kmeans_update(keys, a, ref)
+        data.append((keys, a, c0, ref))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[], []]
+    for _ in range(6):
+        for i, s in enumerate(streams):
+            keys, a, c0, _ = data[i]
+            with torch.cuda.stream(s):
+                c = c0.clone()
+                kmeans_update(keys, a, c, stream=s)
+                outs[i].append(c)
+    torch.cuda.synchronize()
+    for i in range(2):
+        for c in outs[i]:
+            assert torch.equal(c, data[i][3])

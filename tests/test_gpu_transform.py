@@ -114,3 +114,26 @@ def test_transform_argument_errors(gpu_lib):
     assert lib.dresd_transform(None, 0, 4, None, None, 1e-5, None, 2, 1e-12, None, None) == 0
     assert lib.dresd_transform(None, 0, 0, None, None, 1e-5, None, 2, 1e-12, None, None) == 1
     assert lib.dresd_transform(None, 0, 4, None, None, -1.0, None, 2, 1e-12, None, None) == 1
+
+
+def test_transform_on_two_streams(gpu_lib):
+    """Transforms with split partial sums issued back to back on two streams
+    (each stream has its own library buffer): every result equals the one
+    computed alone, bit for bit."""
+    from paper_2502_15572_amd import transform
+    t = lambda a: torch.from_numpy(a).to(DEV)
+    cases = [make_case(16, 4096, 256, 21), make_case(8, 4096, 512, 22)]
+    args = [tuple(t(a) for a in c) for c in cases]
+    refs = [transform(*a) for a in args]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[], []]
+    torch.cuda.synchronize()
+    for _ in range(8):
+        for i, s in enumerate(streams):
+            with torch.cuda.stream(s):
+                outs[i].append(transform(*args[i], stream=s))
+    torch.cuda.synchronize()
+    for i in range(2):
+        for y in outs[i]:
+            assert torch.equal(y, refs[i])
