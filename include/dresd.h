@@ -123,10 +123,12 @@ dresd_status dresd_index_create(const void *embeddings,
  * 2e-3 parity bound for 16-bit keys.
  * Determinism: identical inputs give bitwise identical outputs.
  * Ownership: outputs are caller-owned and must stay alive until `stream`
- * completes.  The index owns a workspace that grows on first use with a new
- * batch shape (that growth allocates and synchronises; outgrown workspaces
- * are kept until the index is destroyed); concurrent searches on one index
- * are not supported.
+ * completes.  The index owns a workspace per stream it is searched on, which
+ * grows on first use with a new batch shape (that growth allocates and
+ * synchronises; outgrown workspaces are kept until the index is destroyed):
+ * searches on different streams may overlap on the device, searches on one
+ * stream are ordered by it.  The calls themselves are not thread-safe: calls
+ * on one index from several host threads must be serialised by the caller.
  * Errors: EINVAL (null index/queries/idx/score, k out of range, B < 0),
  * ENOMEM (workspace growth failed; no output written), EUNSUPPORTED (the
  * workspace would have to grow during stream capture), EDEVICE.
@@ -331,8 +333,10 @@ dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,
  * dresd_ivf_search: like dresd_search, probing 1 <= nprobe <= min(P,
  *   DRESD_K_MAX) partitions per query (the nprobe best centroids by inner
  *   product, ties to the lower id).  Ranks past the keys of the probed
- *   partitions hold index -1, score -inf and zero tokens.  One search at a
- *   time per index.
+ *   partitions hold index -1, score -inf and zero tokens.  Workspaces and
+ *   the probe buffer are per stream, as for dresd_search: searches on
+ *   different streams may overlap on the device; calls from several host
+ *   threads must be serialised by the caller.
  * dresd_ivf_search_filtered: dresd_ivf_search with the next-token filter of
  *   dresd_search_filtered (next_tok device [B] int32): among the keys of the
  *   probed partitions only those whose continuation starts with the query's

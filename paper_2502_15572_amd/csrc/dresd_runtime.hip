@@ -35,10 +35,10 @@ struct dresd_index {
   int32_t *ftok = nullptr;  // first token of each row's value [T * 16] (filtered search)
   int cus = 0;
   size_t lds_max = 0;
-  // workspace; buffers it outgrew stay allocated until destroy (a captured
-  // graph may still use them)
-  unsigned char *ws = nullptr;
-  size_t ws_bytes = 0;
+  // workspaces, one per stream the index is searched on (searches on
+  // different streams may overlap); buffers they outgrew stay allocated
+  // until destroy (a captured graph may still use them)
+  std::map<hipStream_t, std::pair<unsigned char *, size_t>> ws;
   std::vector<void *> retired;
   // measurement
   bool prof = false;
@@ -461,8 +461,12 @@ int64_t pass_wgs(const Plan &pl, const Group &gr, int64_t nvisit, bool main_pass
   return wgs;
 }
 
-dresd_status ensure_workspace(dresd_index *ix, size_t bytes, hipStream_t st) {
-  if (ix->ws_bytes >= bytes) return DRESD_OK;
+// The index's workspace for stream st, grown to at least `bytes`.
+dresd_status ensure_workspace(dresd_index *ix, size_t bytes, hipStream_t st,
+                              unsigned char **out) {
+  auto &w = ix->ws[st];
+  *out = w.first;
+  if (w.second >= bytes) return DRESD_OK;
   if (capturing(st))
     return fail(DRESD_EUNSUPPORTED,
                 "the search needs a larger workspace while its stream is being captured; run one "
@@ -473,16 +477,18 @@ dresd_status ensure_workspace(dresd_index *ix, size_t bytes, hipStream_t st) {
     return fail(DRESD_ENOMEM, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
   }
   // Every region is written before it is read in each search; clearing it
-  // once keeps a fresh workspace deterministic to inspect.
-  if (hipMemset(p, 0, bytes) != hipSuccess) {
+  // once keeps a fresh workspace deterministic to inspect.  The clear is
+  // ordered on the search's own stream (not capturing: growth is refused
+  // then), ahead of the kernels that use the workspace.
+  if (hipMemsetAsync(p, 0, bytes, st) != hipSuccess) {
     (void)hipFree(p);
     return fail(DRESD_EDEVICE, "workspace clear failed");
   }
   // The outgrown buffer is kept until the index is destroyed: a graph
   // captured from an earlier search may still replay on it.
-  if (ix->ws) ix->retired.push_back(ix->ws);
-  ix->ws = static_cast<unsigned char *>(p);
-  ix->ws_bytes = bytes;
+  if (w.first) ix->retired.push_back(w.first);
+  w = {static_cast<unsigned char *>(p), bytes};
+  *out = w.first;
   return DRESD_OK;
 }
 
@@ -732,7 +738,8 @@ void dresd_index_destroy(dresd_index *ix) {
   if (ix->data) (void)hipFree(ix->data);
   if (ix->cont) (void)hipFree(ix->cont);
   if (ix->ftok) (void)hipFree(ix->ftok);
-  if (ix->ws) (void)hipFree(ix->ws);
+  for (auto &w : ix->ws)
+    if (w.second.first) (void)hipFree(w.second.first);
   for (void *r : ix->retired) (void)hipFree(r);
   for (auto e : ix->ev_free) (void)hipEventDestroy(e);
   for (auto e : profile_events(ix)) (void)hipEventDestroy(e);
@@ -842,9 +849,8 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
                                     std::to_string(fixed_bytes) +
                                     " bytes of the fixed scratch (use dresd_search)");
   } else {
-    s = ensure_workspace(ix, pl.bytes, st);
+    s = ensure_workspace(ix, pl.bytes, st, &ws);
     if (s != DRESD_OK) return s;
-    ws = ix->ws;
   }
   const bool prof = ix->prof && !fixed;
   uint64_t *tau = reinterpret_cast<uint64_t *>(ws + pl.off_tau);
@@ -1121,8 +1127,8 @@ struct dresd_ivf {
   int32_t *ftok_slot = nullptr;  // [T * 16] first token of each slot's value (0: padding)
   int32_t *part_tile = nullptr;  // [P + 1] first tile of each partition
   int32_t P = 0;
-  int64_t probe_bytes = 0;       // probe results of the last search: ids + scores
-  unsigned char *probe = nullptr;
+  // probe results (ids + scores) of a search, one buffer per stream
+  std::map<hipStream_t, std::pair<unsigned char *, int64_t>> probe;
   std::vector<void *> retired;   // outgrown probe buffers, freed at destroy
 };
 
@@ -1135,7 +1141,8 @@ void ivf_free(dresd_ivf *v) {
   if (v->slot_row) (void)hipFree(v->slot_row);
   if (v->ftok_slot) (void)hipFree(v->ftok_slot);
   if (v->part_tile) (void)hipFree(v->part_tile);
-  if (v->probe) (void)hipFree(v->probe);
+  for (auto &pb : v->probe)
+    if (pb.second.first) (void)hipFree(pb.second.first);
   for (void *r : v->retired) (void)hipFree(r);
   delete v;
 }
@@ -1179,9 +1186,9 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   const size_t off_lists = off_lfirst + up(nb * G * 8);
   const size_t off_spill = off_lists + up(nb * G * (size_t)C * 8);
   const size_t bytes = off_spill + up(nb * (size_t)std::max<int64_t>(1, spill_cap) * 8);
-  dresd_status s = ensure_workspace(ix, bytes, st);
+  unsigned char *ws = nullptr;
+  dresd_status s = ensure_workspace(ix, bytes, st, &ws);
   if (s != DRESD_OK) return s;
-  unsigned char *ws = ix->ws;
 
   SegParams gp;
   gp.probes64 = nullptr;
@@ -1400,7 +1407,8 @@ dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *
   if (B == 0) return DRESD_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t need = (int64_t)B * nprobe * 12;
-  if (v->probe_bytes < need) {
+  auto &pb = v->probe[st];
+  if (pb.second < need) {
     if (capturing(st))
       return fail(DRESD_EUNSUPPORTED,
                   "the probe buffer must grow while the stream is being captured; run one "
@@ -1410,17 +1418,16 @@ dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *
       (void)hipGetLastError();
       return fail(DRESD_ENOMEM, "probe buffer allocation failed");
     }
-    if (hipMemset(p, 0, (size_t)need) != hipSuccess) {
+    if (hipMemsetAsync(p, 0, (size_t)need, st) != hipSuccess) {  // ordered on the search's stream
       (void)hipFree(p);
       return fail(DRESD_EDEVICE, "probe buffer clear failed");
     }
     // kept until destroy: a captured graph may still use the outgrown buffer
-    if (v->probe) v->retired.push_back(v->probe);
-    v->probe = static_cast<unsigned char *>(p);
-    v->probe_bytes = need;
+    if (pb.first) v->retired.push_back(pb.first);
+    pb = {static_cast<unsigned char *>(p), need};
   }
-  int64_t *pid = reinterpret_cast<int64_t *>(v->probe);
-  float *psc = reinterpret_cast<float *>(v->probe + (size_t)B * nprobe * 8);
+  int64_t *pid = reinterpret_cast<int64_t *>(pb.first);
+  float *psc = reinterpret_cast<float *>(pb.first + (size_t)B * nprobe * 8);
   hipEvent_t a0 = nullptr, a1 = nullptr;
   dresd_index *ix = v->ix;
   Launcher launch;

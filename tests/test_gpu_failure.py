@@ -234,8 +234,8 @@ def test_no_workspace_growth_inside_capture(gpu_lib):
 
 def test_graph_survives_later_workspace_growth(gpu_lib):
     """A graph captured at B = 1 still replays correctly after a larger
-    eager search has grown (replaced) the index's workspace: the outgrown
-    workspace is kept until the index is destroyed."""
+    eager search on the same stream has grown (replaced) that stream's
+    workspace: the outgrown workspace is kept until the index is destroyed."""
     from paper_2502_15572_amd import Index
     x, cont, q = datastore()
     ix = Index(x, cont)
@@ -257,7 +257,8 @@ def test_graph_survives_later_workspace_growth(gpu_lib):
     ws64 = ix.plan(64, 32)["workspace_bytes"]
     assert ws64 > ws1
     before = free_bytes()
-    big = ix.search(q[:64].contiguous(), 32)  # grows the workspace
+    with torch.cuda.stream(s):  # grows the stream's workspace
+        big = ix.search(q[:64].contiguous(), 32, stream=s)
     torch.cuda.synchronize()
     # the new workspace was allocated and the outgrown one not returned
     assert before - free_bytes() >= ws64 - (2 << 20)
