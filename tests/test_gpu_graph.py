@@ -79,7 +79,8 @@ def test_captured_step_replays_match_eager(gpu_lib, partitioned):
 @pytest.mark.parametrize("kind,N,d,B,k", [
     ("shared_key", 60000, 128, 64, 16),   # queries in registers, keys through the LDS ring
     ("tiled", 20011, 2048, 24, 12),       # both operands through the LDS ring, sampled pass
-], ids=["shared_key", "tiled"])
+    ("tiled", 20011, 1024, 200, 12),      # two query groups per launch, two launches
+], ids=["shared_key", "tiled", "tiled_groups"])
 def test_captured_search_replays_match_eager(gpu_lib, kind, N, d, B, k):
     """The batched scans in a captured graph (after one warm-up search of the
     same shape): each replay, with other work and synchronisations between
