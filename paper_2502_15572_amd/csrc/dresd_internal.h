@@ -102,9 +102,10 @@ __host__ __device__ inline size_t scan_mq_wave_bytes(int nqw, int C, int cb = kM
 }
 // The tiled contraction tests a tile once per K loop: a smaller buffer.
 constexpr int kTcCandBuf = 128;
-__host__ __device__ inline size_t scan_mq_lds_bytes(int stages, int nqw, int C) {
-  return (size_t)stages * kMqStageBlocks * kBlockBytes +
-         (size_t)(kScanThreads / kWaveSize) * scan_mq_wave_bytes(nqw, C);
+// LDS of the shared-key scan: ring | one candidate region per wave (nw
+// waves per workgroup).
+__host__ __device__ inline size_t scan_mq_lds_bytes(int stages, int nqw, int C, int nw = 4) {
+  return (size_t)stages * kMqStageBlocks * kBlockBytes + (size_t)nw * scan_mq_wave_bytes(nqw, C);
 }
 
 // A list summary flag: the list is sorted, best key first.
@@ -169,14 +170,17 @@ typedef void (*ScanKernel)(ScanParams);
 // groups (one query tile only, else null)
 ScanKernel scan_kernel(int dtype, int qt, int cpq, bool main_pass, bool shared = false);
 // Shared-key scan (dresd_scan_mq.hip): qtw query tiles per wave, kbt blocks
-// per key tile, filtered = next-token-filtered search; *stages receives the
-// depth of its LDS ring of key stages.
-ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, bool filtered, int *stages);
-ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, bool filtered, int *stages);
+// per key tile, filtered = next-token-filtered search, nwq waves per
+// workgroup (4, or 1 for a wave holding the whole batch: qtw 4 with 8-block
+// tiles); *stages receives the depth of its LDS ring of key stages.
+ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, bool filtered, int *stages,
+                              int nwq);
+ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, bool filtered, int *stages,
+                               int nwq);
 inline ScanKernel scan_mq_kernel(int dtype, int qtw, int kbt, bool main_pass, bool filtered,
-                                 int *stages) {
-  if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass, filtered, stages);
-  if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass, filtered, stages);
+                                 int *stages, int nwq = 4) {
+  if (dtype == kF16) return scan_mq_kernel_f16(qtw, kbt, main_pass, filtered, stages, nwq);
+  if (dtype == kBF16) return scan_mq_kernel_bf16(qtw, kbt, main_pass, filtered, stages, nwq);
   return nullptr;
 }
 // Tiled contraction (both operands through LDS): qtw query tiles per wave

@@ -163,6 +163,7 @@ constexpr int kGroupsPerLaunch = 8;
 struct Plan {
   int terms = 1, qpt = 16, qt = 1;  // columns per query, queries per tile, tiles
   bool mq = false;                  // shared-key scan (queries in registers)
+  int nwq = 4;                      // shared-key scan: waves per workgroup
   bool tc = false;                  // tiled contraction (queries and keys through LDS)
   // tiled contraction: key tiles per wave and key groups of waves per pass
   // kind, query groups of waves (waves per workgroup: nk * nq)
@@ -189,6 +190,7 @@ struct Plan {
 
 // Threads per workgroup of a plan's main or sampled scan.
 int threads_of(const Plan &pl, bool main_pass) {
+  if (pl.mq) return pl.nwq * kWaveSize;
   if (!pl.tc) return kScanThreads;
   return (main_pass ? pl.nk_main : pl.nk_sample) * pl.nq * kWaveSize;
 }
@@ -325,14 +327,26 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
     int qtw = 1;
     while (qtw < 4 && 4 * qtw < qt_all && 2 * qtw * ix->KB <= 32) qtw <<= 1;
     pl.qt = 4 * qtw;
-    pl.bmax = std::min(B, pl.qt * pl.qpt);
+    pl.nwq = 4;
     int stages = 0;
-    pl.kmain = scan_mq_kernel(ix->dtype, qtw, ix->KB, true, filt, &stages);
-    pl.ksample = scan_mq_kernel(ix->dtype, qtw, ix->KB, false, filt, &stages);
+    // 8-block key tiles (256 dims) at 2-4 query tiles: one wave per
+    // workgroup holds the whole batch (32 chunks of 16 bytes), so no wave
+    // waits at a barrier for another's candidates (measured, 10M x 256:
+    // main pass 0.776 -> 0.749 ms at B = 64, 0.759 -> 0.740 ms at B = 32;
+    // at 128 dims and 64-128 queries it was 15-20% slower: four waves per
+    // CU leave too little to overlap).
+    if (ix->KB == 8 && qt_all >= 2 && qt_all * ix->KB <= 32 &&
+        scan_mq_kernel(ix->dtype, 4, ix->KB, true, filt, &stages, 1)) {
+      qtw = 4;
+      pl.qt = qtw;
+      pl.nwq = 1;
+    }
+    pl.bmax = std::min(B, pl.qt * pl.qpt);
+    pl.kmain = scan_mq_kernel(ix->dtype, qtw, ix->KB, true, filt, &stages, pl.nwq);
+    pl.ksample = scan_mq_kernel(ix->dtype, qtw, ix->KB, false, filt, &stages, pl.nwq);
     pl.CL = 0;
-    pl.lds = scan_mq_lds_bytes(stages, qtw * pl.qpt, pl.C) +
-             (filt ? (size_t)(kScanThreads / kWaveSize) * scan_mq_filter_bytes(stages, qtw * (4 / pl.terms))
-                   : 0);
+    pl.lds = scan_mq_lds_bytes(stages, qtw * pl.qpt, pl.C, pl.nwq) +
+             (filt ? (size_t)pl.nwq * scan_mq_filter_bytes(stages, qtw * (4 / pl.terms)) : 0);
   } else {
     // Largest group (power-of-two number of query tiles, at most 16) whose
     // query operand and per-wave state fit in the workgroup's LDS.
@@ -651,15 +665,17 @@ dresd_status index_build(const void *embeddings, const int32_t *continuations, i
   }
   // Raise the dynamic-LDS limit of every scan kernel to the device's.
   for (int v = 0; v < 3; ++v)
-    for (int qtw : {1, 2, 4})
+    for (int qtw : {1, 2, 4, 8})
       for (int kbt : {4, 8, 16, 32})
-        for (int mp = 0; mp < 4; ++mp) {
-          int stages = 0;
-          ScanKernel kf = scan_mq_kernel(v, qtw, kbt, (mp & 1) != 0, mp >= 2, &stages);
-          if (kf)
-            (void)hipFuncSetAttribute((const void *)kf, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                      (int)ix->lds_max);
-        }
+        for (int nwq : {1, 4})
+          for (int mp = 0; mp < 4; ++mp) {
+            int stages = 0;
+            ScanKernel kf = scan_mq_kernel(v, qtw, kbt, (mp & 1) != 0, mp >= 2, &stages, nwq);
+            if (kf)
+              (void)hipFuncSetAttribute((const void *)kf,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)ix->lds_max);
+          }
   for (int v = 0; v < 3; ++v)
     for (int qt : {1, 2, 4, 8, 16})
       for (int cpq : {1, 2, 4})

@@ -487,7 +487,7 @@ struct WaveCands {
 // index's blocks per tile), CPQ operand columns per query, S LDS stages;
 // FILT: next-token-filtered search (a separate instantiation, so the
 // unfiltered stream loop carries none of its code).
-template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
+template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT, int NWQ>
 __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   using WC = WaveCands<DT, QTW, CPQ, FILT>;
   constexpr int NQW = WC::NQW;  // queries per wave
@@ -496,7 +496,8 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   constexpr int TPS = KBT >= SB ? 1 : SB / KBT;  // key tiles per stage
   constexpr int SPT = KBT >= SB ? KBT / SB : 1;  // stages per key tile
   constexpr int BPT = KBT >= SB ? SB : KBT;      // blocks of a tile per stage
-  constexpr int WAIT = 2 * (S - 2);  // copies of later stages still in flight
+  constexpr int CPW = 4 / NWQ;  // pairs of blocks each wave copies per stage
+  constexpr int WAIT = 2 * CPW * (S - 2);  // copies of later stages still in flight
   // Interleave each tile's threshold test with the next tile's matrix
   // instructions when a key tile carries few of them (measured: 33.5M keys x
   // 128 dims at 128 queries, 8 per tile, main pass 1.43 -> 1.37 ms; at
@@ -517,7 +518,7 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   const size_t wreg = scan_mq_wave_bytes(NQW, p.C);
   constexpr bool filt = FILT;
   int32_t *nt_slot = reinterpret_cast<int32_t *>(
-      smem + (size_t)S * SB * kBlockBytes + (size_t)(kScanThreads / kWaveSize) * wreg +
+      smem + (size_t)S * SB * kBlockBytes + (size_t)NWQ * wreg +
       (size_t)wv * scan_mq_filter_bytes(S, NP));  // [4 lane groups][NP]
   int32_t *fring = nt_slot + 4 * NP;              // [S][64]
 
@@ -552,24 +553,28 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     // LDS offsets: the low half of a generic LDS address.
     const uint32_t ring = (uint32_t)(uintptr_t)smem;
     const uint32_t fring_lds = (uint32_t)(uintptr_t)fring;
-    // Source of this wave's 2 blocks of stage `st` (blocks j = st*SB + 2wv,
-    // +1 of the visited sequence; past the end, the last two blocks again).
+    // Source of pair c of this wave's blocks of stage `st` (blocks
+    // j = st*SB + 2(wv CPW + c), +1 of the visited sequence; past the end,
+    // the last two blocks again).
     const int64_t jl = NB - 2;
     const unsigned char *last_src =
         dbase + (jl / KBT) * tstep + (jl - (jl / KBT) * KBT) * kBlockBytes;
     const int64_t stage_step = (SPT == 1) ? (int64_t)TPS * tstep : 0;
-    const int64_t woff = (SPT == 1) ? (int64_t)((wv * 2) / KBT) * tstep +
-                                          (int64_t)((wv * 2) % KBT) * kBlockBytes
-                                    : 0;
-    auto src_of = [&](int64_t st) -> const unsigned char * {
-      if (st * SB + wv * 2 > jl) return last_src;
-      if constexpr (SPT == 1) return dbase + st * stage_step + woff;
-      return dbase + (st / SPT) * tstep + ((st % SPT) * SB + wv * 2) * kBlockBytes;
+    auto pair_blk = [&](int c) { return (wv * CPW + c) * 2; };
+    auto src_of = [&](int64_t st, int c) -> const unsigned char * {
+      const int bj = pair_blk(c);
+      if (st * SB + bj > jl) return last_src;
+      if constexpr (SPT == 1)
+        return dbase + st * stage_step + (int64_t)(bj / KBT) * tstep +
+               (int64_t)(bj % KBT) * kBlockBytes;
+      return dbase + (st / SPT) * tstep + ((st % SPT) * SB + bj) * kBlockBytes;
     };
-    // Copy this wave's 2 blocks of stage `st` into ring slot `slot`.
+    // Copy this wave's blocks of stage `st` into ring slot `slot`.
     auto issue = [&](int64_t st, int slot) {
-      copy2_to_lds(src_of(st), voff0, voff1,
-                   ring + (uint32_t)(slot * SB + wv * 2) * (uint32_t)kBlockBytes);
+#pragma unroll
+      for (int c = 0; c < CPW; ++c)
+        copy2_to_lds(src_of(st, c), voff0, voff1,
+                     ring + (uint32_t)(slot * SB + pair_blk(c)) * (uint32_t)kBlockBytes);
       if (filt) {
         // first tokens of the stage's tiles: lane l takes row l % 16 of the
         // stage's (l / 16)-th tile (clamped to the last tile)
@@ -585,28 +590,43 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
     // by a fixed step per stage (and per key tile when a tile spans several
     // stages) instead of being recomputed; stages past last_ok repeat the
     // last two blocks.
-    const int last_ok = jl >= wv * 2 ? (int)((jl - wv * 2) / SB) : -1;
+    int last_ok[CPW];
+    const unsigned char *next_src[CPW];
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) {
+      last_ok[c] = jl >= pair_blk(c) ? (int)((jl - pair_blk(c)) / SB) : -1;
+      next_src[c] = src_of(S - 1, c);
+    }
     int next_st = S - 1;  // next stage to copy
     int next_c = (S - 1) % SPT;  // its stage within its key tile
-    const unsigned char *next_src = src_of(S - 1);
     int next_slot = S - 1;    // its ring slot
     int cur_slot = 0;         // ring slot of the stage being consumed
     auto issue_next = [&]() {
-      if (filt || next_st > last_ok) {
+      if (filt) {
         issue(next_st, next_slot);
       } else {
-        copy2_to_lds(next_src, voff0, voff1,
-                     ring + (uint32_t)(next_slot * SB + wv * 2) * (uint32_t)kBlockBytes);
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) {
+          if (next_st > last_ok[c])
+            copy2_to_lds(last_src, voff0, voff1,
+                         ring + (uint32_t)(next_slot * SB + pair_blk(c)) * (uint32_t)kBlockBytes);
+          else
+            copy2_to_lds(next_src[c], voff0, voff1,
+                         ring + (uint32_t)(next_slot * SB + pair_blk(c)) * (uint32_t)kBlockBytes);
+        }
       }
       ++next_st;
-      if constexpr (SPT == 1) {
-        next_src += stage_step;
-      } else if (++next_c == SPT) {
-        next_c = 0;
-        next_src += tstep - (int64_t)(SPT - 1) * SB * kBlockBytes;
-      } else {
-        next_src += SB * kBlockBytes;
+      int64_t step = stage_step;
+      if constexpr (SPT > 1) {
+        if (++next_c == SPT) {
+          next_c = 0;
+          step = tstep - (int64_t)(SPT - 1) * SB * kBlockBytes;
+        } else {
+          step = (int64_t)SB * kBlockBytes;
+        }
       }
+#pragma unroll
+      for (int c = 0; c < CPW; ++c) next_src[c] += step;
       next_slot = next_slot == S - 1 ? 0 : next_slot + 1;
     };
     // Stage bookkeeping at the start of a key tile's c-th stage: this wave's
@@ -763,14 +783,19 @@ __device__ __forceinline__ void scan_mq_body(const ScanParams &p) {
   wc.publish();
 }
 
-template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
-__global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_main(ScanParams p) {
-  scan_mq_body<DT, QTW, KBT, CPQ, S, FILT>(p);
+// NWQ waves per workgroup: 4 (two workgroups per CU), or 1 holding the
+// whole batch (one wave per SIMD, up to 512 registers; four workgroups per
+// CU, none waiting at a barrier for another wave's candidates).
+template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT, int NWQ>
+__global__ void __launch_bounds__(NWQ * kWaveSize, NWQ == 4 ? 2 : 1)
+    dresd_scanmq_main(ScanParams p) {
+  scan_mq_body<DT, QTW, KBT, CPQ, S, FILT, NWQ>(p);
 }
 
-template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT>
-__global__ void __launch_bounds__(kScanThreads, 2) dresd_scanmq_sample(ScanParams p) {
-  scan_mq_body<DT, QTW, KBT, CPQ, S, FILT>(p);
+template <int DT, int QTW, int KBT, int CPQ, int S, bool FILT, int NWQ>
+__global__ void __launch_bounds__(NWQ * kWaveSize, NWQ == 4 ? 2 : 1)
+    dresd_scanmq_sample(ScanParams p) {
+  scan_mq_body<DT, QTW, KBT, CPQ, S, FILT, NWQ>(p);
 }
 
 // Copy one 1 KiB block at `src` into LDS at `lds` (lane l's 16 bytes to
@@ -1092,21 +1117,22 @@ __global__ void __launch_bounds__(256) dresd_query_operand(QopParams p) {
 
 // (QTW, KBT) pairs with QTW * KBT <= 32 (query operands <= 128 VGPRs), each
 // with its ring depth S.
-#define DRESD_MQ_CASE(DT, CPQ, QTW, KBT, S)                                               \
-  if (qtw == QTW && kbt == KBT) {                                                         \
-    *stages = S;                                                                          \
-    if (filtered)                                                                         \
-      return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S, true>        \
-                       : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S, true>;     \
-    return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S, false>         \
-                     : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S, false>;      \
+#define DRESD_MQ_CASE_W(DT, CPQ, QTW, KBT, S, NWQ)                                           \
+  if (qtw == QTW && kbt == KBT && nwq == NWQ) {                                             \
+    *stages = S;                                                                            \
+    if (filtered)                                                                           \
+      return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S, true, NWQ>     \
+                       : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S, true, NWQ>;  \
+    return main_pass ? (ScanKernel)dresd_scanmq_main<DT, QTW, KBT, CPQ, S, false, NWQ>      \
+                     : (ScanKernel)dresd_scanmq_sample<DT, QTW, KBT, CPQ, S, false, NWQ>;   \
   }
+#define DRESD_MQ_CASE(DT, CPQ, QTW, KBT, S) DRESD_MQ_CASE_W(DT, CPQ, QTW, KBT, S, 4)
 #define DRESD_MQ_ALL(DT, CPQ)                                                     \
   DRESD_MQ_CASE(DT, CPQ, 1, 4, 4) DRESD_MQ_CASE(DT, CPQ, 1, 8, 4)                 \
   DRESD_MQ_CASE(DT, CPQ, 1, 16, 4) DRESD_MQ_CASE(DT, CPQ, 1, 32, 6)               \
   DRESD_MQ_CASE(DT, CPQ, 2, 4, 4) DRESD_MQ_CASE(DT, CPQ, 2, 8, 4)                 \
   DRESD_MQ_CASE(DT, CPQ, 2, 16, 6) DRESD_MQ_CASE(DT, CPQ, 4, 4, 4)                \
-  DRESD_MQ_CASE(DT, CPQ, 4, 8, 6)
+  DRESD_MQ_CASE(DT, CPQ, 4, 8, 6) DRESD_MQ_CASE_W(DT, CPQ, 4, 8, 4, 1)
 
 // Tiled contraction, one query group (NQ = 1): main passes with 4 key
 // tiles per wave, 8 waves (3 stages: one query read per 32 key tiles) or 4
@@ -1150,14 +1176,16 @@ ScanKernel scan_tc_kernel_bf16(int qtw, int tpw, int nk, int nq, int stages, boo
 #endif
 
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 0
-ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, bool filtered, int *stages) {
+ScanKernel scan_mq_kernel_f16(int qtw, int kbt, bool main_pass, bool filtered, int *stages,
+                              int nwq) {
   DRESD_MQ_ALL(kF16, 1)
   return nullptr;
 }
 void *qop_kernel_f16() { return (void *)dresd_query_operand<kF16, 1>; }
 #endif
 #if !defined(DRESD_MQ_TU) || DRESD_MQ_TU == 1
-ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, bool filtered, int *stages) {
+ScanKernel scan_mq_kernel_bf16(int qtw, int kbt, bool main_pass, bool filtered, int *stages,
+                               int nwq) {
   DRESD_MQ_ALL(kBF16, 2)
   return nullptr;
 }

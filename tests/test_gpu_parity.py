@@ -177,6 +177,11 @@ MQ_EDGE = [
     ("bf16", 999, 64, 8, 999),        # k == N, two padded query tiles
     ("f16", 5000, 128, 600, 20),      # three groups of 256 queries
     ("f16", 90001, 128, 24, 300),     # published lists past 256 keys, 300 winners
+    # 256-dim keys at 2-4 query tiles: one wave per workgroup holds the batch
+    ("f16", 30011, 256, 64, 32),      # four query tiles
+    ("f16", 5003, 256, 20, 7),        # two query tiles padded to four
+    ("bf16", 8191, 256, 32, 16),      # bf16 two-part queries, four tiles
+    ("f16", 300, 256, 48, 100),       # 19 key tiles, fewer than workgroups; k near N
 ]
 
 
