@@ -144,6 +144,36 @@ def test_filtered_few_blocks_per_tile(gpu_lib, dt, N, d, B, k):
     say("  exact-order rate %.3f" % rep["exact_order_rate"])
 
 
+# 256-dim keys at two to four query tiles: one shared-key wave per workgroup
+# holds every query tile and filters each key tile against all of them.
+FILTERED_ONE_WAVE = [
+    # (dtype, N, d, B, k)
+    ("bf16", 9001, 256, 20, 12),   # two-part bf16 queries, three tiles padded to four
+    ("f16", 30011, 256, 64, 32),   # four query tiles
+]
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", FILTERED_ONE_WAVE,
+                         ids=["%s-N%d-d%d-B%d-k%d" % c for c in FILTERED_ONE_WAVE])
+def test_filtered_one_wave_shared_key(gpu_lib, dt, N, d, B, k):
+    from paper_2502_15572_amd import Index
+    say("filtered one-wave shared-key", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N + d * 19 + B * 5 + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    src = torch.randint(0, N, (B,), generator=gen)
+    q = x[src].to(torch.float64) + 0.05 * torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 4, (N, 3), generator=gen, dtype=torch.int32)  # ~1/4 of rows match
+    nt = cont[src, 0].numpy().astype(np.int32)
+    nt[2::5] = NO_ROW_TOKEN
+    ix = Index(x.to(DEV), cont.to(DEV))
+    assert ix.plan(B, k)["scan_kernel"] == "shared_key"
+    ix.close()
+    rep = run_filtered(x, cont, q, nt, k, dt)
+    say("  exact-order rate %.3f" % rep["exact_order_rate"])
+
+
 def test_filtered_all_rows_match_equals_unfiltered(gpu_lib):
     """A token every row starts with filters nothing: same result as the
     unfiltered search, bit for bit (shared-key scan and sampled passes)."""
