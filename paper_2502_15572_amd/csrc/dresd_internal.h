@@ -119,7 +119,10 @@ struct MergeParams {
   uint64_t *spill;           // [B][spill_cap] candidates past the LDS cache
   int64_t spill_cap;
   int B, k, C, G;
-  uint64_t *tau_out;         // sample mode: k-th best key per query (0 if < k)
+  uint64_t *tau_out;         // sample mode: k-th best key per query, else tau_fb (0 if none)
+  const uint64_t *tau_fb;    // sample mode: the bound the pass's sample falls back to (may be null)
+  uint64_t *spec_out;        // sample mode: spec_rank-th best key per query (may be null)
+  int spec_rank;             // 1 <= spec_rank <= k when spec_out is set
   int64_t *idx;              // final mode outputs
   float *score;
   int32_t *tokens;           // may be null

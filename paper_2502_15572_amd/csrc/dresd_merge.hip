@@ -178,7 +178,21 @@ __device__ uint64_t radix_kth(MergeShared &sh, Src src, uint32_t M, uint32_t kk)
 __device__ inline void write_result(const MergeParams &p, int b, const uint64_t *win,
                                     uint32_t kk, int tid, int nth) {
   if (!p.final_mode) {
-    if (tid == 0) p.tau_out[b] = (kk >= (uint32_t)p.k) ? win[p.k - 1] : 0ull;
+    // The k-th best key of any subset of the rows is a lower bound of the
+    // k-th best of all of them; a pass that found fewer than k keys at or
+    // above its (speculative) threshold keeps the bound it started from.
+    // The speculative key for the next pass is the spec_rank-th best found,
+    // never below the bound.
+    if (tid == 0) {
+      const uint64_t fb = p.tau_fb ? p.tau_fb[b] : 0ull;
+      uint64_t v = (kk >= (uint32_t)p.k) ? win[p.k - 1] : 0ull;
+      v = v > fb ? v : fb;
+      p.tau_out[b] = v;
+      if (p.spec_out) {
+        const uint64_t s = (kk >= (uint32_t)p.spec_rank) ? win[p.spec_rank - 1] : 0ull;
+        p.spec_out[b] = s > v ? s : v;
+      }
+    }
     return;
   }
   for (int r = tid; r < p.k; r += nth) {

@@ -175,6 +175,7 @@ struct Plan {
   int C = 0;                    // per-wave list capacity
   int CL = 0;                   // per-query LDS stage
   int64_t strides[3] = {0, 0, 0};  // sampled passes, sparsest first
+  int spec[3] = {0, 0, 0};         // rank of the speculative key each pass hands the next (0: none)
   int npass = 0;                   // sampled passes used
   ScanKernel kmain = nullptr, ksample = nullptr;
   size_t lds = 0, lds_s = 0;    // LDS bytes of the main and the sampled scans
@@ -240,6 +241,27 @@ dresd_status validate_search(const dresd_index *ix, int32_t B, int32_t k) {
   if (k < 1 || k > DRESD_K_MAX) return fail(DRESD_EINVAL, "k must be in [1, DRESD_K_MAX]");
   if ((int64_t)k > ix->N) return fail(DRESD_EINVAL, "k exceeds the number of keys");
   return DRESD_OK;
+}
+
+// Rank j of the key a sampled pass hands the next, denser pass as its
+// starting threshold.  The denser pass visits every tile of this one and
+// r - 1 others in each stretch of r, so each of its k best keys lies in this
+// pass's sample with probability 1/r; it finds fewer than k keys at or above
+// this sample's j-th best only if at least j of them do, which happens with
+// probability P[Binomial(k, 1/r) >= j].  The smallest j that keeps this at
+// most 1e-3 is taken.  When it happens the pass falls back to the exact
+// bound it would have started from, so results never depend on the choice.
+int spec_rank(int k, int64_t r) {
+  const double p = 1.0 / (double)r, q = 1.0 - p;
+  double pmf = 1.0;  // P[X = 0] = q^k
+  for (int i = 0; i < k; ++i) pmf *= q;
+  double below = 0.0;  // P[X < j]
+  for (int j = 1; j <= k; ++j) {
+    below += pmf;                                    // adds P[X = j - 1]
+    if (1.0 - below <= 1e-3) return j;
+    pmf *= (double)(k - j + 1) / (double)j * p / q;  // P[X = j]
+  }
+  return k;
 }
 
 dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = false,
@@ -444,14 +466,16 @@ dresd_status make_plan(dresd_index *ix, int B, int k, Plan &pl, bool filt = fals
         if (pl.tc) break;
       }
     }
+    for (int i = 0; i + 1 < pl.npass; ++i)
+      pl.spec[i] = spec_rank(k, pl.strides[i] / pl.strides[i + 1]);
   }
   // Lists end with at most k keys each, so a query never has more than
   // G_max * k merge candidates.
   pl.spill_cap = std::max<int64_t>(0, (int64_t)pl.G_max * k - kMergeCap);
   size_t nb = (size_t)pl.bl;
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
-  pl.off_tau = 0;
-  pl.off_lcnt = up(2 * kMaxGroup * 8);
+  pl.off_tau = 0;  // [2 levels][kMaxGroup] bounds, then [2 levels][kMaxGroup] speculative keys
+  pl.off_lcnt = up(4 * kMaxGroup * 8);
   pl.off_lkth = pl.off_lcnt + up(nb * pl.G_max * 4);
   pl.off_lfirst = pl.off_lkth + up(nb * pl.G_max * 8);
   pl.off_lists = pl.off_lfirst + up(nb * pl.G_max * 8);
@@ -938,12 +962,15 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
     mp.cont = ix->cont;
     mp.L = ix->L;
     mp.N = ix->N;
-    const uint64_t *tau_in = nullptr;
+    // tau_in: the exact bound from the last pass (keys at or above the k-th
+    // best of its sample); spec_in: the key a sampled pass starts from
+    // instead, at or above tau_in.  The main pass starts from tau_in.
+    const uint64_t *tau_in = nullptr, *spec_in = nullptr;
     int level = 0;
-    auto run_pass = [&](int64_t stride, bool main_pass) -> dresd_status {
+    auto run_pass = [&](int64_t stride, bool main_pass, int spec_rank_out) -> dresd_status {
       sp.stride = stride;
       sp.nvisit = ceil_div(ix->T, stride);
-      sp.tau = tau_in;
+      sp.tau = (main_pass || !spec_in) ? tau_in : spec_in;
       const int64_t wgs = pass_wgs(pl, gr, sp.nvisit, main_pass);
       const int threads = threads_of(pl, main_pass);
       sp.G = (int)(pl.mq ? wgs
@@ -966,6 +993,9 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       mp.G = sp.G;
       mp.final_mode = main_pass ? 1 : 0;
       mp.tau_out = tau + (size_t)(level & 1) * pl.bl;
+      mp.tau_fb = tau_in;
+      mp.spec_out = spec_rank_out > 0 ? tau + 2 * kMaxGroup + (size_t)(level & 1) * pl.bl : nullptr;
+      mp.spec_rank = spec_rank_out;
       mp.idx = idx + (size_t)gr.b0 * k;
       mp.score = score + (size_t)gr.b0 * k;
       mp.tokens = tokens ? tokens + (size_t)gr.b0 * k * ix->L : nullptr;
@@ -973,14 +1003,15 @@ dresd_status search_impl(dresd_index *ix, const float *queries, const int32_t *n
       DRESD_HIP(launch(merge_kernel_ptr(), dim3((unsigned)gr.nb), dim3(kMergeThreads), margs, 0,
                        nullptr, nullptr, main_pass && li == pl.nl - 1));
       tau_in = mp.tau_out;
+      spec_in = mp.spec_out;
       ++level;
       return DRESD_OK;
     };
     for (int pi = 0; pi < pl.npass; ++pi) {
-      s = run_pass(pl.strides[pi], false);
+      s = run_pass(pl.strides[pi], false, pl.spec[pi]);
       if (s != DRESD_OK) return s;
     }
-    s = run_pass(1, true);
+    s = run_pass(1, true, 0);
     if (s != DRESD_OK) return s;
   }
   if (e_all0) {
@@ -1273,6 +1304,9 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   mp.C = C;
   mp.G = G;
   mp.tau_out = nullptr;
+  mp.tau_fb = nullptr;
+  mp.spec_out = nullptr;
+  mp.spec_rank = 0;
   mp.idx = idx;
   mp.score = score;
   mp.tokens = tokens;
