@@ -373,6 +373,41 @@ def test_shared_key_scan_all_scores_equal(gpu_lib):
     assert (gi == np.arange(k)[None, :]).all()
 
 
+@pytest.mark.parametrize("period", [256, 4096])
+def test_sampled_pass_fallback_to_exact_bound(gpu_lib, period):
+    """Each sampled pass after the first starts from a speculative key (the
+    j-th best of the sparser sample, j < k).  Here every high-scoring row
+    lies in tiles at multiples of `period`, i.e. inside the sparser samples
+    only, so the denser passes find fewer than k keys at or above that key
+    (the last pass at period 256; both at 4096) and have to keep the exact
+    bound they started from.  The result must still be the exact top-k."""
+    say("sampled fallback", period)
+    N, d, B, k = 61441 * 16, 128, 128, 64  # 3 sampled passes: 4096 holds 16 tiles = 4k rows
+    gen = torch.Generator().manual_seed(period)
+    u = torch.randn(d, generator=gen, dtype=torch.float64)
+    u = u / u.norm()
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    tile = torch.arange(N) // 16
+    high = tile % period == 0
+    x[high] = u + 0.03 * x[high]
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(torch.float16)
+    q = u + 0.03 * torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    # every high row outscores every other row, for every query
+    sc = x.float() @ q.T
+    assert sc[high].min() > sc[~high].max() + 0.1
+    assert int(high.sum()) >= k
+    del sc
+    cont = torch.randint(0, 32000, (N, 2), generator=gen, dtype=torch.int32)
+    from paper_2502_15572_amd import Index
+    ix = Index(x.to(DEV), cont.to(DEV))
+    pl = ix.plan(B, k)
+    ix.close()
+    assert pl["scan_kernel"] == "shared_key" and pl["sample_passes"] == 3, pl
+    rep, (gi, _, _) = run_case(gpu_lib, x, cont, q, k, "f16")
+    assert high[torch.from_numpy(gi).flatten()].all()
+
+
 def test_all_negative_scores_never_return_padding(gpu_lib):
     """Keys in one half-space, queries in the other: every score is negative,
     so zero-scoring padding rows of the last tile would win if not masked."""
