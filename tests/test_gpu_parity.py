@@ -334,6 +334,63 @@ def test_tiled_contraction_random_shapes(gpu_lib, dt, N, d, B, k):
     run_case(gpu_lib, x, cont, q, k, dt, kind="tiled")
 
 
+def _random_ladder_cases(n, seed):
+    """Seeded random shapes for the shared-key scan with two or three
+    sampled passes, so that a pass starts from the previous one's
+    speculative key: the dense ladder (B*k >= 8192: strides 256 and 16,
+    and 4096 once the datastore has 16,384 tiles) and the sparse one
+    (strides 4096 and 64, at least 16,384 tiles), ragged row counts, f16 and
+    bf16, k up to 250."""
+    import random
+    rng = random.Random(seed)
+    out = []
+    while len(out) < n:
+        dt = rng.choice(["f16", "bf16"])
+        dense = len(out) % 2 == 0
+        if dense:
+            d = [256, 512, 128, 256][len(out) // 2 % 4]
+            B = rng.randint(64, 256 if dt == "f16" else 128)
+            k = rng.choice([32, 64, 100, 250])
+            if B * k < 8192:
+                continue
+            N = rng.randint(1024 * 16, 300000)
+            if k > (N // 16 // 256) * 4:
+                continue
+        else:
+            d = 128
+            B = rng.randint(17, 60)
+            k = rng.choice([5, 10, 16, 20])
+            if B * k >= 8192:
+                continue
+            N = rng.randint(16384 * 16 + 1, 330000)
+        if N * d * B <= 6e9:
+            out.append((dt, N, d, B, k))
+    return out
+
+
+LADDER_RANDOM = _random_ladder_cases(8, 77)
+
+
+@pytest.mark.parametrize("dt,N,d,B,k", LADDER_RANDOM,
+                         ids=["%s-N%d-d%d-B%d-k%d" % e for e in LADDER_RANDOM])
+def test_shared_key_sampled_ladders(gpu_lib, dt, N, d, B, k):
+    say("ladder random", dt, N, d, B, k)
+    gen = torch.Generator().manual_seed(N + d * 7 + B * 13 + k)
+    x = torch.randn(N, d, generator=gen, dtype=torch.float64)
+    x = (x / x.norm(dim=1, keepdim=True)).to(torch.float32).to(_TD[dt])
+    src = torch.randint(0, N, (B,), generator=gen)
+    q = x[src].to(torch.float64) + 0.3 * torch.randn(B, d, generator=gen, dtype=torch.float64)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.float32)
+    cont = torch.randint(0, 32000, (N, 2), generator=gen, dtype=torch.int32)
+    from paper_2502_15572_amd import Index
+    ix = Index(x.to(DEV), cont.to(DEV))
+    pl = ix.plan(B, k)
+    ix.close()
+    say("  plan", pl)
+    assert pl["scan_kernel"] == "shared_key" and pl["sample_passes"] >= 2, pl
+    run_case(gpu_lib, x, cont, q, k, dt)
+
+
 def test_grouped_launch_matches_split_batches(gpu_lib):
     """A batch whose single-tile groups share one launch returns, bit for
     bit, what the same queries return as separate batches of one group each
