@@ -345,6 +345,28 @@ dresd_status dresd_search_plan(const dresd_index *ix, int32_t B, int32_t k,
  *   device [B, S] int32, 1 <= S <= DRESD_K_MAX; entries outside [0, P) are
  *   ignored and repeats count once; next_tok: NULL, or device [B] int32 for
  *   the next-token filter.
+ * dresd_ivf_create_by_token: the next-token filter of Section 3.5 (a draft
+ *   that does not start with the next token is dropped) as a partitioning:
+ *   partition p holds the keys whose continuation starts with the p-th
+ *   smallest distinct first token (P = the number of distinct first tokens,
+ *   at most DRESD_PARTS_MAX); no centroids.  Arguments as in
+ *   dresd_index_create.  Copies everything and reads the first column of
+ *   `continuations` back to the host (synchronises `stream`); the grouping is
+ *   a host sort of the first tokens.  Errors as dresd_ivf_create.
+ *   dresd_ivf_search and dresd_ivf_search_filtered reject such an index
+ *   (EINVAL: no centroids); dresd_ivf_search_probes takes partition ids in
+ *   ascending token order.
+ * dresd_ivf_search_next_token: on an index from dresd_ivf_create_by_token,
+ *   the result of dresd_search_filtered (same keys compete, same ranking and
+ *   tie rule, exact top-k) computed by scanning only the query's next-token
+ *   partition: next_tok device [B] int32, any value (a token no key starts
+ *   with gives a fully padded row).  Its cost follows the probed partitions'
+ *   sizes, so it pays when the batch's next tokens together select fewer
+ *   keys than the datastore holds (small batches); the full filtered scan
+ *   reads every key once for the whole batch.  Scores come from the
+ *   three-part exact query split at every batch size (within the 1e-5 bound
+ *   of the small-batch scans).  Errors: EINVAL (NULLs, B < 0, k out of range,
+ *   an index not grouped by token), ENOMEM, EUNSUPPORTED, EDEVICE.
  * dresd_ivf_info: host outputs (NULL allowed); tiles = 16-row tiles of the
  *   partitioned layout (padding included).
  * dresd_ivf_profile_enable / _read: as dresd_profile_*, for the scan of the
@@ -368,6 +390,13 @@ dresd_status dresd_ivf_search_probes(dresd_ivf *ivf, const float *queries, const
                                      int32_t S, const int32_t *next_tok, int32_t B, int32_t k,
                                      int64_t *idx, float *score, int32_t *tokens,
                                      dresd_stream stream);
+dresd_status dresd_ivf_create_by_token(const void *embeddings, const int32_t *continuations,
+                                       int64_t N, int32_t d, int32_t L, int32_t dtype,
+                                       dresd_stream stream, dresd_ivf **out);
+dresd_status dresd_ivf_search_next_token(dresd_ivf *ivf, const float *queries,
+                                         const int32_t *next_tok, int32_t B, int32_t k,
+                                         int64_t *idx, float *score, int32_t *tokens,
+                                         dresd_stream stream);
 /*
  * Spherical k-means, the partitioning of the partitioned search (the
  * centroids and assignment that dresd_ivf_create takes).  Cosine similarity

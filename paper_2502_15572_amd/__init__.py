@@ -175,6 +175,49 @@ class PartitionedIndex:
             self.L, _dtype_code(keys), ctypes.c_void_p(centroids.data_ptr()), self.P,
             ctypes.c_void_p(assign.data_ptr()), _stream_handle(stream), ctypes.byref(self._h)))
 
+    @classmethod
+    def by_first_token(cls, keys, cont, stream=None):
+        """Keys grouped by the first token of their continuation (one
+        partition per distinct first token, in ascending token order, no
+        centroids), for ``search_next_token``.  Copies everything."""
+        import torch
+        for t in (keys, cont):
+            if not t.is_cuda:
+                raise ValueError("all inputs must be GPU tensors")
+        if keys.dim() != 2 or cont.dim() != 2 or cont.shape[0] != keys.shape[0]:
+            raise ValueError("keys must be [N, d] and continuations [N, L]")
+        if cont.dtype != torch.int32:
+            raise TypeError("continuations must be int32")
+        keys, cont = keys.contiguous(), cont.contiguous()
+        self = cls.__new__(cls)
+        self._lib = _lib.load()
+        self._h = ctypes.c_void_p()
+        self.N, self.d = int(keys.shape[0]), int(keys.shape[1])
+        self.L = int(cont.shape[1])
+        _lib.check(self._lib.dresd_ivf_create_by_token(
+            ctypes.c_void_p(keys.data_ptr()), ctypes.c_void_p(cont.data_ptr()), self.N, self.d,
+            self.L, _dtype_code(keys), _stream_handle(stream), ctypes.byref(self._h)))
+        self.P = self.info()["P"]
+        return self
+
+    def search_next_token(self, queries, next_tok, k: int, tokens: bool = True, out=None,
+                          stream=None):
+        """Next-token-filtered exact top-k (the result of ``Index.search``
+        with ``next_tok``) over an index from ``by_first_token``: each query
+        scans only the keys whose continuation starts with its next token
+        (``next_tok``, int32 GPU tensor [B])."""
+        q = self._check_q(queries)
+        B = int(q.shape[0])
+        nt = self._next_tok(next_tok, B)
+        if nt is None:
+            raise TypeError("next_tok is required")
+        idx, score, tok = _search_out(B, k, self.L, tokens, q.device, out)
+        _lib.check(self._lib.dresd_ivf_search_next_token(
+            self._h, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(nt.data_ptr()), B, int(k),
+            ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(score.data_ptr()),
+            ctypes.c_void_p(tok.data_ptr()) if tok is not None else None, _stream_handle(stream)))
+        return idx, score, tok
+
     def _check_q(self, queries):
         import torch
         if not queries.is_cuda or queries.dtype != torch.float32:

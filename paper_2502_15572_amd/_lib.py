@@ -22,7 +22,7 @@ EXPORTS = ["dresd_index_create", "dresd_search", "dresd_index_info", "dresd_inde
            "dresd_search_plan", "dresd_search_filtered", "dresd_transform",
            "dresd_pack_drafts", "dresd_ivf_create", "dresd_ivf_destroy", "dresd_ivf_info",
            "dresd_ivf_search", "dresd_ivf_search_filtered", "dresd_ivf_search_probes",
-           "dresd_ivf_profile_enable",
+           "dresd_ivf_create_by_token", "dresd_ivf_search_next_token", "dresd_ivf_profile_enable",
            "dresd_ivf_profile_read", "dresd_kmeans_assign", "dresd_kmeans_update",
            "dresd_kmeans_init", "dresd_bw_probe", "dresd_search_noalloc"]
 
@@ -63,6 +63,10 @@ def _declare(lib):
     lib.dresd_ivf_search_filtered.restype = ctypes.c_int
     lib.dresd_ivf_search_probes.argtypes = [P, P, P, I32, P, I32, I32, P, P, P, P]
     lib.dresd_ivf_search_probes.restype = ctypes.c_int
+    lib.dresd_ivf_create_by_token.argtypes = [P, P, I64, I32, I32, I32, P, ctypes.POINTER(P)]
+    lib.dresd_ivf_create_by_token.restype = ctypes.c_int
+    lib.dresd_ivf_search_next_token.argtypes = [P, P, P, I32, I32, P, P, P, P]
+    lib.dresd_ivf_search_next_token.restype = ctypes.c_int
     lib.dresd_ivf_profile_enable.argtypes = [P, I32]
     lib.dresd_ivf_profile_enable.restype = ctypes.c_int
     lib.dresd_ivf_profile_read.argtypes = [P, ctypes.POINTER(ctypes.c_double),

@@ -226,8 +226,10 @@ ScanKernel scan_parts_kernel(int dtype);  // partitioned search, one query per w
 // Probed segments of a partitioned search (dresd_parts.hip): one workgroup
 // per query turns its probe list into seg_off / seg_tile.
 struct SegParams {
-  const int64_t *probes64;   // [B][S] partition ids (one of the two is set)
+  const int64_t *probes64;   // [B][S] partition ids (one of the three is set)
   const int32_t *probes32;
+  const int32_t *tok;        // [P] ascending first tokens, partition p holding tok[p]; with
+  const int32_t *next_tok;   //   next_tok [B] each query probes its token's partition (S = 1)
   const int32_t *part_tile;  // [P + 1] first tile of each partition
   int32_t *seg_off, *seg_tile;
   int B, S, P;

@@ -2,7 +2,10 @@
 // inverted file): turn each query's probe list into the segments its scan
 // walks.  One workgroup per query, one thread per probe: ids outside [0, P)
 // and repeats of an earlier probe get an empty segment; a workgroup prefix
-// sum of the partitions' tile counts gives the segment offsets.
+// sum of the partitions' tile counts gives the segment offsets.  Keys grouped
+// by their value's first token (the next-token filter of Section 3.5 as a
+// partition) probe instead the one partition of the query's next token,
+// found among the sorted tokens by the workgroup.
 #include "dresd_device.h"
 
 namespace dresd {
@@ -14,10 +17,29 @@ constexpr int kSegThreads = 1024;
 __global__ void __launch_bounds__(kSegThreads) dresd_segments(SegParams p) {
   __shared__ int32_t pid[kSegThreads];
   __shared__ int32_t wsum[kSegThreads / kWaveSize];
+  __shared__ int32_t found;
   const int b = blockIdx.x;
   const int i = threadIdx.x, lane = i & 63, wid = i >> 6;
   int32_t id = -1;
-  if (i < p.S) {
+  if (p.tok) {
+    // Thread i owns the sorted tokens [lo, hi); the tokens are distinct, so
+    // at most one thread's range [tok[lo], tok[hi - 1]] holds t, and that
+    // thread scans its range for it.
+    const int32_t t = p.next_tok[b];
+    const int64_t chunk = ((int64_t)p.P + kSegThreads - 1) / kSegThreads;
+    const int64_t lo = (int64_t)i * chunk;
+    const int64_t hi = lo + chunk < (int64_t)p.P ? lo + chunk : (int64_t)p.P;
+    if (i == 0) found = -1;
+    __syncthreads();
+    if (lo < hi && p.tok[lo] <= t && t <= p.tok[hi - 1])
+      for (int64_t j = lo; j < hi; ++j)
+        if (p.tok[j] == t) {
+          found = (int32_t)j;
+          break;
+        }
+    __syncthreads();
+    if (i == 0) id = found;  // S == 1
+  } else if (i < p.S) {
     const size_t o = (size_t)b * p.S + i;
     const int64_t v = p.probes64 ? p.probes64[o] : (int64_t)p.probes32[o];
     id = (v >= 0 && v < p.P) ? (int32_t)v : -1;

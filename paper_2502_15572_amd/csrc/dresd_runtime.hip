@@ -1173,6 +1173,8 @@ struct dresd_ivf {
   uint32_t *slot_row = nullptr;  // [T * 16] row of each slot, kPadRow for padding
   int32_t *ftok_slot = nullptr;  // [T * 16] first token of each slot's value (0: padding)
   int32_t *part_tile = nullptr;  // [P + 1] first tile of each partition
+  int32_t *tok = nullptr;        // grouped by first token: [P] ascending, partition p's token
+  int64_t probe_tiles = 0;       // grouped by first token: size-biased mean tiles of a partition
   int32_t P = 0;
   // probe results (ids + scores) of a search, one buffer per stream
   std::map<hipStream_t, std::pair<unsigned char *, int64_t>> probe;
@@ -1188,6 +1190,7 @@ void ivf_free(dresd_ivf *v) {
   if (v->slot_row) (void)hipFree(v->slot_row);
   if (v->ftok_slot) (void)hipFree(v->ftok_slot);
   if (v->part_tile) (void)hipFree(v->part_tile);
+  if (v->tok) (void)hipFree(v->tok);
   for (auto &pb : v->probe)
     if (pb.second.first) (void)hipFree(pb.second.first);
   for (void *r : v->retired) (void)hipFree(r);
@@ -1197,8 +1200,9 @@ void ivf_free(dresd_ivf *v) {
 // Scan of the probed partitions + merge.  probes64 (from the centroid
 // search) or probes32 (caller's) is [B][S] on the device.
 dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *probes64,
-                          const int32_t *probes32, int32_t S, const int32_t *next_tok, int32_t B,
-                          int32_t k, int64_t *idx, float *score, int32_t *tokens, Launcher &launch) {
+                          const int32_t *probes32, const int32_t *tok_next, int32_t S,
+                          const int32_t *next_tok, int32_t B, int32_t k, int64_t *idx,
+                          float *score, int32_t *tokens, Launcher &launch) {
   dresd_index *ix = v->ix;
   hipStream_t st = launch.st;
   const int terms = ix->dtype == kF32 ? 1 : 4;  // the query as three exact 16-bit parts
@@ -1218,7 +1222,10 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   // (tens of MB), and one wave streams it slowly (its loads in flight bound
   // it), so short waves in large numbers finish first; the merge of their
   // lists costs less than longer waves do.
-  const int64_t avg_tiles = std::max<int64_t>(1, (int64_t)S * ix->T / v->P);
+  // Partitions of one first token each differ widely in size, and a query
+  // probes one in proportion to its rows: their size-biased mean.
+  const int64_t avg_tiles =
+      tok_next ? v->probe_tiles : std::max<int64_t>(1, (int64_t)S * ix->T / v->P);
   int64_t wgq = std::min<int64_t>(ceil_div(4LL * ix->cus, B), ceil_div(avg_tiles, 16));
   wgq = std::max<int64_t>(1, std::min<int64_t>(wgq, kMergeLists / 4));
   const int G = (int)wgq * (kScanThreads / kWaveSize);
@@ -1240,6 +1247,8 @@ dresd_status parts_search(dresd_ivf *v, const float *queries, const int64_t *pro
   SegParams gp;
   gp.probes64 = nullptr;
   gp.probes32 = probes32;
+  gp.tok = tok_next ? v->tok : nullptr;
+  gp.next_tok = tok_next;
   gp.part_tile = v->part_tile;
   gp.seg_off = reinterpret_cast<int32_t *>(ws + off_seg);
   gp.seg_tile = reinterpret_cast<int32_t *>(ws + off_tile);
@@ -1329,23 +1338,26 @@ dresd_status validate_ivf_search(const dresd_ivf *v, int32_t B, int32_t k) {
 
 extern "C" {
 
-static dresd_status ivf_create_impl(const void *embeddings, const int32_t *continuations, int64_t N,
-                              int32_t d, int32_t L, int32_t dtype, const float *centroids,
-                              int32_t P, const int32_t *assign, dresd_stream stream,
-                              dresd_ivf **out) {
-  if (!embeddings || !continuations || !centroids || !assign || !out)
-    return fail(DRESD_EINVAL, "NULL pointer argument");
+static dresd_status check_ivf_args(const void *embeddings, const int32_t *continuations,
+                                   int64_t N, int32_t d, int32_t L, int32_t dtype) {
+  if (!embeddings || !continuations) return fail(DRESD_EINVAL, "NULL pointer argument");
   if (N < 1 || N > DRESD_N_MAX) return fail(DRESD_EINVAL, "N out of range");
   if (d < 1 || d > 16384) return fail(DRESD_EINVAL, "d out of range");
   if (L < 1 || L > 4096) return fail(DRESD_EINVAL, "L out of range");
   if (dtype < DRESD_F32 || dtype > DRESD_BF16) return fail(DRESD_EINVAL, "unknown dtype");
-  if (P < 1 || P > DRESD_PARTS_MAX) return fail(DRESD_EINVAL, "P out of range");
-  hipStream_t st = static_cast<hipStream_t>(stream);
+  return DRESD_OK;
+}
+
+// The partitioned index of a host assignment a [N] (ids checked against
+// [0, P)); without centroids it has no centroid index, and its searches
+// take their probes from the caller.
+static dresd_status ivf_build(const void *embeddings, const int32_t *continuations, int64_t N,
+                              int32_t d, int32_t L, int32_t dtype, const float *centroids,
+                              int32_t P, std::vector<int32_t> &a, hipStream_t st,
+                              dresd_ivf **out) {
+  const dresd_stream stream = st;
   // Slot table: partitions in id order, each padded to whole tiles, rows of
   // a partition in row order (a stable counting sort of the assignment).
-  std::vector<int32_t> a((size_t)N);
-  DRESD_HIP(hipMemcpyAsync(a.data(), assign, (size_t)N * 4, hipMemcpyDeviceToHost, st));
-  DRESD_HIP(hipStreamSynchronize(st));
   std::vector<int64_t> cnt((size_t)P, 0);
   for (int64_t i = 0; i < N; ++i) {
     if (a[i] < 0 || a[i] >= P) return fail(DRESD_EINVAL, "assignment outside [0, P)");
@@ -1358,6 +1370,8 @@ static dresd_status ivf_create_impl(const void *embeddings, const int32_t *conti
     T += ceil_div(cnt[p], kTileRows);
   }
   pt[P] = (int32_t)T;
+  double sq = 0.0;  // sum over partitions of their tile counts squared
+  for (int32_t p = 0; p < P; ++p) sq += (double)(pt[p + 1] - pt[p]) * (double)(pt[p + 1] - pt[p]);
   std::vector<uint32_t> slot((size_t)T * kTileRows, kPadRow);
   std::vector<int64_t> next((size_t)P);
   for (int32_t p = 0; p < P; ++p) next[p] = (int64_t)pt[p] * kTileRows;
@@ -1368,6 +1382,7 @@ static dresd_status ivf_create_impl(const void *embeddings, const int32_t *conti
   dresd_ivf *v = new (std::nothrow) dresd_ivf();
   if (!v) return fail(DRESD_ENOMEM, "host allocation failed");
   v->P = P;
+  v->probe_tiles = std::max<int64_t>(1, (int64_t)(sq / (double)std::max<int64_t>(1, T)));
   auto bail = [&](dresd_status s) {
     ivf_free(v);
     return s;
@@ -1389,6 +1404,10 @@ static dresd_status ivf_create_impl(const void *embeddings, const int32_t *conti
   dresd_status s = index_build(embeddings, continuations, N, d, L, dtype, v->slot_row, T, stream,
                                &v->ix);
   if (s != DRESD_OK) return bail(s);
+  if (!centroids) {
+    *out = v;
+    return DRESD_OK;
+  }
   // Centroid index: fp32 keys, value = the partition id.
   std::vector<int32_t> ids((size_t)P);
   for (int32_t p = 0; p < P; ++p) ids[p] = p;
@@ -1408,6 +1427,57 @@ static dresd_status ivf_create_impl(const void *embeddings, const int32_t *conti
   return DRESD_OK;
 }
 
+static dresd_status ivf_create_impl(const void *embeddings, const int32_t *continuations, int64_t N,
+                              int32_t d, int32_t L, int32_t dtype, const float *centroids,
+                              int32_t P, const int32_t *assign, dresd_stream stream,
+                              dresd_ivf **out) {
+  if (!centroids || !assign || !out) return fail(DRESD_EINVAL, "NULL pointer argument");
+  dresd_status s = check_ivf_args(embeddings, continuations, N, d, L, dtype);
+  if (s != DRESD_OK) return s;
+  if (P < 1 || P > DRESD_PARTS_MAX) return fail(DRESD_EINVAL, "P out of range");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  std::vector<int32_t> a((size_t)N);
+  DRESD_HIP(hipMemcpyAsync(a.data(), assign, (size_t)N * 4, hipMemcpyDeviceToHost, st));
+  DRESD_HIP(hipStreamSynchronize(st));
+  return ivf_build(embeddings, continuations, N, d, L, dtype, centroids, P, a, st, out);
+}
+
+// Keys grouped by the first token of their value: partition p holds the
+// rows whose continuation starts with the p-th smallest distinct token.
+static dresd_status ivf_by_token_impl(const void *embeddings, const int32_t *continuations,
+                                      int64_t N, int32_t d, int32_t L, int32_t dtype,
+                                      dresd_stream stream, dresd_ivf **out) {
+  if (!out) return fail(DRESD_EINVAL, "NULL pointer argument");
+  dresd_status s = check_ivf_args(embeddings, continuations, N, d, L, dtype);
+  if (s != DRESD_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  std::vector<int32_t> a((size_t)N);  // first tokens, then their partitions
+  DRESD_HIP(hipMemcpy2DAsync(a.data(), 4, continuations, (size_t)L * 4, 4, (size_t)N,
+                             hipMemcpyDeviceToHost, st));
+  DRESD_HIP(hipStreamSynchronize(st));
+  std::vector<int32_t> tok(a);
+  std::sort(tok.begin(), tok.end());
+  tok.erase(std::unique(tok.begin(), tok.end()), tok.end());
+  if ((int64_t)tok.size() > DRESD_PARTS_MAX)
+    return fail(DRESD_EINVAL, "more distinct first tokens than DRESD_PARTS_MAX");
+  const int32_t P = (int32_t)tok.size();
+  for (int32_t &x : a) x = (int32_t)(std::lower_bound(tok.begin(), tok.end(), x) - tok.begin());
+  dresd_ivf *v = nullptr;
+  s = ivf_build(embeddings, continuations, N, d, L, dtype, nullptr, P, a, st, &v);
+  if (s != DRESD_OK) return s;
+  if (dev_alloc((void **)&v->tok, (size_t)P * 4) != hipSuccess) {
+    (void)hipGetLastError();
+    ivf_free(v);
+    return fail(DRESD_ENOMEM, "token table allocation failed");
+  }
+  if (hipMemcpy(v->tok, tok.data(), (size_t)P * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    ivf_free(v);
+    return fail(DRESD_EDEVICE, "token table upload failed");
+  }
+  *out = v;
+  return DRESD_OK;
+}
+
 dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuations, int64_t N,
                               int32_t d, int32_t L, int32_t dtype, const float *centroids,
                               int32_t P, const int32_t *assign, dresd_stream stream,
@@ -1416,6 +1486,16 @@ dresd_status dresd_ivf_create(const void *embeddings, const int32_t *continuatio
   try {
     return ivf_create_impl(embeddings, continuations, N, d, L, dtype, centroids, P, assign, stream,
                            out);
+  } catch (const std::bad_alloc &) {
+    return fail(DRESD_ENOMEM, "host allocation for the slot table failed");
+  }
+}
+
+dresd_status dresd_ivf_create_by_token(const void *embeddings, const int32_t *continuations,
+                                       int64_t N, int32_t d, int32_t L, int32_t dtype,
+                                       dresd_stream stream, dresd_ivf **out) {
+  try {
+    return ivf_by_token_impl(embeddings, continuations, N, d, L, dtype, stream, out);
   } catch (const std::bad_alloc &) {
     return fail(DRESD_ENOMEM, "host allocation for the slot table failed");
   }
@@ -1451,6 +1531,10 @@ dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *
                              int32_t *tokens, dresd_stream stream) {
   dresd_status s = validate_ivf_search(v, B, k);
   if (s != DRESD_OK) return s;
+  if (!v->cix)
+    return fail(DRESD_EINVAL,
+                "the index is grouped by first token and has no centroids to probe "
+                "(dresd_ivf_search_next_token searches it)");
   if (nprobe < 1 || nprobe > std::min<int32_t>(v->P, DRESD_K_MAX))
     return fail(DRESD_EINVAL, "nprobe must be in [1, min(P, DRESD_K_MAX)]");
   if (B > 0 && (!queries || !idx || !score)) return fail(DRESD_EINVAL, "NULL pointer argument");
@@ -1493,7 +1577,8 @@ dresd_status ivf_search_impl(dresd_ivf *v, const float *queries, const int32_t *
   if (s != DRESD_OK) return s;
   // 2. exact top-k over the probed partitions (its merge ends the search)
   launch.last = a1;
-  s = parts_search(v, queries, pid, nullptr, nprobe, next_tok, B, k, idx, score, tokens, launch);
+  s = parts_search(v, queries, pid, nullptr, nullptr, nprobe, next_tok, B, k, idx, score, tokens,
+                   launch);
   if (s != DRESD_OK) return s;
   if (a0) {
     if (launch.first_used != a0) ix->ev_free.push_back(a0);
@@ -1532,7 +1617,40 @@ dresd_status dresd_ivf_search_probes(dresd_ivf *v, const float *queries, const i
   if (B == 0) return DRESD_OK;
   Launcher launch;
   launch.st = static_cast<hipStream_t>(stream);
-  return parts_search(v, queries, nullptr, probes, S, next_tok, B, k, idx, score, tokens, launch);
+  return parts_search(v, queries, nullptr, probes, nullptr, S, next_tok, B, k, idx, score, tokens,
+                      launch);
+}
+
+dresd_status dresd_ivf_search_next_token(dresd_ivf *v, const float *queries,
+                                         const int32_t *next_tok, int32_t B, int32_t k,
+                                         int64_t *idx, float *score, int32_t *tokens,
+                                         dresd_stream stream) {
+  dresd_status s = validate_ivf_search(v, B, k);
+  if (s != DRESD_OK) return s;
+  if (!v->tok)
+    return fail(DRESD_EINVAL, "the index was not grouped by first token (dresd_ivf_create_by_token)");
+  if (B > 0 && (!queries || !next_tok || !idx || !score))
+    return fail(DRESD_EINVAL, "NULL pointer argument");
+  if (B == 0) return DRESD_OK;
+  Launcher launch;
+  launch.st = static_cast<hipStream_t>(stream);
+  dresd_index *ix = v->ix;
+  hipEvent_t a0 = nullptr, a1 = nullptr;
+  if (ix->prof) {
+    a0 = take_event(ix);
+    a1 = take_event(ix);
+    if (!a0 || !a1) return fail(DRESD_EDEVICE, "hipEventCreate failed");
+    DRESD_HIP(hipEventRecord(a0, launch.st));  // ahead of the token lookup
+    launch.last = a1;
+  }
+  s = parts_search(v, queries, nullptr, nullptr, next_tok, 1, nullptr, B, k, idx, score, tokens,
+                   launch);
+  if (s != DRESD_OK) return s;
+  if (a0) {
+    ix->ev_all.push_back(a0);
+    ix->ev_all.push_back(a1);
+  }
+  return DRESD_OK;
 }
 
 dresd_status dresd_kmeans_assign(const void *x, int64_t n, int32_t d, int32_t dtype,
