@@ -414,6 +414,110 @@ def time_partitioned(args):
     ivf.close()
 
 
+def time_token_groups(args):
+    """Next-token-filtered search over keys grouped by the first token of
+    their continuation: each query's next token is its source row's first
+    token (as with --filtered), and each query scans only that token's group.
+    The same batches also run through the full filtered scan, for the
+    comparison and the agreement of the two results.  The scan bandwidth
+    counts the bytes of the probed groups' keys (padding rows included)."""
+    import torch
+    from datagen import WORKLOADS, generate
+    from paper_2502_15572_amd import Index, PartitionedIndex
+    w = WORKLOADS[args.workload]
+    if args.n:
+        w = w.scaled(args.n)
+    k = args.k or w.k
+    B = args.batch
+    w = w.with_pool(B)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t0 = time.time()
+    g = generate(w, dev)
+    keys, cont, pool = g["keys"], g["cont"], g["queries"]
+    torch.cuda.synchronize()
+    log("generated %s N=%d d=%d %s in %.1fs" % (w.name, w.N, w.d, w.dtype, time.time() - t0))
+    log("grouping the keys by first token ...")
+    t0 = time.time()
+    tix = PartitionedIndex.by_first_token(keys, cont)
+    build_s = time.time() - t0
+    info = tix.info()
+    log("grouped by first token: %d groups, %d tiles, built in %.2fs"
+        % (info["P"], info["tiles"], build_s))
+    nb = max(1, pool.shape[0] // B)
+    batches = [pool[i * B:(i + 1) * B].contiguous() for i in range(nb)]
+    assert all(b.shape[0] == B for b in batches), "query pool smaller than the batch"
+    c0 = cont[:, 0]
+    frequent = int(torch.mode(c0[: min(w.N, 1 << 20)]).values)
+    src = g["query_src"]
+    nt = torch.where(src >= 0, c0[src.clamp(min=0)], torch.full_like(src, frequent))
+    nt = nt.to(torch.int32)
+    nts = [nt[i * B:(i + 1) * B].contiguous() for i in range(nb)]
+    vals, counts = torch.unique(c0, return_counts=True)
+    padded = (counts + 15) // 16 * 16
+    pos = torch.searchsorted(vals, nt[: nb * B]).clamp(max=vals.numel() - 1)
+    rows = torch.where(vals[pos] == nt[: nb * B], padded[pos], torch.zeros_like(padded[pos]))
+    probe_rows = float(rows.float().mean())
+    exact = Index(keys, cont)
+    out_t = _search_buffers(B, k, w.L, dev)
+    out_e = _search_buffers(B, k, w.L, dev)
+    same, total = 0, 0
+    for i, b in enumerate(batches):
+        tix.search_next_token(b, nts[i], k, out=out_t)
+        exact.search(b, k, out=out_e, next_tok=nts[i])
+        same += int((out_t[0] == out_e[0]).all(dim=1).sum())
+        total += B
+
+    def timed(fn, prof_on, prof_read):
+        for i in range(args.warmup):
+            fn(i)
+        torch.cuda.synchronize()
+        prof_on(True)
+        prof_read()
+        t1 = time.perf_counter()
+        for i in range(args.steps):
+            fn(i)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t1
+        prof = prof_read()
+        prof_on(False)
+        p50, _ = search_latency(fn, args.steps)
+        return args.steps * B / el, p50, prof
+
+    qps_t, p50_t, prof_t = timed(
+        lambda i: tix.search_next_token(batches[i % nb], nts[i % nb], k, out=out_t),
+        tix.profile, tix.profile_read)
+    qps_e, p50_e, prof_e = timed(
+        lambda i: exact.search(batches[i % nb], k, out=out_e, next_tok=nts[i % nb]),
+        exact.profile, exact.profile_read)
+    scan_ms = prof_t["scan_ms"] / max(1, prof_t["searches"])
+    search_ms = prof_t["search_ms"] / max(1, prof_t["searches"])
+    scan_bytes = probe_rows * B * w.d * w.elem_bytes
+    print(json.dumps({
+        "token_groups": {"workload": w.name, "N": w.N, "d": w.d, "key_dtype": w.dtype, "B": B,
+                         "k": k, "groups": info["P"], "queries_per_s": qps_t,
+                         "p50_latency_us": p50_t * 1e3, "scan_ms": scan_ms,
+                         "search_ms": search_ms, "probed_rows_per_query": probe_rows,
+                         "probed_fraction": probe_rows / w.N,
+                         "scan_GBps": scan_bytes / (scan_ms * 1e-3) / 1e9,
+                         "scan_hbm_frac": scan_bytes / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                         "same_result_as_full_scan": same / max(1, total),
+                         "full_filtered_scan": {"queries_per_s": qps_e,
+                                                "p50_latency_us": p50_e * 1e3,
+                                                "search_ms": prof_e["search_ms"]
+                                                / max(1, prof_e["searches"])},
+                         "speedup_p50": p50_e / p50_t, "index_build_s": build_s}}), flush=True)
+    exact.close()
+    tix.close()
+
+
+def _search_buffers(B, k, L, dev):
+    import torch
+    return (torch.empty((B, k), dtype=torch.int64, device=dev),
+            torch.empty((B, k), dtype=torch.float32, device=dev),
+            torch.empty((B, k, L), dtype=torch.int32, device=dev))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -434,6 +538,9 @@ def main():
                     help="next-token-filtered search: each query's next token is the first "
                          "token of its source row's continuation (the most frequent first "
                          "token for queries without a source row)")
+    ap.add_argument("--token-groups", action="store_true",
+                    help="only time the next-token-filtered search over keys grouped by first "
+                         "token (next tokens as with --filtered), beside the full filtered scan")
     ap.add_argument("--transform", type=int, default=0, metavar="D",
                     help="only time the query-side transform: B rows of D fp32 dims projected "
                          "to the workload's d (Eq. 1, Section 3.3, Eq. 2)")
@@ -479,6 +586,9 @@ def main():
         return
     if args.ivf:
         time_partitioned(args)
+        return
+    if args.token_groups:
+        time_token_groups(args)
         return
     if args.drafts:
         time_drafts(args)

@@ -235,6 +235,9 @@ struct SegParams {
   int B, S, P;
 };
 hipError_t launch_segments(const SegParams &p, hipStream_t st);
+// out[i] = cont[i][0], the first token of row i's value.
+hipError_t launch_first_tokens(const int32_t *cont, int L, int64_t n, int32_t *out,
+                               hipStream_t st);
 // ftok[s] = first token of slot s's value (0 for padding slots).
 hipError_t launch_slot_first_tokens(const uint32_t *slot_row, const int32_t *cont, int L,
                                     int64_t nslot, int32_t *ftok, hipStream_t st);

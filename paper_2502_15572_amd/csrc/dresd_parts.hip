@@ -86,7 +86,23 @@ __global__ void __launch_bounds__(256) dresd_slot_first_tokens(const uint32_t *s
   }
 }
 
+// First token of each row's value: out[i] = cont[i][0].
+__global__ void __launch_bounds__(256) dresd_first_tokens(const int32_t *cont, int L, int64_t n,
+                                                          int32_t *out) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = cont[i * L];
+}
+
 }  // namespace
+
+hipError_t launch_first_tokens(const int32_t *cont, int L, int64_t n, int32_t *out,
+                               hipStream_t st) {
+  const int64_t want = (n + 255) / 256;
+  const unsigned blocks = (unsigned)(want < 65536 ? (want > 0 ? want : 1) : 65536);
+  hipLaunchKernelGGL(dresd_first_tokens, dim3(blocks), dim3(256), 0, st, cont, L, n, out);
+  return hipGetLastError();
+}
 
 hipError_t launch_slot_first_tokens(const uint32_t *slot_row, const int32_t *cont, int L,
                                     int64_t nslot, int32_t *ftok, hipStream_t st) {

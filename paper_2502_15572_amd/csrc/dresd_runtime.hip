@@ -1452,9 +1452,19 @@ static dresd_status ivf_by_token_impl(const void *embeddings, const int32_t *con
   if (s != DRESD_OK) return s;
   hipStream_t st = static_cast<hipStream_t>(stream);
   std::vector<int32_t> a((size_t)N);  // first tokens, then their partitions
-  DRESD_HIP(hipMemcpy2DAsync(a.data(), 4, continuations, (size_t)L * 4, 4, (size_t)N,
-                             hipMemcpyDeviceToHost, st));
-  DRESD_HIP(hipStreamSynchronize(st));
+  {
+    // gathered on the device, then one contiguous copy
+    int32_t *col = nullptr;
+    if (dev_alloc((void **)&col, (size_t)N * 4) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(DRESD_ENOMEM, "first-token column allocation failed");
+    }
+    hipError_t e = launch_first_tokens(continuations, L, N, col, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(a.data(), col, (size_t)N * 4, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    (void)hipFree(col);
+    if (e != hipSuccess) return fail(DRESD_EDEVICE, std::string("first-token column: ") + hipGetErrorString(e));
+  }
   std::vector<int32_t> tok(a);
   std::sort(tok.begin(), tok.end());
   tok.erase(std::unique(tok.begin(), tok.end()), tok.end());
