@@ -255,12 +255,17 @@ def time_pipeline(args):
         cents, _ = train_partitions(sample, args.ivf, iters=args.train_iters, seed=2)
         ix = PartitionedIndex(keys, cont, cents, kmeans_assign(keys, cents))
         search = lambda y, nt, out: ix.search(y, k, nprobe, out=out, next_tok=nt)
+        kind = "partitioned P=%d nprobe=%d" % (args.ivf, nprobe)
+    elif args.token_groups:
+        ix = PartitionedIndex.by_first_token(keys, cont)
+        search = lambda y, nt, out: ix.search_next_token(y, nt, k, out=out)
+        kind = "exact, keys grouped by first token"
     else:
         ix = Index(keys, cont)
         search = lambda y, nt, out: ix.search(y, k, out=out, next_tok=nt)
+        kind = "exact"
     torch.cuda.synchronize()
-    log("index ready: %s, %s" % (w.name, "partitioned P=%d nprobe=%d" % (args.ivf, nprobe)
-                                  if args.ivf else "exact"))
+    log("index ready: %s, %s" % (w.name, kind))
     gen = torch.Generator(device="cuda").manual_seed(0)
     xs = torch.randn(64, B, D, device=dev, generator=gen)
     mean = torch.randn(D, device=dev, generator=gen)
@@ -294,7 +299,7 @@ def time_pipeline(args):
     p50, _ = search_latency(step, args.steps)
     print(json.dumps({"pipeline": {
         "workload": w.name, "N": w.N, "d": w.d, "D": D, "B": B, "k": k, "drafts": r,
-        "search": ("partitioned P=%d nprobe=%d" % (args.ivf, nprobe)) if args.ivf else "exact",
+        "search": kind,
         "steps_per_s": args.steps / el, "queries_per_s": args.steps * B / el,
         "p50_us": p50 * 1e3,
         "mean_drafts_kept": float(dout[1].float().mean())}}), flush=True)
@@ -540,7 +545,8 @@ def main():
                          "token for queries without a source row)")
     ap.add_argument("--token-groups", action="store_true",
                     help="only time the next-token-filtered search over keys grouped by first "
-                         "token (next tokens as with --filtered), beside the full filtered scan")
+                         "token (next tokens as with --filtered), beside the full filtered scan; "
+                         "with --pipeline, the step's search")
     ap.add_argument("--transform", type=int, default=0, metavar="D",
                     help="only time the query-side transform: B rows of D fp32 dims projected "
                          "to the workload's d (Eq. 1, Section 3.3, Eq. 2)")

@@ -24,8 +24,9 @@ def hidden(rng, n, D, centres):
     return (centres[a] + 0.4 * rng.standard_normal((n, D))).astype(np.float32)
 
 
-@pytest.mark.parametrize("partitioned", [False, True], ids=["exact", "partitioned"])
-def test_decode_step_chain(gpu_lib, partitioned):
+@pytest.mark.parametrize("mode", ["exact", "partitioned", "token_groups"])
+def test_decode_step_chain(gpu_lib, mode):
+    partitioned = mode == "partitioned"
     from paper_2502_15572_amd import Index, PartitionedIndex, pack_drafts, transform
     rng = np.random.default_rng(5)
     N, D, l, L, B, k, r = 20000, 256, 64, 6, 12, 40, 8
@@ -56,6 +57,9 @@ def test_decode_step_chain(gpu_lib, partitioned):
         p_idx, p_sc, _, _ = oracle.topk(c32, "f32", q_or, S + 1)
         sel = np.nonzero(p_sc[:, S - 1] - p_sc[:, S] >= 1e-5)[0]
         probes = p_idx[:, :S].astype(np.int32)
+    elif mode == "token_groups":
+        ix = PartitionedIndex.by_first_token(t(keys), t(cont))
+        sel = np.arange(B)
     else:
         ix = Index(t(keys), t(cont))
         sel = np.arange(B)
@@ -63,6 +67,8 @@ def test_decode_step_chain(gpu_lib, partitioned):
     y = transform(t(xq), t(mean), t(var), t(W))
     if partitioned:
         gi, gs, gt = ix.search(y, k, S, next_tok=t(nt))
+    elif mode == "token_groups":
+        gi, gs, gt = ix.search_next_token(y, t(nt), k)
     else:
         gi, gs, gt = ix.search(y, k, next_tok=t(nt))
     drafts, count = pack_drafts(gt, r, L)
