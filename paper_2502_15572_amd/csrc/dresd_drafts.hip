@@ -10,6 +10,7 @@
 // of all earlier ranks (exact comparison on a hash match), and a workgroup
 // prefix sum over the kept flags gives every kept draft its row.
 #include "dresd_device.h"
+#include "dresd_ops.h"
 
 namespace dresd {
 

@@ -18,6 +18,7 @@
 //            through the row order from a seeded offset, each scaled to unit
 //            length.
 #include "dresd_device.h"
+#include "dresd_ops.h"
 
 namespace dresd {
 

@@ -10,6 +10,7 @@
 // list summaries, then all listed keys at once (flattened over lists), and
 // radix selections that start at the highest bit where the keys differ.
 #include "dresd_device.h"
+#include "dresd_ops.h"
 
 namespace dresd {
 

@@ -7,6 +7,7 @@
 // partition) probe instead the one partition of the query's next token,
 // found among the sorted tokens by the workgroup.
 #include "dresd_device.h"
+#include "dresd_ops.h"
 
 namespace dresd {
 

@@ -14,6 +14,7 @@
 #include <math.h>
 
 #include "dresd_internal.h"
+#include "dresd_ops.h"
 
 using namespace dresd;
 

@@ -15,6 +15,7 @@
 // workspace; a second kernel adds them in a fixed order (deterministic) and
 // scales every row to unit length.
 #include "dresd_device.h"
+#include "dresd_ops.h"
 
 namespace dresd {
 
