@@ -10,9 +10,12 @@ Default workload: 1,048,576 keys x 4096 dims bf16 (a 7B model's hidden width),
 continuations [N,10], B = 1 query per step, k = 10.  The default run also
 measures, in the same JSON line under "secondary", the 33.5M x 128 f16
 datastore at B = 1 and B = 128 (k = 100) and the 10M x 256 f16 datastore at
-B = 256 (k = 32), each with its own roofline block; the achievable read
-bandwidth of the device (a probe with the scans' access pattern) is measured
-on the same run and each bandwidth is also given as a fraction of it.  The
+B = 256 (k = 32), each with its own roofline block, and under
+"filtered_token_groups" the next-token-filtered search of the 33.5M-key
+datastore grouped by first token at B = 1 beside the full filtered scan.  The
+achievable read bandwidth of the device (a probe with the scans' access
+pattern) is measured on the same run and each bandwidth is also given as a
+fraction of it.  The
 CPU-baseline leg times the oracle and checks query 0 of every measured
 workload against it (outside the timed regions).
 """
@@ -106,30 +109,36 @@ def copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
 
 
-def cpu_baseline_leg(keys_dev, cont_dev, queries, k, device_result, budget_s=12.0, time_it=True):
+def cpu_baseline_leg(keys_dev, cont_dev, queries, k, device_result, budget_s=12.0, time_it=True,
+                     next_tok=None):
     """The oracle (untuned) on this host's cores.  Checks the device's result
     for queries[0] against the oracle's exact top-k (rules R1-R7 of the
-    parity tests; outside every timed region) and, with ``time_it``, times
+    parity tests; outside every timed region; with ``next_tok``, the
+    next-token-filtered top-k for next_tok[0]) and, with ``time_it``, times
     single-query oracle searches over a bounded sample.  Returns
     (cpu_baseline dict or None, parity dict)."""
     import numpy as np
     import oracle
     from datagen import to_numpy_bits
     sys.path.insert(0, os.path.join(ROOT, "tests"))
-    from parity import TOL, ParityError, check_query
+    from parity import TOL, ParityError, check_query, check_query_filtered
     threads = len(os.sched_getaffinity(0))
     t0 = time.time()
     kb, dt = to_numpy_bits(keys_dev)
     cont = cont_dev.cpu().numpy()
     log("cpu_baseline: host copy of keys %.1fs" % (time.time() - t0))
     q = queries.cpu().numpy().astype(np.float32)
-    o_idx, o_score, _, o_next = oracle.topk(kb, dt, q[:1], k, cont, threads=threads)
+    nt0 = None if next_tok is None else int(next_tok[0])
+    o_idx, o_score, _, o_next = oracle.topk(kb, dt, q[:1], k, cont, threads=threads,
+                                            next_tok=None if nt0 is None else [nt0])
     g_idx, g_score, g_tok = (t[0].cpu().numpy() for t in device_result)
-    parity = {"queries_checked": 1, "against": "oracle exact top-k (fp64 sums rounded once)"}
+    parity = {"queries_checked": 1, "against": "oracle exact top-k (fp64 sums rounded once)"
+              + ("" if nt0 is None else ", next-token filtered")}
     try:
-        rep = check_query(g_idx, g_score, g_tok, o_idx[0], o_score[0], o_next[0],
-                          lambda rows: oracle.score_rows(kb, dt, q[0], rows), kb.shape[0], cont,
-                          TOL[dt])
+        args = (g_idx, g_score, g_tok, o_idx[0], o_score[0], o_next[0],
+                lambda rows: oracle.score_rows(kb, dt, q[0], rows), kb.shape[0], cont)
+        rep = (check_query(*args, TOL[dt]) if nt0 is None
+               else check_query_filtered(*args, nt0, TOL[dt]))
         parity.update({"verdict": "pass", "tol": TOL[dt], "exact_order": rep["exact_order"],
                        "max_abs_vs_exact": rep["max_abs_vs_exact"]})
     except ParityError as e:
@@ -421,22 +430,31 @@ def time_partitioned(args):
 
 def time_token_groups(args):
     """Next-token-filtered search over keys grouped by the first token of
-    their continuation: each query's next token is its source row's first
-    token (as with --filtered), and each query scans only that token's group.
-    The same batches also run through the full filtered scan, for the
-    comparison and the agreement of the two results.  The scan bandwidth
-    counts the bytes of the probed groups' keys (padding rows included)."""
+    their continuation (see token_groups_result); prints one JSON line."""
     import torch
-    from datagen import WORKLOADS, generate
-    from paper_2502_15572_amd import Index, PartitionedIndex
+    from datagen import WORKLOADS
     w = WORKLOADS[args.workload]
     if args.n:
         w = w.scaled(args.n)
-    k = args.k or w.k
-    B = args.batch
-    w = w.with_pool(B)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    r = token_groups_result(w, args.batch, args.k or w.k, args, dev,
+                            cpu=not args.no_cpu_baseline and not args.n)
+    print(json.dumps({"token_groups": r}), flush=True)
+
+
+def token_groups_result(w, B, k, args, dev, cpu=False):
+    """Each query's next token is its source row's first token (as with
+    --filtered), and each query scans only that token's group of keys.  The
+    same batches also run through the full filtered scan, for the comparison
+    and the agreement of the two results.  The scan bandwidth counts the
+    bytes of the probed groups' keys (padding rows included).  With ``cpu``,
+    query 0's grouped result is checked against the oracle's filtered top-k
+    (outside the timed regions)."""
+    import torch
+    from datagen import generate
+    from paper_2502_15572_amd import Index, PartitionedIndex
+    w = w.with_pool(B)
     t0 = time.time()
     g = generate(w, dev)
     keys, cont, pool = g["keys"], g["cont"], g["queries"]
@@ -498,22 +516,26 @@ def time_token_groups(args):
     scan_ms = prof_t["scan_ms"] / max(1, prof_t["searches"])
     search_ms = prof_t["search_ms"] / max(1, prof_t["searches"])
     scan_bytes = probe_rows * B * w.d * w.elem_bytes
-    print(json.dumps({
-        "token_groups": {"workload": w.name, "N": w.N, "d": w.d, "key_dtype": w.dtype, "B": B,
-                         "k": k, "groups": info["P"], "queries_per_s": qps_t,
-                         "p50_latency_us": p50_t * 1e3, "scan_ms": scan_ms,
-                         "search_ms": search_ms, "probed_rows_per_query": probe_rows,
-                         "probed_fraction": probe_rows / w.N,
-                         "scan_GBps": scan_bytes / (scan_ms * 1e-3) / 1e9,
-                         "scan_hbm_frac": scan_bytes / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-                         "same_result_as_full_scan": same / max(1, total),
-                         "full_filtered_scan": {"queries_per_s": qps_e,
-                                                "p50_latency_us": p50_e * 1e3,
-                                                "search_ms": prof_e["search_ms"]
-                                                / max(1, prof_e["searches"])},
-                         "speedup_p50": p50_e / p50_t, "index_build_s": build_s}}), flush=True)
+    res = {"workload": w.name, "N": w.N, "d": w.d, "key_dtype": w.dtype, "B": B, "k": k,
+           "metric": "next-token-filtered retrieval over keys grouped by first token",
+           "groups": info["P"], "queries_per_s": qps_t, "p50_latency_us": p50_t * 1e3,
+           "scan_kernel": "dresd_scan_parts", "scan_ms": scan_ms, "search_ms": search_ms,
+           "probed_rows_per_query": probe_rows, "probed_fraction": probe_rows / w.N,
+           "scan_GBps": scan_bytes / (scan_ms * 1e-3) / 1e9,
+           "scan_hbm_frac": scan_bytes / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+           "same_result_as_full_scan": same / max(1, total),
+           "full_filtered_scan": {"queries_per_s": qps_e, "p50_latency_us": p50_e * 1e3,
+                                  "search_ms": prof_e["search_ms"] / max(1, prof_e["searches"])},
+           "speedup_p50": p50_e / p50_t, "index_build_s": build_s}
     exact.close()
+    if cpu:
+        checked = tuple(t.clone() for t in tix.search_next_token(batches[0], nts[0], k))
+        torch.cuda.synchronize()
+        log("oracle on the host (%s B=%d, grouped by first token) ..." % (w.name, B))
+        _, res["parity"] = cpu_baseline_leg(keys, cont, batches[0], k, checked, time_it=False,
+                                            next_tok=nts[0].cpu().tolist())
     tix.close()
+    return res
 
 
 def _search_buffers(B, k, L, dev):
@@ -627,6 +649,10 @@ def main():
         if cache.get("ix") is not None:
             cache["ix"].close()
         cache.clear()
+        torch.cuda.empty_cache()
+        wf = WORKLOADS[FILTERED_SECONDARY[0]]
+        res["filtered_token_groups"] = token_groups_result(wf, FILTERED_SECONDARY[1], wf.k, args,
+                                                           dev, cpu=want_cpu)
     print(json.dumps(res), flush=True)
 
 
@@ -636,6 +662,9 @@ def main():
 # regime).
 SECONDARY = [("zipf33m_d128_f16", 1), ("zipf33m_d128_f16", 128), ("hidden1m_d4096_bf16", 64),
              ("batch10m_d256_f16", 256)]
+# and the next-token-filtered search over the same 33.5M-key datastore grouped
+# by first token, at one query per step, beside the full filtered scan
+FILTERED_SECONDARY = ("zipf33m_d128_f16", 1)
 
 
 def measure(w, B, k, args, dev, probe=False, cpu=False, time_cpu=False, measured_peak=None,
