@@ -78,16 +78,28 @@ def search(lib, h, q, out):
 
 @pytest.fixture(scope="module", autouse=True)
 def warm(gpu_lib):
-    """One full cycle first, so that the library's kernels are loaded before
-    any free-memory comparison."""
-    x, cont, q = datastore(N=4096)
+    """One full cycle of every path first, at the shapes the tests use (a
+    search's plan queries its kernels, and the first query of a kernel loads
+    it), so that no free-memory comparison sees a kernel's first use."""
+    x, cont, q = datastore()
     st, h = create(gpu_lib, x, cont)
     assert st == OK
-    st, _ = search(gpu_lib, h, q[:8], outputs(8, 16, cont.shape[1]))
+    st, _ = search(gpu_lib, h, q[:8], outputs(8, 16, cont.shape[1]))  # sampled pass + main pass
     assert st == OK
     gpu_lib.dresd_index_destroy(h)
+    x, cont, q = datastore(N=1 << 16)
     st, h = ivf_create(gpu_lib, x, cont)
     assert st == OK
+    idx, score, tok = outputs(4, 10, cont.shape[1])
+    assert gpu_lib.dresd_ivf_search(h, P(q.data_ptr()), 4, 10, 8, P(idx.data_ptr()),
+                                    P(score.data_ptr()), P(tok.data_ptr()), None) == OK
+    gpu_lib.dresd_ivf_destroy(h)
+    st, h = token_create(gpu_lib, x, cont)
+    assert st == OK
+    nt = cont[:4, 0].contiguous()
+    assert gpu_lib.dresd_ivf_search_next_token(h, P(q.data_ptr()), P(nt.data_ptr()), 4, 10,
+                                               P(idx.data_ptr()), P(score.data_ptr()),
+                                               P(tok.data_ptr()), None) == OK
     gpu_lib.dresd_ivf_destroy(h)
     torch.cuda.synchronize()
 
@@ -134,9 +146,11 @@ def test_search_workspace_allocation_failure(gpu_lib):
     after_create = free_bytes()
     with fail_alloc_at(1):
         st, out = search(gpu_lib, h, q[:8], out)
+    # read before the checks below, whose torch temporaries may map memory of their own
+    after_fail = free_bytes()
     assert st == ENOMEM, gpu_lib.dresd_last_error()
     assert untouched(out)
-    assert free_bytes() == after_create
+    assert after_fail == after_create
     st, out = search(gpu_lib, h, q[:8], out)
     assert st == OK and (out[0] >= 0).all()
     gpu_lib.dresd_index_destroy(h)
@@ -186,6 +200,60 @@ def test_ivf_create_allocation_count(gpu_lib):
     assert st == OK
     gpu_lib.dresd_ivf_destroy(h)
     assert free_bytes() == before
+
+
+def token_create(lib, x, cont):
+    h = P()
+    st = lib.dresd_ivf_create_by_token(P(x.data_ptr()), P(cont.data_ptr()), x.shape[0],
+                                       x.shape[1], cont.shape[1], 1, None, ctypes.byref(h))
+    return st, h
+
+
+# grouping by first token: the first-token column (freed before the next),
+# slot table (3), keys and continuations (2), the sorted token table (1)
+TOKEN_ALLOCS = 7
+
+
+@pytest.mark.parametrize("n", list(range(1, TOKEN_ALLOCS + 1)))
+def test_token_create_allocation_failure(gpu_lib, n):
+    x, cont, _ = datastore(N=1 << 16)
+    before = free_bytes()
+    with fail_alloc_at(n):
+        st, h = token_create(gpu_lib, x, cont)
+    say("token create, allocation %d fails: status %d, %s" % (n, st,
+                                                              gpu_lib.dresd_last_error().decode()))
+    assert st == ENOMEM and h.value is None
+    assert free_bytes() == before
+
+
+def test_token_create_allocation_count(gpu_lib):
+    x, cont, _ = datastore(N=1 << 16)
+    before = free_bytes()
+    with fail_alloc_at(TOKEN_ALLOCS + 1):
+        st, h = token_create(gpu_lib, x, cont)
+    assert st == OK
+    gpu_lib.dresd_ivf_destroy(h)
+    assert free_bytes() == before
+
+
+def test_token_search_allocation_failure(gpu_lib):
+    x, cont, q = datastore(N=1 << 16)
+    st, h = token_create(gpu_lib, x, cont)
+    assert st == OK
+    B, k, L = 4, 10, cont.shape[1]
+    nt = cont[:B, 0].contiguous()
+    idx, score, tok = outputs(B, k, L)
+    args = (h, P(q.data_ptr()), P(nt.data_ptr()), B, k, P(idx.data_ptr()), P(score.data_ptr()),
+            P(tok.data_ptr()), None)
+    with fail_alloc_at(1):  # the partition-scan workspace
+        st = gpu_lib.dresd_ivf_search_next_token(*args)
+    torch.cuda.synchronize()
+    assert st == ENOMEM
+    assert untouched((idx, score, tok))
+    st = gpu_lib.dresd_ivf_search_next_token(*args)
+    torch.cuda.synchronize()
+    assert st == OK and (idx[:, 0] >= 0).all()
+    gpu_lib.dresd_ivf_destroy(h)
 
 
 @pytest.mark.parametrize("n,what", [(1, "probe buffer"), (2, "centroid-search workspace"),
