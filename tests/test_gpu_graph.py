@@ -122,3 +122,51 @@ def test_captured_search_replays_match_eager(gpu_lib, kind, N, d, B, k):
             assert torch.equal(a, b), i
     assert (out[0] >= 0).all()
     ix.close()
+
+
+def test_captured_token_search_replays_match_eager(gpu_lib):
+    """The filtered search over keys grouped by first token in a captured
+    graph (token lookup, group scan, merge): each replay, with new queries
+    and next tokens copied in and other work between replays, returns what
+    the eager search returns, bit for bit."""
+    from paper_2502_15572_amd import PartitionedIndex
+    dev = torch.device(DEV)
+    gen = torch.Generator(device="cuda").manual_seed(6)
+    N, d, B, k = 60000, 128, 4, 16
+    keys = torch.randn(N, d, device=dev, generator=gen)
+    keys = (keys / keys.norm(dim=1, keepdim=True)).to(torch.float16)
+    cont = torch.randint(0, 50, (N, 3), device=dev, generator=gen, dtype=torch.int32)
+    qs = torch.randn(4, B, d, device=dev, generator=gen)
+    qs = qs / qs.norm(dim=2, keepdim=True)
+    nts = torch.randint(0, 52, (4, B), device=dev, generator=gen, dtype=torch.int32)  # 50, 51: no key
+    ix = PartitionedIndex.by_first_token(keys, cont)
+    q_in = torch.empty(B, d, device=dev)
+    nt_in = torch.empty(B, dtype=torch.int32, device=dev)
+    out = (torch.empty((B, k), dtype=torch.int64, device=dev),
+           torch.empty((B, k), dtype=torch.float32, device=dev),
+           torch.empty((B, k, 3), dtype=torch.int32, device=dev))
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        q_in.copy_(qs[0])
+        nt_in.copy_(nts[0])
+        ix.search_next_token(q_in, nt_in, k, out=out, stream=s)  # warm-up: the workspace
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        ix.search_next_token(q_in, nt_in, k, out=out, stream=s)
+    torch.cuda.synchronize()
+    for i in range(6):
+        q_in.copy_(qs[i % 4])
+        nt_in.copy_(nts[(i + 1) % 4])
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        replayed = [t.clone() for t in out]
+        torch.randn(4096, device=dev).sum().item()  # other work between replays
+        with torch.cuda.stream(s):
+            ix.search_next_token(q_in, nt_in, k, out=out, stream=s)
+        torch.cuda.synchronize()
+        for a, b in zip(replayed, out):
+            assert torch.equal(a, b), i
+    assert (out[0] >= -1).all()
+    ix.close()
