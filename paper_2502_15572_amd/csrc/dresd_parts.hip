@@ -19,25 +19,31 @@ __global__ void __launch_bounds__(kSegThreads) dresd_segments(SegParams p) {
   __shared__ int32_t pid[kSegThreads];
   __shared__ int32_t wsum[kSegThreads / kWaveSize];
   __shared__ int32_t found;
+  __shared__ int64_t own;
   const int b = blockIdx.x;
   const int i = threadIdx.x, lane = i & 63, wid = i >> 6;
   int32_t id = -1;
   if (p.tok) {
     // Thread i owns the sorted tokens [lo, hi); the tokens are distinct, so
-    // at most one thread's range [tok[lo], tok[hi - 1]] holds t, and that
-    // thread scans its range for it.
+    // at most one thread's range [tok[lo], tok[hi - 1]] can hold t.  That
+    // thread names its range, and the workgroup reads the range together.
     const int32_t t = p.next_tok[b];
     const int64_t chunk = ((int64_t)p.P + kSegThreads - 1) / kSegThreads;
     const int64_t lo = (int64_t)i * chunk;
     const int64_t hi = lo + chunk < (int64_t)p.P ? lo + chunk : (int64_t)p.P;
-    if (i == 0) found = -1;
+    if (i == 0) {
+      found = -1;
+      own = -1;
+    }
     __syncthreads();
-    if (lo < hi && p.tok[lo] <= t && t <= p.tok[hi - 1])
-      for (int64_t j = lo; j < hi; ++j)
-        if (p.tok[j] == t) {
-          found = (int32_t)j;
-          break;
-        }
+    if (lo < hi && p.tok[lo] <= t && t <= p.tok[hi - 1]) own = lo;
+    __syncthreads();
+    const int64_t o = own;
+    if (o >= 0) {
+      const int64_t oe = o + chunk < (int64_t)p.P ? o + chunk : (int64_t)p.P;
+      for (int64_t j = o + i; j < oe; j += kSegThreads)
+        if (p.tok[j] == t) found = (int32_t)j;
+    }
     __syncthreads();
     if (i == 0) id = found;  // S == 1
   } else if (i < p.S) {
